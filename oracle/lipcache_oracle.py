@@ -1,0 +1,332 @@
+"""Plain, slow, fp64 CPU oracle of LipCache's certified cache path.
+
+TEST INFRASTRUCTURE.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this module.  The product path
+(the HIP library and its Python binding) never calls it and shares no code
+with it: nothing here is imported by, or imports, ``paper_2608_13144_amd``.
+
+Every function writes out the paper's definition on the exact values the
+device path consumes (float32 inputs, or their bfloat16-rounded values for a
+bfloat16 cache), with float64 as the stand-in for exact arithmetic:
+
+  * ``spectral_norm``  - sigma_max(W), the Lipschitz bound of the affine head
+                         (Sec. 5.1, Eq. (18)-(19)); computed by power iteration
+                         as construction step "compute sigma_max(W)" of Alg. 1.
+  * ``certify``        - logits s = W z + b (Sec. 4.1, Eq. (5)), label = argmax
+                         (Eq. (6)), margin m = s_y - max_{j != y} s_j (Eq. (20)),
+                         conservative radius r = m / (sigma_max(W) sqrt 2)
+                         (Eq. (21)); optional tight radius
+                         r* = min_j (s_y - s_j) / ||W_y - W_j|| (Remark 5.1, Eq. (29)).
+  * ``lookup``         - hit set H = {i : ||z - z_i|| < r_i} (Eq. (13)), nearest
+                         hit i* (Eq. (14)), payload or miss (Eq. (15)).
+  * ``insert``         - write-back of missed samples (Sec. 4.4, Alg. 2).
+  * ``bf16_round``     - round-to-nearest-even float32 -> bfloat16 (storage).
+
+Pins: every function is checked in ``tests/`` against closed forms, brute
+force on tiny inputs, Jacobi SVD, Lemma 5.1 and hand cases; see the tests.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+MISS = -1
+BAND_REL = 1e-5          # relative width of the ball-boundary band
+SQRT2 = float(np.sqrt(np.float64(2.0)))
+
+
+class DegenerateHead(ValueError):
+    """sigma_max(W) <= 0: Alg. 1 reports a degenerate head and stops."""
+
+
+class CapacityError(ValueError):
+    """Appending would exceed the cache budget; nothing is appended."""
+
+
+# ---------------------------------------------------------------- bfloat16
+def bf16_round(x) -> np.ndarray:
+    """Round float32 values to the nearest bfloat16 (ties to even), as float32.
+
+    bfloat16 keeps the upper 16 bits of the float32 pattern; the discarded
+    lower half decides the rounding: above half -> up, below -> down, exactly
+    half -> towards the even upper half.  NaN stays NaN.
+    """
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+    bits = a.view(np.uint32).astype(np.uint64)
+    upper = bits >> np.uint64(16)
+    lower = bits & np.uint64(0xFFFF)
+    half = np.uint64(0x8000)
+    round_up = (lower > half) | ((lower == half) & ((upper & np.uint64(1)) == np.uint64(1)))
+    upper = upper + round_up.astype(np.uint64)
+    out = (upper << np.uint64(16)).astype(np.uint32).view(np.float32).copy()
+    nan = np.isnan(a)
+    out[nan] = a[nan]
+    return out.reshape(a.shape)
+
+
+def stored_values(z, store: str) -> np.ndarray:
+    """The values a cache of dtype ``store`` ("f32" or "bf16") holds for z."""
+    z32 = np.asarray(z, dtype=np.float32)
+    if store == "f32":
+        return z32.copy()
+    if store == "bf16":
+        return bf16_round(z32)
+    raise ValueError(f"unknown store dtype {store!r}")
+
+
+# ---------------------------------------------------------- spectral norm
+@dataclass
+class SpectralNorm:
+    sigma: float
+    iterations: int
+    converged: bool
+
+
+def spectral_norm(W, max_iters: int = 20000, rel_tol: float = 1e-13,
+                  seed: int = 0) -> SpectralNorm:
+    """sigma_max(W) by power iteration on W^T W, in float64.
+
+    Alg. 1 computes sigma_max(W) before certifying any candidate; the head is
+    sigma_max(W)-Lipschitz (Eq. (18)).  Start from a seeded Gaussian unit
+    vector v.  Each iteration: u = W v, sigma_k = ||u|| (= ||W v|| with
+    ||v|| = 1), w = W^T u, v = w / ||w||.  Converged once
+    |sigma_k - sigma_{k-1}| <= rel_tol * sigma_k holds on two consecutive
+    iterations.  Raises DegenerateHead when sigma <= 0 (Alg. 1: report and
+    stop).
+    """
+    A = np.asarray(W, dtype=np.float64)
+    if A.ndim != 2 or A.shape[0] < 1 or A.shape[1] < 1:
+        raise ValueError("W must be a non-empty C x d matrix")
+    rng = np.random.default_rng(seed)
+    v = rng.standard_normal(A.shape[1])
+    v /= np.linalg.norm(v)
+    prev = None
+    stable = 0
+    sigma = 0.0
+    for it in range(1, max_iters + 1):
+        u = A @ v
+        sigma = float(np.linalg.norm(u))
+        w = A.T @ u
+        nw = float(np.linalg.norm(w))
+        if nw == 0.0 or sigma <= 0.0:
+            raise DegenerateHead("sigma_max(W) <= 0: degenerate classification head")
+        v = w / nw
+        if prev is not None and abs(sigma - prev) <= rel_tol * sigma:
+            stable += 1
+            if stable >= 2:
+                return SpectralNorm(sigma, it, True)
+        else:
+            stable = 0
+        prev = sigma
+    return SpectralNorm(sigma, max_iters, False)
+
+
+# ----------------------------------------------------------------- certify
+@dataclass
+class Certified:
+    label: np.ndarray      # int32, argmax of the logits (lowest index on ties)
+    r: np.ndarray          # float32 radius, round-to-nearest of the float64 value
+    r64: np.ndarray        # float64 radius before rounding
+    margin: np.ndarray     # float64 top-1 minus top-2 logit
+    norm2: np.ndarray      # float64 squared norm of the stored feature
+    stored: np.ndarray     # float32 values certified (bf16-rounded for a bf16 store)
+    logits: np.ndarray     # float64 (N, C)
+
+
+def logits_of(z, W, b=None) -> np.ndarray:
+    """s(z) = W z + b for every row z (Eq. (5)), in float64."""
+    Z = np.asarray(z, dtype=np.float64)
+    A = np.asarray(W, dtype=np.float64)
+    s = Z @ A.T
+    if b is not None:
+        s = s + np.asarray(b, dtype=np.float64)[None, :]
+    return s
+
+
+def certify(z, W, b, sigma: float, store: str = "f32",
+            radius_mode: str = "conservative") -> Certified:
+    """Label, margin and certified radius of every row of z.
+
+    label y = argmax_c s_c (Eq. (6); lowest index on ties),
+    margin m = s_y - max_{j != y} s_j (Eq. (20)),
+    conservative radius r = m / (sigma sqrt 2) (Eq. (21)), or with
+    ``radius_mode="tight"`` r* = min_{j != y} (s_y - s_j) / ||W_y - W_j||
+    (Remark 5.1, Eq. (29)), where a competitor with W_y = W_j sets no finite
+    constraint.  A radius <= 0 marks a candidate that construction discards
+    (Alg. 1).  For a bfloat16 store the rounded feature is certified.
+    """
+    A = np.asarray(W, dtype=np.float32)
+    C = A.shape[0]
+    if C < 2:
+        raise ValueError("the margin needs at least two classes")
+    if not sigma > 0.0:
+        raise DegenerateHead("sigma_max(W) <= 0")
+    zs = stored_values(z, store)
+    s = logits_of(zs, A, b)
+    n = s.shape[0]
+    label = np.argmax(s, axis=1) if n else np.zeros(0, dtype=np.int64)
+    rows = np.arange(n)
+    top1 = s[rows, label]
+    others = s.copy()
+    others[rows, label] = -np.inf
+    top2 = others.max(axis=1) if n else np.zeros(0)
+    margin = top1 - top2
+    if radius_mode == "conservative":
+        r64 = margin / (float(sigma) * SQRT2)
+    elif radius_mode == "tight":
+        A64 = A.astype(np.float64)
+        r64 = np.empty(n)
+        for i in range(n):
+            y = label[i]
+            best = np.inf
+            for j in range(C):
+                if j == y:
+                    continue
+                den = float(np.linalg.norm(A64[y] - A64[j]))
+                if den == 0.0:
+                    continue
+                best = min(best, (top1[i] - s[i, j]) / den)
+            r64[i] = best
+    else:
+        raise ValueError(f"unknown radius mode {radius_mode!r}")
+    r = r64.astype(np.float32)
+    norm2 = np.sum(zs.astype(np.float64) ** 2, axis=1)
+    return Certified(label.astype(np.int32), r, r64, margin, norm2, zs, s)
+
+
+# ------------------------------------------------------------------ lookup
+@dataclass
+class LookupResult:
+    label: np.ndarray       # int32 payload of i*, MISS on a miss
+    index: np.ndarray       # int64 i*, -1 on a miss
+    dist2: np.ndarray       # float64 ||z - z_i*||^2, +inf on a miss
+    n_hits: np.ndarray      # int64 |H|
+    n_band: np.ndarray      # int64 pairs with |D - r| <= BAND_REL * r
+    flagged: np.ndarray     # bool: a band pair could change this query's answer
+
+
+def lookup(zq, cache_z, cache_r, cache_label, band_rel: float = BAND_REL) -> LookupResult:
+    """Certified lookup of every query against every cache entry (Eq. (13)-(15)).
+
+    For query z: D_i^2 = sum_k (z_k - z_{i,k})^2 in float64 over the stored
+    entry values; H = {i : D_i < r_i}, evaluated as D_i^2 < r_i^2 with r_i > 0
+    (r_i^2 of a float32 r_i is exact in float64); a miss if H is empty, else
+    i* = the hit of least D_i, lowest index among equal distances, and the
+    answer is (label[i*], i*, D_{i*}^2).
+
+    The boundary band is the set of pairs with |D_i - r_i| <= band_rel * r_i.
+    A query is flagged when such a pair could change its answer: it has a
+    band pair and either no hit outside the band, or a band pair no farther
+    than (1 + band_rel) times its nearest non-band hit, or its two nearest
+    hits lie within band_rel of each other.
+    """
+    Q = np.asarray(zq, dtype=np.float64)
+    Z = np.asarray(cache_z)
+    r = np.asarray(cache_r, dtype=np.float32).astype(np.float64)
+    lab = np.asarray(cache_label, dtype=np.int32)
+    B = Q.shape[0]
+    out_label = np.full(B, MISS, dtype=np.int32)
+    out_index = np.full(B, -1, dtype=np.int64)
+    out_d2 = np.full(B, np.inf)
+    n_hits = np.zeros(B, dtype=np.int64)
+    n_band = np.zeros(B, dtype=np.int64)
+    flagged = np.zeros(B, dtype=bool)
+    if Z.shape[0] == 0:
+        return LookupResult(out_label, out_index, out_d2, n_hits, n_band, flagged)
+    r2 = r * r
+    live = r > 0
+    for qi in range(B):
+        D2 = _dist2_to_all(Z, Q[qi])
+        hit = live & (D2 < r2)
+        D = np.sqrt(D2)
+        band = live & (np.abs(D - r) <= band_rel * r)
+        n_hits[qi] = int(hit.sum())
+        n_band[qi] = int(band.sum())
+        if n_hits[qi]:
+            hd = D2[hit]
+            best = hd.min()
+            i_star = int(np.flatnonzero(hit & (D2 == best))[0])
+            out_index[qi] = i_star
+            out_label[qi] = lab[i_star]
+            out_d2[qi] = D2[i_star]
+        if n_band[qi]:
+            solid = hit & ~band
+            if not solid.any():
+                flagged[qi] = True
+            else:
+                d_solid = np.sqrt(D2[solid].min())
+                if np.any(D[band] <= (1.0 + band_rel) * d_solid):
+                    flagged[qi] = True
+        if n_hits[qi] >= 2:
+            hd = np.sort(np.sqrt(D2[hit]))
+            if hd[1] - hd[0] <= band_rel * max(hd[1], 1e-300):
+                flagged[qi] = True
+    return LookupResult(out_label, out_index, out_d2, n_hits, n_band, flagged)
+
+
+def _dist2_to_all(Z, q, chunk: int = 1 << 15) -> np.ndarray:
+    """D_i^2 = sum_k (q_k - z_{i,k})^2 in float64 for every row of Z (rows in chunks)."""
+    out = np.empty(Z.shape[0])
+    for s in range(0, Z.shape[0], chunk):
+        e = min(Z.shape[0], s + chunk)
+        out[s:e] = np.sum((Z[s:e].astype(np.float64) - q) ** 2, axis=1)
+    return out
+
+
+def lookup_rows(zq, cache_z, cache_r, cache_label, rows, band_rel: float = BAND_REL) -> LookupResult:
+    """``lookup`` on the selected query rows only (sampled checks at full size)."""
+    Q = np.asarray(zq)[np.asarray(rows, dtype=np.int64)]
+    return lookup(Q, cache_z, cache_r, cache_label, band_rel)
+
+
+# ------------------------------------------------------------------ insert
+@dataclass
+class CacheState:
+    """Feature cache C = {(z_i, y~_i, r_i)} (Sec. 4.1) with a budget (capacity)."""
+
+    d: int
+    capacity: int
+    store: str = "f32"
+    z: np.ndarray = None          # (n, d) float32 stored values
+    r: np.ndarray = None          # (n,) float32
+    label: np.ndarray = None      # (n,) int32
+    norm2: np.ndarray = None      # (n,) float64 squared norm of the stored values
+
+    def __post_init__(self):
+        if self.z is None:
+            self.z = np.zeros((0, self.d), dtype=np.float32)
+            self.r = np.zeros(0, dtype=np.float32)
+            self.label = np.zeros(0, dtype=np.int32)
+            self.norm2 = np.zeros(0, dtype=np.float64)
+
+    @property
+    def n(self) -> int:
+        return int(self.r.shape[0])
+
+
+def insert(state: CacheState, z_src, label_src, r_src, selector=None) -> int:
+    """Append selected rows in ascending row order (write-back, Sec. 4.4, Alg. 2).
+
+    Row j is taken when ``selector`` is None or ``selector[j] == MISS``, and
+    its radius is positive (a non-positive radius is never cached, Alg. 1).
+    The stored feature is the row cast to the store dtype (bfloat16 rounding to
+    nearest even for a bfloat16 cache); its squared norm is recomputed from the
+    stored values.  All-or-nothing: raises CapacityError, appending nothing,
+    when the selected rows do not fit.  Returns the number of rows appended.
+    """
+    zs = np.asarray(z_src, dtype=np.float32)
+    rs = np.asarray(r_src, dtype=np.float32)
+    ls = np.asarray(label_src, dtype=np.int32)
+    take = rs > 0
+    if selector is not None:
+        take &= np.asarray(selector) == MISS
+    idx = np.flatnonzero(take)
+    if state.n + idx.size > state.capacity:
+        raise CapacityError(f"{state.n} + {idx.size} rows exceed capacity {state.capacity}")
+    stored = stored_values(zs[idx], state.store) if idx.size else np.zeros((0, state.d), np.float32)
+    state.z = np.concatenate([state.z, stored], axis=0)
+    state.r = np.concatenate([state.r, rs[idx]])
+    state.label = np.concatenate([state.label, ls[idx]])
+    state.norm2 = np.concatenate([state.norm2, np.sum(stored.astype(np.float64) ** 2, axis=1)])
+    return int(idx.size)

@@ -1,0 +1,203 @@
+#!/usr/bin/env python3
+"""Throughput of the certified cache path on one MI355X.
+
+One step = one pass of the whole path over one batch of B queries:
+  spectral norm of the head (sync) -> lookup of the batch against the cache
+  -> certification of the batch (labels, radii for write-back) -> insert of
+  the misses (sync) -> the cache is rolled back to its N construction rows,
+  so every step sees the same cache.
+Inputs are resident in device memory before the timed region.  The cache is
+built once beforehand (spectral norm, certification of N candidates, insert),
+and that construction is timed and reported separately.
+
+Prints ONE JSON line (rank 0): value = whole-step lookups/s; the fused lookup
+kernel's roofline (HIP events on the stream the library launches on); and the
+CPU oracle timed on a bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # MI355X dense matrix peaks
+METRIC = "certified lookups/s and query·entry pairs/s at N=1M cache, d=256, C=200"
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(wl, zq_host, target_s: float):
+    """The CPU oracle (as it is) on a bounded sample of the same lookup."""
+    import numpy as np
+
+    import oracle
+    t0 = time.perf_counter()
+    sig = oracle.spectral_norm(wl.W).sigma
+    cert = oracle.certify(wl.z, wl.W, wl.b, sig, store=wl.config.store_dtype)
+    keep = cert.r > 0
+    Z, R, Lb = cert.stored[keep], cert.r[keep], cert.label[keep]
+    t_cert = time.perf_counter() - t0
+    log(f"cpu oracle: certify of {wl.z.shape[0]} candidates in {t_cert:.1f} s")
+    t0 = time.perf_counter()
+    oracle.lookup_rows(zq_host, Z, R, Lb, [0])
+    t1 = time.perf_counter() - t0
+    m = int(max(1, min(256, target_s / max(t1, 1e-6))))
+    rows = np.linspace(0, zq_host.shape[0] - 1, m).astype(np.int64)
+    t0 = time.perf_counter()
+    oracle.lookup_rows(zq_host, Z, R, Lb, rows)
+    t = time.perf_counter() - t0
+    log(f"cpu oracle: {m} lookups in {t:.1f} s")
+    return {"value": m / t, "unit": "lookups/s", "cores": 1, "kind": "oracle",
+            "sample": f"{m} queries of the batch, each against all {Z.shape[0]} entries "
+                      f"(float64 numpy, single thread); pairs/s = {m * Z.shape[0] / t:.3e}",
+            "seconds": t, "cpu_model": _cpu_model(), "certify_seconds": t_cert}
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mix-d256-c200")
+    ap.add_argument("--precision", default="bf16", choices=["bf16", "f32"])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the lookup would shard by queries or by cache rows; see DESIGN.md)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2608_13144_amd import api
+    from paper_2608_13144_amd import workload as wlmod
+
+    dev = torch.device("cuda:0")
+    cfg = wlmod.CONFIGS[args.workload]
+    if cfg.rounds != 1:
+        print(f"{args.workload} is a streaming workload; bench.py times the single-batch workloads",
+              file=sys.stderr)
+        return 2
+    N, B, d, C = cfg.n_cache, cfg.batch, cfg.d, cfg.C
+
+    def g(x):
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+    t0 = time.perf_counter()
+    wl = wlmod.make_workload(cfg, seed=0)
+    log(f"workload {cfg.name}: N={N} B={B} d={d} C={C} drawn in {time.perf_counter() - t0:.1f} s")
+    W, b, zc = g(wl.W), g(wl.b), g(wl.z)
+
+    # ---- cache construction (untimed here, reported)
+    torch.cuda.synchronize()
+    tc = time.perf_counter()
+    sig = api.spectral_norm(W)
+    cert = api.certify(zc, W, b, sig.sigma, store=cfg.store_dtype)
+    cache = api.LipCache(d, N + B, store=cfg.store_dtype, device=dev)
+    cache.insert(zc, cert.label, cert.r)
+    torch.cuda.synchronize()
+    t_build = time.perf_counter() - tc
+    n0 = cache.n
+    log(f"cache built: n={n0} sigma={sig.sigma:.12f} ({sig.iterations} iterations) in {t_build * 1e3:.1f} ms")
+
+    draws = wlmod.draw_queries(wl, 0)
+    idx = wlmod.near_indices(draws, n0)
+    it = torch.from_numpy(idx).to(dev)
+    centres = cache.z[it].float().cpu().numpy()
+    radii = cache.r[it].cpu().numpy()
+    zq_host = wlmod.compose_queries(draws, centres, radii)
+    zq = g(zq_host)
+    res = api.LookupResult(torch.empty(B, dtype=torch.int32, device=dev),
+                           torch.empty(B, dtype=torch.int64, device=dev),
+                           torch.empty(B, dtype=torch.float32, device=dev),
+                           torch.zeros(4, dtype=torch.int64, device=dev),
+                           torch.empty(B, dtype=torch.uint8, device=dev))
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    inserted = []
+
+    def step(i: int | None):
+        s = api.spectral_norm(W).sigma
+        if i is not None:
+            ev[i][0].record()
+        cache.lookup(zq, precision=args.precision, out=res)
+        if i is not None:
+            ev[i][1].record()
+        cq = api.certify(zq, W, b, s, store=cfg.store_dtype)
+        inserted.append(cache.insert(zq, cq.label, cq.r, res.label))
+        cache.n = n0
+
+    for _ in range(args.warmup):
+        step(None)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    lk_ms = [a.elapsed_time(bb) for a, bb in ev]
+    lk = sum(lk_ms) / len(lk_ms)
+    stats = res.stats.cpu().tolist()
+    hits = int(stats[0])
+    log(f"{args.steps} steps in {elapsed:.3f} s; lookup {lk:.3f} ms avg (min {min(lk_ms):.3f}); "
+        f"hits {hits}/{B}; rechecked {stats[1]}; band pairs {stats[2]}; inserted/step {inserted[-1]}")
+
+    flops = 2.0 * B * n0 * d
+    achieved = flops / (lk * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[args.precision]
+    out = {
+        "metric": METRIC,
+        "value": B * args.steps / elapsed,
+        "unit": "lookups/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.precision,
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "N": n0, "B": B, "d": d, "C": C, "store": cfg.store_dtype,
+                   "precision": args.precision, "step": "spectral_norm+lookup+certify(B)+insert(misses)"},
+        "pairs_per_s": B * n0 * args.steps / elapsed,
+        "lookup_ms": lk,
+        "lookup_lookups_per_s": B / (lk * 1e-3),
+        "lookup_pairs_per_s": B * n0 / (lk * 1e-3),
+        "hit_rate": hits / B,
+        "cache_build_ms": t_build * 1e3,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None,
+                     "kernel": "lookup_kernel (fused contraction + filter + re-check)",
+                     "algorithmic": f"2*B*N*d = {flops:.4e} flop per launch"},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, zq_host, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

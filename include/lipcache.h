@@ -1,0 +1,221 @@
+/*
+ * lipcache.h - C ABI of the certified feature cache (LipCache) on gfx950.
+ *
+ * The library implements the certified cache path of "LipCache: A Local
+ * Inference Proxy with Certified Caching for Edge Image Classification
+ * Service": the spectral norm of the guard network's linear head, the
+ * per-entry certified reuse radius, the batched strict-ball lookup with
+ * nearest-hit selection, and the write-back of misses.
+ *
+ * Conventions shared by every entry point
+ *  - Pointers are DEVICE pointers owned by the caller unless marked (host).
+ *    The library never allocates, frees or retains memory and keeps no
+ *    global mutable state: calls on different streams are independent.
+ *    Scratch memory is passed in as a workspace (`ws`, `ws_bytes`); each
+ *    entry point has a *_workspace_bytes query.  `ws` must be 256-byte
+ *    aligned.
+ *  - Matrices are row-major and contiguous; a feature is one row of d
+ *    elements.  Supported feature sizes: 32 <= d <= 1024, d % 32 == 0.
+ *  - Arguments are validated on the host before any device work; a
+ *    validation failure (LIPCACHE_EINVAL, LIPCACHE_EUNSUPPORTED,
+ *    LIPCACHE_EWORKSPACE, LIPCACHE_ECAPACITY) writes nothing.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Calls marked
+ *    (async) only enqueue work: outputs are valid once the stream reaches
+ *    that point.  Calls marked (sync) block until their result is on the
+ *    host.  A failing HIP call returns LIPCACHE_EHIP.
+ *  - Inputs are assumed finite with |component| < 1e15.  A query holding a
+ *    NaN misses; an entry whose radius is NaN or <= 0 is never a hit.
+ */
+#ifndef LIPCACHE_H
+#define LIPCACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LIPCACHE_ABI_VERSION 1
+
+/* Same type as hipStream_t. */
+typedef struct ihipStream_t* lipcache_stream_t;
+
+typedef enum lipcache_status {
+  LIPCACHE_OK = 0,
+  LIPCACHE_EINVAL = 1,        /* invalid argument (null pointer, size, enum)          */
+  LIPCACHE_EDEGENERATE = 2,   /* sigma_max(W) <= 0: construction stops (Alg. 1)        */
+  LIPCACHE_ENOCONV = 3,       /* power iteration hit max_iters; sigma still written    */
+  LIPCACHE_ECAPACITY = 4,     /* insert would exceed the cache capacity; nothing added */
+  LIPCACHE_EUNSUPPORTED = 5,  /* valid request this build does not implement           */
+  LIPCACHE_EWORKSPACE = 6,    /* workspace missing, too small or misaligned            */
+  LIPCACHE_EHIP = 7           /* a HIP runtime call or kernel launch failed            */
+} lipcache_status;
+
+/* Element types: storage of cache features (store_dtype) and the matrix-core
+ * precision of the lookup's distance filter (precision). */
+enum { LIPCACHE_F32 = 0, LIPCACHE_BF16 = 1 };
+
+/* Radius modes (policy component rho, Sec. 4.3): the conservative radius of
+ * Eq. (21) or the tight per-pair radius of Remark 5.1, Eq. (29). */
+enum { LIPCACHE_RADIUS_CONSERVATIVE = 0, LIPCACHE_RADIUS_TIGHT = 1 };
+
+/* Label written for a query whose hit set is empty (falls back to MainNet,
+ * Eq. (15)). */
+#define LIPCACHE_MISS (-1)
+
+/* Indices of the lookup statistics counters (uint64_t stats[4]). */
+enum {
+  LIPCACHE_STAT_HITS = 0,        /* queries with a non-empty hit set                   */
+  LIPCACHE_STAT_RECHECKED = 1,   /* (query, entry) pairs the exact re-check evaluated  */
+  LIPCACHE_STAT_BAND_PAIRS = 2,  /* re-checked pairs with |D - r| <= 1e-5 r            */
+  LIPCACHE_STAT_BAND_QUERIES = 3 /* queries with at least one such pair                */
+};
+
+/*
+ * The feature cache C = {(z_i, y~_i, r_i)} (Sec. 4.1; Alg. 2 input) with its
+ * budget B_C (`capacity`, Alg. 1).  Struct-of-arrays, every device array
+ * holds `capacity` rows, rows [0, n) are live.  The caller owns the arrays;
+ * lipcache_insert writes rows and advances `n`.
+ */
+typedef struct lipcache_cache {
+  void*    z;           /* [capacity][d] features; float (F32) or bf16 bits (BF16)   */
+  float*   r;           /* [capacity] certified radius r_i                           */
+  int32_t* label;       /* [capacity] payload y~_i                                   */
+  float*   norm2;       /* [capacity] ||z_i||^2 of the stored values (derived)       */
+  int64_t  n;           /* live rows; host-side value                                */
+  int64_t  capacity;    /* rows allocated in each array                              */
+  int32_t  d;           /* feature size                                              */
+  int32_t  store_dtype; /* LIPCACHE_F32 or LIPCACHE_BF16                             */
+} lipcache_cache;
+
+/*
+ * sigma_max(W), the spectral norm of the head f(z) = W z + b (Sec. 5.1,
+ * Eq. (18)): the Lipschitz constant every certificate divides by.  Alg. 1
+ * computes it before certifying any candidate and stops when it is <= 0.
+ *
+ * Power iteration in float64 on the Gram matrix of W (W W^T when C <= d,
+ * else W^T W; same non-zero spectrum): v <- G v / ||G v||, with the estimate
+ * sigma_k = sqrt(v_k^T G v_k) (= ||W v_k|| for unit v_k).  Stops after two
+ * consecutive iterations with |sigma_k - sigma_{k-1}| <= rel_tol sigma_k.
+ *
+ *  W          [C][d] float head, C >= 1, 1 <= d, min(C, d) <= 1024
+ *  max_iters  >= 1
+ *  rel_tol    > 0 (1e-13 gives sigma to about 1e-12 relative)
+ *  sigma      (host) out: the estimate, written on OK, ENOCONV and EDEGENERATE
+ *  iterations (host, nullable) out: iterations run
+ *  ws         lipcache_spectral_norm_workspace_bytes(C, d) bytes
+ * Returns OK, ENOCONV (max_iters reached), EDEGENERATE (sigma <= 0). (sync)
+ */
+lipcache_status lipcache_spectral_norm(const float* W, int32_t C, int32_t d,
+                                       int32_t max_iters, double rel_tol,
+                                       double* sigma, int32_t* iterations,
+                                       void* ws, size_t ws_bytes,
+                                       lipcache_stream_t stream);
+size_t lipcache_spectral_norm_workspace_bytes(int32_t C, int32_t d);
+
+/*
+ * Certification of N candidate features (Sec. 4.3, Alg. 1; Sec. 5.2).
+ * For every row z_i (rounded to bf16, ties to even, first when store_dtype
+ * is BF16: the stored centre is what is certified):
+ *   logits s = W z_i + b accumulated in float64 (Eq. (5)),
+ *   label y_i = argmax_c s_c, lowest index on ties (Eq. (6)),
+ *   margin m_i = s_y - max_{j != y} s_j (Eq. (20)),
+ *   radius r_i = m_i / (sigma sqrt 2) (Eq. (21)), rounded to nearest float.
+ * A radius <= 0 (a tie) marks a candidate that must be discarded (Alg. 1).
+ *
+ *  z [N][d] float; W [C][d] float, C >= 2; b [C] float or NULL (= 0)
+ *  sigma       > 0, normally lipcache_spectral_norm's result
+ *  radius_mode LIPCACHE_RADIUS_CONSERVATIVE (TIGHT returns EUNSUPPORTED)
+ *  label_out [N] int32, r_out [N] float (required)
+ *  margin_out [N] float, norm2_out [N] float (nullable): m_i and ||z_i||^2
+ *  ws          lipcache_certify_workspace_bytes(C, d, radius_mode) bytes
+ * N = 0 is valid and does nothing. (async)
+ */
+lipcache_status lipcache_certify(const float* z, int64_t N, int32_t d,
+                                 const float* W, const float* b, int32_t C,
+                                 double sigma, int32_t radius_mode,
+                                 int32_t store_dtype, int32_t* label_out,
+                                 float* r_out, float* margin_out,
+                                 float* norm2_out, void* ws, size_t ws_bytes,
+                                 lipcache_stream_t stream);
+size_t lipcache_certify_workspace_bytes(int32_t C, int32_t d, int32_t radius_mode);
+
+/*
+ * Batched certified lookup (Sec. 4.4, Eq. (13)-(15); Alg. 2).  For every
+ * query q the hit set is H(q) = {i < n : ||q - z_i||_2 < r_i} (strict) and
+ * the answer is the nearest hit i* (least distance, lowest index among equal
+ * float32-rounded distances) with its payload, or a miss.
+ *
+ * Distances are filtered on the matrix cores (bf16 or fp32 MFMA) with a
+ * rigorous error slack, so no true hit is ever dropped; every surviving pair
+ * is re-checked as sum_k (q_k - z_ik)^2 in float64, which decides the hit.
+ *
+ *  c          cache (host struct; its arrays on the device), n >= 0
+ *  zq         [B][c->d] float queries, B >= 0
+ *  precision  LIPCACHE_BF16 or LIPCACHE_F32 (F32 requires d <= 512)
+ *  label_out  [B] int32: y~_{i*}, or LIPCACHE_MISS (required)
+ *  index_out  [B] int64: i*, or -1 (nullable)
+ *  dist2_out  [B] float: ||q - z_{i*}||^2 rounded to nearest, +inf on a miss (nullable)
+ *  stats      [4] uint64 counters, see LIPCACHE_STAT_* (nullable; overwritten)
+ *  band_flag  [B] uint8: 1 if a re-checked pair of the query lies within
+ *             relative 1e-5 of its ball boundary (nullable)
+ *  ws         lipcache_lookup_workspace_bytes(B, n, d, precision) bytes
+ * (async)
+ */
+lipcache_status lipcache_lookup(const lipcache_cache* c, const float* zq, int64_t B,
+                                int32_t precision, int32_t* label_out,
+                                int64_t* index_out, float* dist2_out,
+                                uint64_t* stats, uint8_t* band_flag,
+                                void* ws, size_t ws_bytes, lipcache_stream_t stream);
+size_t lipcache_lookup_workspace_bytes(int64_t B, int64_t N, int32_t d, int32_t precision);
+
+/*
+ * Write-back (Sec. 4.4, Alg. 2; construction, Alg. 1): append, in ascending
+ * row order, every row j of z_src with r_src[j] > 0 and (miss_selector ==
+ * NULL or miss_selector[j] == LIPCACHE_MISS).  The feature is stored in the
+ * cache's dtype (bf16 rounded to nearest even), with its label, radius and
+ * the squared norm of the stored values.  All-or-nothing: when the selected
+ * rows do not fit into capacity - n, returns ECAPACITY and appends nothing.
+ *
+ *  c              cache; c->n is advanced by the rows appended
+ *  z_src [k][c->d] float, label_src [k] int32, r_src [k] float (required)
+ *  miss_selector  [k] int32 or NULL (e.g. lipcache_lookup's label_out)
+ *  inserted       (host, nullable) out: rows appended
+ *  ws             lipcache_insert_workspace_bytes(k) bytes
+ * (sync: one device-to-host read of the selected count)
+ */
+lipcache_status lipcache_insert(lipcache_cache* c, const float* z_src,
+                                const int32_t* label_src, const float* r_src,
+                                const int32_t* miss_selector, int64_t k,
+                                int64_t* inserted, void* ws, size_t ws_bytes,
+                                lipcache_stream_t stream);
+size_t lipcache_insert_workspace_bytes(int64_t k);
+
+/*
+ * Diagnostic view of the lookup's distance filter for small problems.  For
+ * every pair (q, i < n) writes the matrix-core dot product g_hat = q . z_i
+ * exactly as the lookup kernel computes it, and cand = 1 if the pair passes
+ * the filter (and is re-checked by lipcache_lookup), else 0.
+ *
+ *  g_hat [B][n] float, cand [B][n] uint8 (required); B * n <= 2^26
+ *  ws    lipcache_lookup_workspace_bytes(B, n, d, precision) bytes
+ * (async)
+ */
+lipcache_status lipcache_lookup_filter_dump(const lipcache_cache* c, const float* zq,
+                                            int64_t B, int32_t precision,
+                                            float* g_hat, uint8_t* cand,
+                                            void* ws, size_t ws_bytes,
+                                            lipcache_stream_t stream);
+
+/* Static description of a status code. */
+const char* lipcache_status_string(lipcache_status status);
+
+/* LIPCACHE_ABI_VERSION of the built library. */
+int32_t lipcache_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIPCACHE_H */

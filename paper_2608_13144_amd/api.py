@@ -1,0 +1,192 @@
+"""Torch-facing binding of the certified cache library.
+
+PyTorch provides device memory and the current HIP stream; every step of the
+path runs in the HIP kernels behind ``liblipcache.so``.  The functions mirror
+the C ABI names (``lipcache_spectral_norm`` -> ``spectral_norm`` ...).
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+
+import torch
+
+from . import _lib as L
+
+_STORE = {"f32": L.F32, "bf16": L.BF16}
+_PRECISION = {"f32": L.F32, "bf16": L.BF16}
+_RADIUS = {"conservative": L.RADIUS_CONSERVATIVE, "tight": L.RADIUS_TIGHT}
+
+
+def _p(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _need_cuda(t: torch.Tensor, name: str, dtype: torch.dtype, ndim: int | None = None) -> None:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions")
+
+
+def workspace(nbytes: int, device: torch.device) -> torch.Tensor:
+    """Scratch buffer from torch's allocator (block starts are 512-byte aligned)."""
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+@dataclass
+class SpectralNorm:
+    sigma: float
+    iterations: int
+    converged: bool
+
+
+def spectral_norm(W: torch.Tensor, max_iters: int = 20000, rel_tol: float = 1e-13) -> SpectralNorm:
+    """lipcache_spectral_norm: sigma_max(W) by float64 power iteration (sync)."""
+    _need_cuda(W, "W", torch.float32, 2)
+    lib = L.load()
+    C, d = W.shape
+    ws = workspace(lib.lipcache_spectral_norm_workspace_bytes(C, d), W.device)
+    sigma = ctypes.c_double(0.0)
+    iters = ctypes.c_int32(0)
+    st = lib.lipcache_spectral_norm(_p(W), C, d, int(max_iters), float(rel_tol), ctypes.byref(sigma),
+                                    ctypes.byref(iters), _p(ws), ws.numel(), _stream(W.device))
+    L.check("lipcache_spectral_norm", st, allow=(L.OK, L.ENOCONV))
+    return SpectralNorm(sigma.value, iters.value, st == L.OK)
+
+
+@dataclass
+class Certified:
+    label: torch.Tensor          # int32 [N]
+    r: torch.Tensor              # float32 [N]
+    margin: torch.Tensor | None  # float32 [N]
+    norm2: torch.Tensor | None   # float32 [N]
+
+
+def certify(z: torch.Tensor, W: torch.Tensor, b: torch.Tensor | None, sigma: float, store: str = "f32",
+            radius_mode: str = "conservative", want_margin: bool = False,
+            want_norm2: bool = False) -> Certified:
+    """lipcache_certify: labels, margins and certified radii of the rows of z (async)."""
+    _need_cuda(z, "z", torch.float32, 2)
+    _need_cuda(W, "W", torch.float32, 2)
+    if b is not None:
+        _need_cuda(b, "b", torch.float32, 1)
+    lib = L.load()
+    N, d = z.shape
+    C = W.shape[0]
+    dev = z.device
+    label = torch.empty(N, dtype=torch.int32, device=dev)
+    r = torch.empty(N, dtype=torch.float32, device=dev)
+    margin = torch.empty(N, dtype=torch.float32, device=dev) if want_margin else None
+    norm2 = torch.empty(N, dtype=torch.float32, device=dev) if want_norm2 else None
+    mode = _RADIUS[radius_mode]
+    ws = workspace(lib.lipcache_certify_workspace_bytes(C, d, mode), dev)
+    st = lib.lipcache_certify(_p(z), N, d, _p(W), _p(b), C, float(sigma), mode, _STORE[store], _p(label),
+                              _p(r), _p(margin), _p(norm2), _p(ws), ws.numel(), _stream(dev))
+    L.check("lipcache_certify", st)
+    return Certified(label, r, margin, norm2)
+
+
+@dataclass
+class LookupResult:
+    label: torch.Tensor           # int32 [B], MISS on a miss
+    index: torch.Tensor | None    # int64 [B], -1 on a miss
+    dist2: torch.Tensor | None    # float32 [B], +inf on a miss
+    stats: torch.Tensor           # int64 [4]: hits, re-checked pairs, band pairs, band queries
+    band: torch.Tensor | None     # uint8 [B]
+
+
+class LipCache:
+    """The feature cache C = {(z_i, y~_i, r_i)} in device memory (caller-owned tensors)."""
+
+    def __init__(self, d: int, capacity: int, store: str = "f32", device: str | torch.device = "cuda"):
+        self.d = int(d)
+        self.capacity = int(capacity)
+        self.store = store
+        self.device = torch.device(device)
+        zdt = torch.float32 if store == "f32" else torch.bfloat16
+        self.z = torch.empty((self.capacity, self.d), dtype=zdt, device=self.device)
+        self.r = torch.empty(self.capacity, dtype=torch.float32, device=self.device)
+        self.label = torch.empty(self.capacity, dtype=torch.int32, device=self.device)
+        self.norm2 = torch.empty(self.capacity, dtype=torch.float32, device=self.device)
+        self.n = 0
+        self._ws = None
+
+    def cstruct(self) -> L.LipcacheCache:
+        return L.LipcacheCache(self.z.data_ptr(), self.r.data_ptr(), self.label.data_ptr(),
+                               self.norm2.data_ptr(), self.n, self.capacity, self.d, _STORE[self.store])
+
+    def _workspace(self, nbytes: int) -> torch.Tensor:
+        if self._ws is None or self._ws.numel() < nbytes:
+            self._ws = workspace(nbytes, self.device)
+        return self._ws
+
+    def insert(self, z_src: torch.Tensor, label_src: torch.Tensor, r_src: torch.Tensor,
+               miss_selector: torch.Tensor | None = None) -> int:
+        """lipcache_insert: append selected rows (ascending), all-or-nothing (sync)."""
+        _need_cuda(z_src, "z_src", torch.float32, 2)
+        _need_cuda(label_src, "label_src", torch.int32, 1)
+        _need_cuda(r_src, "r_src", torch.float32, 1)
+        if miss_selector is not None:
+            _need_cuda(miss_selector, "miss_selector", torch.int32, 1)
+        lib = L.load()
+        k = z_src.shape[0]
+        if z_src.shape[1] != self.d or label_src.shape[0] != k or r_src.shape[0] != k:
+            raise ValueError("insert: shapes do not match the cache")
+        if miss_selector is not None and miss_selector.shape[0] != k:
+            raise ValueError("insert: selector length")
+        ws = self._workspace(lib.lipcache_insert_workspace_bytes(k))
+        cs = self.cstruct()
+        got = ctypes.c_int64(0)
+        st = lib.lipcache_insert(ctypes.byref(cs), _p(z_src), _p(label_src), _p(r_src), _p(miss_selector), k,
+                                 ctypes.byref(got), _p(ws), ws.numel(), _stream(self.device))
+        L.check("lipcache_insert", st)
+        self.n = int(cs.n)
+        return int(got.value)
+
+    def lookup(self, zq: torch.Tensor, precision: str = "bf16", want_index: bool = True,
+               want_dist2: bool = True, want_band: bool = True, out: LookupResult | None = None) -> LookupResult:
+        """lipcache_lookup: nearest certified hit per query, or MISS (async)."""
+        _need_cuda(zq, "zq", torch.float32, 2)
+        if zq.shape[1] != self.d:
+            raise ValueError("lookup: query width differs from the cache's d")
+        lib = L.load()
+        B = zq.shape[0]
+        dev = self.device
+        if out is None:
+            out = LookupResult(
+                torch.empty(B, dtype=torch.int32, device=dev),
+                torch.empty(B, dtype=torch.int64, device=dev) if want_index else None,
+                torch.empty(B, dtype=torch.float32, device=dev) if want_dist2 else None,
+                torch.zeros(4, dtype=torch.int64, device=dev),
+                torch.empty(B, dtype=torch.uint8, device=dev) if want_band else None)
+        prec = _PRECISION[precision]
+        ws = self._workspace(lib.lipcache_lookup_workspace_bytes(B, self.n, self.d, prec))
+        cs = self.cstruct()
+        st = lib.lipcache_lookup(ctypes.byref(cs), _p(zq), B, prec, _p(out.label), _p(out.index), _p(out.dist2),
+                                 _p(out.stats), _p(out.band), _p(ws), ws.numel(), _stream(dev))
+        L.check("lipcache_lookup", st)
+        return out
+
+    def filter_dump(self, zq: torch.Tensor, precision: str = "bf16"):
+        """lipcache_lookup_filter_dump: matrix-core dot products and filter decisions (small sizes)."""
+        _need_cuda(zq, "zq", torch.float32, 2)
+        lib = L.load()
+        B = zq.shape[0]
+        g_hat = torch.full((B, self.n), float("nan"), dtype=torch.float32, device=self.device)
+        cand = torch.zeros((B, self.n), dtype=torch.uint8, device=self.device)
+        prec = _PRECISION[precision]
+        ws = self._workspace(lib.lipcache_lookup_workspace_bytes(B, self.n, self.d, prec))
+        cs = self.cstruct()
+        st = lib.lipcache_lookup_filter_dump(ctypes.byref(cs), _p(zq), B, prec, _p(g_hat), _p(cand), _p(ws),
+                                             ws.numel(), _stream(self.device))
+        L.check("lipcache_lookup_filter_dump", st)
+        return g_hat, cand

@@ -1,0 +1,105 @@
+// Internal helpers shared by the HIP sources of liblipcache (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "lipcache.h"
+
+namespace lc {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+// ------------------------------------------------------------------ status
+#define LC_HIP(call)                                  \
+  do {                                                \
+    hipError_t lc_e_ = (call);                        \
+    if (lc_e_ != hipSuccess) return LIPCACHE_EHIP;    \
+  } while (0)
+
+#define LC_LAUNCHED()                                          \
+  do {                                                         \
+    if (hipGetLastError() != hipSuccess) return LIPCACHE_EHIP; \
+  } while (0)
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+inline bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+
+// ------------------------------------------------------------- bfloat16
+// Round to nearest even via the hardware conversion (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint16_t bf16_bits(float x) {
+  __bf16 h = static_cast<__bf16>(x);
+  return __builtin_bit_cast(uint16_t, h);
+}
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __builtin_bit_cast(float, static_cast<uint32_t>(b) << 16);
+}
+__device__ __forceinline__ float bf16_round_f32(float x) { return bf16_to_f32(bf16_bits(x)); }
+
+// Pack 8 floats into 8 bf16 (one 16-byte MFMA operand chunk).
+__device__ __forceinline__ u32x4 pack_bf16x8(const float* v) {
+  u32x4 o;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    o[i] = static_cast<uint32_t>(bf16_bits(v[2 * i])) |
+           (static_cast<uint32_t>(bf16_bits(v[2 * i + 1])) << 16);
+  return o;
+}
+
+// ------------------------------------------------------------- reductions
+// Butterfly sum over the 64 lanes of a wave; fixed order, so bitwise
+// reproducible from run to run.
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+__device__ __forceinline__ int lane_id() { return static_cast<int>(threadIdx.x) & (kWave - 1); }
+
+// Wave-uniform value (lets the compiler keep it in a scalar register).
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Next float towards -infinity (finite input).
+__device__ __forceinline__ float f32_step_down(float f) {
+  const uint32_t b = __builtin_bit_cast(uint32_t, f);
+  if (f > 0.0f) return __builtin_bit_cast(float, b - 1u);
+  if (f < 0.0f) return __builtin_bit_cast(float, b + 1u);
+  return __builtin_bit_cast(float, 0x80000001u);  // below +-0: the negative sub-normal of least magnitude
+}
+
+// Largest float <= x (x in float64; +-inf and NaN pass through the conversion).
+__device__ __forceinline__ float f32_round_down(double x) {
+  float f = static_cast<float>(x);
+  if (static_cast<double>(f) > x) f = f32_step_down(f);
+  return f;
+}
+
+// --------------------------------------------------------- filter slack
+// Bound on |g_hat - q.c| relative to sum_k |q_k c_k| for the matrix-core dot
+// product of d_pad terms: bf16 rounding of the operands plus float32
+// accumulation in any order (gamma_n = n u / (1 - n u), u = 2^-24).
+inline double filter_kappa(int precision, int store_dtype, int d_pad) {
+  const double u32 = 1.0 / 16777216.0;        // 2^-24
+  const double ub = 1.0 / 256.0;              // 2^-8, bf16 unit roundoff
+  const double n = static_cast<double>(d_pad) + 2.0;
+  const double gam = n * u32 / (1.0 - n * u32);
+  double k;
+  if (precision == LIPCACHE_F32) {
+    k = gam;                                              // products and sums in fp32
+  } else if (store_dtype == LIPCACHE_BF16) {
+    k = ub + gam * (1.0 + ub);                            // only the query is rounded
+  } else {
+    k = 2.0 * ub + ub * ub + gam * (1.0 + ub) * (1.0 + ub); // both operands rounded
+  }
+  return 2.0 * k;  // safety factor: the accumulation order inside MFMA is not specified
+}
+
+// Absolute slack that covers flushed sub-normal products.
+constexpr double kFilterAbsSlack = 1e-25;
+
+}  // namespace lc

@@ -1,0 +1,147 @@
+"""The C ABI on the host: symbols, workspace queries and argument validation.
+
+No call here reaches the device: every case returns from host-side
+validation before any HIP call is made.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_13144_amd import _lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lipcache.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(L.LIB_PATH), reason="liblipcache.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lipcache_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported_and_bound():
+    lib = L.load()
+    names = declared_functions()
+    assert len(names) >= 11
+    for name in names:
+        assert hasattr(lib, name), name
+        assert name in L.SIGNATURES, f"binding lacks {name}"
+    assert lib.lipcache_abi_version() == 1
+
+
+def test_status_strings():
+    for s in range(8):
+        assert L.status_string(s)
+    assert "degenerate" in L.status_string(L.EDEGENERATE)
+
+
+def test_workspace_queries():
+    lib = L.load()
+    assert lib.lipcache_spectral_norm_workspace_bytes(200, 256) >= 200 * 200 * 8
+    assert lib.lipcache_spectral_norm_workspace_bytes(300, 64) >= 64 * 64 * 8
+    assert lib.lipcache_certify_workspace_bytes(200, 256, 0) >= 200 * 256 * 8
+    assert lib.lipcache_lookup_workspace_bytes(32768, 1 << 20, 256, L.BF16) >= 32768 * 16
+    assert lib.lipcache_insert_workspace_bytes(65536) >= 2 * 64 * 8
+
+
+FAKE = ctypes.c_void_p(0x100000)  # never dereferenced: validation fails first
+
+
+def _cache(**kw):
+    c = L.LipcacheCache(FAKE.value, FAKE.value, FAKE.value, FAKE.value, 0, 16, 64, L.F32)
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+def test_spectral_norm_validation():
+    lib = L.load()
+    s = ctypes.c_double()
+    it = ctypes.c_int32()
+    ws = ctypes.create_string_buffer(1 << 16)
+    assert lib.lipcache_spectral_norm(None, 4, 4, 10, 1e-12, ctypes.byref(s), ctypes.byref(it), ws, 1 << 16, None) == L.EINVAL
+    assert lib.lipcache_spectral_norm(FAKE, 0, 4, 10, 1e-12, ctypes.byref(s), None, ws, 1 << 16, None) == L.EINVAL
+    assert lib.lipcache_spectral_norm(FAKE, 4, 4, 0, 1e-12, ctypes.byref(s), None, ws, 1 << 16, None) == L.EINVAL
+    assert lib.lipcache_spectral_norm(FAKE, 4, 4, 10, 0.0, ctypes.byref(s), None, ws, 1 << 16, None) == L.EINVAL
+    assert lib.lipcache_spectral_norm(FAKE, 4, 4, 10, 1e-12, None, None, ws, 1 << 16, None) == L.EINVAL
+    assert lib.lipcache_spectral_norm(FAKE, 2000, 2000, 10, 1e-12, ctypes.byref(s), None, ws, 1 << 16, None) == L.EUNSUPPORTED
+    assert lib.lipcache_spectral_norm(FAKE, 4, 4, 10, 1e-12, ctypes.byref(s), None, None, 0, None) == L.EWORKSPACE
+
+
+def test_certify_validation():
+    lib = L.load()
+    args = dict(z=FAKE, N=10, d=64, W=FAKE, b=None, C=10, sigma=1.0, mode=0, store=0,
+                label=FAKE, r=FAKE, margin=None, norm2=None, ws=FAKE, wsb=1 << 20)
+
+    def call(**over):
+        a = dict(args, **over)
+        return lib.lipcache_certify(a["z"], a["N"], a["d"], a["W"], a["b"], a["C"], a["sigma"], a["mode"],
+                                    a["store"], a["label"], a["r"], a["margin"], a["norm2"], a["ws"], a["wsb"], None)
+    assert call(d=33) == L.EINVAL
+    assert call(d=16) == L.EINVAL
+    assert call(d=2048) == L.EINVAL
+    assert call(C=1) == L.EINVAL
+    assert call(N=-1) == L.EINVAL
+    assert call(sigma=0.0) == L.EINVAL
+    assert call(sigma=-1.0) == L.EINVAL
+    assert call(store=7) == L.EINVAL
+    assert call(mode=9) == L.EINVAL
+    assert call(label=None) == L.EINVAL
+    assert call(z=ctypes.c_void_p(0x100004)) == L.EINVAL  # misaligned
+    assert call(mode=L.RADIUS_TIGHT) == L.EUNSUPPORTED
+    assert call(ws=None) == L.EWORKSPACE
+    assert call(wsb=16) == L.EWORKSPACE
+    assert call(ws=ctypes.c_void_p(0x100040)) == L.EWORKSPACE  # not 256-aligned
+
+
+def test_lookup_validation():
+    lib = L.load()
+
+    def call(c, B=8, prec=L.BF16, zq=FAKE, label=FAKE, ws=FAKE, wsb=1 << 20):
+        return lib.lipcache_lookup(ctypes.byref(c) if c is not None else None, zq, B, prec, label, None, None,
+                                   None, None, ws, wsb, None)
+    assert call(None) == L.EINVAL
+    assert call(_cache(d=48)) == L.EINVAL
+    assert call(_cache(store_dtype=3)) == L.EINVAL
+    assert call(_cache(n=20)) == L.EINVAL            # n > capacity
+    assert call(_cache(z=None)) == L.EINVAL
+    assert call(_cache(), B=-1) == L.EINVAL
+    assert call(_cache(), prec=5) == L.EINVAL
+    assert call(_cache(), zq=None) == L.EINVAL
+    assert call(_cache(), label=None) == L.EINVAL
+    assert call(_cache(d=1024), prec=L.F32) == L.EUNSUPPORTED
+    assert call(_cache(), ws=None) == L.EWORKSPACE
+    assert call(_cache(), wsb=64) == L.EWORKSPACE
+
+
+def test_insert_validation():
+    lib = L.load()
+
+    def call(c, k=4, z=FAKE, lab=FAKE, r=FAKE, ws=FAKE, wsb=1 << 20):
+        n = ctypes.c_int64(-5)
+        st = lib.lipcache_insert(ctypes.byref(c) if c is not None else None, z, lab, r, None, k,
+                                 ctypes.byref(n), ws, wsb, None)
+        return st, n.value
+    assert call(None)[0] == L.EINVAL
+    assert call(_cache(), k=-1)[0] == L.EINVAL
+    assert call(_cache(d=40))[0] == L.EINVAL
+    assert call(_cache(), z=None)[0] == L.EINVAL
+    assert call(_cache(), r=None)[0] == L.EINVAL
+    assert call(_cache(n=-1))[0] == L.EINVAL
+    assert call(_cache(), ws=None)[0] == L.EWORKSPACE
+    st, n = call(_cache(), k=0)
+    assert st == L.OK and n == 0
+
+
+def test_binding_refuses_without_library(tmp_path):
+    saved = L._LIB
+    try:
+        L._LIB = None
+        with pytest.raises(RuntimeError, match="not built"):
+            L.load(str(tmp_path / "missing.so"))
+    finally:
+        L._LIB = saved

@@ -1,0 +1,374 @@
+"""HIP path vs the fp64 CPU oracle on the same seeded inputs (needs the GPU).
+
+Bars (written here, from the required tolerances):
+  * labels, hit/miss and indices bit-exact on every query the oracle does not
+    flag (a flagged query has a pair within relative 1e-5 of its ball
+    boundary, or two hits within 1e-5 of each other); flagged queries are
+    counted and checked for validity instead;
+  * radii and returned distances within relative 1e-5; sigma within 1e-9;
+  * stored bf16 values and insert order bit-exact;
+  * the matrix-core filter never rejects a true hit, and its pre-re-check
+    distance is within 1e-5 (fp32 MFMA) / 1e-3 (bf16 MFMA) of
+    ||q||^2 + ||z||^2.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_13144_amd import _lib as L
+from paper_2608_13144_amd import api
+from paper_2608_13144_amd import workload as wlmod
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def say(*a):
+    print("[gpu-test]", *a, file=sys.stderr, flush=True)
+
+
+def gpu(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def build_cache(state: "oracle.CacheState", capacity=None, store=None):
+    """GPU cache holding the same rows as an oracle state (inserted through the HIP path)."""
+    store = store or state.store
+    cap = capacity or max(state.n, 1)
+    c = api.LipCache(state.d, cap, store=store, device=DEV)
+    if state.n:
+        got = c.insert(gpu(state.z.astype(np.float32)), gpu(state.label), gpu(state.r))
+        assert got == state.n
+    return c
+
+
+def oracle_cache(z, label, r, d, store="f32", capacity=None):
+    st = oracle.CacheState(d=d, capacity=capacity or max(len(r), 1), store=store)
+    oracle.insert(st, z, label, r)
+    return st
+
+
+def compare_lookup(res_gpu, ref, what):
+    lab = host(res_gpu.label)
+    idx = host(res_gpu.index)
+    d2 = host(res_gpu.dist2)
+    ok = ~ref.flagged
+    nflag = int(ref.flagged.sum())
+    bad_lab = np.flatnonzero(ok & (lab != ref.label))
+    bad_idx = np.flatnonzero(ok & (idx != ref.index))
+    assert bad_lab.size == 0, f"{what}: label mismatch at {bad_lab[:10]} gpu={lab[bad_lab[:10]]} ref={ref.label[bad_lab[:10]]}"
+    assert bad_idx.size == 0, f"{what}: index mismatch at {bad_idx[:10]}"
+    hit = ok & (ref.index >= 0)
+    if hit.any():
+        rel = np.abs(d2[hit].astype(np.float64) - ref.dist2[hit]) / np.maximum(ref.dist2[hit], 1e-300)
+        assert rel.max() <= 1e-5, f"{what}: dist2 rel err {rel.max()}"
+    assert np.all(np.isinf(d2[ok & (ref.index < 0)]))
+    return nflag
+
+
+# --------------------------------------------------------------- fixtures
+@pytest.fixture(scope="module")
+def tiny():
+    say("fixture tiny-d64-c10")
+    wl = wlmod.make_workload("tiny-d64-c10", seed=0)
+    sig = oracle.spectral_norm(wl.W).sigma
+    cert = oracle.certify(wl.z, wl.W, wl.b, sig)
+    st = oracle_cache(wl.z, cert.label, cert.r, 64)
+    draws = wlmod.draw_queries(wl, 0)
+    idx = wlmod.near_indices(draws, st.n)
+    zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
+    ref = oracle.lookup(zq, st.z, st.r, st.label)
+    return dict(wl=wl, sigma=sig, cert=cert, state=st, zq=zq, ref=ref)
+
+
+# --------------------------------------------------------------- spectral norm
+@pytest.mark.parametrize("C,d", [(10, 64), (10, 128), (100, 128), (200, 256), (300, 64), (1000, 96),
+                                 (600, 700), (2, 32), (1, 5)])
+def test_spectral_norm_matches_oracle(C, d):
+    say("spectral_norm", C, d)
+    rng = np.random.default_rng(C * 1000 + d)
+    W = (rng.standard_normal((C, d)) / math.sqrt(d)).astype(np.float32)
+    ref = oracle.spectral_norm(W)
+    got = api.spectral_norm(gpu(W))
+    assert got.converged and ref.converged
+    assert abs(got.sigma - ref.sigma) <= 1e-9 * ref.sigma, (got.sigma, ref.sigma)
+
+
+def test_spectral_norm_closed_forms_and_errors():
+    say("spectral_norm closed forms")
+    W = np.zeros((2, 64), np.float32)
+    W[0, 0], W[1, 0] = 1.0, -1.0
+    assert abs(api.spectral_norm(gpu(W)).sigma - math.sqrt(2)) <= 1e-13
+    D = np.zeros((3, 32), np.float32)
+    D[0, 0], D[1, 1], D[2, 2] = 0.5, -3.25, 2.0
+    assert abs(api.spectral_norm(gpu(D)).sigma - 3.25) <= 1e-12 * 3.25
+    with pytest.raises(L.LipcacheError) as e:
+        api.spectral_norm(gpu(np.zeros((4, 32), np.float32)))
+    assert e.value.status == L.EDEGENERATE
+    rng = np.random.default_rng(1)
+    W = rng.standard_normal((8, 32)).astype(np.float32)
+    res = api.spectral_norm(gpu(W), max_iters=1)
+    assert not res.converged and res.sigma > 0 and res.iterations == 1
+
+
+# --------------------------------------------------------------- certify
+def _certify_case(N, d, C, seed, store="f32", bias=True):
+    rng = np.random.default_rng(seed)
+    W = (rng.standard_normal((C, d)) / math.sqrt(d)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(C)).astype(np.float32) if bias else None
+    mu = 2.0 * rng.standard_normal((C, d))
+    z = (mu[rng.integers(0, C, N)] + 0.7 * rng.standard_normal((N, d))).astype(np.float32)
+    sig = oracle.spectral_norm(W).sigma
+    return W, b, z, sig
+
+
+@pytest.mark.parametrize("N,d,C,store", [(4096, 64, 10, "f32"), (1000, 128, 100, "f32"), (3000, 256, 200, "f32"),
+                                         (777, 1024, 13, "f32"), (2048, 256, 200, "bf16"), (130, 32, 2, "f32"),
+                                         (65, 512, 9, "bf16")])
+def test_certify_matches_oracle(N, d, C, store):
+    say("certify", N, d, C, store)
+    W, b, z, sig = _certify_case(N, d, C, seed=N + d + C, store=store)
+    ref = oracle.certify(z, W, b, sig, store=store)
+    out = api.certify(gpu(z), gpu(W), None if b is None else gpu(b), sig, store=store, want_margin=True,
+                      want_norm2=True)
+    lab, r, m, n2 = host(out.label), host(out.r), host(out.margin), host(out.norm2)
+    # a near-tie of the top two logits (margin below the float64 rounding of
+    # the logits) may legitimately change the argmax
+    scale = np.abs(ref.logits).max(axis=1) + 1.0
+    tie = ref.margin <= 1e-9 * scale
+    assert np.array_equal(lab[~tie], ref.label[~tie])
+    ok = ~tie
+    rel = np.abs(r[ok].astype(np.float64) - ref.r64[ok]) / np.abs(ref.r64[ok])
+    assert rel.max() <= 1e-5, rel.max()
+    assert np.abs(m[ok] - ref.margin[ok]).max() <= 1e-5 * np.abs(ref.margin[ok]).max()
+    assert np.allclose(n2.astype(np.float64), ref.norm2, rtol=1e-6, atol=0)
+
+
+def test_certify_ties_and_empty():
+    say("certify ties")
+    W = np.zeros((3, 32), np.float32)
+    W[0, 0] = W[1, 1] = W[2, 2] = 1.0
+    z = np.zeros((4, 32), np.float32)
+    z[0, :3] = [3, 1, 2]
+    z[1, :3] = [2, 2, 1]
+    z[2, :3] = [-1, 0.5, -4]
+    z[3, :3] = [1, 1, 1]
+    out = api.certify(gpu(z), gpu(W), None, 1.0, want_margin=True)
+    assert host(out.label).tolist() == [0, 0, 1, 0]
+    r = host(out.r)
+    assert r[1] == 0.0 and r[3] == 0.0
+    assert r[0] == np.float32(1 / math.sqrt(2)) and r[2] == np.float32(1.5 / math.sqrt(2))
+    e = api.certify(gpu(np.zeros((0, 32), np.float32)), gpu(W), None, 1.0)
+    assert e.label.numel() == 0
+
+
+# --------------------------------------------------------------- insert
+@pytest.mark.parametrize("store", ["f32", "bf16"])
+def test_insert_matches_oracle(store):
+    say("insert", store)
+    rng = np.random.default_rng(11)
+    d, k = 96, 3000
+    z = (3 * rng.standard_normal((k, d))).astype(np.float32)
+    r = rng.uniform(-0.2, 1.0, k).astype(np.float32)
+    lab = rng.integers(0, 50, k).astype(np.int32)
+    sel = np.where(rng.random(k) < 0.6, -1, 3).astype(np.int32)
+    st = oracle.CacheState(d=d, capacity=5000, store=store)
+    oracle.insert(st, z[:100], lab[:100], np.abs(r[:100]) + 0.1)
+    n_ref = oracle.insert(st, z, lab, r, sel)
+    c = api.LipCache(d, 5000, store=store, device=DEV)
+    c.insert(gpu(z[:100]), gpu(lab[:100]), gpu(np.abs(r[:100]) + 0.1))
+    got = c.insert(gpu(z), gpu(lab), gpu(r), gpu(sel))
+    assert got == n_ref and c.n == st.n
+    zz = c.z[: c.n].float()
+    assert np.array_equal(host(zz).view(np.uint32), st.z.view(np.uint32))
+    assert np.array_equal(host(c.label[: c.n]), st.label)
+    assert np.array_equal(host(c.r[: c.n]), st.r)
+    assert np.allclose(host(c.norm2[: c.n]).astype(np.float64), st.norm2, rtol=1e-6, atol=0)
+    # all or nothing: 5000 - n free rows, offer more
+    before = host(c.r[: c.n]).copy()
+    big = 5000 - c.n + 1
+    with pytest.raises(L.LipcacheError) as e:
+        c.insert(gpu(np.ones((big, d), np.float32)), gpu(np.zeros(big, np.int32)), gpu(np.ones(big, np.float32)))
+    assert e.value.status == L.ECAPACITY and c.n == st.n
+    assert np.array_equal(host(c.r[: c.n]), before)
+
+
+# --------------------------------------------------------------- lookup
+@pytest.mark.parametrize("precision", ["bf16", "f32"])
+def test_lookup_tiny_full(tiny, precision):
+    say("lookup tiny", precision)
+    c = build_cache(tiny["state"])
+    res = c.lookup(gpu(tiny["zq"]), precision=precision)
+    nflag = compare_lookup(res, tiny["ref"], f"tiny/{precision}")
+    stats = host(res.stats)
+    assert stats[L.STAT_HITS] == int((host(res.label) >= 0).sum())
+    assert stats[L.STAT_RECHECKED] >= stats[L.STAT_HITS]
+    hits = tiny["ref"].index >= 0
+    assert 0.15 < hits.mean() < 0.4
+    say("tiny", precision, "hits", int(hits.sum()), "flagged", nflag, "stats", stats.tolist())
+
+
+@pytest.mark.parametrize("precision", ["bf16", "f32"])
+@pytest.mark.parametrize("d,N,B,store", [(32, 1000, 333, "f32"), (96, 700, 130, "f32"), (128, 5000, 517, "bf16"),
+                                         (256, 3001, 300, "f32"), (512, 900, 70, "bf16"), (1024, 300, 40, "f32")])
+def test_lookup_ragged_shapes(precision, d, N, B, store):
+    if precision == "f32" and d > 512:
+        pytest.skip("the fp32 filter supports d <= 512")
+    say("lookup ragged", precision, d, N, B, store)
+    rng = np.random.default_rng(d + N + B)
+    C = 7
+    W = (rng.standard_normal((C, d)) / math.sqrt(d)).astype(np.float32)
+    mu = 2.0 * rng.standard_normal((C, d))
+    z = (mu[rng.integers(0, C, N)] + 0.5 * rng.standard_normal((N, d))).astype(np.float32)
+    sig = oracle.spectral_norm(W).sigma
+    cert = oracle.certify(z, W, None, sig, store=store)
+    st = oracle_cache(z, cert.label, cert.r, d, store=store)
+    pick = rng.integers(0, st.n, B)
+    v = rng.standard_normal((B, d))
+    v /= np.linalg.norm(v, axis=1, keepdims=True)
+    u = rng.uniform(0, 2, B)
+    zq = (st.z[pick].astype(np.float64) + (u * st.r[pick])[:, None] * v).astype(np.float32)
+    zq[::5] = (mu[rng.integers(0, C, zq[::5].shape[0])] + 0.5 * rng.standard_normal(zq[::5].shape)).astype(np.float32)
+    ref = oracle.lookup(zq, st.z, st.r, st.label)
+    c = build_cache(st)
+    res = c.lookup(gpu(zq), precision=precision)
+    compare_lookup(res, ref, f"ragged d={d} N={N} B={B} {store}/{precision}")
+    assert (ref.index >= 0).sum() > 0
+
+
+def _embed(rows, d=32):
+    out = np.zeros((len(rows), d), np.float32)
+    for i, r in enumerate(rows):
+        out[i, : len(r)] = r
+    return out
+
+
+@pytest.mark.parametrize("precision", ["bf16", "f32"])
+def test_lookup_hand_cases(precision):
+    say("lookup hand cases", precision)
+    import json
+    import os
+    fx = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "strict_ball_lookup.json")))
+    z = _embed(fx["z"])
+    zq = _embed(fx["zq"])
+    st = oracle_cache(z, np.array(fx["label"], np.int32), np.array(fx["r"], np.float32), 32)
+    c = build_cache(st)
+    res = c.lookup(gpu(zq), precision=precision)
+    assert host(res.label).tolist() == fx["want_label"]
+    assert host(res.index).tolist() == fx["want_index"]
+    # duplicates -> lower index; NaN query -> miss; non-positive radius never hits
+    e1 = np.zeros(32, np.float32)
+    e1[0] = 1
+    z2 = np.stack([e1, e1, 0.5 * e1, 0.5 * e1, 0 * e1, 0 * e1])
+    st2 = oracle.CacheState(d=32, capacity=8)
+    oracle.insert(st2, z2, np.array([4, 5, 6, 7, 8, 9], np.int32), np.array([1, 1, 1, 1, 1, 1], np.float32))
+    c2 = build_cache(st2)
+    c2.r[4] = 0.0   # rows 4, 5 keep their place but can never be hit
+    c2.r[5] = -1.0
+    q = np.stack([0.5 * e1, np.full(32, np.nan, np.float32), 0 * e1 + 1e-3 * e1]).astype(np.float32)
+    res2 = c2.lookup(gpu(q), precision=precision)
+    assert host(res2.label).tolist() == [6, -1, 6]
+    assert host(res2.index).tolist() == [2, -1, 2]
+
+
+@pytest.mark.parametrize("precision", ["bf16", "f32"])
+def test_lookup_empty_cache_and_batch(precision):
+    say("lookup empty", precision)
+    c = api.LipCache(64, 16, device=DEV)
+    zq = np.random.default_rng(0).standard_normal((37, 64)).astype(np.float32)
+    res = c.lookup(gpu(zq), precision=precision)
+    assert np.all(host(res.label) == -1) and np.all(host(res.index) == -1)
+    assert np.all(np.isinf(host(res.dist2)))
+    res0 = c.lookup(gpu(np.zeros((0, 64), np.float32)), precision=precision)
+    assert res0.label.numel() == 0
+
+
+@pytest.mark.parametrize("precision", ["bf16", "f32"])
+def test_lookup_deterministic(tiny, precision):
+    say("lookup determinism", precision)
+    c = build_cache(tiny["state"])
+    zq = gpu(tiny["zq"])
+    a = c.lookup(zq, precision=precision)
+    outs_a = [host(t).copy() for t in (a.label, a.index, a.dist2, a.stats, a.band)]
+    b = c.lookup(zq, precision=precision)
+    outs_b = [host(t) for t in (b.label, b.index, b.dist2, b.stats, b.band)]
+    for x, y in zip(outs_a, outs_b):
+        assert x.tobytes() == y.tobytes()
+
+
+# --------------------------------------------------------------- filter soundness
+@pytest.mark.parametrize("precision,tol", [("bf16", 1e-3), ("f32", 1e-5)])
+@pytest.mark.parametrize("store", ["f32", "bf16"])
+def test_filter_sound_and_accurate(tiny, precision, tol, store):
+    say("filter dump", precision, store)
+    st0 = tiny["state"]
+    st = oracle_cache(st0.z, st0.label, st0.r, 64, store=store)
+    c = build_cache(st)
+    zq = tiny["zq"][:512]
+    g_hat, cand = c.filter_dump(gpu(zq), precision=precision)
+    g_hat, cand = host(g_hat).astype(np.float64), host(cand).astype(bool)
+    Q = zq.astype(np.float64)
+    Z = st.z.astype(np.float64)
+    G = Q @ Z.T
+    nq = (Q ** 2).sum(1)
+    nc = (Z ** 2).sum(1)
+    D2 = nq[:, None] + nc[None, :] - 2 * G
+    D2_direct = ((Q[:, None, :] - Z[None, :, :]) ** 2).sum(-1)
+    true_hit = (D2_direct < (st.r.astype(np.float64) ** 2)[None, :]) & (st.r > 0)[None, :]
+    assert true_hit.sum() > 50
+    assert not np.any(true_hit & ~cand), "filter rejected a true hit"
+    scale = nq[:, None] + nc[None, :]
+    d2_hat = scale - 2 * g_hat
+    rel = np.abs(d2_hat - D2_direct) / scale
+    assert rel.max() <= tol, rel.max()
+    say("filter", precision, store, "max rel", float(rel.max()), "cand/query", float(cand.sum() / cand.shape[0]))
+
+
+# --------------------------------------------------------------- end-to-end chain
+def test_end_to_end_chain_tiny():
+    """spectral_norm -> certify -> insert -> lookup on the device, against the oracle chain."""
+    say("chain tiny")
+    wl = wlmod.make_workload("tiny-d64-c10", seed=0)
+    sig_g = api.spectral_norm(gpu(wl.W)).sigma
+    sig_o = oracle.spectral_norm(wl.W).sigma
+    assert abs(sig_g - sig_o) <= 1e-9 * sig_o
+    cert_g = api.certify(gpu(wl.z), gpu(wl.W), gpu(wl.b), sig_g)
+    c = api.LipCache(64, wl.z.shape[0] + 1024, device=DEV)
+    n = c.insert(gpu(wl.z), cert_g.label, cert_g.r)
+    cert_o = oracle.certify(wl.z, wl.W, wl.b, sig_o)
+    st = oracle_cache(wl.z, cert_o.label, cert_o.r, 64, capacity=wl.z.shape[0] + 1024)
+    assert n == st.n
+    draws = wlmod.draw_queries(wl, 0)
+    idx = wlmod.near_indices(draws, st.n)
+    zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
+    res = c.lookup(gpu(zq))
+    ref = oracle.lookup(zq, st.z, st.r, st.label)
+    lab = host(res.label)
+    # radii may differ in the last float bit between the two chains: compare
+    # outside the band, which the oracle flags
+    ok = ~ref.flagged
+    assert np.array_equal(lab[ok], ref.label[ok])
+    # write-back of the misses with the queries' own certificates
+    cq = api.certify(gpu(zq), gpu(wl.W), gpu(wl.b), sig_g)
+    before = c.n
+    added = c.insert(gpu(zq), cq.label, cq.r, res.label)
+    assert added == int((lab == -1).sum()) - int((host(cq.r)[lab == -1] <= 0).sum())
+    assert c.n == before + added
+    # a repeated lookup now hits every inserted query at distance 0
+    res2 = c.lookup(gpu(zq))
+    lab2, d2 = host(res2.label), host(res2.dist2)
+    inserted = (lab == -1) & (host(cq.r) > 0)
+    assert np.all(lab2[inserted] >= 0) and np.all(d2[inserted] == 0.0)
+    # proxy payload: the label returned is the head's argmax at the query (Lemma 5.1)
+    hits = lab2 >= 0
+    s = zq.astype(np.float64) @ wl.W.astype(np.float64).T + wl.b.astype(np.float64)
+    assert np.array_equal(np.argmax(s, axis=1)[hits], lab2[hits])

@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define LIPCACHE_ABI_VERSION 1
+#define LIPCACHE_ABI_VERSION 2
 
 /* Same type as hipStream_t. */
 typedef struct ihipStream_t* lipcache_stream_t;
@@ -80,6 +80,11 @@ enum {
  */
 typedef struct lipcache_cache {
   void*    z;           /* [capacity][d] features; float (F32) or bf16 bits (BF16)   */
+  void*    zimg;        /* [capacity][d] bf16 image of z for the bf16 distance
+                           filter, or NULL.  Only read for an F32 store; insert
+                           keeps it equal to bf16(z) (round to nearest even). The
+                           bf16 lookup streams it (half the bytes of z); without
+                           it each workgroup converts z on the fly.                   */
   float*   r;           /* [capacity] certified radius r_i                           */
   int32_t* label;       /* [capacity] payload y~_i                                   */
   float*   norm2;       /* [capacity] ||z_i||^2 of the stored values (derived)       */

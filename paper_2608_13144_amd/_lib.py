@@ -25,6 +25,7 @@ class LipcacheCache(ctypes.Structure):
 
     _fields_ = [
         ("z", ctypes.c_void_p),
+        ("zimg", ctypes.c_void_p),
         ("r", ctypes.c_void_p),
         ("label", ctypes.c_void_p),
         ("norm2", ctypes.c_void_p),

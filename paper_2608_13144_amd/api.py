@@ -107,13 +107,18 @@ class LookupResult:
 class LipCache:
     """The feature cache C = {(z_i, y~_i, r_i)} in device memory (caller-owned tensors)."""
 
-    def __init__(self, d: int, capacity: int, store: str = "f32", device: str | torch.device = "cuda"):
+    def __init__(self, d: int, capacity: int, store: str = "f32", device: str | torch.device = "cuda",
+                 image: bool = True):
+        """``image``: for an f32 store, also keep the bf16 image that the bf16
+        filter streams (half the bytes of z; costs 2 bytes per element)."""
         self.d = int(d)
         self.capacity = int(capacity)
         self.store = store
         self.device = torch.device(device)
         zdt = torch.float32 if store == "f32" else torch.bfloat16
         self.z = torch.empty((self.capacity, self.d), dtype=zdt, device=self.device)
+        self.zimg = (torch.empty((self.capacity, self.d), dtype=torch.bfloat16, device=self.device)
+                     if (image and store == "f32") else None)
         self.r = torch.empty(self.capacity, dtype=torch.float32, device=self.device)
         self.label = torch.empty(self.capacity, dtype=torch.int32, device=self.device)
         self.norm2 = torch.empty(self.capacity, dtype=torch.float32, device=self.device)
@@ -121,8 +126,9 @@ class LipCache:
         self._ws = None
 
     def cstruct(self) -> L.LipcacheCache:
-        return L.LipcacheCache(self.z.data_ptr(), self.r.data_ptr(), self.label.data_ptr(),
-                               self.norm2.data_ptr(), self.n, self.capacity, self.d, _STORE[self.store])
+        return L.LipcacheCache(self.z.data_ptr(), None if self.zimg is None else self.zimg.data_ptr(),
+                               self.r.data_ptr(), self.label.data_ptr(), self.norm2.data_ptr(), self.n,
+                               self.capacity, self.d, _STORE[self.store])
 
     def _workspace(self, nbytes: int) -> torch.Tensor:
         if self._ws is None or self._ws.numel() < nbytes:

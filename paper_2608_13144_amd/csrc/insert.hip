@@ -64,6 +64,7 @@ struct InsertParams {
   int64_t k;
   const int64_t* offsets;
   void* cz;
+  uint16_t* cimg;
   float* cr;
   int32_t* clabel;
   float* cnorm2;
@@ -107,9 +108,11 @@ __global__ __launch_bounds__(kInsBlock) void insert_scatter_kernel(const InsertP
       }
     } else {
       float* out = static_cast<float*>(p.cz) + dst * p.d;
+      uint16_t* img = p.cimg ? p.cimg + dst * p.d : nullptr;
       for (int k = lane; k < p.d; k += kWave) {
         const float f = zr[k];
         out[k] = f;
+        if (img) img[k] = bf16_bits(f);
         s = __builtin_fma(static_cast<double>(f), static_cast<double>(f), s);
       }
     }
@@ -174,6 +177,7 @@ extern "C" lipcache_status lipcache_insert(lipcache_cache* c, const float* z_src
   p.k = k;
   p.offsets = offsets;
   p.cz = c->z;
+  p.cimg = c->store_dtype == LIPCACHE_F32 ? static_cast<uint16_t*>(c->zimg) : nullptr;
   p.cr = c->r;
   p.clabel = c->label;
   p.cnorm2 = c->norm2;

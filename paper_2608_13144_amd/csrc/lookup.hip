@@ -57,6 +57,8 @@ struct LookupParams {
   unsigned int* bflag;
   unsigned long long* stats;
   double kappa_c;        // 1 - k - 4u, applied to ||z_i||^2
+  const float* athr;     // [n_pad] per-entry filter thresholds A_i (+inf past n)
+  const void* cimg;      // rows streamed by the DMA kernel (bf16 image or z)
   int n_qblocks;
   int64_t slice_len;
   float* g_hat;          // dump mode only
@@ -80,6 +82,23 @@ __global__ void lookup_prep_kernel(const float* __restrict__ zq, int64_t B, int 
     best[q] = kNoHit;
     bflag[q] = 0u;
   }
+}
+
+// Per-entry threshold A_i = RD(((1 - k - 4u) ||z_i||^2 - r_i^2) / 2), +inf for
+// rows that can never be hit (r_i <= 0 or NaN) and for the padding past n.
+__global__ void lookup_athr_kernel(const float* __restrict__ cr, const float* __restrict__ cnorm2, int64_t n,
+                                   int64_t n_pad, double kappa_c, float* __restrict__ athr) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= n_pad) return;
+  float at = __builtin_inff();
+  if (i < n) {
+    const float rr = cr[i];
+    if (rr > 0.0f) {
+      const double r2 = static_cast<double>(rr) * static_cast<double>(rr);
+      at = f32_round_down((kappa_c * static_cast<double>(cnorm2[i]) - r2) * 0.5 - 0.5 * kFilterAbsSlack);
+    }
+  }
+  athr[i] = at;
 }
 
 // ------------------------------------------------------------- finalize
@@ -182,12 +201,30 @@ __device__ __forceinline__ double cache_value(const void* cz, int64_t row, int d
   }
 }
 
+// Everything the exact re-check touches, passed by value so that calling it
+// does not force the kernel arguments into scratch memory.
+struct RecheckArgs {
+  const float* zq;
+  const void* cz;
+  const float* cr;
+  unsigned long long* best;
+  unsigned int* bflag;
+  unsigned long long* stats;
+  int64_t B;
+  int64_t n;
+  int d;
+};
+
+__device__ __forceinline__ RecheckArgs recheck_args(const LookupParams& p) {
+  return RecheckArgs{p.zq, p.cz, p.cr, p.best, p.bflag, p.stats, p.B, p.n, p.d};
+}
+
 // Exact re-check of the pairs whose bits are set in `mask` (bit rt*4+i of a
 // lane = accumulator i of row tile rt).  The whole wave evaluates one pair
 // at a time: sum_k (q_k - z_ik)^2 in float64, lane-strided then a fixed
 // butterfly, so the result does not depend on scheduling.
-template <int SRC, int RT>
-__device__ __noinline__ void recheck_pairs(const LookupParams& p, uint32_t mask, int64_t qwave, int64_t ebase) {
+template <int SRC>
+__device__ __noinline__ void recheck_pairs(const RecheckArgs p, uint32_t mask, int64_t qwave, int64_t ebase) {
   const int lane = lane_id();
   while (true) {
     const unsigned long long bal = __ballot(mask != 0u);
@@ -226,6 +263,37 @@ __device__ __noinline__ void recheck_pairs(const LookupParams& p, uint32_t mask,
   }
 }
 
+// Queries as MFMA A operands: lane holds row m16 of each row tile and k-chunk
+// g of each k-step (the cache operand uses the same (k-step, chunk) -> k map,
+// so the contraction covers every k exactly once).  Rows past B load row
+// B - 1 (any finite values do): their thresholds are +inf.
+template <int MODE, int KS, int RT>
+__device__ __forceinline__ void load_query_operands(const LookupParams& p, int64_t qwave, int m16, int g,
+                                                    u32x4 (&a)[RT][KS]) {
+  using T = ModeTraits<MODE>;
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    int64_t row = qwave + rt * 16 + m16;
+    row = row < p.B ? row : p.B - 1;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) a[rt][ks] = load_chunk<MODE, LIPCACHE_F32>(p.zq, row, p.d, ks * T::kPerStep + g * T::kPerChunk);
+  }
+}
+
+template <int MODE, int KS, int RT>
+__device__ __forceinline__ void load_queries(const LookupParams& p, int64_t qwave, int m16, int g, u32x4 (&a)[RT][KS],
+                                             float (&qt)[RT][4]) {
+  load_query_operands<MODE, KS, RT>(p, qwave, m16, g, a);
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t qr = qwave + rt * 16 + 4 * g + i;
+      qt[rt][i] = qr < p.B ? p.qthr[qr] : __builtin_inff();
+    }
+  }
+}
+
 template <int MODE, int SRC, int KS, int RT, bool DUMP>
 __global__ __launch_bounds__(kLkThreads, 2) void lookup_kernel(const LookupParams p) {
   using T = ModeTraits<MODE>;
@@ -249,25 +317,9 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_kernel(const LookupParam
   const int g = lane >> 4;
   const int64_t qwave = static_cast<int64_t>(qb) * (kLkWaves * RT * 16) + wave * (RT * 16);
 
-  // Queries as A operands: lane holds row m16 of each row tile, k-chunk g of
-  // each k-step.  The same (k-step, chunk) -> k map is used for the cache
-  // operand, so the contraction covers every k exactly once.
   u32x4 a[RT][KS];
   float qt[RT][4];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const int64_t row = qwave + rt * 16 + m16;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      a[rt][ks] = row < p.B ? load_chunk<MODE, LIPCACHE_F32>(p.zq, row, p.d, ks * T::kPerStep + g * T::kPerChunk)
-                            : u32x4{0u, 0u, 0u, 0u};
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t qr = qwave + rt * 16 + 4 * g + i;
-      qt[rt][i] = qr < p.B ? p.qthr[qr] : __builtin_inff();
-    }
-  }
+  load_queries<MODE, KS, RT>(p, qwave, m16, g, a, qt);
 
   const int64_t e_begin = static_cast<int64_t>(slice) * p.slice_len;
   const int64_t e_end = e_begin + p.slice_len < p.n ? e_begin + p.slice_len : p.n;
@@ -347,10 +399,224 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_kernel(const LookupParam
 #pragma unroll
             for (int i = 0; i < 4; ++i) mask |= static_cast<uint32_t>((acc[rt][i] - qt[rt][i]) >= an) << (rt * 4 + i);
           }
-          recheck_pairs<SRC, RT>(p, mask, qwave, ebase);
+          recheck_pairs<SRC>(recheck_args(p), mask, qwave, ebase);
         }
       }
     }
+  }
+}
+
+// ------------------------------------------------------------- DMA pipeline kernel
+// Same contraction, filter and re-check as lookup_kernel, but the cache tiles
+// already have the MFMA element type in memory (a bf16 store, the bf16 image
+// of an fp32 store, or an fp32 store for the fp32 filter), so they move from
+// global memory straight into LDS with global_load_lds_dwordx4 (no registers,
+// no conversion), double-buffered: the copy of tile t+1 is issued right after
+// the barrier that publishes tile t and overlaps its computation.
+//
+// LDS rows are not padded; instead 16-byte chunk c of row `row` is stored in
+// slot c ^ swz(row), so the 16 lanes that read one k-chunk of 16 consecutive
+// rows hit 16 different bank groups.  The swizzle is applied to the global
+// addresses of the copy (a permutation within each row, so reads stay
+// coalesced).
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int CPR>
+__device__ __forceinline__ int lds_swizzle(int row) {
+  constexpr int kRowsPerBankSweep = CPR >= 16 ? 1 : 16 / CPR;
+  constexpr int kMask = (CPR >= 16 ? 16 : CPR) - 1;
+  return (row / kRowsPerBankSweep) & kMask;
+}
+
+// vmcnt(0): wait for this wave's outstanding copies into LDS.
+__device__ __forceinline__ void wait_copies() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+template <int MODE>
+struct DmaTraits {
+  static constexpr int kRows = MODE == kModeBF16 ? 64 : 32;  // cache rows per LDS tile
+};
+
+template <int MODE, int KS>
+__device__ __forceinline__ void issue_tile(unsigned char* buf, float* athr_buf, const LookupParams& p, int64_t t0,
+                                           int64_t e_end, int wave) {
+  using T = ModeTraits<MODE>;
+  constexpr int kCPR = 4 * KS;  // 16-byte chunks per LDS row
+  constexpr int kRows = DmaTraits<MODE>::kRows;
+  constexpr int kIters = kRows * kCPR / kLkThreads;
+  constexpr int kRowsPerIter = kLkThreads / kCPR;
+  const int d_chunks = p.d * T::kElemBytes / 16;
+  const int row_bytes = p.d * T::kElemBytes;
+  const int tid = static_cast<int>(threadIdx.x);
+  const int r0 = tid / kCPR;
+  const int cs = tid % kCPR;
+  // Wave-uniform tile base; per-thread 32-bit offsets inside the tile.
+  const unsigned char* base = static_cast<const unsigned char*>(p.cimg) + t0 * static_cast<int64_t>(row_bytes);
+  // Rows past the slice end repeat its last row (their thresholds are +inf).
+  const int last = e_end - t0 < kRows ? static_cast<int>(e_end - t0) - 1 : kRows - 1;
+#pragma unroll
+  for (int j = 0; j < kIters; ++j) {
+    const int row = j * kRowsPerIter + r0;
+    int c = cs ^ lds_swizzle<kCPR>(row);
+    // Chunks past d hold a copy of a real chunk: the query operand is zero
+    // there, so they add nothing.
+    if (c >= d_chunks) c -= d_chunks;
+    const int rr = row < last ? row : last;
+    __builtin_amdgcn_global_load_lds(base + (rr * row_bytes + c * 16),
+                                     (lds_void_t*)(buf + (j * kLkThreads + wave * kWave) * 16), 16, 0, 0);
+  }
+  if (wave == 0) __builtin_amdgcn_global_load_lds(p.athr + t0 + lane_id(), (lds_void_t*)athr_buf, 4, 0, 0);
+}
+
+// The cache operand of (column tile `sub`, k-step ks) for this lane: chunk
+// 4 ks + g of row sub*16 + m16.  For rows of >= 16 chunks the swizzle is a
+// 4-bit XOR, so the slot splits into a part that depends on ks only through
+// its low two bits and a multiple of 256 bytes: four base addresses and
+// immediate offsets cover all k-steps.
+template <int KS>
+__device__ __forceinline__ u32x4 lds_operand(const unsigned char* buf, int sub, int ks, int m16, int g) {
+  constexpr int kCPR = 4 * KS;
+  const int row = sub * kColTile + m16;
+  const int sw = lds_swizzle<kCPR>(row);
+  if constexpr (kCPR >= 16) {
+    const int off = row * kCPR * 16 + ((g ^ (sw & 3)) * 16) + (((ks & 3) ^ (sw >> 2)) * 64) + (ks >> 2) * 256;
+    return *reinterpret_cast<const u32x4*>(buf + off);
+  } else {
+    return *reinterpret_cast<const u32x4*>(buf + row * kCPR * 16 + (((ks * 4 + g) ^ sw) * 16));
+  }
+}
+
+// One LDS tile: for each 16-entry column tile, KS k-steps of RT MFMAs, then
+// the filter.  The cache operands are read from LDS two k-steps ahead of
+// their use (continuing into the next column tile), so LDS latency overlaps
+// the MFMAs.  The filter takes max_j (acc_j - Q_j) over the lane's 16
+// accumulators (maxnum ignores NaN, so a NaN pair never hides another pair)
+// and compares once against A_i; the exact per-pair mask is only rebuilt on
+// the rare path.
+template <int MODE, int STORE, int KS, int RT, bool DUMP>
+__device__ __forceinline__ void compute_tile(const unsigned char* buf, const float* athr_buf, const LookupParams& p,
+                                             int64_t t0, int64_t e_end, int64_t qwave, int m16, int g,
+                                             const u32x4 (&a)[RT][KS], const float* qt_lds) {
+  constexpr int kRows = DmaTraits<MODE>::kRows;
+  const int64_t left = e_end - t0;
+  const int nsub = left >= kRows ? kRows / kColTile : static_cast<int>((left + kColTile - 1) / kColTile);
+  u32x4 b0 = lds_operand<KS>(buf, 0, 0, m16, g);
+  u32x4 b1 = KS > 1 ? lds_operand<KS>(buf, 0, 1, m16, g) : b0;
+  // Fully unrolled so every LDS address is a fixed offset from `buf`, which
+  // lets the compiler see that these reads do not touch the other buffer
+  // (whose copy is still in flight) and skip a wait on it.
+#pragma unroll
+  for (int sub = 0; sub < kRows / kColTile; ++sub) {
+    if (sub >= nsub) break;
+    const float an = athr_buf[sub * kColTile + m16];
+    f32x4 acc[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const u32x4 cur = (ks & 1) ? b1 : b0;
+      int nks = ks + 2, nsb = sub;
+      if (nks >= KS) {
+        nks -= KS;
+        nsb += 1;
+      }
+      u32x4 pre = cur;
+      if (KS > 1 && nsb < nsub) pre = lds_operand<KS>(buf, nsb, nks, m16, g);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) acc[rt] = mfma_step<MODE>(a[rt][ks], cur, acc[rt]);
+      if (ks & 1) {
+        b1 = pre;
+      } else {
+        b0 = pre;
+      }
+    }
+    if constexpr (KS == 1) {
+      if (sub + 1 < nsub) b0 = lds_operand<KS>(buf, sub + 1, 0, m16, g);
+    }
+    const int64_t ebase = t0 + sub * kColTile;
+    // Q_q of the four rows 4g..4g+3 of each row tile (this lane's accumulators)
+    f32x4 qt[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) qt[rt] = *reinterpret_cast<const f32x4*>(qt_lds + rt * 16 + 4 * g);
+    if constexpr (DUMP) {
+      const int64_t e = ebase + m16;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t q = qwave + rt * 16 + 4 * g + i;
+          if (q < p.B && e < e_end) {
+            p.g_hat[q * p.n + e] = acc[rt][i];
+            p.cand[q * p.n + e] = static_cast<uint8_t>((acc[rt][i] - qt[rt][i]) >= an);
+          }
+        }
+      }
+    } else {
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mx = __builtin_fmaxf(mx, acc[rt][i] - qt[rt][i]);
+      }
+      if (__ballot(mx >= an) != 0ull) {
+        uint32_t mask = 0u;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) mask |= static_cast<uint32_t>((acc[rt][i] - qt[rt][i]) >= an) << (rt * 4 + i);
+        }
+        recheck_pairs<STORE>(recheck_args(p), mask, qwave, ebase);
+      }
+    }
+  }
+}
+
+template <int MODE, int STORE, int KS, int RT, bool DUMP>
+__global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupParams p) {
+  using T = ModeTraits<MODE>;
+  constexpr int kCPR = 4 * KS;
+  constexpr int kRows = DmaTraits<MODE>::kRows;
+  constexpr int kTileBytes = kRows * kCPR * 16;
+  __shared__ __attribute__((aligned(16))) unsigned char buf0[kTileBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char buf1[kTileBytes];
+  __shared__ __attribute__((aligned(16))) float ath0[kWave];
+  __shared__ __attribute__((aligned(16))) float ath1[kWave];
+  __shared__ __attribute__((aligned(16))) float qts[kLkWaves * RT * 16];
+
+  const int bid = static_cast<int>(blockIdx.x);
+  const int xcd = bid % kXcds;
+  const int local = bid / kXcds;
+  const int slice = xcd + kXcds * (local / p.n_qblocks);
+  const int qb = local % p.n_qblocks;
+
+  const int lane = lane_id();
+  const int wave = uniform(static_cast<int>(threadIdx.x) / kWave);
+  const int m16 = lane & 15;
+  const int g = lane >> 4;
+  const int64_t qwave = static_cast<int64_t>(qb) * (kLkWaves * RT * 16) + wave * (RT * 16);
+
+  const int64_t e_begin = static_cast<int64_t>(slice) * p.slice_len;
+  const int64_t e_end = e_begin + p.slice_len < p.n ? e_begin + p.slice_len : p.n;
+  if (e_begin >= e_end) return;  // whole workgroup: an empty slice
+  issue_tile<MODE, KS>(buf0, ath0, p, e_begin, e_end, wave);
+
+  u32x4 a[RT][KS];
+  load_query_operands<MODE, KS, RT>(p, qwave, m16, g, a);
+  float* qt_lds = qts + wave * (RT * 16);
+  for (int r = lane; r < RT * 16; r += kWave) qt_lds[r] = qwave + r < p.B ? p.qthr[qwave + r] : __builtin_inff();
+
+  for (int64_t t0 = e_begin;; t0 += 2 * kRows) {
+    wait_copies();
+    __syncthreads();
+    const bool more1 = t0 + kRows < e_end;
+    if (more1) issue_tile<MODE, KS>(buf1, ath1, p, t0 + kRows, e_end, wave);
+    compute_tile<MODE, STORE, KS, RT, DUMP>(buf0, ath0, p, t0, e_end, qwave, m16, g, a, qt_lds);
+    if (!more1) break;
+    wait_copies();
+    __syncthreads();
+    const bool more2 = t0 + 2 * kRows < e_end;
+    if (more2) issue_tile<MODE, KS>(buf0, ath0, p, t0 + 2 * kRows, e_end, wave);
+    compute_tile<MODE, STORE, KS, RT, DUMP>(buf1, ath1, p, t0 + kRows, e_end, qwave, m16, g, a, qt_lds);
+    if (!more2) break;
   }
 }
 
@@ -360,38 +626,71 @@ struct Plan {
   int rt = 0;
   int d_pad = 0;
   int qblock = 0;
+  bool dma = false;
 };
 
-inline bool make_plan(int precision, int d, Plan& pl) {
+inline int rt_for(int ks) { return ks <= 8 ? 4 : (ks == 16 ? 2 : 1); }
+
+inline bool make_plan(int precision, const lipcache_cache* c, Plan& pl) {
   const int per_step = precision == LIPCACHE_BF16 ? 32 : 16;
-  const int max_ks = precision == LIPCACHE_BF16 ? 32 : 32;
   int ks = precision == LIPCACHE_BF16 ? 1 : 2;
-  while (ks * per_step < d) ks *= 2;
-  if (ks > max_ks) return false;
+  while (ks * per_step < c->d) ks *= 2;
+  if (ks > 32) return false;
   pl.ks = ks;
-  pl.rt = 32 / ks > 4 ? 4 : (32 / ks < 1 ? 1 : 32 / ks);
+  pl.rt = rt_for(ks);
   pl.d_pad = ks * per_step;
   pl.qblock = kLkWaves * pl.rt * 16;
+  // The DMA kernel needs rows already in the MFMA element type and two LDS
+  // tiles of at most 64 KiB.
+  const bool same_type = precision == LIPCACHE_BF16 ? (c->store_dtype == LIPCACHE_BF16 || c->zimg != nullptr)
+                                                    : c->store_dtype == LIPCACHE_F32;
+  pl.dma = same_type && ks <= 16;
   return true;
 }
 
-template <int MODE, int SRC, int KS, int RT, bool DUMP>
-hipError_t launch_one(const LookupParams& p, unsigned grid, hipStream_t s) {
-  hipLaunchKernelGGL((lookup_kernel<MODE, SRC, KS, RT, DUMP>), dim3(grid), dim3(kLkThreads), 0, s, p);
+template <int MODE, int SRC, int KS, bool DUMP>
+hipError_t launch_v1(const LookupParams& p, unsigned grid, hipStream_t s) {
+  hipLaunchKernelGGL((lookup_kernel<MODE, SRC, KS, (KS <= 8 ? 4 : (KS == 16 ? 2 : 1)), DUMP>), dim3(grid),
+                     dim3(kLkThreads), 0, s, p);
   return hipGetLastError();
 }
 
+template <int MODE, int STORE, int KS, bool DUMP>
+hipError_t launch_dma(const LookupParams& p, unsigned grid, hipStream_t s) {
+  if constexpr (KS <= 16) {
+    hipLaunchKernelGGL((lookup_dma_kernel<MODE, STORE, KS, (KS <= 8 ? 4 : 2), DUMP>), dim3(grid), dim3(kLkThreads),
+                       0, s, p);
+    return hipGetLastError();
+  } else {
+    return hipErrorInvalidValue;
+  }
+}
+
 template <int MODE, int SRC, bool DUMP>
-hipError_t launch_mode(const Plan& pl, const LookupParams& p, unsigned grid, hipStream_t s) {
+hipError_t launch_ks(const Plan& pl, const LookupParams& p, unsigned grid, hipStream_t s) {
   switch (pl.ks) {
-    case 1: return launch_one<MODE, SRC, 1, 4, DUMP>(p, grid, s);
-    case 2: return launch_one<MODE, SRC, 2, 4, DUMP>(p, grid, s);
-    case 4: return launch_one<MODE, SRC, 4, 4, DUMP>(p, grid, s);
-    case 8: return launch_one<MODE, SRC, 8, 4, DUMP>(p, grid, s);
-    case 16: return launch_one<MODE, SRC, 16, 2, DUMP>(p, grid, s);
-    case 32: return launch_one<MODE, SRC, 32, 1, DUMP>(p, grid, s);
+#define LC_CASE(K) \
+  case K: return pl.dma ? launch_dma<MODE, SRC, K, DUMP>(p, grid, s) : launch_v1<MODE, SRC, K, DUMP>(p, grid, s);
+    LC_CASE(1)
+    LC_CASE(2)
+    LC_CASE(4)
+    LC_CASE(8)
+    LC_CASE(16)
+    LC_CASE(32)
+#undef LC_CASE
     default: return hipErrorInvalidValue;
   }
+}
+
+template <bool DUMP>
+hipError_t launch_lookup(int precision, int store, const Plan& pl, const LookupParams& p, unsigned grid,
+                         hipStream_t s) {
+  if (precision == LIPCACHE_BF16) {
+    return store == LIPCACHE_F32 ? launch_ks<kModeBF16, LIPCACHE_F32, DUMP>(pl, p, grid, s)
+                                 : launch_ks<kModeBF16, LIPCACHE_BF16, DUMP>(pl, p, grid, s);
+  }
+  return store == LIPCACHE_F32 ? launch_ks<kModeF32, LIPCACHE_F32, DUMP>(pl, p, grid, s)
+                               : launch_ks<kModeF32, LIPCACHE_BF16, DUMP>(pl, p, grid, s);
 }
 
 struct Workspace {
@@ -399,9 +698,12 @@ struct Workspace {
   unsigned long long* best;
   unsigned int* bflag;
   unsigned long long* stats;
+  float* athr;
 };
 
-inline size_t ws_layout(int64_t B, Workspace* w, void* base) {
+inline int64_t athr_len(int64_t n) { return ((n > 0 ? n : 0) + kTileN - 1) / kTileN * kTileN + kTileN; }
+
+inline size_t ws_layout(int64_t B, int64_t N, Workspace* w, void* base) {
   const size_t nb = static_cast<size_t>(B > 0 ? B : 0);
   size_t off = 0;
   const size_t o_best = off;
@@ -412,12 +714,15 @@ inline size_t ws_layout(int64_t B, Workspace* w, void* base) {
   off = align_up(off + nb * 4, 256);
   const size_t o_stats = off;
   off = align_up(off + 4 * 8, 256);
+  const size_t o_athr = off;
+  off = align_up(off + static_cast<size_t>(athr_len(N)) * 4, 256);
   if (w && base) {
     char* b = static_cast<char*>(base);
     w->best = reinterpret_cast<unsigned long long*>(b + o_best);
     w->qthr = reinterpret_cast<float*>(b + o_qthr);
     w->bflag = reinterpret_cast<unsigned int*>(b + o_flag);
     w->stats = reinterpret_cast<unsigned long long*>(b + o_stats);
+    w->athr = reinterpret_cast<float*>(b + o_athr);
   }
   return off;
 }
@@ -430,6 +735,7 @@ inline bool cache_ok(const lipcache_cache* c) {
   if (c->n >= static_cast<int64_t>(UINT_MAX)) return false;
   if (c->capacity > 0 && (!c->z || !c->r || !c->label || !c->norm2)) return false;
   if ((reinterpret_cast<uintptr_t>(c->z) & 15u) != 0) return false;
+  if ((reinterpret_cast<uintptr_t>(c->zimg) & 15u) != 0) return false;
   return true;
 }
 
@@ -444,21 +750,28 @@ lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, 
   if (B > static_cast<int64_t>(INT_MAX) / 2) return LIPCACHE_EINVAL;
   if (dump && (!g_hat || !cand || B * c->n > (1ll << 26))) return LIPCACHE_EINVAL;
   Plan pl;
-  if (!make_plan(precision, c->d, pl)) return LIPCACHE_EUNSUPPORTED;
-  const size_t need = ws_layout(B, nullptr, nullptr);
+  if (!make_plan(precision, c, pl)) return LIPCACHE_EUNSUPPORTED;
+  if (precision == LIPCACHE_F32 && pl.ks > 32) return LIPCACHE_EUNSUPPORTED;
+  if (precision == LIPCACHE_F32 && c->d > 512) return LIPCACHE_EUNSUPPORTED;
+  const size_t need = ws_layout(B, c->n, nullptr, nullptr);
   if (!ws || ws_bytes < need || !aligned256(ws)) return LIPCACHE_EWORKSPACE;
   Workspace w;
-  ws_layout(B, &w, ws);
+  ws_layout(B, c->n, &w, ws);
   unsigned long long* st = stats ? reinterpret_cast<unsigned long long*>(stats) : w.stats;
 
   const double kappa = filter_kappa(precision, c->store_dtype, pl.d_pad);
   const double u32 = 1.0 / 16777216.0;
+  const double kappa_c = 1.0 - kappa - 4.0 * u32;
   const unsigned prep_grid = static_cast<unsigned>(B > 0 ? (B + kLkWaves - 1) / kLkWaves : 1);
   hipLaunchKernelGGL(lookup_prep_kernel, dim3(prep_grid), dim3(kLkThreads), 0, s, zq, B, c->d, 1.0 - kappa,
                      w.qthr, w.best, w.bflag, st);
   LC_LAUNCHED();
 
   if (B > 0 && c->n > 0) {
+    const int64_t n_pad = athr_len(c->n);
+    hipLaunchKernelGGL(lookup_athr_kernel, dim3(static_cast<unsigned>((n_pad + 255) / 256)), dim3(256), 0, s, c->r,
+                       c->norm2, c->n, n_pad, kappa_c, w.athr);
+    LC_LAUNCHED();
     LookupParams p;
     p.zq = zq;
     p.B = B;
@@ -471,7 +784,9 @@ lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, 
     p.best = w.best;
     p.bflag = w.bflag;
     p.stats = st;
-    p.kappa_c = 1.0 - kappa - 4.0 * u32;
+    p.kappa_c = kappa_c;
+    p.athr = w.athr;
+    p.cimg = (precision == LIPCACHE_BF16 && c->store_dtype == LIPCACHE_F32) ? c->zimg : c->z;
     p.n_qblocks = static_cast<int>((B + pl.qblock - 1) / pl.qblock);
     p.g_hat = g_hat;
     p.cand = cand;
@@ -487,23 +802,8 @@ lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, 
     p.slice_len = ((tiles + slices - 1) / slices) * kTileN;
     const int64_t grid = slices * p.n_qblocks;
     if (grid > INT_MAX) return LIPCACHE_EUNSUPPORTED;
-    hipError_t e;
-    const bool f32src = c->store_dtype == LIPCACHE_F32;
-    if (precision == LIPCACHE_BF16) {
-      if (dump)
-        e = f32src ? launch_mode<kModeBF16, LIPCACHE_F32, true>(pl, p, static_cast<unsigned>(grid), s)
-                   : launch_mode<kModeBF16, LIPCACHE_BF16, true>(pl, p, static_cast<unsigned>(grid), s);
-      else
-        e = f32src ? launch_mode<kModeBF16, LIPCACHE_F32, false>(pl, p, static_cast<unsigned>(grid), s)
-                   : launch_mode<kModeBF16, LIPCACHE_BF16, false>(pl, p, static_cast<unsigned>(grid), s);
-    } else {
-      if (dump)
-        e = f32src ? launch_mode<kModeF32, LIPCACHE_F32, true>(pl, p, static_cast<unsigned>(grid), s)
-                   : launch_mode<kModeF32, LIPCACHE_BF16, true>(pl, p, static_cast<unsigned>(grid), s);
-      else
-        e = f32src ? launch_mode<kModeF32, LIPCACHE_F32, false>(pl, p, static_cast<unsigned>(grid), s)
-                   : launch_mode<kModeF32, LIPCACHE_BF16, false>(pl, p, static_cast<unsigned>(grid), s);
-    }
+    const hipError_t e = dump ? launch_lookup<true>(precision, c->store_dtype, pl, p, static_cast<unsigned>(grid), s)
+                              : launch_lookup<false>(precision, c->store_dtype, pl, p, static_cast<unsigned>(grid), s);
     if (e != hipSuccess) return LIPCACHE_EHIP;
   }
   if (!dump && B > 0) {
@@ -519,10 +819,9 @@ lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, 
 using namespace lc;
 
 extern "C" size_t lipcache_lookup_workspace_bytes(int64_t B, int64_t N, int32_t d, int32_t precision) {
-  (void)N;
   (void)d;
   (void)precision;
-  return ws_layout(B, nullptr, nullptr);
+  return ws_layout(B, N, nullptr, nullptr);
 }
 
 extern "C" lipcache_status lipcache_lookup(const lipcache_cache* c, const float* zq, int64_t B, int32_t precision,

@@ -4,19 +4,20 @@
 // smaller Gram matrix G (W W^T when C <= d, else W^T W), which has the same
 // non-zero eigenvalues; sigma_max(W)^2 is G's largest eigenvalue.  One
 // kernel forms G in float64 (every product of two floats is exact in float64),
-// a second runs the whole iteration inside one 1024-thread workgroup: the
+// a second runs the whole iteration inside one 512-thread workgroup: the
 // iteration is a chain of dependent matrix-vector products, so it is bound by
-// latency, and keeping G in registers (m <= 256) or L2 (m <= 1024) and the
-// iterate in LDS leaves two workgroup barriers per step.
+// latency.  G stays in registers (m <= 208) or L2 (m <= 1024), the iterate in
+// LDS, reductions use DPP lane exchanges, and each step has one barrier.
 #include "lc_common.hpp"
 
 namespace lc {
 
-constexpr int kPowThreads = 1024;
-constexpr int kPowTPR = 4;                                  // threads per row of G
+constexpr int kPowThreads = 512;
+constexpr int kPowWaves = kPowThreads / kWave;
+constexpr int kPowTPR = 2;                                  // threads per row of G
 constexpr int kPowRowsPerPass = kPowThreads / kPowTPR;      // 256
-constexpr int kPowRegCols = 64;                             // columns per thread (m <= 256)
 constexpr int kPowMaxM = 1024;
+constexpr int kPowRegMaxM = 208;                            // G held in registers up to here
 
 // G[a][b] = sum over the long side of W of products of W's entries.
 __global__ void gram_kernel(const float* __restrict__ W, int C, int d, int side,
@@ -50,12 +51,25 @@ __device__ __forceinline__ double start_component(int i) {
 }
 
 // out[0] = sigma, out[1] = iterations, out[2] = 1 if converged.
-template <bool REG>
+//
+// Layout: two adjacent lanes share a row a of G (columns of one parity each),
+// rows a, a + 256, ... per lane pair.  With NC > 0 the lane keeps its NC
+// columns of G in registers (m <= 2 NC); with NC = 0 it re-reads them from
+// global memory every iteration.  G is first scaled by an exact power of two
+// 2^-e (so its largest eigenvalue is at most 1 and nothing overflows) and
+// sigma = sqrt(lambda 2^e).  The iterate x_k lives in LDS unnormalised
+// (x_{k+1} = G x_k); the normalisation 1/||G x_k|| is applied as a scalar
+// when x_{k+1} is read.  Each step therefore needs one barrier: it publishes
+// the new vector and the per-wave partial sums of x.w, x.x and w.w, which
+// give the Rayleigh quotient lambda_k = x_k.G x_k / x_k.x_k and the next
+// normalisation.
+template <int NC>
 __global__ __launch_bounds__(kPowThreads) void power_kernel(const double* __restrict__ G, int m,
                                                             int max_iters, double rel_tol,
                                                             double* __restrict__ out) {
-  __shared__ double vbuf[2][kPowMaxM];
-  __shared__ double red[3][kPowThreads / kWave];
+  __shared__ double xbuf[2][kPowMaxM];
+  __shared__ double red[2][3][kPowWaves];
+  __shared__ double tr_part[kPowWaves];
 
   const int t = threadIdx.x;
   const int g = t / kPowTPR;
@@ -65,81 +79,103 @@ __global__ __launch_bounds__(kPowThreads) void power_kernel(const double* __rest
   const int passes = (m + kPowRowsPerPass - 1) / kPowRowsPerPass;
 
   for (int i = t; i < kPowMaxM; i += kPowThreads) {
-    vbuf[0][i] = i < m ? start_component(i) : 0.0;
-    vbuf[1][i] = 0.0;
+    xbuf[0][i] = i < m ? start_component(i) : 0.0;
+    xbuf[1][i] = 0.0;
   }
-  double greg[REG ? kPowRegCols : 1];
-  if constexpr (REG) {
+  // trace(G) >= lambda_max > 0 fixes the power-of-two scale
+  double tr = 0.0;
+  for (int a = t; a < m; a += kPowThreads) tr += G[static_cast<int64_t>(a) * m + a];
+  tr = wave_sum_dpp(tr);
+  if (lane == 0) tr_part[wave] = tr;
+  __syncthreads();
+  tr = 0.0;
 #pragma unroll
-    for (int s = 0; s < kPowRegCols; ++s) {
+  for (int w = 0; w < kPowWaves; ++w) tr += tr_part[w];
+  if (!(tr > 0.0)) {  // W = 0: degenerate head
+    if (t == 0) {
+      out[0] = 0.0;
+      out[1] = 0.0;
+      out[2] = 0.0;
+    }
+    return;
+  }
+  const int e = ilogb(tr) + 1;                       // 2^e > trace
+  const double gscale = ldexp(1.0, -e);              // exact
+
+  double greg[NC > 0 ? NC : 1];
+  if constexpr (NC > 0) {
+#pragma unroll
+    for (int s = 0; s < NC; ++s) {
       const int j = p + kPowTPR * s;
-      greg[s] = (g < m && j < m) ? G[static_cast<int64_t>(g) * m + j] : 0.0;
+      greg[s] = (g < m && j < m) ? G[static_cast<int64_t>(g) * m + j] * gscale : 0.0;
     }
   }
-  __syncthreads();
 
   int cur = 0, stable = 0, it = 0, converged = 0;
-  double sigma = 0.0, prev = -1.0;
+  double sigma = 0.0, prev = -1.0, invn = 1.0;
   for (it = 1; it <= max_iters; ++it) {
-    const double* v = vbuf[cur];
-    double ww = 0.0, vw = 0.0, vv = 0.0;
-    double wrow[kPowMaxM / kPowRowsPerPass];
-#pragma unroll
-    for (int rr = 0; rr < kPowMaxM / kPowRowsPerPass; ++rr) {
-      wrow[rr] = 0.0;
-      if (rr >= passes) continue;
+    const double* x = xbuf[cur];
+    double lxw = 0.0, lxx = 0.0, lww = 0.0;
+    for (int rr = 0; rr < passes; ++rr) {  // passes == 1 whenever NC > 0
       const int a = g + kPowRowsPerPass * rr;
-      double part = 0.0;
-      if constexpr (REG) {
+      double acc0 = 0.0, acc1 = 0.0, acc2 = 0.0, acc3 = 0.0;
+      if constexpr (NC > 0) {
 #pragma unroll
-        for (int s = 0; s < kPowRegCols; ++s) part = __builtin_fma(greg[s], v[p + kPowTPR * s], part);
-      } else {
-        if (a < m) {
-          const double* ga = G + static_cast<int64_t>(a) * m;
-          for (int j = p; j < m; j += kPowTPR) part = __builtin_fma(ga[j], v[j], part);
+        for (int s = 0; s < NC; s += 4) {
+          acc0 = __builtin_fma(greg[s], x[p + kPowTPR * s], acc0);
+          if (s + 1 < NC) acc1 = __builtin_fma(greg[s + 1], x[p + kPowTPR * (s + 1)], acc1);
+          if (s + 2 < NC) acc2 = __builtin_fma(greg[s + 2], x[p + kPowTPR * (s + 2)], acc2);
+          if (s + 3 < NC) acc3 = __builtin_fma(greg[s + 3], x[p + kPowTPR * (s + 3)], acc3);
         }
+      } else if (a < m) {
+        const double* ga = G + static_cast<int64_t>(a) * m;
+        int j = p;
+        for (; j + 3 * kPowTPR < m; j += 4 * kPowTPR) {
+          acc0 = __builtin_fma(ga[j], x[j], acc0);
+          acc1 = __builtin_fma(ga[j + kPowTPR], x[j + kPowTPR], acc1);
+          acc2 = __builtin_fma(ga[j + 2 * kPowTPR], x[j + 2 * kPowTPR], acc2);
+          acc3 = __builtin_fma(ga[j + 3 * kPowTPR], x[j + 3 * kPowTPR], acc3);
+        }
+        for (; j < m; j += kPowTPR) acc0 = __builtin_fma(ga[j], x[j], acc0);
+        acc0 *= gscale;
+        acc1 *= gscale;
+        acc2 *= gscale;
+        acc3 *= gscale;
       }
-      // The four partial sums of a row sit in adjacent lanes; after the two
-      // exchanges every one of them holds the same row sum.
-      part += __shfl_xor(part, 1, kWave);
-      part += __shfl_xor(part, 2, kWave);
-      if (a < m && p == 0) {
-        wrow[rr] = part;
-        ww = __builtin_fma(part, part, ww);
-        vw = __builtin_fma(v[a], part, vw);
-        vv = __builtin_fma(v[a], v[a], vv);
+      double row = (acc0 + acc1) + (acc2 + acc3);
+      row += dpp_f64<kDppQuadXor1>(row);  // the two lanes of the row
+      if (p == 0 && a < m) {
+        const double xa = invn * x[a];
+        const double wa = invn * row;   // (G x)_a with x = invn * stored vector
+        xbuf[cur ^ 1][a] = wa;
+        lxw = __builtin_fma(xa, wa, lxw);
+        lxx = __builtin_fma(xa, xa, lxx);
+        lww = __builtin_fma(wa, wa, lww);
       }
     }
-    ww = wave_sum(ww);
-    vw = wave_sum(vw);
-    vv = wave_sum(vv);
+    lxw = wave_sum_dpp(lxw);
+    lxx = wave_sum_dpp(lxx);
+    lww = wave_sum_dpp(lww);
     if (lane == 0) {
-      red[0][wave] = ww;
-      red[1][wave] = vw;
-      red[2][wave] = vv;
+      red[cur][0][wave] = lxw;
+      red[cur][1][wave] = lxx;
+      red[cur][2][wave] = lww;
     }
     __syncthreads();
-    double WW = 0.0, VW = 0.0, VV = 0.0;
+    double XW = 0.0, XX = 0.0, WW = 0.0;
 #pragma unroll
-    for (int w = 0; w < kPowThreads / kWave; ++w) {
-      WW += red[0][w];
-      VW += red[1][w];
-      VV += red[2][w];
+    for (int w = 0; w < kPowWaves; ++w) {
+      XW += red[cur][0][w];
+      XX += red[cur][1][w];
+      WW += red[cur][2][w];
     }
-    const double nrm = __builtin_sqrt(WW);
-    if (!(nrm > 0.0) || !(VV > 0.0)) {  // G v = 0: W = 0, degenerate head
+    if (!(WW > 0.0) || !(XX > 0.0)) {  // G x = 0
       sigma = 0.0;
       break;
     }
-    const double lam = VW / VV;             // Rayleigh quotient v^T G v / v^T v
-    const double sk = __builtin_sqrt(lam > 0.0 ? lam : 0.0);
-    if (p == 0) {
-#pragma unroll
-      for (int rr = 0; rr < kPowMaxM / kPowRowsPerPass; ++rr) {
-        const int a = g + kPowRowsPerPass * rr;
-        if (rr < passes && a < m) vbuf[cur ^ 1][a] = wrow[rr] / nrm;
-      }
-    }
+    const double lam = XW / XX;  // Rayleigh quotient of the scaled G
+    const double sk = __builtin_sqrt(ldexp(lam > 0.0 ? lam : 0.0, e));
+    invn = 1.0 / __builtin_sqrt(WW);
     if (it > 1 && __builtin_fabs(sk - prev) <= rel_tol * sk) {
       ++stable;
     } else {
@@ -151,7 +187,6 @@ __global__ __launch_bounds__(kPowThreads) void power_kernel(const double* __rest
       converged = 1;
       break;
     }
-    __syncthreads();
     cur ^= 1;
   }
   if (t == 0) {
@@ -192,10 +227,26 @@ extern "C" lipcache_status lipcache_spectral_norm(const float* W, int32_t C, int
   hipLaunchKernelGGL(gram_kernel, dim3(static_cast<unsigned>((cells + 255) / 256)), dim3(256), 0, s,
                      W, C, d, side, G);
   LC_LAUNCHED();
-  if (m <= kPowRowsPerPass) {
-    hipLaunchKernelGGL(power_kernel<true>, dim3(1), dim3(kPowThreads), 0, s, G, m, max_iters, rel_tol, out);
+  const int nc = (m + kPowTPR - 1) / kPowTPR;
+  auto launch = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(1), dim3(kPowThreads), 0, s, G, m, max_iters, rel_tol, out); };
+  if (m > kPowRegMaxM) {
+    launch(power_kernel<0>);
+  } else if (nc <= 16) {
+    launch(power_kernel<16>);
+  } else if (nc <= 32) {
+    launch(power_kernel<32>);
+  } else if (nc <= 48) {
+    launch(power_kernel<48>);
+  } else if (nc <= 64) {
+    launch(power_kernel<64>);
+  } else if (nc <= 80) {
+    launch(power_kernel<80>);
+  } else if (nc <= 96) {
+    launch(power_kernel<96>);
+  } else if (nc <= 100) {
+    launch(power_kernel<100>);
   } else {
-    hipLaunchKernelGGL(power_kernel<false>, dim3(1), dim3(kPowThreads), 0, s, G, m, max_iters, rel_tol, out);
+    launch(power_kernel<104>);
   }
   LC_LAUNCHED();
   double host[3] = {0.0, 0.0, 0.0};

@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported_and_bound():
     for name in names:
         assert hasattr(lib, name), name
         assert name in L.SIGNATURES, f"binding lacks {name}"
-    assert lib.lipcache_abi_version() == 1
+    assert lib.lipcache_abi_version() == 2
 
 
 def test_status_strings():
@@ -52,7 +52,7 @@ FAKE = ctypes.c_void_p(0x100000)  # never dereferenced: validation fails first
 
 
 def _cache(**kw):
-    c = L.LipcacheCache(FAKE.value, FAKE.value, FAKE.value, FAKE.value, 0, 16, 64, L.F32)
+    c = L.LipcacheCache(FAKE.value, None, FAKE.value, FAKE.value, FAKE.value, 0, 16, 64, L.F32)
     for k, v in kw.items():
         setattr(c, k, v)
     return c

@@ -492,12 +492,99 @@ __device__ __forceinline__ u32x4 lds_operand(const unsigned char* buf, int sub, 
 // accumulators (maxnum ignores NaN, so a NaN pair never hides another pair)
 // and compares once against A_i; the exact per-pair mask is only rebuilt on
 // the rare path.
+// Rare path of one column tile: rebuild the exact per-pair mask and re-check.
+template <int STORE, int RT>
+__device__ __forceinline__ void filter_and_recheck(const LookupParams& p, const f32x4 (&acc)[RT], const f32x4 (&qt)[RT],
+                                                   float an, int64_t qwave, int64_t ebase) {
+  uint32_t mask = 0u;
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mask |= static_cast<uint32_t>((acc[rt][i] - qt[rt][i]) >= an) << (rt * 4 + i);
+  }
+  recheck_pairs<STORE>(recheck_args(p), mask, qwave, ebase);
+}
+
+// A full LDS tile, software-pipelined: while the MFMAs of column tile s run,
+// the same wave evaluates the filter of column tile s - 1 (its accumulators
+// are kept one step longer), so the filter's VALU work fills the matrix
+// pipe's shadow instead of following it.
+template <int MODE, int STORE, int KS, int RT>
+__device__ __forceinline__ void compute_full_tile(const unsigned char* buf, const float* athr_buf,
+                                                  const LookupParams& p, int64_t t0, int64_t qwave, int m16, int g,
+                                                  const u32x4 (&a)[RT][KS], const float* qt_lds) {
+  constexpr int kSubs = DmaTraits<MODE>::kRows / kColTile;
+  constexpr int kE = RT * 4;                      // accumulators per lane
+  constexpr int kPer = (kE + KS - 1) / KS;        // filter terms folded into each k-step
+  u32x4 b0 = lds_operand<KS>(buf, 0, 0, m16, g);
+  u32x4 b1 = KS > 1 ? lds_operand<KS>(buf, 0, 1, m16, g) : b0;
+  f32x4 accp[RT];
+  float anp = 0.0f;
+#pragma unroll
+  for (int sub = 0; sub <= kSubs; ++sub) {
+    const bool cur = sub < kSubs;   // compile-time after unrolling
+    const bool prev = sub > 0;
+    f32x4 acc[RT];
+    float an = 0.0f;
+    f32x4 qt[RT];
+    if (prev) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) qt[rt] = *reinterpret_cast<const f32x4*>(qt_lds + rt * 16 + 4 * g);
+    }
+    if (cur) {
+      an = athr_buf[sub * kColTile + m16];
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    float mx = -__builtin_inff();
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (cur) {
+        const u32x4 op = (ks & 1) ? b1 : b0;
+        int nks = ks + 2, nsb = sub;
+        if (nks >= KS) {
+          nks -= KS;
+          nsb += 1;
+        }
+        u32x4 pre = op;
+        if (KS > 1 && nsb < kSubs) pre = lds_operand<KS>(buf, nsb, nks, m16, g);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) acc[rt] = mfma_step<MODE>(a[rt][ks], op, acc[rt]);
+        if (ks & 1) {
+          b1 = pre;
+        } else {
+          b0 = pre;
+        }
+      }
+      if (prev) {
+#pragma unroll
+        for (int e = ks * kPer; e < (ks + 1) * kPer && e < kE; ++e) mx = __builtin_fmaxf(mx, accp[e / 4][e % 4] - qt[e / 4][e % 4]);
+      }
+    }
+    if (cur && KS == 1 && sub + 1 < kSubs) b0 = lds_operand<KS>(buf, sub + 1, 0, m16, g);
+    if (prev) {
+      if (__ballot(mx >= anp) != 0ull) filter_and_recheck<STORE, RT>(p, accp, qt, anp, qwave, t0 + (sub - 1) * kColTile);
+    }
+    if (cur) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) accp[rt] = acc[rt];
+      anp = an;
+    }
+  }
+}
+
 template <int MODE, int STORE, int KS, int RT, bool DUMP>
 __device__ __forceinline__ void compute_tile(const unsigned char* buf, const float* athr_buf, const LookupParams& p,
                                              int64_t t0, int64_t e_end, int64_t qwave, int m16, int g,
                                              const u32x4 (&a)[RT][KS], const float* qt_lds) {
   constexpr int kRows = DmaTraits<MODE>::kRows;
   const int64_t left = e_end - t0;
+  if constexpr (!DUMP) {
+    if (left >= kRows) {
+      compute_full_tile<MODE, STORE, KS, RT>(buf, athr_buf, p, t0, qwave, m16, g, a, qt_lds);
+      return;
+    }
+  }
   const int nsub = left >= kRows ? kRows / kColTile : static_cast<int>((left + kColTile - 1) / kColTile);
   u32x4 b0 = lds_operand<KS>(buf, 0, 0, m16, g);
   u32x4 b1 = KS > 1 ? lds_operand<KS>(buf, 0, 1, m16, g) : b0;

@@ -61,6 +61,25 @@ def cpu_baseline(wl, zq_host, target_s: float):
             "seconds": t, "cpu_model": _cpu_model(), "certify_seconds": t_cert}
 
 
+def measured_traffic(workload: str, precision: str):
+    """HBM bytes per launch of the lookup kernel from the committed rocprofv3
+    counter summary, or None when the kernel source changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"lookup_{workload}_{precision}_counters.md")
+    src = os.path.join(ROOT, "paper_2608_13144_amd", "csrc", "lookup.hip")
+    try:
+        with open(path) as f:
+            line = next(l for l in f if l.startswith("traffic_json:"))
+        rec = json.loads(line.split(":", 1)[1])
+        with open(src, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()[:16]
+    except (OSError, StopIteration, ValueError):
+        return None
+    if rec.get("lookup_hip_sha16") != sha:
+        return None
+    return rec
+
+
 def _cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -202,10 +221,16 @@ def main() -> int:
         "cache_build_ms": t_build * 1e3,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": None,
-                     "kernel": "lookup_kernel (fused contraction + filter + re-check)",
+                     "kernel": "lookup_dma_kernel (fused contraction + filter + re-check)",
                      "algorithmic": f"2*B*N*d = {flops:.4e} flop per launch"},
         "cpu_baseline": None,
     }
+    tr = measured_traffic(cfg.name, args.precision)
+    if tr is not None and n0 == N:
+        out["roofline"]["traffic"] = tr["traffic_bytes"]
+        out["roofline"]["traffic_unit"] = "bytes per launch (FETCH_SIZE x %.4f + WRITE_SIZE x %.4f)" % (
+            tr["fetch_scale"], tr["write_scale"])
+        out["roofline"]["hbm_gbs"] = tr["traffic_bytes"] / (lk * 1e-3) / 1e9
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, zq_host, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -6,4 +6,5 @@ leg import this package; the product path never does.
 from .lipcache_oracle import *  # noqa: F401,F403
 from .lipcache_oracle import (MISS, BAND_REL, DegenerateHead, CapacityError,  # noqa: F401
                               bf16_round, stored_values, spectral_norm, certify,
-                              logits_of, lookup, lookup_rows, insert, CacheState)
+                              logits_of, lookup, lookup_rows, lookup_blocked, insert,
+                              CacheState)

@@ -19,6 +19,10 @@ bfloat16 cache), with float64 as the stand-in for exact arithmetic:
                          r* = min_j (s_y - s_j) / ||W_y - W_j|| (Remark 5.1, Eq. (29)).
   * ``lookup``         - hit set H = {i : ||z - z_i|| < r_i} (Eq. (13)), nearest
                          hit i* (Eq. (14)), payload or miss (Eq. (15)).
+  * ``lookup_blocked`` - the same answers with a float32 BLAS prefilter of
+                         rigorous slack and the same float64 distances for
+                         the survivors (for large test batches); pinned
+                         bit-for-bit against ``lookup``.
   * ``insert``         - write-back of missed samples (Sec. 4.4, Alg. 2).
   * ``bf16_round``     - round-to-nearest-even float32 -> bfloat16 (storage).
 
@@ -278,6 +282,104 @@ def lookup_rows(zq, cache_z, cache_r, cache_label, rows, band_rel: float = BAND_
     """``lookup`` on the selected query rows only (sampled checks at full size)."""
     Q = np.asarray(zq)[np.asarray(rows, dtype=np.int64)]
     return lookup(Q, cache_z, cache_r, cache_label, band_rel)
+
+
+def prefilter_rel(d: int) -> float:
+    """Relative slack of the float32 matrix-product prefilter of ``lookup_blocked``.
+
+    With float32 products and sums (any order), the expansion
+    ||q||^2 + ||z||^2 - 2 q.z differs from the exact squared distance by at
+    most about 2 (d + 3) 2^-24 (||q||^2 + ||z||^2): the dot product and the
+    entry norm each contribute gamma_d, the few remaining roundings 6 u.  The
+    slack is four times that.
+    """
+    return 8.0 * (d + 8) * 2.0 ** -24
+
+
+def lookup_blocked(zq, cache_z, cache_r, cache_label, band_rel: float = BAND_REL,
+                   q_chunk: int = 256, n_chunk: int = 1 << 16) -> LookupResult:
+    """``lookup`` with a matrix-product prefilter; the same result.
+
+    For each (query, entry) block the squared distance is first estimated
+    from the expansion ||q||^2 + ||z_i||^2 - 2 q.z_i (one float32 BLAS product
+    per block): a pair whose estimate, less prefilter_rel(d) (||q||^2 +
+    ||z_i||^2), still exceeds (1 + band_rel)^2 r_i^2 can be neither a hit nor
+    a band pair (an entry with r_i <= 0 never is), so only the survivors get
+    the direct float64 sum_k (q_k - z_{i,k})^2 of ``lookup`` (the same
+    expression, row by row), and the answer, band count and flag follow from
+    them exactly as in ``lookup``.
+    """
+    Q = np.asarray(zq, dtype=np.float64)
+    Q32 = np.asarray(zq, dtype=np.float32)
+    Z = np.asarray(cache_z)
+    r = np.asarray(cache_r, dtype=np.float32).astype(np.float64)
+    lab = np.asarray(cache_label, dtype=np.int32)
+    B, N = Q.shape[0], Z.shape[0]
+    out_label = np.full(B, MISS, dtype=np.int32)
+    out_index = np.full(B, -1, dtype=np.int64)
+    out_d2 = np.full(B, np.inf)
+    n_hits = np.zeros(B, dtype=np.int64)
+    n_band = np.zeros(B, dtype=np.int64)
+    flagged = np.zeros(B, dtype=bool)
+    if N == 0 or B == 0:
+        return LookupResult(out_label, out_index, out_d2, n_hits, n_band, flagged)
+    r2 = r * r
+    live = r > 0
+    reach = (1.0 + band_rel) ** 2 * r2
+    c = prefilter_rel(Q.shape[1])
+    # estimate <= reach with estimate = (1 - c)(||q||^2 + ||z||^2) - 2 q.z,
+    # rearranged as q.z >= a_q + b_i (the roundings this adds are inside c)
+    a = ((1.0 - c) * np.sum(Q * Q, axis=1) / 2.0).astype(np.float32)
+    pairs_q, pairs_e = [], []
+    for ns in range(0, N, n_chunk):
+        ne = min(N, ns + n_chunk)
+        Zc = np.asarray(Z[ns:ne], dtype=np.float32)
+        nz = np.sum(Zc * Zc, axis=1, dtype=np.float64)
+        b = ((1.0 - c) * nz - reach[ns:ne]) / 2.0
+        b[~live[ns:ne]] = np.inf          # entries that are never hit
+        b = b.astype(np.float32)
+        for qs in range(0, B, q_chunk):
+            qe = min(B, qs + q_chunk)
+            G = Q32[qs:qe] @ Zc.T
+            G -= b[None, :]
+            qi, ei = np.nonzero(G >= a[qs:qe, None])
+            pairs_q.append(qi + qs)
+            pairs_e.append(ei + ns)
+    pq = np.concatenate(pairs_q)
+    pe = np.concatenate(pairs_e)
+    order = np.lexsort((pe, pq))          # by query, then ascending entry index
+    pq, pe = pq[order], pe[order]
+    starts = np.searchsorted(pq, np.arange(B + 1))
+    for qi in range(B):
+        idx = pe[starts[qi]:starts[qi + 1]]
+        if idx.size == 0:
+            continue
+        D2 = np.sum((Z[idx].astype(np.float64) - Q[qi]) ** 2, axis=1)
+        rr, rr2 = r[idx], r2[idx]
+        hit = D2 < rr2
+        D = np.sqrt(D2)
+        band = np.abs(D - rr) <= band_rel * rr
+        n_hits[qi] = int(hit.sum())
+        n_band[qi] = int(band.sum())
+        if n_hits[qi]:
+            best = D2[hit].min()
+            i_star = int(idx[np.flatnonzero(hit & (D2 == best))[0]])
+            out_index[qi] = i_star
+            out_label[qi] = lab[i_star]
+            out_d2[qi] = best
+        if n_band[qi]:
+            solid = hit & ~band
+            if not solid.any():
+                flagged[qi] = True
+            else:
+                d_solid = np.sqrt(D2[solid].min())
+                if np.any(D[band] <= (1.0 + band_rel) * d_solid):
+                    flagged[qi] = True
+        if n_hits[qi] >= 2:
+            hd = np.sort(np.sqrt(D2[hit]))
+            if hd[1] - hd[0] <= band_rel * max(hd[1], 1e-300):
+                flagged[qi] = True
+    return LookupResult(out_label, out_index, out_d2, n_hits, n_band, flagged)
 
 
 # ------------------------------------------------------------------ insert

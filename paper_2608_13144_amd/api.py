@@ -182,6 +182,18 @@ class LipCache:
         L.check("lipcache_lookup", st)
         return out
 
+    def serve(self, zq: torch.Tensor, W: torch.Tensor, b: torch.Tensor | None, sigma: float,
+              precision: str = "bf16", out: LookupResult | None = None):
+        """One round of certified serving (Alg. 2): look every query up, certify
+        every query with the head (the label and radius a miss is cached with;
+        for a bfloat16 store the rounded query is certified), and write the
+        misses back.  Returns (lookup result, certified queries, rows appended).
+        """
+        res = self.lookup(zq, precision=precision, out=out)
+        cq = certify(zq, W, b, sigma, store=self.store)
+        inserted = self.insert(zq, cq.label, cq.r, res.label)
+        return res, cq, inserted
+
     def filter_dump(self, zq: torch.Tensor, precision: str = "bf16"):
         """lipcache_lookup_filter_dump: matrix-core dot products and filter decisions (small sizes)."""
         _need_cuda(zq, "zq", torch.float32, 2)

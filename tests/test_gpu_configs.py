@@ -1,0 +1,81 @@
+"""The four single-batch workloads at full size, built and launched as bench.py does.
+
+Per workload: sigma, labels and radii of all N cache candidates against the
+oracle's certify; the cache built on the device from the device's own
+certificates; one batch of queries composed from the oracle's cache state;
+the lookup with both filters, compared with the oracle query by query (all
+queries where the blocked oracle finishes in seconds, a seeded sample of
+2,048 at N = 1M), and every hit of the whole batch checked for validity and
+certified consistency.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_13144_amd import api
+from paper_2608_13144_amd import workload as wlmod
+from gpu_helpers import DEV, check_hits_valid, compare_lookup, gpu, host, oracle_cache, say
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+SAMPLE = {"tiny-d64-c10": None, "mix-d128-c10": None, "mix-d128-c100": None, "mix-d256-c200": 2048}
+
+
+def check_certify(cert_gpu, cert_o, W, what):
+    """Labels exact and radii within relative 1e-5, except where the top-2 logits
+    are closer than the float64 accumulation error could reach."""
+    lab = host(cert_gpu.label)
+    r = host(cert_gpu.r).astype(np.float64)
+    # sum_k |W_ck z_k| <= max|W| * ||z||_1 bounds the terms of every logit
+    scale = 2.0 * float(np.abs(W).max()) * np.abs(cert_o.stored.astype(np.float64)).sum(axis=1)
+    near_tie = cert_o.margin <= 1e-9 * scale
+    assert np.array_equal(lab[~near_tie], cert_o.label[~near_tie]), what
+    ok = ~near_tie & (cert_o.r > 0)
+    rel = np.abs(r[ok] - cert_o.r[ok]) / cert_o.r[ok]
+    assert rel.max() <= 1e-5, f"{what}: radius rel {rel.max()}"
+    assert np.array_equal(r[~near_tie] > 0, cert_o.r[~near_tie] > 0), what
+    return int(near_tie.sum())
+
+
+@pytest.mark.parametrize("name", list(SAMPLE))
+def test_workload_full_size(name):
+    cfg = wlmod.CONFIGS[name]
+    say("workload", name, "N", cfg.n_cache, "B", cfg.batch, "d", cfg.d, "C", cfg.C)
+    wl = wlmod.make_workload(cfg, seed=0)
+    N, B, d = cfg.n_cache, cfg.batch, cfg.d
+
+    sig_o = oracle.spectral_norm(wl.W).sigma
+    cert_o = oracle.certify(wl.z, wl.W, wl.b, sig_o, store=cfg.store_dtype)
+    st = oracle_cache(wl.z, cert_o.label, cert_o.r, d, store=cfg.store_dtype)
+    say(name, "oracle chain done, n", st.n)
+
+    W, b, z = gpu(wl.W), gpu(wl.b), gpu(wl.z)
+    sig = api.spectral_norm(W)
+    assert sig.converged and abs(sig.sigma - sig_o) <= 1e-9 * sig_o, (sig.sigma, sig_o)
+    cert = api.certify(z, W, b, sig.sigma, store=cfg.store_dtype)
+    ties = check_certify(cert, cert_o, wl.W, name)
+    cache = api.LipCache(d, N + B, store=cfg.store_dtype, device=DEV)
+    cache.insert(z, cert.label, cert.r)
+    assert cache.n == st.n
+    if ties == 0:
+        assert np.array_equal(host(cache.label[: cache.n]), st.label)
+
+    draws = wlmod.draw_queries(wl, 0)
+    idx = wlmod.near_indices(draws, st.n)
+    zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
+    rows = SAMPLE[name]
+    if rows is not None:
+        rows = np.sort(np.random.default_rng(7).choice(B, rows, replace=False))
+    ref = oracle.lookup_blocked(zq if rows is None else zq[rows], st.z, st.r, st.label)
+    say(name, "oracle lookup of", B if rows is None else rows.size, "queries done")
+    for precision in ("bf16", "f32"):
+        res = cache.lookup(gpu(zq), precision=precision)
+        nflag = compare_lookup(res, ref, f"{name}/{precision}", rows=rows)
+        nhit = check_hits_valid(res, zq, st, wl.W, wl.b, f"{name}/{precision}")
+        stats = host(res.stats)
+        assert stats[0] == nhit
+        assert 0.2 < nhit / B < 0.32, nhit / B
+        say(name, precision, "hits", nhit, "flagged", nflag, "near-tie entries", ties, "stats", stats.tolist())
+    del cache
+    torch.cuda.empty_cache()

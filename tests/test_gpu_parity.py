@@ -22,57 +22,9 @@ import oracle
 from paper_2608_13144_amd import _lib as L
 from paper_2608_13144_amd import api
 from paper_2608_13144_amd import workload as wlmod
+from gpu_helpers import DEV, build_cache, compare_lookup, gpu, host, oracle_cache, say  # noqa: F401
 
 pytestmark = pytest.mark.gpu
-DEV = "cuda:0"
-
-
-def say(*a):
-    print("[gpu-test]", *a, file=sys.stderr, flush=True)
-
-
-def gpu(x):
-    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
-
-
-def host(t):
-    torch.cuda.synchronize()
-    return t.detach().cpu().numpy()
-
-
-def build_cache(state: "oracle.CacheState", capacity=None, store=None, image=True):
-    """GPU cache holding the same rows as an oracle state (inserted through the HIP path)."""
-    store = store or state.store
-    cap = capacity or max(state.n, 1)
-    c = api.LipCache(state.d, cap, store=store, device=DEV, image=image)
-    if state.n:
-        got = c.insert(gpu(state.z.astype(np.float32)), gpu(state.label), gpu(state.r))
-        assert got == state.n
-    return c
-
-
-def oracle_cache(z, label, r, d, store="f32", capacity=None):
-    st = oracle.CacheState(d=d, capacity=capacity or max(len(r), 1), store=store)
-    oracle.insert(st, z, label, r)
-    return st
-
-
-def compare_lookup(res_gpu, ref, what):
-    lab = host(res_gpu.label)
-    idx = host(res_gpu.index)
-    d2 = host(res_gpu.dist2)
-    ok = ~ref.flagged
-    nflag = int(ref.flagged.sum())
-    bad_lab = np.flatnonzero(ok & (lab != ref.label))
-    bad_idx = np.flatnonzero(ok & (idx != ref.index))
-    assert bad_lab.size == 0, f"{what}: label mismatch at {bad_lab[:10]} gpu={lab[bad_lab[:10]]} ref={ref.label[bad_lab[:10]]}"
-    assert bad_idx.size == 0, f"{what}: index mismatch at {bad_idx[:10]}"
-    hit = ok & (ref.index >= 0)
-    if hit.any():
-        rel = np.abs(d2[hit].astype(np.float64) - ref.dist2[hit]) / np.maximum(ref.dist2[hit], 1e-300)
-        assert rel.max() <= 1e-5, f"{what}: dist2 rel err {rel.max()}"
-    assert np.all(np.isinf(d2[ok & (ref.index < 0)]))
-    return nflag
 
 
 # --------------------------------------------------------------- fixtures

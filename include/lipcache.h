@@ -47,7 +47,7 @@ typedef enum lipcache_status {
   LIPCACHE_EDEGENERATE = 2,   /* sigma_max(W) <= 0: construction stops (Alg. 1)        */
   LIPCACHE_ENOCONV = 3,       /* power iteration hit max_iters; sigma still written    */
   LIPCACHE_ECAPACITY = 4,     /* insert would exceed the cache capacity; nothing added */
-  LIPCACHE_EUNSUPPORTED = 5,  /* valid request this build does not implement           */
+  LIPCACHE_EUNSUPPORTED = 5,  /* valid request the library does not implement          */
   LIPCACHE_EWORKSPACE = 6,    /* workspace missing, too small or misaligned            */
   LIPCACHE_EHIP = 7           /* a HIP runtime call or kernel launch failed            */
 } lipcache_status;
@@ -58,7 +58,7 @@ enum { LIPCACHE_F32 = 0, LIPCACHE_BF16 = 1 };
 
 /* Radius modes (policy component rho, Sec. 4.3): the conservative radius of
  * Eq. (21) or the tight per-pair radius of Remark 5.1, Eq. (29). */
-enum { LIPCACHE_RADIUS_CONSERVATIVE = 0, LIPCACHE_RADIUS_TIGHT = 1 };
+enum { LIPCACHE_RADIUS_CONSERVATIVE = 0 /* Eq. (21) */, LIPCACHE_RADIUS_TIGHT = 1 /* Remark 5.1 */ };
 
 /* Label written for a query whose hit set is empty (falls back to MainNet,
  * Eq. (15)). */
@@ -126,12 +126,19 @@ size_t lipcache_spectral_norm_workspace_bytes(int32_t C, int32_t d);
  *   logits s = W z_i + b accumulated in float64 (Eq. (5)),
  *   label y_i = argmax_c s_c, lowest index on ties (Eq. (6)),
  *   margin m_i = s_y - max_{j != y} s_j (Eq. (20)),
- *   radius r_i = m_i / (sigma sqrt 2) (Eq. (21)), rounded to nearest float.
+ *   radius r_i = m_i / (sigma sqrt 2) (Eq. (21)), rounded to nearest float,
+ *   or with LIPCACHE_RADIUS_TIGHT the per-pair radius of Remark 5.1,
+ *   r*_i = min_{j != y} (s_y - s_j) / ||W_y - W_j||_2 (float64, then rounded),
+ *   where a class with W_j = W_y sets no finite constraint (r*_i = +inf when
+ *   no class does).  r*_i >= r_i.
  * A radius <= 0 (a tie) marks a candidate that must be discarded (Alg. 1).
  *
  *  z [N][d] float; W [C][d] float, C >= 2; b [C] float or NULL (= 0)
- *  sigma       > 0, normally lipcache_spectral_norm's result
- *  radius_mode LIPCACHE_RADIUS_CONSERVATIVE (TIGHT returns EUNSUPPORTED)
+ *  sigma       > 0, normally lipcache_spectral_norm's result (used by the
+ *              conservative radius only, but validated in both modes)
+ *  radius_mode LIPCACHE_RADIUS_CONSERVATIVE or LIPCACHE_RADIUS_TIGHT; the
+ *              tight mode evaluates the logits twice and needs a C x C
+ *              float64 table in the workspace
  *  label_out [N] int32, r_out [N] float (required)
  *  margin_out [N] float, norm2_out [N] float (nullable): m_i and ||z_i||^2
  *  ws          lipcache_certify_workspace_bytes(C, d, radius_mode) bytes

@@ -44,6 +44,7 @@ def test_workspace_queries():
     assert lib.lipcache_spectral_norm_workspace_bytes(200, 256) >= 200 * 200 * 8
     assert lib.lipcache_spectral_norm_workspace_bytes(300, 64) >= 64 * 64 * 8
     assert lib.lipcache_certify_workspace_bytes(200, 256, 0) >= 200 * 256 * 8
+    assert lib.lipcache_certify_workspace_bytes(200, 256, L.RADIUS_TIGHT) >= 200 * 256 * 8 + 200 * 200 * 8
     assert lib.lipcache_lookup_workspace_bytes(32768, 1 << 20, 256, L.BF16) >= 32768 * 16
     assert lib.lipcache_insert_workspace_bytes(65536) >= 2 * 64 * 8
 
@@ -92,7 +93,7 @@ def test_certify_validation():
     assert call(mode=9) == L.EINVAL
     assert call(label=None) == L.EINVAL
     assert call(z=ctypes.c_void_p(0x100004)) == L.EINVAL  # misaligned
-    assert call(mode=L.RADIUS_TIGHT) == L.EUNSUPPORTED
+    assert call(mode=L.RADIUS_TIGHT, wsb=10 * 64 * 8 + 256) == L.EWORKSPACE   # no room for the C x C table
     assert call(ws=None) == L.EWORKSPACE
     assert call(wsb=16) == L.EWORKSPACE
     assert call(ws=ctypes.c_void_p(0x100040)) == L.EWORKSPACE  # not 256-aligned

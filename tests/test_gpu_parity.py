@@ -86,12 +86,13 @@ def _certify_case(N, d, C, seed, store="f32", bias=True):
 @pytest.mark.parametrize("N,d,C,store", [(4096, 64, 10, "f32"), (1000, 128, 100, "f32"), (3000, 256, 200, "f32"),
                                          (777, 1024, 13, "f32"), (2048, 256, 200, "bf16"), (130, 32, 2, "f32"),
                                          (65, 512, 9, "bf16")])
-def test_certify_matches_oracle(N, d, C, store):
-    say("certify", N, d, C, store)
+@pytest.mark.parametrize("mode", ["conservative", "tight"])
+def test_certify_matches_oracle(N, d, C, store, mode):
+    say("certify", N, d, C, store, mode)
     W, b, z, sig = _certify_case(N, d, C, seed=N + d + C, store=store)
-    ref = oracle.certify(z, W, b, sig, store=store)
-    out = api.certify(gpu(z), gpu(W), None if b is None else gpu(b), sig, store=store, want_margin=True,
-                      want_norm2=True)
+    ref = oracle.certify(z, W, b, sig, store=store, radius_mode=mode)
+    out = api.certify(gpu(z), gpu(W), None if b is None else gpu(b), sig, store=store, radius_mode=mode,
+                      want_margin=True, want_norm2=True)
     lab, r, m, n2 = host(out.label), host(out.r), host(out.margin), host(out.norm2)
     # a near-tie of the top two logits (margin below the float64 rounding of
     # the logits) may legitimately change the argmax
@@ -121,6 +122,43 @@ def test_certify_ties_and_empty():
     assert r[0] == np.float32(1 / math.sqrt(2)) and r[2] == np.float32(1.5 / math.sqrt(2))
     e = api.certify(gpu(np.zeros((0, 32), np.float32)), gpu(W), None, 1.0)
     assert e.label.numel() == 0
+
+
+def test_certify_tight_hand_cases():
+    """Remark 5.1 on heads small enough to evaluate by hand."""
+    say("certify tight hand cases")
+    d = 32
+
+    def head(rows):
+        W = np.zeros((len(rows), d), np.float32)
+        for i, row in enumerate(rows):
+            W[i, : len(row)] = row
+        return W
+
+    z = np.zeros((1, d), np.float32)
+    z[0, :2] = [1, 1]
+    # rows of different length: s = (2, 1), ||W_0 - W_1|| = sqrt 5, sigma = 2
+    W = head([[2, 0], [0, 1]])
+    t = api.certify(gpu(z), gpu(W), None, 2.0, radius_mode="tight")
+    c = api.certify(gpu(z), gpu(W), None, 2.0)
+    assert host(t.label)[0] == 0
+    assert host(t.r)[0] == np.float32(1 / math.sqrt(5))
+    assert host(c.r)[0] == np.float32(1 / (2 * math.sqrt(2)))
+    # a duplicated row sets no constraint: s = (2, 2.5, 0) at z = (2, 0)
+    z2 = np.zeros((1, d), np.float32)
+    z2[0, 0] = 2
+    W = head([[1, 0], [1, 0], [0, 1]])
+    b = np.array([0, 0.5, 0], np.float32)
+    t = api.certify(gpu(z2), gpu(W), gpu(b), math.sqrt(2), radius_mode="tight")
+    assert host(t.label)[0] == 1
+    assert host(t.r)[0] == np.float32(2.5 / math.sqrt(2))
+    # every competitor duplicated: no finite constraint at all
+    W = head([[1, 0], [1, 0]])
+    b = np.array([0, 1], np.float32)
+    t = api.certify(gpu(z2), gpu(W), gpu(b), math.sqrt(2), radius_mode="tight")
+    assert host(t.label)[0] == 1 and np.isposinf(host(t.r)[0])
+    ref = oracle.certify(z2, W, b, math.sqrt(2), radius_mode="tight")
+    assert np.isposinf(ref.r[0])
 
 
 # --------------------------------------------------------------- insert
@@ -318,17 +356,18 @@ def test_filter_sound_and_accurate(tiny, precision, store, image):
 
 
 # --------------------------------------------------------------- end-to-end chain
-def test_end_to_end_chain_tiny():
+@pytest.mark.parametrize("mode", ["conservative", "tight"])
+def test_end_to_end_chain_tiny(mode):
     """spectral_norm -> certify -> insert -> lookup on the device, against the oracle chain."""
-    say("chain tiny")
+    say("chain tiny", mode)
     wl = wlmod.make_workload("tiny-d64-c10", seed=0)
     sig_g = api.spectral_norm(gpu(wl.W)).sigma
     sig_o = oracle.spectral_norm(wl.W).sigma
     assert abs(sig_g - sig_o) <= 1e-9 * sig_o
-    cert_g = api.certify(gpu(wl.z), gpu(wl.W), gpu(wl.b), sig_g)
+    cert_g = api.certify(gpu(wl.z), gpu(wl.W), gpu(wl.b), sig_g, radius_mode=mode)
     c = api.LipCache(64, wl.z.shape[0] + 1024, device=DEV)
     n = c.insert(gpu(wl.z), cert_g.label, cert_g.r)
-    cert_o = oracle.certify(wl.z, wl.W, wl.b, sig_o)
+    cert_o = oracle.certify(wl.z, wl.W, wl.b, sig_o, radius_mode=mode)
     st = oracle_cache(wl.z, cert_o.label, cert_o.r, 64, capacity=wl.z.shape[0] + 1024)
     assert n == st.n
     draws = wlmod.draw_queries(wl, 0)
@@ -342,7 +381,7 @@ def test_end_to_end_chain_tiny():
     ok = ~ref.flagged
     assert np.array_equal(lab[ok], ref.label[ok])
     # write-back of the misses with the queries' own certificates
-    cq = api.certify(gpu(zq), gpu(wl.W), gpu(wl.b), sig_g)
+    cq = api.certify(gpu(zq), gpu(wl.W), gpu(wl.b), sig_g, radius_mode=mode)
     before = c.n
     added = c.insert(gpu(zq), cq.label, cq.r, res.label)
     assert added == int((lab == -1).sum()) - int((host(cq.r)[lab == -1] <= 0).sum())

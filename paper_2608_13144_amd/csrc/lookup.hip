@@ -35,7 +35,7 @@
 
 namespace lc {
 
-constexpr int kLkThreads = 256;
+constexpr int kLkThreads = 512;
 constexpr int kLkWaves = kLkThreads / kWave;
 constexpr int kTileN = 64;
 constexpr int kColTile = 16;
@@ -431,18 +431,45 @@ __device__ __forceinline__ int lds_swizzle(int row) {
 // vmcnt(0): wait for this wave's outstanding copies into LDS.
 __device__ __forceinline__ void wait_copies() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-template <int MODE>
+// Global -> LDS copies (global_load_lds, saddr form): lane i's BYTES bytes at
+// sbase + voff land at LDS byte address lds + BYTES * i (sbase and lds
+// wave-uniform).  Written as inline assembly because the compiler models the
+// intrinsic form as an out-of-order LDS event: while one is in flight every
+// wait for an ordinary LDS read degrades to lgkmcnt(0), which serialises the
+// operand prefetch of the matrix loop behind the latest read.  The copy is
+// only counted by vmcnt, which the kernel waits on explicitly (wait_copies)
+// before the barrier that publishes a tile; an unknown extra vmcnt entry can
+// only make the compiler's own vmcnt waits stricter.  M0 carries the LDS
+// address; SALU writes to M0 need one wait state before the copy reads it.
+template <int BYTES>
+__device__ __forceinline__ void lds_copy(const void* sbase, uint32_t voff, const void* lds) {
+  const uint32_t m = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_void_t*)lds));
+  if constexpr (BYTES == 16) {
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(m)
+                 : "memory", "m0");
+  } else {
+    static_assert(BYTES == 4, "16- or 4-byte copies");
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1" ::"v"(voff), "s"(sbase), "s"(m)
+                 : "memory", "m0");
+  }
+}
+
+// Cache rows per LDS tile of the DMA kernel: 64 KiB per buffer (rows of
+// 64 * KS bytes in either element type), at most 128 rows.
+template <int KS>
 struct DmaTraits {
-  static constexpr int kRows = MODE == kModeBF16 ? 64 : 32;  // cache rows per LDS tile
+  static constexpr int kRows = KS <= 8 ? 128 : 64;
 };
+constexpr int kDmaMaxRows = 128;
 
 template <int MODE, int KS>
 __device__ __forceinline__ void issue_tile(unsigned char* buf, float* athr_buf, const LookupParams& p, int64_t t0,
                                            int64_t e_end, int wave) {
   using T = ModeTraits<MODE>;
   constexpr int kCPR = 4 * KS;  // 16-byte chunks per LDS row
-  constexpr int kRows = DmaTraits<MODE>::kRows;
+  constexpr int kRows = DmaTraits<KS>::kRows;
   constexpr int kIters = kRows * kCPR / kLkThreads;
+  static_assert(kIters >= 1 && kIters * kLkThreads == kRows * kCPR, "whole copies per thread");
   constexpr int kRowsPerIter = kLkThreads / kCPR;
   const int d_chunks = p.d * T::kElemBytes / 16;
   const int row_bytes = p.d * T::kElemBytes;
@@ -461,10 +488,12 @@ __device__ __forceinline__ void issue_tile(unsigned char* buf, float* athr_buf, 
     // there, so they add nothing.
     if (c >= d_chunks) c -= d_chunks;
     const int rr = row < last ? row : last;
-    __builtin_amdgcn_global_load_lds(base + (rr * row_bytes + c * 16),
-                                     (lds_void_t*)(buf + (j * kLkThreads + wave * kWave) * 16), 16, 0, 0);
+    lds_copy<16>(base, static_cast<uint32_t>(rr * row_bytes + c * 16), buf + (j * kLkThreads + wave * kWave) * 16);
   }
-  if (wave == 0) __builtin_amdgcn_global_load_lds(p.athr + t0 + lane_id(), (lds_void_t*)athr_buf, 4, 0, 0);
+  // thresholds of the tile's rows (+inf padding past n): one wave per 64
+  if (wave < kRows / kWave)
+    lds_copy<4>(p.athr + t0 + wave * kWave, static_cast<uint32_t>(lane_id() * 4),
+                static_cast<unsigned char*>(static_cast<void*>(athr_buf)) + wave * kWave * 4);
 }
 
 // The cache operand of (column tile `sub`, k-step ks) for this lane: chunk
@@ -512,8 +541,8 @@ __device__ __forceinline__ void filter_and_recheck(const LookupParams& p, const 
 template <int MODE, int STORE, int KS, int RT>
 __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, const float* athr_buf,
                                                   const LookupParams& p, int64_t t0, int64_t qwave, int m16, int g,
-                                                  const u32x4 (&a)[RT][KS], const float* qt_lds) {
-  constexpr int kSubs = DmaTraits<MODE>::kRows / kColTile;
+                                                  const u32x4 (&a)[RT][KS], const f32x4 (&qv)[RT]) {
+  constexpr int kSubs = DmaTraits<KS>::kRows / kColTile;
   constexpr int kE = RT * 4;                      // accumulators per lane
   constexpr int kPer = (kE + KS - 1) / KS;        // filter terms folded into each k-step
   u32x4 b0 = lds_operand<KS>(buf, 0, 0, m16, g);
@@ -529,7 +558,7 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
     f32x4 qt[RT];
     if (prev) {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) qt[rt] = *reinterpret_cast<const f32x4*>(qt_lds + rt * 16 + 4 * g);
+      for (int rt = 0; rt < RT; ++rt) qt[rt] = qv[rt];
     }
     if (cur) {
       an = athr_buf[sub * kColTile + m16];
@@ -560,6 +589,10 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
 #pragma unroll
         for (int e = ks * kPer; e < (ks + 1) * kPer && e < kE; ++e) mx = __builtin_fmaxf(mx, accp[e / 4][e % 4] - qt[e / 4][e % 4]);
       }
+      // Keep the operand read for k-step ks + 2 in this step: left to
+      // itself the scheduler sinks it next to its use and the wave stalls
+      // on the LDS latency every few MFMAs.
+      __builtin_amdgcn_sched_barrier(0);
     }
     if (cur && KS == 1 && sub + 1 < kSubs) b0 = lds_operand<KS>(buf, sub + 1, 0, m16, g);
     if (prev) {
@@ -576,12 +609,12 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
 template <int MODE, int STORE, int KS, int RT, bool DUMP>
 __device__ __forceinline__ void compute_tile(const unsigned char* buf, const float* athr_buf, const LookupParams& p,
                                              int64_t t0, int64_t e_end, int64_t qwave, int m16, int g,
-                                             const u32x4 (&a)[RT][KS], const float* qt_lds) {
-  constexpr int kRows = DmaTraits<MODE>::kRows;
+                                             const u32x4 (&a)[RT][KS], const f32x4 (&qv)[RT]) {
+  constexpr int kRows = DmaTraits<KS>::kRows;
   const int64_t left = e_end - t0;
   if constexpr (!DUMP) {
     if (left >= kRows) {
-      compute_full_tile<MODE, STORE, KS, RT>(buf, athr_buf, p, t0, qwave, m16, g, a, qt_lds);
+      compute_full_tile<MODE, STORE, KS, RT>(buf, athr_buf, p, t0, qwave, m16, g, a, qv);
       return;
     }
   }
@@ -623,7 +656,7 @@ __device__ __forceinline__ void compute_tile(const unsigned char* buf, const flo
     // Q_q of the four rows 4g..4g+3 of each row tile (this lane's accumulators)
     f32x4 qt[RT];
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) qt[rt] = *reinterpret_cast<const f32x4*>(qt_lds + rt * 16 + 4 * g);
+    for (int rt = 0; rt < RT; ++rt) qt[rt] = qv[rt];
     if constexpr (DUMP) {
       const int64_t e = ebase + m16;
 #pragma unroll
@@ -661,13 +694,12 @@ template <int MODE, int STORE, int KS, int RT, bool DUMP>
 __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupParams p) {
   using T = ModeTraits<MODE>;
   constexpr int kCPR = 4 * KS;
-  constexpr int kRows = DmaTraits<MODE>::kRows;
+  constexpr int kRows = DmaTraits<KS>::kRows;
   constexpr int kTileBytes = kRows * kCPR * 16;
   __shared__ __attribute__((aligned(16))) unsigned char buf0[kTileBytes];
   __shared__ __attribute__((aligned(16))) unsigned char buf1[kTileBytes];
-  __shared__ __attribute__((aligned(16))) float ath0[kWave];
-  __shared__ __attribute__((aligned(16))) float ath1[kWave];
-  __shared__ __attribute__((aligned(16))) float qts[kLkWaves * RT * 16];
+  __shared__ __attribute__((aligned(16))) float ath0[kRows];
+  __shared__ __attribute__((aligned(16))) float ath1[kRows];
 
   const int bid = static_cast<int>(blockIdx.x);
   const int xcd = bid % kXcds;
@@ -688,21 +720,31 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
 
   u32x4 a[RT][KS];
   load_query_operands<MODE, KS, RT>(p, qwave, m16, g, a);
-  float* qt_lds = qts + wave * (RT * 16);
-  for (int r = lane; r < RT * 16; r += kWave) qt_lds[r] = qwave + r < p.B ? p.qthr[qwave + r] : __builtin_inff();
+  // Q_q of this lane's accumulator rows 4g .. 4g + 3 of each row tile, kept
+  // in registers for the whole slice (reading them from LDS per column tile
+  // costs a third of the operand traffic); +inf past B.
+  f32x4 qv[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t q = qwave + rt * 16 + 4 * g + i;
+      qv[rt][i] = q < p.B ? p.qthr[q] : __builtin_inff();
+    }
+  }
 
   for (int64_t t0 = e_begin;; t0 += 2 * kRows) {
     wait_copies();
     __syncthreads();
     const bool more1 = t0 + kRows < e_end;
     if (more1) issue_tile<MODE, KS>(buf1, ath1, p, t0 + kRows, e_end, wave);
-    compute_tile<MODE, STORE, KS, RT, DUMP>(buf0, ath0, p, t0, e_end, qwave, m16, g, a, qt_lds);
+    compute_tile<MODE, STORE, KS, RT, DUMP>(buf0, ath0, p, t0, e_end, qwave, m16, g, a, qv);
     if (!more1) break;
     wait_copies();
     __syncthreads();
     const bool more2 = t0 + 2 * kRows < e_end;
     if (more2) issue_tile<MODE, KS>(buf0, ath0, p, t0 + 2 * kRows, e_end, wave);
-    compute_tile<MODE, STORE, KS, RT, DUMP>(buf1, ath1, p, t0 + kRows, e_end, qwave, m16, g, a, qt_lds);
+    compute_tile<MODE, STORE, KS, RT, DUMP>(buf1, ath1, p, t0 + kRows, e_end, qwave, m16, g, a, qv);
     if (!more2) break;
   }
 }
@@ -714,6 +756,7 @@ struct Plan {
   int d_pad = 0;
   int qblock = 0;
   bool dma = false;
+  int tile_rows = 0;  // cache rows per LDS tile of the chosen kernel
 };
 
 inline int rt_for(int ks) { return ks <= 8 ? 4 : (ks == 16 ? 2 : 1); }
@@ -732,6 +775,7 @@ inline bool make_plan(int precision, const lipcache_cache* c, Plan& pl) {
   const bool same_type = precision == LIPCACHE_BF16 ? (c->store_dtype == LIPCACHE_BF16 || c->zimg != nullptr)
                                                     : c->store_dtype == LIPCACHE_F32;
   pl.dma = same_type && ks <= 16;
+  pl.tile_rows = pl.dma ? (ks <= 8 ? 128 : 64) : kTileN;  // DmaTraits<KS>::kRows
   return true;
 }
 
@@ -788,7 +832,11 @@ struct Workspace {
   float* athr;
 };
 
-inline int64_t athr_len(int64_t n) { return ((n > 0 ? n : 0) + kTileN - 1) / kTileN * kTileN + kTileN; }
+// A_i padded with +inf so that any tile that starts below n reads thresholds
+// only from this array.
+inline int64_t athr_len(int64_t n) {
+  return ((n > 0 ? n : 0) + kDmaMaxRows - 1) / kDmaMaxRows * kDmaMaxRows + kDmaMaxRows;
+}
 
 inline size_t ws_layout(int64_t B, int64_t N, Workspace* w, void* base) {
   const size_t nb = static_cast<size_t>(B > 0 ? B : 0);
@@ -879,14 +927,14 @@ lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, 
     p.cand = cand;
     // Cache slices: a multiple of 8 (one set per XCD), enough blocks to fill
     // the chip (~1024), but at least 4 tiles per slice.
-    const int64_t tiles = (c->n + kTileN - 1) / kTileN;
+    const int64_t tiles = (c->n + pl.tile_rows - 1) / pl.tile_rows;
     int64_t s8 = (1024 + kXcds * p.n_qblocks - 1) / (kXcds * static_cast<int64_t>(p.n_qblocks));
     int64_t s8_max = tiles / (kXcds * 4);
     if (s8_max < 1) s8_max = 1;
     if (s8 > s8_max) s8 = s8_max;
     if (s8 < 1) s8 = 1;
     const int64_t slices = kXcds * s8;
-    p.slice_len = ((tiles + slices - 1) / slices) * kTileN;
+    p.slice_len = ((tiles + slices - 1) / slices) * pl.tile_rows;
     const int64_t grid = slices * p.n_qblocks;
     if (grid > INT_MAX) return LIPCACHE_EUNSUPPORTED;
     const hipError_t e = dump ? launch_lookup<true>(precision, c->store_dtype, pl, p, static_cast<unsigned>(grid), s)

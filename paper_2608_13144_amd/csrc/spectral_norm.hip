@@ -1,13 +1,19 @@
 // sigma_max(W) by float64 power iteration (Sec. 5.1, Eq. (18); Alg. 1).
 //
-// The head W is C x d.  The iteration v <- W^T W v / ||.|| is run on the
-// smaller Gram matrix G (W W^T when C <= d, else W^T W), which has the same
-// non-zero eigenvalues; sigma_max(W)^2 is G's largest eigenvalue.  One
-// kernel forms G in float64 (every product of two floats is exact in float64),
-// a second runs the whole iteration inside one 512-thread workgroup: the
-// iteration is a chain of dependent matrix-vector products, so it is bound by
-// latency.  G stays in registers (m <= 208) or L2 (m <= 1024), the iterate in
-// LDS, reductions use DPP lane exchanges, and each step has one barrier.
+// The head W is C x d.  The iteration runs on the smaller Gram matrix G
+// (W W^T when C <= d, else W^T W), which has the same non-zero eigenvalues;
+// sigma_max(W)^2 is G's largest eigenvalue.  G is formed in float64 (every
+// product of two floats is exact in float64).  Power iteration on G alone
+// converges like (lambda_2 / lambda_1)^k, about 400 dependent matrix-vector
+// products for the heads of interest (sigma_2 / sigma_1 ~ 0.98), each bound
+// by latency.  Instead G is scaled by a power of two and squared
+// kSquarings times on the whole chip (P = (G 2^-e)^64, a few parallel
+// products), power iteration runs on P, whose eigenvalue ratio is the 64th
+// power of G's (a dozen steps), and sigma_max^2 is the Rayleigh quotient of
+// G itself at P's converged vector.  The iteration runs inside one
+// 512-thread workgroup: the matrix stays in registers (m <= 208) or L2
+// (m <= 1024), the iterate in LDS, reductions use DPP lane exchanges, and
+// each step has one barrier.
 #include "lc_common.hpp"
 
 namespace lc {
@@ -17,7 +23,8 @@ constexpr int kPowWaves = kPowThreads / kWave;
 constexpr int kPowTPR = 2;                                  // threads per row of G
 constexpr int kPowRowsPerPass = kPowThreads / kPowTPR;      // 256
 constexpr int kPowMaxM = 1024;
-constexpr int kPowRegMaxM = 208;                            // G held in registers up to here
+constexpr int kPowRegMaxM = 208;                            // matrix held in registers up to here
+constexpr int kSquarings = 6;                               // P = (G 2^-e)^(2^6)
 
 // G[a][b] = sum over the long side of W of products of W's entries.
 __global__ void gram_kernel(const float* __restrict__ W, int C, int d, int side,
@@ -41,6 +48,39 @@ __global__ void gram_kernel(const float* __restrict__ W, int C, int d, int side,
   G[idx] = s;
 }
 
+// Out = A A for a symmetric m x m A (so row b of A is also its column b).
+// With SCALE, A is first multiplied by 2^-e, 2^e > trace(A) >= lambda_max,
+// so every eigenvalue of Out is at most 1 and 64th powers neither overflow
+// nor, for the top eigenvalue (>= trace / m), underflow.  A zero trace (a
+// zero head) gives Out = 0.
+template <bool SCALE>
+__global__ void gram_square_kernel(const double* __restrict__ A, int m, double* __restrict__ Out) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= static_cast<int64_t>(m) * m) return;
+  const int a = static_cast<int>(idx / m);
+  const int b = static_cast<int>(idx % m);
+  double scale = 1.0;
+  if constexpr (SCALE) {
+    double tr = 0.0;
+    for (int i = 0; i < m; ++i) tr += A[static_cast<int64_t>(i) * m + i];
+    if (!(tr > 0.0)) {
+      Out[idx] = 0.0;
+      return;
+    }
+    scale = ldexp(1.0, -(ilogb(tr) + 1));
+  }
+  const double* ra = A + static_cast<int64_t>(a) * m;
+  const double* rb = A + static_cast<int64_t>(b) * m;
+  double s0 = 0.0, s1 = 0.0;
+  int k = 0;
+  for (; k + 1 < m; k += 2) {
+    s0 = __builtin_fma(ra[k], rb[k], s0);
+    s1 = __builtin_fma(ra[k + 1], rb[k + 1], s1);
+  }
+  if (k < m) s0 = __builtin_fma(ra[k], rb[k], s0);
+  Out[idx] = (s0 + s1) * (scale * scale);
+}
+
 // Start vector: SplitMix64 of the component index mapped to [-1, 1).
 __device__ __forceinline__ double start_component(int i) {
   uint64_t x = (static_cast<uint64_t>(i) + 1u) * 0x9E3779B97F4A7C15ull;
@@ -50,26 +90,30 @@ __device__ __forceinline__ double start_component(int i) {
   return static_cast<double>(x >> 11) * (2.0 / 9007199254740992.0) - 1.0;
 }
 
-// out[0] = sigma, out[1] = iterations, out[2] = 1 if converged.
+// Power iteration on the symmetric m x m matrix M (a power of G), then
+// sigma = sqrt of G's Rayleigh quotient at the final vector.
+// out[0] = sigma, out[1] = iterations on M, out[2] = 1 if converged.
 //
-// Layout: two adjacent lanes share a row a of G (columns of one parity each),
+// Layout: two adjacent lanes share a row a of M (columns of one parity each),
 // rows a, a + 256, ... per lane pair.  With NC > 0 the lane keeps its NC
-// columns of G in registers (m <= 2 NC); with NC = 0 it re-reads them from
-// global memory every iteration.  G is first scaled by an exact power of two
-// 2^-e (so its largest eigenvalue is at most 1 and nothing overflows) and
-// sigma = sqrt(lambda 2^e).  The iterate x_k lives in LDS unnormalised
-// (x_{k+1} = G x_k); the normalisation 1/||G x_k|| is applied as a scalar
-// when x_{k+1} is read.  Each step therefore needs one barrier: it publishes
-// the new vector and the per-wave partial sums of x.w, x.x and w.w, which
-// give the Rayleigh quotient lambda_k = x_k.G x_k / x_k.x_k and the next
-// normalisation.
+// columns of M in registers (m <= 2 NC); with NC = 0 it re-reads them from
+// global memory every iteration.  M is first scaled by an exact power of two
+// (so its largest eigenvalue is at most 1).  The iterate x_k lives in LDS
+// unnormalised (x_{k+1} = M x_k); the normalisation 1/||M x_k|| is applied as
+// a scalar when x_{k+1} is read.  Each step therefore needs one barrier: it
+// publishes the new vector and the per-wave partial sums of x.w, x.x and w.w,
+// which give the Rayleigh quotient lambda_k = x_k.M x_k / x_k.x_k and the
+// next normalisation.  The iteration stops when lambda_k changes by at most
+// rel_tol relative on two consecutive steps.
 template <int NC>
-__global__ __launch_bounds__(kPowThreads) void power_kernel(const double* __restrict__ G, int m,
+__global__ __launch_bounds__(kPowThreads) void power_kernel(const double* __restrict__ G,
+                                                            const double* __restrict__ Gram, int m,
                                                             int max_iters, double rel_tol,
                                                             double* __restrict__ out) {
   __shared__ double xbuf[2][kPowMaxM];
   __shared__ double red[2][3][kPowWaves];
   __shared__ double tr_part[kPowWaves];
+  __shared__ double fin[2][kPowWaves];
 
   const int t = threadIdx.x;
   const int g = t / kPowTPR;
@@ -111,8 +155,8 @@ __global__ __launch_bounds__(kPowThreads) void power_kernel(const double* __rest
     }
   }
 
-  int cur = 0, stable = 0, it = 0, converged = 0;
-  double sigma = 0.0, prev = -1.0, invn = 1.0;
+  int cur = 0, stable = 0, it = 0, converged = 0, last = -1;
+  double prev = -1.0, invn = 1.0;
   for (it = 1; it <= max_iters; ++it) {
     const double* x = xbuf[cur];
     double lxw = 0.0, lxx = 0.0, lww = 0.0;
@@ -169,25 +213,65 @@ __global__ __launch_bounds__(kPowThreads) void power_kernel(const double* __rest
       XX += red[cur][1][w];
       WW += red[cur][2][w];
     }
-    if (!(WW > 0.0) || !(XX > 0.0)) {  // G x = 0
-      sigma = 0.0;
+    if (!(WW > 0.0) || !(XX > 0.0)) {  // M x = 0
+      last = -1;
       break;
     }
-    const double lam = XW / XX;  // Rayleigh quotient of the scaled G
-    const double sk = __builtin_sqrt(ldexp(lam > 0.0 ? lam : 0.0, e));
+    last = cur ^ 1;                // M x_k, the newest vector
+    const double lam = XW / XX;    // Rayleigh quotient of the scaled M
     invn = 1.0 / __builtin_sqrt(WW);
-    if (it > 1 && __builtin_fabs(sk - prev) <= rel_tol * sk) {
+    if (it > 1 && __builtin_fabs(lam - prev) <= rel_tol * lam) {
       ++stable;
     } else {
       stable = 0;
     }
-    prev = sk;
-    sigma = sk;
+    prev = lam;
     if (stable >= 2) {
       converged = 1;
       break;
     }
     cur ^= 1;
+  }
+
+  // sigma^2 = y.G y / y.y at the newest vector y (G unscaled, from memory).
+  double sigma = 0.0;
+  if (last >= 0) {
+    const double* y = xbuf[last];
+    double lyg = 0.0, lyy = 0.0;
+    for (int rr = 0; rr < passes; ++rr) {
+      const int a = g + kPowRowsPerPass * rr;
+      double acc0 = 0.0, acc1 = 0.0;
+      if (a < m) {
+        const double* ga = Gram + static_cast<int64_t>(a) * m;
+        int j = p;
+        for (; j + kPowTPR < m; j += 2 * kPowTPR) {
+          acc0 = __builtin_fma(ga[j], y[j], acc0);
+          acc1 = __builtin_fma(ga[j + kPowTPR], y[j + kPowTPR], acc1);
+        }
+        for (; j < m; j += kPowTPR) acc0 = __builtin_fma(ga[j], y[j], acc0);
+      }
+      double row = acc0 + acc1;
+      row += dpp_f64<kDppQuadXor1>(row);
+      if (p == 0 && a < m) {
+        lyg = __builtin_fma(y[a], row, lyg);
+        lyy = __builtin_fma(y[a], y[a], lyy);
+      }
+    }
+    lyg = wave_sum_dpp(lyg);
+    lyy = wave_sum_dpp(lyy);
+    if (lane == 0) {
+      fin[0][wave] = lyg;
+      fin[1][wave] = lyy;
+    }
+    __syncthreads();
+    double YG = 0.0, YY = 0.0;
+#pragma unroll
+    for (int w = 0; w < kPowWaves; ++w) {
+      YG += fin[0][w];
+      YY += fin[1][w];
+    }
+    const double rho = YY > 0.0 ? YG / YY : 0.0;
+    sigma = __builtin_sqrt(rho > 0.0 ? rho : 0.0);
   }
   if (t == 0) {
     out[0] = sigma;
@@ -203,7 +287,8 @@ using namespace lc;
 extern "C" size_t lipcache_spectral_norm_workspace_bytes(int32_t C, int32_t d) {
   if (C < 1 || d < 1) return 0;
   const int64_t m = C <= d ? C : d;
-  return align_up(static_cast<size_t>(m * m) * sizeof(double), 256) + 256;
+  // G and two buffers for the squarings, then the 3 result words
+  return 3 * align_up(static_cast<size_t>(m * m) * sizeof(double), 256) + 256;
 }
 
 extern "C" lipcache_status lipcache_spectral_norm(const float* W, int32_t C, int32_t d,
@@ -219,16 +304,27 @@ extern "C" lipcache_status lipcache_spectral_norm(const float* W, int32_t C, int
   const size_t need = lipcache_spectral_norm_workspace_bytes(C, d);
   if (!ws || ws_bytes < need || !aligned256(ws)) return LIPCACHE_EWORKSPACE;
 
+  const size_t mat = align_up(static_cast<size_t>(m) * m * sizeof(double), 256);
   double* G = static_cast<double*>(ws);
-  double* out = reinterpret_cast<double*>(static_cast<char*>(ws) +
-                                          align_up(static_cast<size_t>(m) * m * sizeof(double), 256));
+  double* P[2] = {reinterpret_cast<double*>(static_cast<char*>(ws) + mat),
+                  reinterpret_cast<double*>(static_cast<char*>(ws) + 2 * mat)};
+  double* out = reinterpret_cast<double*>(static_cast<char*>(ws) + 3 * mat);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int64_t cells = static_cast<int64_t>(m) * m;
-  hipLaunchKernelGGL(gram_kernel, dim3(static_cast<unsigned>((cells + 255) / 256)), dim3(256), 0, s,
-                     W, C, d, side, G);
+  const dim3 cgrid(static_cast<unsigned>((cells + 255) / 256));
+  hipLaunchKernelGGL(gram_kernel, cgrid, dim3(256), 0, s, W, C, d, side, G);
   LC_LAUNCHED();
+  hipLaunchKernelGGL(gram_square_kernel<true>, cgrid, dim3(256), 0, s, G, m, P[0]);
+  LC_LAUNCHED();
+  for (int i = 1; i < kSquarings; ++i) {
+    hipLaunchKernelGGL(gram_square_kernel<false>, cgrid, dim3(256), 0, s, P[(i + 1) & 1], m, P[i & 1]);
+    LC_LAUNCHED();
+  }
+  const double* M = P[(kSquarings + 1) & 1];
   const int nc = (m + kPowTPR - 1) / kPowTPR;
-  auto launch = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(1), dim3(kPowThreads), 0, s, G, m, max_iters, rel_tol, out); };
+  auto launch = [&](auto kern) {
+    hipLaunchKernelGGL(kern, dim3(1), dim3(kPowThreads), 0, s, M, G, m, max_iters, rel_tol, out);
+  };
   if (m > kPowRegMaxM) {
     launch(power_kernel<0>);
   } else if (nc <= 16) {

@@ -191,7 +191,9 @@ size_t lipcache_lookup_workspace_bytes(int64_t B, int64_t N, int32_t d, int32_t 
  * rows do not fit into capacity - n, returns ECAPACITY and appends nothing.
  *
  *  c              cache; c->n is advanced by the rows appended
- *  z_src [k][c->d] float, label_src [k] int32, r_src [k] float (required)
+ *  z_src [k][c->d] float, 16-byte aligned; label_src [k] int32,
+ *                 r_src [k] float (required); c->z must be 16-byte and
+ *                 c->zimg 8-byte aligned (rows move as 16-byte vectors)
  *  miss_selector  [k] int32 or NULL (e.g. lipcache_lookup's label_out)
  *  inserted       (host, nullable) out: rows appended
  *  ws             lipcache_insert_workspace_bytes(k) bytes

@@ -2,14 +2,16 @@
 // construction, Alg. 1).
 //
 // Rows are taken in ascending order (a stable compaction), so the same input
-// always produces the same cache rows.  Three kernels:
+// always produces the same cache rows.  Four kernels:
 //   count   - per 1024-row block, how many rows are selected;
 //   scan    - one workgroup turns the block counts into block offsets and the
 //             total (read back by the host for the all-or-nothing capacity
 //             check: nothing is written to the cache before it passes);
-//   scatter - each block ranks its selected rows with wave ballots and copies
-//             them, one wave per row (coalesced), casting to the store dtype
-//             and recomputing ||z||^2 of the stored values in float64.
+//   rank    - each block ranks its selected rows with wave ballots and writes
+//             the source row of every destination row;
+//   copy    - one wave per destination row over the whole chip, 16-byte
+//             loads and stores, casting to the store dtype and recomputing
+//             ||z||^2 of the stored values in float64.
 #include "lc_common.hpp"
 
 namespace lc {
@@ -56,13 +58,31 @@ __global__ __launch_bounds__(kInsBlock) void insert_scan_kernel(const int64_t* _
   if (threadIdx.x == 0) *total = running;
 }
 
+// src_of[offsets[block] + t] = the t-th selected row of the block.
+__global__ __launch_bounds__(kInsBlock) void insert_rank_kernel(const float* __restrict__ r_src,
+                                                                const int32_t* __restrict__ sel, int64_t k,
+                                                                const int64_t* __restrict__ offsets,
+                                                                int64_t* __restrict__ src_of) {
+  __shared__ int wave_count[kInsWaves];
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * kInsBlock + threadIdx.x;
+  const bool take = selected(j, k, r_src, sel);
+  const int lane = lane_id();
+  const int wave = static_cast<int>(threadIdx.x) / kWave;
+  const unsigned long long bal = __ballot(take);
+  const int below = __builtin_popcountll(bal & ((1ull << lane) - 1ull));
+  if (lane == 0) wave_count[wave] = __builtin_popcountll(bal);
+  __syncthreads();
+  int before = 0;
+  for (int w = 0; w < wave; ++w) before += wave_count[w];
+  if (take) src_of[offsets[blockIdx.x] + before + below] = j;
+}
+
 struct InsertParams {
   const float* z_src;
   const int32_t* label_src;
   const float* r_src;
-  const int32_t* sel;
-  int64_t k;
-  const int64_t* offsets;
+  const int64_t* src_of;
+  int64_t count;
   void* cz;
   uint16_t* cimg;
   float* cr;
@@ -73,55 +93,45 @@ struct InsertParams {
   int store;
 };
 
-__global__ __launch_bounds__(kInsBlock) void insert_scatter_kernel(const InsertParams p) {
-  __shared__ int wave_count[kInsWaves];
-  __shared__ int src_local[kInsBlock];
-  const int64_t j = static_cast<int64_t>(blockIdx.x) * kInsBlock + threadIdx.x;
-  const bool take = selected(j, p.k, p.r_src, p.sel);
-  const int lane = lane_id();
-  const int wave = static_cast<int>(threadIdx.x) / kWave;
-  const unsigned long long bal = __ballot(take);
-  const int below = __builtin_popcountll(bal & ((1ull << lane) - 1ull));
-  if (lane == 0) wave_count[wave] = __builtin_popcountll(bal);
-  __syncthreads();
-  int before = 0, total = 0;
-  for (int w = 0; w < kInsWaves; ++w) {
-    before += w < wave ? wave_count[w] : 0;
-    total += wave_count[w];
-  }
-  if (take) src_local[before + below] = static_cast<int>(threadIdx.x);
-  __syncthreads();
+constexpr int kCopyThreads = 256;
+constexpr int kCopyWaves = kCopyThreads / kWave;
 
-  const int64_t dst0 = p.n0 + p.offsets[blockIdx.x];
-  for (int t = wave; t < total; t += kInsWaves) {
-    const int64_t src = static_cast<int64_t>(blockIdx.x) * kInsBlock + src_local[t];
-    const int64_t dst = dst0 + t;
-    const float* zr = p.z_src + src * p.d;
-    double s = 0.0;
+// One wave per destination row t: lane l moves elements 4 l .. 4 l + 3 of
+// each 256-element stretch of the row.
+__global__ __launch_bounds__(kCopyThreads) void insert_copy_kernel(const InsertParams p) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * kCopyWaves + threadIdx.x / kWave;
+  if (t >= p.count) return;
+  const int lane = lane_id();
+  const int64_t src = p.src_of[t];
+  const int64_t dst = p.n0 + t;
+  const float* zr = p.z_src + src * p.d;
+  double s = 0.0;
+  for (int k = 4 * lane; k < p.d; k += 4 * kWave) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(zr + k);
+    uint16_t h[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) h[i] = bf16_bits(v[i]);
+    const uint2 packed = {static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16),
+                          static_cast<uint32_t>(h[2]) | (static_cast<uint32_t>(h[3]) << 16)};
     if (p.store == LIPCACHE_BF16) {
-      uint16_t* out = static_cast<uint16_t*>(p.cz) + dst * p.d;
-      for (int k = lane; k < p.d; k += kWave) {
-        const uint16_t h = bf16_bits(zr[k]);
-        out[k] = h;
-        const double v = static_cast<double>(bf16_to_f32(h));
-        s = __builtin_fma(v, v, s);
+      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.cz) + dst * p.d + k) = packed;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const double x = static_cast<double>(bf16_to_f32(h[i]));
+        s = __builtin_fma(x, x, s);
       }
     } else {
-      float* out = static_cast<float*>(p.cz) + dst * p.d;
-      uint16_t* img = p.cimg ? p.cimg + dst * p.d : nullptr;
-      for (int k = lane; k < p.d; k += kWave) {
-        const float f = zr[k];
-        out[k] = f;
-        if (img) img[k] = bf16_bits(f);
-        s = __builtin_fma(static_cast<double>(f), static_cast<double>(f), s);
-      }
+      *reinterpret_cast<f32x4*>(static_cast<float*>(p.cz) + dst * p.d + k) = v;
+      if (p.cimg) *reinterpret_cast<uint2*>(p.cimg + dst * p.d + k) = packed;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s = __builtin_fma(static_cast<double>(v[i]), static_cast<double>(v[i]), s);
     }
-    s = wave_sum(s);
-    if (lane == 0) {
-      p.cnorm2[dst] = static_cast<float>(s);
-      p.cr[dst] = p.r_src[src];
-      p.clabel[dst] = p.label_src[src];
-    }
+  }
+  s = wave_sum(s);
+  if (lane == 0) {
+    p.cnorm2[dst] = static_cast<float>(s);
+    p.cr[dst] = p.r_src[src];
+    p.clabel[dst] = p.label_src[src];
   }
 }
 
@@ -131,7 +141,8 @@ using namespace lc;
 
 extern "C" size_t lipcache_insert_workspace_bytes(int64_t k) {
   const int64_t nb = k > 0 ? (k + kInsBlock - 1) / kInsBlock : 1;
-  return 2 * align_up(static_cast<size_t>(nb) * sizeof(int64_t), 256) + 256;
+  return 2 * align_up(static_cast<size_t>(nb) * sizeof(int64_t), 256) + 256 +
+         align_up(static_cast<size_t>(k > 0 ? k : 1) * sizeof(int64_t), 256);
 }
 
 extern "C" lipcache_status lipcache_insert(lipcache_cache* c, const float* z_src, const int32_t* label_src,
@@ -145,6 +156,11 @@ extern "C" lipcache_status lipcache_insert(lipcache_cache* c, const float* z_src
   if (c->capacity > 0 && (!c->z || !c->r || !c->label || !c->norm2)) return LIPCACHE_EINVAL;
   if (k > 0 && (!z_src || !label_src || !r_src)) return LIPCACHE_EINVAL;
   if (k > (static_cast<int64_t>(1) << 40)) return LIPCACHE_EINVAL;
+  // rows move as 16-byte vectors
+  if (k > 0 && (reinterpret_cast<uintptr_t>(z_src) & 15u) != 0) return LIPCACHE_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(c->z) & 15u) != 0 || (reinterpret_cast<uintptr_t>(c->zimg) & 7u) != 0)
+    return LIPCACHE_EINVAL;
+  if ((k + kCopyWaves - 1) / kCopyWaves > static_cast<int64_t>(UINT32_MAX)) return LIPCACHE_EUNSUPPORTED;
   const size_t need = lipcache_insert_workspace_bytes(k);
   if (!ws || ws_bytes < need || !aligned256(ws)) return LIPCACHE_EWORKSPACE;
   if (inserted) *inserted = 0;
@@ -156,6 +172,7 @@ extern "C" lipcache_status lipcache_insert(lipcache_cache* c, const float* z_src
   int64_t* counts = reinterpret_cast<int64_t*>(base);
   int64_t* offsets = reinterpret_cast<int64_t*>(base + align_up(static_cast<size_t>(nb) * 8, 256));
   int64_t* total = reinterpret_cast<int64_t*>(base + 2 * align_up(static_cast<size_t>(nb) * 8, 256));
+  int64_t* src_of = reinterpret_cast<int64_t*>(base + 2 * align_up(static_cast<size_t>(nb) * 8, 256) + 256);
 
   hipLaunchKernelGGL(insert_count_kernel, dim3(static_cast<unsigned>(nb)), dim3(kInsBlock), 0, s, r_src,
                      miss_selector, k, counts);
@@ -169,13 +186,15 @@ extern "C" lipcache_status lipcache_insert(lipcache_cache* c, const float* z_src
   if (c->n + host_total > c->capacity) return LIPCACHE_ECAPACITY;
   if (host_total == 0) return LIPCACHE_OK;
 
+  hipLaunchKernelGGL(insert_rank_kernel, dim3(static_cast<unsigned>(nb)), dim3(kInsBlock), 0, s, r_src,
+                     miss_selector, k, offsets, src_of);
+  LC_LAUNCHED();
   InsertParams p;
   p.z_src = z_src;
   p.label_src = label_src;
   p.r_src = r_src;
-  p.sel = miss_selector;
-  p.k = k;
-  p.offsets = offsets;
+  p.src_of = src_of;
+  p.count = host_total;
   p.cz = c->z;
   p.cimg = c->store_dtype == LIPCACHE_F32 ? static_cast<uint16_t*>(c->zimg) : nullptr;
   p.cr = c->r;
@@ -184,7 +203,8 @@ extern "C" lipcache_status lipcache_insert(lipcache_cache* c, const float* z_src
   p.n0 = c->n;
   p.d = c->d;
   p.store = c->store_dtype;
-  hipLaunchKernelGGL(insert_scatter_kernel, dim3(static_cast<unsigned>(nb)), dim3(kInsBlock), 0, s, p);
+  hipLaunchKernelGGL(insert_copy_kernel, dim3(static_cast<unsigned>((host_total + kCopyWaves - 1) / kCopyWaves)),
+                     dim3(kCopyThreads), 0, s, p);
   LC_LAUNCHED();
   c->n += host_total;
   if (inserted) *inserted = host_total;

@@ -131,6 +131,7 @@ def test_insert_validation():
     assert call(_cache(), k=-1)[0] == L.EINVAL
     assert call(_cache(d=40))[0] == L.EINVAL
     assert call(_cache(), z=None)[0] == L.EINVAL
+    assert call(_cache(), z=ctypes.c_void_p(0x100008))[0] == L.EINVAL   # rows move as 16-byte vectors
     assert call(_cache(), r=None)[0] == L.EINVAL
     assert call(_cache(n=-1))[0] == L.EINVAL
     assert call(_cache(), ws=None)[0] == L.EWORKSPACE

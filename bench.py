@@ -39,7 +39,13 @@ def log(*a):
 
 
 def cpu_baseline(wl, zq_host, target_s: float):
-    """The CPU oracle (as it is) on a bounded sample of the same lookup."""
+    """The CPU oracle on a bounded sample of the same lookup.
+
+    Main figure: ``oracle.lookup_blocked`` (float32 BLAS prefilter with a
+    rigorous slack, float64 distances for the survivors; bit-identical to the
+    plain definition) on every core the BLAS library uses.  Secondary: the
+    plain definition ``oracle.lookup`` (float64 numpy, one thread).
+    """
     import numpy as np
 
     import oracle
@@ -50,19 +56,43 @@ def cpu_baseline(wl, zq_host, target_s: float):
     Z, R, Lb = cert.stored[keep], cert.r[keep], cert.label[keep]
     t_cert = time.perf_counter() - t0
     log(f"cpu oracle: certify of {wl.z.shape[0]} candidates in {t_cert:.1f} s")
-    t0 = time.perf_counter()
-    oracle.lookup_rows(zq_host, Z, R, Lb, [0])
-    t1 = time.perf_counter() - t0
-    m = int(max(1, min(256, target_s / max(t1, 1e-6))))
-    rows = np.linspace(0, zq_host.shape[0] - 1, m).astype(np.int64)
-    t0 = time.perf_counter()
-    oracle.lookup_rows(zq_host, Z, R, Lb, rows)
-    t = time.perf_counter() - t0
-    log(f"cpu oracle: {m} lookups in {t:.1f} s")
-    return {"value": m / t, "unit": "lookups/s", "cores": 1, "kind": "oracle",
-            "sample": f"{m} queries of the batch, each against all {Z.shape[0]} entries "
-                      f"(float64 numpy, single thread); pairs/s = {m * Z.shape[0] / t:.3e}",
-            "seconds": t, "cpu_model": _cpu_model(), "certify_seconds": t_cert}
+    threads, blas = _blas_threads()
+
+    def timed(fn, m, budget):
+        rows = np.linspace(0, zq_host.shape[0] - 1, m).astype(np.int64)
+        t0 = time.perf_counter()
+        fn(zq_host[rows], Z, R, Lb)
+        return time.perf_counter() - t0
+
+    # blocked oracle: grow the sample until it takes a good share of the budget
+    m, t = 64, 0.0
+    while True:
+        t = timed(oracle.lookup_blocked, m, target_s)
+        if t > 0.4 * target_s or m >= zq_host.shape[0]:
+            break
+        m = int(min(zq_host.shape[0], max(2 * m, m * 0.6 * target_s / max(t, 1e-3))))
+    log(f"cpu oracle (blocked, {threads} BLAS threads): {m} lookups in {t:.1f} s")
+    t1 = timed(oracle.lookup, 1, 0)
+    m1 = int(max(1, min(64, 0.25 * target_s / max(t1, 1e-6))))
+    tp = timed(oracle.lookup, m1, 0)
+    log(f"cpu oracle (plain definition, one thread): {m1} lookups in {tp:.1f} s")
+    return {"value": m / t, "unit": "lookups/s", "cores": threads, "kind": "oracle",
+            "sample": f"{m} queries of the batch, each against all {Z.shape[0]} entries with oracle.lookup_blocked "
+                      f"({blas}, {threads} threads); pairs/s = {m * Z.shape[0] / t:.3e}",
+            "seconds": t, "cpu_model": _cpu_model(), "certify_seconds": t_cert,
+            "plain_definition": {"value": m1 / tp, "unit": "lookups/s", "cores": 1, "queries": m1,
+                                 "seconds": tp, "function": "oracle.lookup (float64 numpy)"}}
+
+
+def _blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if info:
+            return int(info[0]["num_threads"]), f"{info[0]['internal_api']} {info[0].get('version', '')}".strip()
+    except Exception:
+        pass
+    return len(os.sched_getaffinity(0)), "blas"
 
 
 def measured_traffic(workload: str, precision: str):
@@ -267,19 +297,25 @@ def main() -> int:
                            torch.empty(B, dtype=torch.float32, device=dev),
                            torch.zeros(4, dtype=torch.int64, device=dev),
                            torch.empty(B, dtype=torch.uint8, device=dev))
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
+    # events per step: 0 before sigma, 1 before lookup, 2 after lookup, 3 after certify, 4 after insert
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     inserted = []
 
     def step(i: int | None):
-        s = api.spectral_norm(W).sigma
         if i is not None:
             ev[i][0].record()
-        cache.lookup(zq, precision=args.precision, out=res)
+        s = api.spectral_norm(W).sigma
         if i is not None:
             ev[i][1].record()
+        cache.lookup(zq, precision=args.precision, out=res)
+        if i is not None:
+            ev[i][2].record()
         cq = api.certify(zq, W, b, s, store=cfg.store_dtype)
+        if i is not None:
+            ev[i][3].record()
         inserted.append(cache.insert(zq, cq.label, cq.r, res.label))
+        if i is not None:
+            ev[i][4].record()
         cache.n = n0
 
     for _ in range(args.warmup):
@@ -290,8 +326,13 @@ def main() -> int:
         step(i)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    lk_ms = [a.elapsed_time(bb) for a, bb in ev]
+    parts = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(4)] for e in ev])
+    lk_ms = parts[:, 1].tolist()
     lk = sum(lk_ms) / len(lk_ms)
+    comp = {"spectral_norm_ms": float(parts[:, 0].mean()), "lookup_ms": lk,
+            "lookup_median_ms": float(np.median(parts[:, 1])), "certify_batch_ms": float(parts[:, 2].mean()),
+            "insert_ms": float(parts[:, 3].mean())}
+    log("per step: " + ", ".join(f"{k} {v:.3f}" for k, v in comp.items()))
     stats = res.stats.cpu().tolist()
     hits = int(stats[0])
     log(f"{args.steps} steps in {elapsed:.3f} s; lookup {lk:.3f} ms avg (min {min(lk_ms):.3f}); "
@@ -317,6 +358,7 @@ def main() -> int:
                    "precision": args.precision, "step": "spectral_norm+lookup+certify(B)+insert(misses)"},
         "pairs_per_s": B * n0 * args.steps / elapsed,
         "lookup_ms": lk,
+        "components_ms": comp,
         "lookup_lookups_per_s": B / (lk * 1e-3),
         "lookup_pairs_per_s": B * n0 / (lk * 1e-3),
         "hit_rate": hits / B,

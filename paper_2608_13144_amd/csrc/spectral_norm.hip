@@ -48,27 +48,33 @@ __global__ void gram_kernel(const float* __restrict__ W, int C, int d, int side,
   G[idx] = s;
 }
 
-// Out = A A for a symmetric m x m A (so row b of A is also its column b).
-// With SCALE, A is first multiplied by 2^-e, 2^e > trace(A) >= lambda_max,
-// so every eigenvalue of Out is at most 1 and 64th powers neither overflow
-// nor, for the top eigenvalue (>= trace / m), underflow.  A zero trace (a
-// zero head) gives Out = 0.
-template <bool SCALE>
-__global__ void gram_square_kernel(const double* __restrict__ A, int m, double* __restrict__ Out) {
+// scale[0] = 2^-e with 2^e > trace(A) >= lambda_max (0 for a zero trace):
+// after this scaling every eigenvalue is at most 1, so 64th powers neither
+// overflow nor, for the top eigenvalue (>= trace / m), underflow.
+__global__ __launch_bounds__(256) void gram_scale_kernel(const double* __restrict__ A, int m,
+                                                         double* __restrict__ scale) {
+  __shared__ double part[256 / kWave];
+  double tr = 0.0;
+  for (int i = threadIdx.x; i < m; i += 256) tr += A[static_cast<int64_t>(i) * m + i];
+  tr = wave_sum_dpp(tr);
+  if (lane_id() == 0) part[threadIdx.x / kWave] = tr;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double t = 0.0;
+    for (int w = 0; w < 256 / kWave; ++w) t += part[w];
+    scale[0] = t > 0.0 ? ldexp(1.0, -(ilogb(t) + 1)) : 0.0;
+  }
+}
+
+// Out = (s A)(s A) for a symmetric m x m A (so row b of A is also its
+// column b), s = scale[0] when given, else 1.
+__global__ void gram_square_kernel(const double* __restrict__ A, int m, const double* __restrict__ scale,
+                                   double* __restrict__ Out) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (idx >= static_cast<int64_t>(m) * m) return;
   const int a = static_cast<int>(idx / m);
   const int b = static_cast<int>(idx % m);
-  double scale = 1.0;
-  if constexpr (SCALE) {
-    double tr = 0.0;
-    for (int i = 0; i < m; ++i) tr += A[static_cast<int64_t>(i) * m + i];
-    if (!(tr > 0.0)) {
-      Out[idx] = 0.0;
-      return;
-    }
-    scale = ldexp(1.0, -(ilogb(tr) + 1));
-  }
+  const double sc = scale ? scale[0] : 1.0;
   const double* ra = A + static_cast<int64_t>(a) * m;
   const double* rb = A + static_cast<int64_t>(b) * m;
   double s0 = 0.0, s1 = 0.0;
@@ -78,7 +84,7 @@ __global__ void gram_square_kernel(const double* __restrict__ A, int m, double* 
     s1 = __builtin_fma(ra[k + 1], rb[k + 1], s1);
   }
   if (k < m) s0 = __builtin_fma(ra[k], rb[k], s0);
-  Out[idx] = (s0 + s1) * (scale * scale);
+  Out[idx] = (s0 + s1) * (sc * sc);
 }
 
 // Start vector: SplitMix64 of the component index mapped to [-1, 1).
@@ -314,10 +320,13 @@ extern "C" lipcache_status lipcache_spectral_norm(const float* W, int32_t C, int
   const dim3 cgrid(static_cast<unsigned>((cells + 255) / 256));
   hipLaunchKernelGGL(gram_kernel, cgrid, dim3(256), 0, s, W, C, d, side, G);
   LC_LAUNCHED();
-  hipLaunchKernelGGL(gram_square_kernel<true>, cgrid, dim3(256), 0, s, G, m, P[0]);
+  double* scale = out + 4;
+  hipLaunchKernelGGL(gram_scale_kernel, dim3(1), dim3(256), 0, s, G, m, scale);
+  LC_LAUNCHED();
+  hipLaunchKernelGGL(gram_square_kernel, cgrid, dim3(256), 0, s, G, m, scale, P[0]);
   LC_LAUNCHED();
   for (int i = 1; i < kSquarings; ++i) {
-    hipLaunchKernelGGL(gram_square_kernel<false>, cgrid, dim3(256), 0, s, P[(i + 1) & 1], m, P[i & 1]);
+    hipLaunchKernelGGL(gram_square_kernel, cgrid, dim3(256), 0, s, P[(i + 1) & 1], m, nullptr, P[i & 1]);
     LC_LAUNCHED();
   }
   const double* M = P[(kSquarings + 1) & 1];

@@ -276,6 +276,16 @@ def test_lookup_hand_cases(precision):
     res2 = c2.lookup(gpu(q), precision=precision)
     assert host(res2.label).tolist() == [6, -1, 6]
     assert host(res2.index).tolist() == [2, -1, 2]
+    # a non-finite entry is never hit, and does not disturb its neighbours
+    z3 = np.stack([e1, 0.9 * e1, 2.0 * e1]).astype(np.float32)
+    z3[0, 5] = np.nan
+    z3[2, 7] = np.inf
+    st3 = oracle.CacheState(d=32, capacity=4)
+    oracle.insert(st3, z3, np.array([1, 2, 3], np.int32), np.array([5, 1, 5], np.float32))
+    c3 = build_cache(st3)
+    res3 = c3.lookup(gpu(np.stack([e1, 1.5 * e1]).astype(np.float32)), precision=precision)
+    assert host(res3.index).tolist() == [1, 1]
+    assert host(res3.label).tolist() == [2, 2]
 
 
 @pytest.mark.parametrize("precision", ["bf16", "f32"])

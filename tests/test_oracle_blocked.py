@@ -71,6 +71,23 @@ def test_blocked_equals_definition_on_tiny_workload():
     assert 0.15 < (a.index >= 0).mean() < 0.4
 
 
+@pytest.mark.parametrize("name", ["mix-d128-c10", "mix-d128-c100", "mix-d256-c200", "stream-d256-c200-bf16"])
+def test_blocked_equals_definition_on_workload_sub_blocks(name):
+    cfg = wlmod.CONFIGS[name]
+    wl = wlmod.make_workload(cfg, seed=0, n_cache=3000)
+    sig = oracle.spectral_norm(wl.W).sigma
+    cert = oracle.certify(wl.z, wl.W, wl.b, sig, store=cfg.store_dtype)
+    st = oracle.CacheState(d=cfg.d, capacity=3000, store=cfg.store_dtype)
+    oracle.insert(st, wl.z, cert.label, cert.r)
+    draws = wlmod.draw_queries(wl, 0, batch=160)
+    idx = wlmod.near_indices(draws, st.n)
+    zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
+    a = oracle.lookup(zq, st.z, st.r, st.label)
+    b = oracle.lookup_blocked(zq, st.z, st.r, st.label, q_chunk=48, n_chunk=700)
+    assert same(a, b)
+    assert (a.index >= 0).sum() > 20
+
+
 def test_blocked_empty_inputs():
     z = np.zeros((0, 32), np.float32)
     q = np.ones((3, 32), np.float32)

@@ -24,6 +24,10 @@ bfloat16 cache), with float64 as the stand-in for exact arithmetic:
                          the survivors (for large test batches); pinned
                          bit-for-bit against ``lookup``.
   * ``insert``         - write-back of missed samples (Sec. 4.4, Alg. 2).
+  * ``construct``      - offline construction of the feature store (Sec. 4.3,
+                         Alg. 1): eligibility, budgets and the selection
+                         strategies (radius-prioritised de-duplication,
+                         caller priority / random, K-center).
   * ``bf16_round``     - round-to-nearest-even float32 -> bfloat16 (storage).
 
 Pins: every function is checked in ``tests/`` against closed forms, brute
@@ -432,3 +436,109 @@ def insert(state: CacheState, z_src, label_src, r_src, selector=None) -> int:
     state.label = np.concatenate([state.label, ls[idx]])
     state.norm2 = np.concatenate([state.norm2, np.sum(stored.astype(np.float64) ** 2, axis=1)])
     return int(idx.size)
+
+
+# ------------------------------------------------------------ construction
+SELECT_STRATEGIES = ("radius_dedup", "priority", "kcenter")
+
+
+def construct(state: CacheState, z, label, r, strategy: str = "radius_dedup", budget_total=None,
+              budget_per_class: int = 0, priority=None, guard_label=None) -> np.ndarray:
+    """Offline construction of the feature store (Alg. 1): select and append.
+
+    Eligible candidates have r_i > 0 and, when ``guard_label`` is given (the
+    cache-centre label-consistency flag of Alg. 1), guard_label_i == label_i.
+    At most ``budget_total`` entries are appended (default: the free
+    capacity; more than the free capacity raises CapacityError) and, when
+    ``budget_per_class`` > 0, at most that many per payload label.  Distances
+    are float64 over the stored values (bfloat16-rounded for a bf16 store).
+
+    * ``radius_dedup`` - visit eligible candidates by decreasing r (ties:
+      lower index); skip one whose class is full; skip a duplicate, i.e. a
+      candidate strictly inside the ball ||z_i - z_j|| < r_j of an entry
+      already in the cache (present before the call or appended earlier);
+      append the rest until the total budget is used.
+    * ``priority`` - the same visit, by decreasing ``priority`` (e.g. random
+      keys: the random strategy), without the duplicate test.
+    * ``kcenter`` - farthest-first traversal: start at the eligible candidate
+      of largest r (ties: lower index), then repeatedly append the eligible,
+      not yet chosen candidate (of a class that is not full) whose distance to
+      the nearest chosen candidate is largest (ties: lower index).  With a
+      per-class budget each class is traversed on its own (distances to its
+      own chosen candidates), classes in ascending label order.  Entries
+      present before the call are not used.
+
+    Returns the selected candidate indices in the order they were appended.
+    """
+    if strategy not in SELECT_STRATEGIES:
+        raise ValueError(f"unknown strategy {strategy!r}")
+    zs = stored_values(np.asarray(z, dtype=np.float32), state.store)
+    lab = np.asarray(label, dtype=np.int32)
+    rr = np.asarray(r, dtype=np.float32)
+    n = zs.shape[0]
+    free = state.capacity - state.n
+    budget = free if budget_total is None else int(budget_total)
+    if budget < 0 or budget > free:
+        raise CapacityError(f"budget {budget} exceeds the free capacity {free}")
+    eligible = rr > 0
+    if guard_label is not None:
+        eligible &= np.asarray(guard_label, dtype=np.int32) == lab
+    counts: dict[int, int] = {}
+
+    def class_open(c: int) -> bool:
+        return budget_per_class <= 0 or counts.get(c, 0) < budget_per_class
+
+    chosen: list[int] = []
+    if strategy in ("radius_dedup", "priority"):
+        key = rr if strategy == "radius_dedup" else np.asarray(priority, dtype=np.float32)
+        idx = np.flatnonzero(eligible)
+        order = idx[np.lexsort((idx, -key[idx].astype(np.float64)))]
+        cz = state.z.astype(np.float64)
+        cr2 = state.r.astype(np.float64) ** 2
+        clive = state.r > 0
+        for i in order:
+            if len(chosen) >= budget:
+                break
+            c = int(lab[i])
+            if not class_open(c):
+                continue
+            if strategy == "radius_dedup" and cz.shape[0]:
+                d2 = np.sum((cz - zs[i].astype(np.float64)) ** 2, axis=1)
+                if np.any(clive & (d2 < cr2)):
+                    continue
+            chosen.append(int(i))
+            counts[c] = counts.get(c, 0) + 1
+            if strategy == "radius_dedup":
+                cz = np.concatenate([cz, zs[i:i + 1].astype(np.float64)])
+                cr2 = np.concatenate([cr2, [float(rr[i]) ** 2]])
+                clive = np.concatenate([clive, [True]])
+    else:
+        groups = [np.flatnonzero(eligible)]
+        if budget_per_class > 0:
+            groups = [np.flatnonzero(eligible & (lab == c)) for c in np.unique(lab[eligible])]
+        for g in groups:
+            if len(chosen) >= budget or g.size == 0:
+                continue
+            first = g[np.lexsort((g, -rr[g].astype(np.float64)))[0]]
+            picked = [int(first)]
+            mind = np.sum((zs[g].astype(np.float64) - zs[first].astype(np.float64)) ** 2, axis=1)
+            taken = np.zeros(g.size, dtype=bool)
+            taken[np.flatnonzero(g == first)[0]] = True
+            limit = budget - len(chosen)
+            if budget_per_class > 0:
+                limit = min(limit, budget_per_class)
+            while len(picked) < limit and not taken.all():
+                cand = np.where(taken, -1.0, mind)
+                j = int(np.flatnonzero(cand == cand.max())[0])   # lowest index among the farthest
+                picked.append(int(g[j]))
+                taken[j] = True
+                mind = np.minimum(mind, np.sum((zs[g].astype(np.float64) - zs[g[j]].astype(np.float64)) ** 2,
+                                               axis=1))
+            chosen.extend(picked)
+    sel = np.asarray(chosen, dtype=np.int64)
+    if sel.size:
+        state.z = np.concatenate([state.z, zs[sel]], axis=0)
+        state.r = np.concatenate([state.r, rr[sel]])
+        state.label = np.concatenate([state.label, lab[sel]])
+        state.norm2 = np.concatenate([state.norm2, np.sum(zs[sel].astype(np.float64) ** 2, axis=1)])
+    return sel

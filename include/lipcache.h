@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define LIPCACHE_ABI_VERSION 2
+#define LIPCACHE_ABI_VERSION 3
 
 /* Same type as hipStream_t. */
 typedef struct ihipStream_t* lipcache_stream_t;
@@ -59,6 +59,13 @@ enum { LIPCACHE_F32 = 0, LIPCACHE_BF16 = 1 };
 /* Radius modes (policy component rho, Sec. 4.3): the conservative radius of
  * Eq. (21) or the tight per-pair radius of Remark 5.1, Eq. (29). */
 enum { LIPCACHE_RADIUS_CONSERVATIVE = 0 /* Eq. (21) */, LIPCACHE_RADIUS_TIGHT = 1 /* Remark 5.1 */ };
+
+/* Cache selection strategies S of the offline construction (Alg. 1). */
+enum {
+  LIPCACHE_SELECT_RADIUS_DEDUP = 0, /* by decreasing radius, skipping duplicates  */
+  LIPCACHE_SELECT_PRIORITY = 1,     /* by decreasing caller priority (random keys) */
+  LIPCACHE_SELECT_KCENTER = 2       /* farthest-first traversal                   */
+};
 
 /* Label written for a query whose hit set is empty (falls back to MainNet,
  * Eq. (15)). */
@@ -205,6 +212,53 @@ lipcache_status lipcache_insert(lipcache_cache* c, const float* z_src,
                                 int64_t* inserted, void* ws, size_t ws_bytes,
                                 lipcache_stream_t stream);
 size_t lipcache_insert_workspace_bytes(int64_t k);
+
+/*
+ * Offline construction of the feature store (Sec. 4.3, Alg. 1): select at
+ * most `budget` of N candidates (z_i, label_i, r_i) and append them to the
+ * cache.  r_i and label_i normally come from lipcache_certify (payload =
+ * proxy label) or carry another payload source.  A candidate is eligible
+ * when r_i > 0, guard_label_i == label_i if guard_label is given (the
+ * cache-centre label-consistency flag), its priority is not NaN, and, with
+ * a per-class budget, 0 <= label_i < n_classes.  Distances are exact
+ * (float64) over the stored values (bf16-rounded for a bf16 store).
+ *
+ *  strategy LIPCACHE_SELECT_RADIUS_DEDUP: visit eligible candidates by
+ *           decreasing r_i (ties: lower index); skip one whose class already
+ *           holds per_class entries; skip a duplicate - a candidate strictly
+ *           inside the ball ||z_i - z_j|| < r_j of an entry already in the
+ *           cache (present before the call or appended earlier in it);
+ *           append the rest in visit order until `budget` are appended.
+ *           LIPCACHE_SELECT_PRIORITY: the same visit by decreasing
+ *           priority_i, with no duplicate test (random keys give the random
+ *           strategy; the caller draws them).
+ *           LIPCACHE_SELECT_KCENTER: farthest-first traversal - start at the
+ *           largest-radius eligible candidate (ties: lower index), then
+ *           repeatedly append the candidate whose squared distance to the
+ *           nearest chosen one is largest (ties: lower index).  With a
+ *           per-class budget each class 0 .. n_classes-1 is traversed on its
+ *           own, in that order; entries present before the call are not used.
+ *  z [N][c->d] float, 16-byte aligned; label [N] int32; r [N] float
+ *  guard_label [N] int32 or NULL; priority [N] float (PRIORITY only, else
+ *           ignored)
+ *  budget   maximum rows to append; < 0 means the free capacity; more than
+ *           the free capacity returns ECAPACITY (nothing appended)
+ *  per_class, n_classes  per-label budget (0 = none) and label range
+ *           (1 <= n_classes <= 16384 when per_class > 0)
+ *  selected_out [budget] int64 or NULL: candidate indices in append order
+ *  appended (host, nullable) out: rows appended; c->n advances by it
+ *  ws       lipcache_construct_workspace_bytes(c, N, n_classes, budget)
+ *           bytes (depends on the cache's capacity and d)
+ * (sync: the host drives the visit in chunks of 1024 candidates)
+ */
+lipcache_status lipcache_construct(lipcache_cache* c, const float* z, const int32_t* label,
+                                   const float* r, const int32_t* guard_label,
+                                   const float* priority, int64_t N, int32_t strategy,
+                                   int64_t budget, int32_t per_class, int32_t n_classes,
+                                   int64_t* selected_out, int64_t* appended,
+                                   void* ws, size_t ws_bytes, lipcache_stream_t stream);
+size_t lipcache_construct_workspace_bytes(const lipcache_cache* c, int64_t N, int32_t n_classes,
+                                          int64_t budget);
 
 /*
  * Diagnostic view of the lookup's distance filter for small problems.  For

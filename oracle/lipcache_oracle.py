@@ -443,11 +443,14 @@ SELECT_STRATEGIES = ("radius_dedup", "priority", "kcenter")
 
 
 def construct(state: CacheState, z, label, r, strategy: str = "radius_dedup", budget_total=None,
-              budget_per_class: int = 0, priority=None, guard_label=None) -> np.ndarray:
+              budget_per_class: int = 0, priority=None, guard_label=None, n_classes=None) -> np.ndarray:
     """Offline construction of the feature store (Alg. 1): select and append.
 
     Eligible candidates have r_i > 0 and, when ``guard_label`` is given (the
-    cache-centre label-consistency flag of Alg. 1), guard_label_i == label_i.
+    cache-centre label-consistency flag of Alg. 1), guard_label_i == label_i;
+    with the priority strategy a NaN priority is not eligible, and with a
+    per-class budget and ``n_classes`` given, neither is a label outside
+    [0, n_classes).
     At most ``budget_total`` entries are appended (default: the free
     capacity; more than the free capacity raises CapacityError) and, when
     ``budget_per_class`` > 0, at most that many per payload label.  Distances
@@ -483,6 +486,10 @@ def construct(state: CacheState, z, label, r, strategy: str = "radius_dedup", bu
     eligible = rr > 0
     if guard_label is not None:
         eligible &= np.asarray(guard_label, dtype=np.int32) == lab
+    if strategy == "priority":
+        eligible &= ~np.isnan(np.asarray(priority, dtype=np.float32))
+    if budget_per_class > 0 and n_classes is not None:
+        eligible &= (lab >= 0) & (lab < n_classes)
     counts: dict[int, int] = {}
 
     def class_open(c: int) -> bool:

@@ -13,6 +13,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblipcache
 OK, EINVAL, EDEGENERATE, ENOCONV, ECAPACITY, EUNSUPPORTED, EWORKSPACE, EHIP = range(8)
 F32, BF16 = 0, 1
 RADIUS_CONSERVATIVE, RADIUS_TIGHT = 0, 1
+SELECT_RADIUS_DEDUP, SELECT_PRIORITY, SELECT_KCENTER = 0, 1, 2
 MISS = -1
 STAT_HITS, STAT_RECHECKED, STAT_BAND_PAIRS, STAT_BAND_QUERIES = range(4)
 
@@ -50,6 +51,9 @@ SIGNATURES = {
     "lipcache_insert": (_i32, [_PCACHE, _vp, _vp, _vp, _vp, _i64, ctypes.POINTER(_i64), _vp, _sz, _vp]),
     "lipcache_insert_workspace_bytes": (_sz, [_i64]),
     "lipcache_lookup_filter_dump": (_i32, [_PCACHE, _vp, _i64, _i32, _vp, _vp, _vp, _sz, _vp]),
+    "lipcache_construct": (_i32, [_PCACHE, _vp, _vp, _vp, _vp, _vp, _i64, _i32, _i64, _i32, _i32, _vp,
+                                  ctypes.POINTER(_i64), _vp, _sz, _vp]),
+    "lipcache_construct_workspace_bytes": (_sz, [_PCACHE, _i64, _i32, _i64]),
     "lipcache_status_string": (ctypes.c_char_p, [_i32]),
     "lipcache_abi_version": (_i32, []),
 }

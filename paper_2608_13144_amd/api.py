@@ -16,6 +16,7 @@ from . import _lib as L
 _STORE = {"f32": L.F32, "bf16": L.BF16}
 _PRECISION = {"f32": L.F32, "bf16": L.BF16}
 _RADIUS = {"conservative": L.RADIUS_CONSERVATIVE, "tight": L.RADIUS_TIGHT}
+_SELECT = {"radius_dedup": L.SELECT_RADIUS_DEDUP, "priority": L.SELECT_PRIORITY, "kcenter": L.SELECT_KCENTER}
 
 
 def _p(t: torch.Tensor | None):
@@ -193,6 +194,37 @@ class LipCache:
         cq = certify(zq, W, b, sigma, store=self.store)
         inserted = self.insert(zq, cq.label, cq.r, res.label)
         return res, cq, inserted
+
+    def construct(self, z: torch.Tensor, label: torch.Tensor, r: torch.Tensor, strategy: str = "radius_dedup",
+                  budget: int = -1, per_class: int = 0, n_classes: int = 0, priority: torch.Tensor | None = None,
+                  guard_label: torch.Tensor | None = None):
+        """lipcache_construct: select candidates (Alg. 1) and append them (sync).
+
+        Returns (rows appended, int64 tensor of the selected candidate indices
+        in append order)."""
+        _need_cuda(z, "z", torch.float32, 2)
+        _need_cuda(label, "label", torch.int32, 1)
+        _need_cuda(r, "r", torch.float32, 1)
+        if priority is not None:
+            _need_cuda(priority, "priority", torch.float32, 1)
+        if guard_label is not None:
+            _need_cuda(guard_label, "guard_label", torch.int32, 1)
+        n = z.shape[0]
+        if z.shape[1] != self.d or label.shape[0] != n or r.shape[0] != n:
+            raise ValueError("construct: shapes do not match the cache")
+        lib = L.load()
+        strat = _SELECT[strategy]
+        cs = self.cstruct()
+        bud = self.capacity - self.n if budget < 0 else int(budget)
+        sel = torch.full((max(bud, 1),), -1, dtype=torch.int64, device=self.device)
+        ws = self._workspace(lib.lipcache_construct_workspace_bytes(ctypes.byref(cs), n, int(n_classes), int(budget)))
+        got = ctypes.c_int64(0)
+        st = lib.lipcache_construct(ctypes.byref(cs), _p(z), _p(label), _p(r), _p(guard_label), _p(priority), n,
+                                    strat, int(budget), int(per_class), int(n_classes), _p(sel), ctypes.byref(got),
+                                    _p(ws), ws.numel(), _stream(self.device))
+        L.check("lipcache_construct", st)
+        self.n = int(cs.n)
+        return int(got.value), sel[: got.value]
 
     def filter_dump(self, zq: torch.Tensor, precision: str = "bf16"):
         """lipcache_lookup_filter_dump: matrix-core dot products and filter decisions (small sizes)."""

@@ -1,0 +1,742 @@
+// Offline construction of the feature store (Sec. 4.3, Alg. 1).
+//
+// Candidates (z_i, payload y~_i, certified radius r_i) are eligible when
+// r_i > 0 and, with the cache-centre label-consistency flag, when the guard
+// label equals the payload.  At most `budget` entries are appended, at most
+// `per_class` per payload label when that budget is set.  Strategies:
+//
+//   radius de-dup - visit eligible candidates by decreasing r (ties: lower
+//                   index), skip a full class, skip a duplicate (strictly
+//                   inside the ball of an entry already in the cache), append
+//                   the rest.
+//   priority      - the same visit by a caller-given priority (random keys
+//                   give the random strategy), no duplicate test.
+//   K-center      - farthest-first traversal from the largest-radius
+//                   candidate, per class when a per-class budget is set.
+//
+// Device plan.  A stable LSD radix sort (four 8-bit passes over a 32-bit
+// descending key; ties keep index order) orders the eligible candidates.
+// The greedy visit then runs in chunks of kChunk candidates: the chunk is
+// looked up against the cache (lipcache_lookup: a hit means a duplicate),
+// an exact float64 relation "b lies in the ball of a" is formed for all
+// pairs a < b of the chunk (bit matrix), one wave decides the chunk in order
+// (AND of the relation row with the bits of the candidates accepted so far,
+// class counts in LDS), and lipcache_insert appends the accepted rows in
+// visit order.  K-center keeps every candidate's squared distance to the
+// chosen set in float64 and alternates a fused update/arg-max kernel with a
+// one-block reduction, with no host round trip per pick.
+#include <limits.h>
+
+#include "lc_common.hpp"
+
+namespace lc {
+
+constexpr int kSortThreads = 1024;  // one item per thread
+constexpr int kSortWaves = kSortThreads / kWave;
+constexpr int kBins = 256;
+constexpr int kChunk = 1024;              // candidates per greedy step
+constexpr int kChunkWords = kChunk / 32;  // relation row length in 32-bit words
+constexpr int kMaxClasses = 16384;        // class counts live in LDS
+constexpr uint32_t kNotEligible = 0xFFFFFFFFu;
+
+__global__ void fill_u64_kernel(unsigned long long* __restrict__ p, int64_t n, unsigned long long v) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+__global__ void fill_i32_kernel(int32_t* __restrict__ p, int64_t n, int32_t v) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// Larger float -> smaller key (finite floats; order-preserving bit trick).
+__device__ __forceinline__ uint32_t descending_key(float f) {
+  uint32_t u = __builtin_bit_cast(uint32_t, f);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ~u;
+}
+
+__device__ __forceinline__ bool eligible(int64_t i, const float* __restrict__ r, const float* __restrict__ prio,
+                                         const int32_t* __restrict__ label, const int32_t* __restrict__ guard,
+                                         int n_classes) {
+  bool e = r[i] > 0.0f;
+  if (guard) e = e && guard[i] == label[i];
+  if (n_classes > 0) e = e && label[i] >= 0 && label[i] < n_classes;
+  if (prio) e = e && prio[i] == prio[i];
+  return e;
+}
+
+__global__ void construct_keys_kernel(const float* __restrict__ r, const float* __restrict__ prio,
+                                      const int32_t* __restrict__ label, const int32_t* __restrict__ guard,
+                                      int64_t n, int n_classes, uint32_t* __restrict__ keys,
+                                      uint32_t* __restrict__ vals, unsigned long long* __restrict__ n_elig) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const bool e = i < n && eligible(i, r, prio, label, guard, n_classes);
+  if (i < n) {
+    keys[i] = e ? descending_key(prio ? prio[i] : r[i]) : kNotEligible;
+    vals[i] = static_cast<uint32_t>(i);
+  }
+  const unsigned long long bal = __ballot(e);
+  if (lane_id() == 0 && bal != 0ull) atomicAdd(n_elig, static_cast<unsigned long long>(__builtin_popcountll(bal)));
+}
+
+// hist[d * nb + b] = number of items of block b whose digit is d.
+__global__ __launch_bounds__(kSortThreads) void radix_hist_kernel(const uint32_t* __restrict__ keys, int64_t n,
+                                                                  int shift, int64_t nb, uint32_t* __restrict__ hist) {
+  __shared__ uint32_t h[kBins];
+  if (threadIdx.x < kBins) h[threadIdx.x] = 0u;
+  __syncthreads();
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kSortThreads + threadIdx.x;
+  if (i < n) atomicAdd(&h[(keys[i] >> shift) & (kBins - 1)], 1u);
+  __syncthreads();
+  if (threadIdx.x < kBins) hist[static_cast<int64_t>(threadIdx.x) * nb + blockIdx.x] = h[threadIdx.x];
+}
+
+// Inclusive prefix sum over the 1024 threads of the block (wave shuffles,
+// then the 16 wave totals).
+__device__ __forceinline__ uint32_t block_inclusive_scan(uint32_t v, uint32_t* wave_tot, uint32_t& block_total) {
+  const int lane = lane_id();
+  const int wave = static_cast<int>(threadIdx.x) / kWave;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t o = static_cast<uint32_t>(__shfl_up(static_cast<int>(v), off, kWave));
+    if (lane >= off) v += o;
+  }
+  if (lane == kWave - 1) wave_tot[wave] = v;
+  __syncthreads();
+  uint32_t before = 0, total = 0;
+  for (int w = 0; w < kSortWaves; ++w) {
+    const uint32_t t = wave_tot[w];
+    before += w < wave ? t : 0u;
+    total += t;
+  }
+  __syncthreads();
+  block_total = total;
+  return before + v;
+}
+
+// Block d: exclusive scan of hist[d * nb .. d * nb + nb) in place; the digit
+// total goes to dsum[d].
+__global__ __launch_bounds__(kSortThreads) void radix_digit_scan_kernel(uint32_t* __restrict__ hist, int64_t nb,
+                                                                        uint32_t* __restrict__ dsum) {
+  __shared__ uint32_t wave_tot[kSortWaves];
+  uint32_t* row = hist + static_cast<int64_t>(blockIdx.x) * nb;
+  uint32_t running = 0;
+  for (int64_t base = 0; base < nb; base += kSortThreads) {
+    const int64_t j = base + threadIdx.x;
+    const uint32_t v = j < nb ? row[j] : 0u;
+    uint32_t tot = 0;
+    const uint32_t incl = block_inclusive_scan(v, wave_tot, tot);
+    if (j < nb) row[j] = running + incl - v;
+    running += tot;
+  }
+  if (threadIdx.x == 0) dsum[blockIdx.x] = running;
+}
+
+// dbase[d] = sum of dsum[0 .. d) (one block of 256 threads, serial is fine).
+__global__ void radix_base_kernel(const uint32_t* __restrict__ dsum, uint32_t* __restrict__ dbase) {
+  if (threadIdx.x == 0) {
+    uint32_t s = 0;
+    for (int d = 0; d < kBins; ++d) {
+      dbase[d] = s;
+      s += dsum[d];
+    }
+  }
+}
+
+// Stable scatter: within a block, items keep their order among equal digits
+// (rank inside the wave from eight digit-bit ballots, then the counts of the
+// same digit in the block's earlier waves).
+__global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
+    const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in, int64_t n, int shift, int64_t nb,
+    const uint32_t* __restrict__ hist, const uint32_t* __restrict__ dbase, uint32_t* __restrict__ keys_out,
+    uint32_t* __restrict__ vals_out) {
+  __shared__ uint32_t wcount[kSortWaves][kBins];
+  for (int t = threadIdx.x; t < kSortWaves * kBins; t += kSortThreads) (&wcount[0][0])[t] = 0u;
+  __syncthreads();
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kSortThreads + threadIdx.x;
+  const bool valid = i < n;
+  const uint32_t key = valid ? keys_in[i] : 0u;
+  const int dig = static_cast<int>((key >> shift) & (kBins - 1));
+  const int lane = lane_id();
+  const int wave = static_cast<int>(threadIdx.x) / kWave;
+  unsigned long long same = __ballot(valid);
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const bool bit = (dig >> b) & 1;
+    const unsigned long long bal = __ballot(bit);
+    same &= bit ? bal : ~bal;
+  }
+  const int rank = __builtin_popcountll(same & ((1ull << lane) - 1ull));
+  if (valid && rank == 0) wcount[wave][dig] = static_cast<uint32_t>(__builtin_popcountll(same));
+  __syncthreads();
+  if (valid) {
+    uint32_t before = 0;
+    for (int w = 0; w < wave; ++w) before += wcount[w][dig];
+    const uint32_t pos = dbase[dig] + hist[static_cast<int64_t>(dig) * nb + blockIdx.x] + before + rank;
+    keys_out[pos] = key;
+    vals_out[pos] = vals_in[i];
+  }
+}
+
+// Chunk rows in visit order: the stored values (bf16-rounded for a bf16
+// cache) as float32, with their payload and radius.  One wave per row.
+__global__ void construct_gather_kernel(const float* __restrict__ z, const int32_t* __restrict__ label,
+                                        const float* __restrict__ r, const uint32_t* __restrict__ order, int k, int d,
+                                        int bf16, float* __restrict__ zc, int32_t* __restrict__ lc,
+                                        float* __restrict__ rc, int64_t* __restrict__ src_c) {
+  const int j = static_cast<int>(blockIdx.x) * (blockDim.x / kWave) + static_cast<int>(threadIdx.x) / kWave;
+  if (j >= k) return;
+  const int64_t src = order[j];
+  const float* zr = z + src * d;
+  float* out = zc + static_cast<int64_t>(j) * d;
+  for (int c = lane_id(); c < d; c += kWave) out[c] = bf16 ? bf16_round_f32(zr[c]) : zr[c];
+  if (lane_id() == 0) {
+    lc[j] = label[src];
+    rc[j] = r[src];
+    src_c[j] = src;
+  }
+}
+
+// rel[b * kChunkWords + a / 32] bit a % 32 set iff a < b and
+// ||z_b - z_a||^2 < r_a^2 (float64 over the chunk's stored values).  A block
+// of 1024 threads takes a 32 x 32 tile of (b, a) pairs, rows staged in LDS
+// 64 elements at a time; each wave covers two b rows, and one ballot per
+// wave gives their two words.
+__global__ __launch_bounds__(1024) void construct_relation_kernel(const float* __restrict__ zc,
+                                                                  const float* __restrict__ rc, int k, int d,
+                                                                  uint32_t* __restrict__ rel) {
+  __shared__ float za[32][65];
+  __shared__ float zb[32][65];
+  const int tb = static_cast<int>(blockIdx.y);  // tile of b rows
+  const int ta = static_cast<int>(blockIdx.x);  // tile of a rows
+  const int t = static_cast<int>(threadIdx.x);
+  const int bl = t / 32, al = t % 32;
+  const int b = tb * 32 + bl, a = ta * 32 + al;
+  bool inside = false;
+  if (ta <= tb) {
+    double acc = 0.0;
+    for (int c0 = 0; c0 < d; c0 += 64) {
+      __syncthreads();
+      for (int e = t; e < 32 * 64; e += 1024) {
+        const int row = e / 64, col = e % 64;
+        const int ra = ta * 32 + row, rb = tb * 32 + row;
+        const bool in_row = c0 + col < d;
+        za[row][col] = (ra < k && in_row) ? zc[static_cast<int64_t>(ra) * d + c0 + col] : 0.0f;
+        zb[row][col] = (rb < k && in_row) ? zc[static_cast<int64_t>(rb) * d + c0 + col] : 0.0f;
+      }
+      __syncthreads();
+#pragma unroll 8
+      for (int c = 0; c < 64; ++c) {
+        const double diff = static_cast<double>(zb[bl][c]) - static_cast<double>(za[al][c]);
+        acc = __builtin_fma(diff, diff, acc);
+      }
+    }
+    if (a < b && b < k) {
+      const double ra = static_cast<double>(rc[a]);
+      inside = acc < ra * ra;
+    }
+  }
+  const unsigned long long bal = __ballot(inside);
+  const int lane = lane_id();
+  if (b < k && (lane == 0 || lane == 32)) {
+    const uint32_t word = lane == 0 ? static_cast<uint32_t>(bal) : static_cast<uint32_t>(bal >> 32);
+    rel[static_cast<int64_t>(b) * kChunkWords + ta] = word;
+  }
+}
+
+struct AcceptParams {
+  int k;
+  int dedup;
+  const int32_t* dup_label;   // lookup result per chunk candidate (MISS = not inside a cached ball); may be null
+  const uint32_t* rel;        // chunk relation; null without de-dup
+  const int32_t* lc;          // payload labels of the chunk
+  const int64_t* src_c;       // candidate index of each chunk row
+  int32_t* sel;               // out: LIPCACHE_MISS = append, 0 = skip
+  int32_t* class_count;       // [n_classes] running counts (global)
+  int n_classes;
+  int per_class;
+  unsigned long long* total;  // running number appended
+  unsigned long long budget;
+  int64_t* selected_out;      // may be null
+};
+
+// One workgroup decides the chunk in visit order.  All threads stage the
+// relation and the class counts in LDS; wave 0 then walks the chunk: lane l
+// keeps bits 32 l .. 32 l + 31 of the accepted set, so "inside an accepted
+// earlier ball" is one AND per lane and one ballot.
+__global__ __launch_bounds__(1024) void construct_accept_kernel(const AcceptParams p) {
+  __shared__ uint32_t srel[kChunk * kChunkWords];  // 128 KiB
+  __shared__ int32_t scount[kMaxClasses / 16];      // first 1024 classes cached; the rest from global
+  const int t = static_cast<int>(threadIdx.x);
+  if (p.dedup) {
+    for (int e = t; e < p.k * kChunkWords; e += 1024) srel[e] = p.rel[e];
+  }
+  const int cached = p.n_classes < kMaxClasses / 16 ? p.n_classes : kMaxClasses / 16;
+  if (p.per_class > 0)
+    for (int c = t; c < cached; c += 1024) scount[c] = p.class_count[c];
+  __syncthreads();
+  if (t >= kWave) return;
+  const int lane = t;
+  uint32_t acc_bits = 0u;  // lane's word of the accepted set (lanes >= kChunkWords stay 0)
+  unsigned long long total = *p.total;
+  for (int j = 0; j < p.k; ++j) {
+    bool take = total < p.budget;
+    if (take && p.dup_label) take = p.dup_label[j] == LIPCACHE_MISS;
+    const int c = p.lc[j];
+    if (take && p.per_class > 0) {
+      const int cnt = c < cached ? scount[c] : p.class_count[c];
+      take = cnt < p.per_class;
+    }
+    if (take && p.dedup) {
+      const uint32_t row = lane < kChunkWords ? srel[j * kChunkWords + lane] : 0u;
+      take = __ballot((row & acc_bits) != 0u) == 0ull;
+    }
+    if (lane == 0) p.sel[j] = take ? LIPCACHE_MISS : 0;
+    if (take) {
+      if (lane == j / 32) acc_bits |= 1u << (j % 32);
+      if (lane == 0) {
+        if (p.per_class > 0) {
+          if (c < cached) {
+            scount[c] += 1;
+          } else {
+            p.class_count[c] += 1;
+          }
+        }
+        if (p.selected_out) p.selected_out[total] = p.src_c[j];
+      }
+      total += 1;
+    }
+  }
+  if (lane == 0) *p.total = total;
+  if (p.per_class > 0)
+    for (int c = lane; c < cached; c += kWave) p.class_count[c] = scount[c];
+}
+
+// ---------------------------------------------------------------- K-center
+struct KcParams {
+  const float* z;
+  const float* r;
+  const float* prio;
+  const int32_t* label;
+  const int32_t* guard;
+  int64_t n;
+  int d;
+  int bf16;
+  int n_classes;
+  int group;                 // -1: all eligible candidates, else this payload label
+  double* mind;              // [n] squared distance to the chosen set; < 0: not a candidate
+  int64_t* pick;             // [1] newest pick (-1: none)
+  double* part_v;            // [blocks] block maxima
+  int64_t* part_i;           // [blocks] their indices
+  unsigned long long* total; // appended so far (all groups)
+  unsigned long long budget;
+  int64_t* picks;            // [budget] picks in order
+  int* group_count;          // [1] picks in the current group
+  int limit;                 // picks allowed in this group
+};
+
+__device__ __forceinline__ float stored(const KcParams& p, int64_t i, int c) {
+  const float v = p.z[i * p.d + c];
+  return p.bf16 ? bf16_round_f32(v) : v;
+}
+
+__device__ __forceinline__ double dist2(const KcParams& p, int64_t i, int64_t j) {
+  double acc = 0.0;
+  for (int c = 0; c < p.d; ++c) {
+    const double diff = static_cast<double>(stored(p, i, c)) - static_cast<double>(stored(p, j, c));
+    acc = __builtin_fma(diff, diff, acc);
+  }
+  return acc;
+}
+
+// Block arg-max of (v, -i): larger v, then lower index.
+__device__ __forceinline__ void better(double& v, int64_t& i, double v2, int64_t i2) {
+  if (v2 > v || (v2 == v && i2 >= 0 && (i < 0 || i2 < i))) {
+    v = v2;
+    i = i2;
+  }
+}
+
+__device__ void block_argmax(double v, int64_t i, double* sv, int64_t* si, double& out_v, int64_t& out_i) {
+  const int t = static_cast<int>(threadIdx.x);
+  sv[t] = v;
+  si[t] = i;
+  __syncthreads();
+  for (int s = static_cast<int>(blockDim.x) / 2; s > 0; s >>= 1) {
+    if (t < s) {
+      double a = sv[t];
+      int64_t ai = si[t];
+      better(a, ai, sv[t + s], si[t + s]);
+      sv[t] = a;
+      si[t] = ai;
+    }
+    __syncthreads();
+  }
+  out_v = sv[0];
+  out_i = si[0];
+}
+
+// The group's start: its first candidate in visit order (largest r, lower
+// index).  One block walks the order 256 positions at a time.
+__global__ __launch_bounds__(256) void kcenter_start_kernel(const int32_t* __restrict__ label,
+                                                            const uint32_t* __restrict__ order, int64_t n_elig,
+                                                            int group, int64_t* __restrict__ start) {
+  __shared__ unsigned long long best;
+  if (threadIdx.x == 0) best = ~0ull;
+  __syncthreads();
+  for (int64_t base = 0; base < n_elig; base += 256) {
+    const int64_t q = base + threadIdx.x;
+    if (q < n_elig && (group < 0 || label[order[q]] == group)) atomicMin(&best, static_cast<unsigned long long>(q));
+    __syncthreads();
+    const bool found = best != ~0ull;
+    __syncthreads();
+    if (found) break;
+  }
+  if (threadIdx.x == 0) *start = best != ~0ull ? static_cast<int64_t>(order[best]) : -1;
+}
+
+// First step of a group: mind = squared distance to the start.
+__global__ __launch_bounds__(256) void kcenter_init_kernel(const KcParams p, const int64_t* __restrict__ start) {
+  const int64_t s = *start;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < p.n) {
+    const bool in = s >= 0 && eligible(i, p.r, p.prio, p.label, p.guard, p.n_classes) &&
+                    (p.group < 0 || p.label[i] == p.group);
+    p.mind[i] = (!in || i == s) ? -1.0 : dist2(p, i, s);
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    const bool ok = s >= 0 && *p.total < p.budget && p.limit > 0;
+    *p.pick = ok ? s : -1;
+    *p.group_count = ok ? 1 : 0;
+    if (ok) {
+      p.picks[*p.total] = s;
+      *p.total += 1ull;
+    }
+  }
+}
+
+// Fold the newest pick into mind (unless it is -1), then block arg-max.
+__global__ __launch_bounds__(256) void kcenter_step_kernel(const KcParams p) {
+  __shared__ double sv[256];
+  __shared__ int64_t si[256];
+  const int64_t pk = *p.pick;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  double v = -1.0;
+  int64_t vi = -1;
+  if (i < p.n) {
+    double m = p.mind[i];
+    if (m >= 0.0 && pk >= 0) {
+      if (i == pk) {
+        m = -1.0;
+      } else {
+        const double d2 = dist2(p, i, pk);
+        m = d2 < m ? d2 : m;
+      }
+      p.mind[i] = m;
+    }
+    if (m >= 0.0) {
+      v = m;
+      vi = i;
+    }
+  }
+  double ov;
+  int64_t oi;
+  block_argmax(v, vi, sv, si, ov, oi);
+  if (threadIdx.x == 0) {
+    p.part_v[blockIdx.x] = ov;
+    p.part_i[blockIdx.x] = oi;
+  }
+}
+
+// Reduce the block maxima to the next pick.
+__global__ __launch_bounds__(256) void kcenter_pick_kernel(const KcParams p, int nblocks) {
+  __shared__ double sv[256];
+  __shared__ int64_t si[256];
+  double v = -1.0;
+  int64_t vi = -1;
+  for (int b = threadIdx.x; b < nblocks; b += 256) better(v, vi, p.part_v[b], p.part_i[b]);
+  double ov;
+  int64_t oi;
+  block_argmax(v, vi, sv, si, ov, oi);
+  if (threadIdx.x == 0) {
+    const bool ok = oi >= 0 && ov >= 0.0 && *p.total < p.budget && *p.group_count < p.limit;
+    *p.pick = ok ? oi : -1;
+    if (ok) {
+      p.picks[*p.total] = oi;
+      *p.total += 1ull;
+      *p.group_count += 1;
+    }
+  }
+}
+
+// Rows of the picks [t0, t0 + k) as float32 stored values, with their
+// payload and radius (for the append).
+__global__ void kcenter_gather_kernel(const float* __restrict__ z, const int32_t* __restrict__ label,
+                                      const float* __restrict__ r, const int64_t* __restrict__ picks, int64_t t0,
+                                      int k, int d, int bf16, float* __restrict__ zc, int32_t* __restrict__ lc,
+                                      float* __restrict__ rc) {
+  const int j = static_cast<int>(blockIdx.x) * (blockDim.x / kWave) + static_cast<int>(threadIdx.x) / kWave;
+  if (j >= k) return;
+  const int64_t src = picks[t0 + j];
+  const float* zr = z + src * d;
+  float* out = zc + static_cast<int64_t>(j) * d;
+  for (int c = lane_id(); c < d; c += kWave) out[c] = bf16 ? bf16_round_f32(zr[c]) : zr[c];
+  if (lane_id() == 0) {
+    lc[j] = label[src];
+    rc[j] = r[src];
+  }
+}
+
+// ------------------------------------------------------------- workspace
+struct CWs {
+  uint32_t* keys[2];
+  uint32_t* vals[2];
+  uint32_t* hist;
+  uint32_t* dsum;
+  uint32_t* dbase;
+  unsigned long long* counters;  // [0] eligible, [1] appended
+  float* zc;
+  int32_t* lc;
+  float* rc;
+  int64_t* src_c;
+  int32_t* dup;
+  int32_t* sel;
+  uint32_t* rel;
+  int32_t* class_count;
+  double* mind;
+  int64_t* pick;
+  int64_t* start;
+  int* group_count;
+  double* part_v;
+  int64_t* part_i;
+  int64_t* picks;
+  void* sub_ws;  // lookup / insert workspace
+  size_t sub_bytes;
+  size_t total;
+};
+
+inline size_t sub_ws_bytes(const lipcache_cache* c) {
+  const size_t a = lipcache_lookup_workspace_bytes(kChunk, c->capacity, c->d, LIPCACHE_BF16);
+  const size_t b = lipcache_insert_workspace_bytes(kChunk);
+  return a > b ? a : b;
+}
+
+inline CWs cws_layout(int64_t n, int d, int n_classes, int64_t budget, size_t sub_bytes, char* base) {
+  CWs w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* p = base ? base + off : nullptr;
+    off = align_up(off + bytes, 256);
+    return p;
+  };
+  const int64_t nb = (n + kSortThreads - 1) / kSortThreads;
+  for (int s = 0; s < 2; ++s) {
+    w.keys[s] = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(n) * 4));
+    w.vals[s] = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(n) * 4));
+  }
+  w.hist = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(nb) * kBins * 4));
+  w.dsum = reinterpret_cast<uint32_t*>(take(kBins * 4));
+  w.dbase = reinterpret_cast<uint32_t*>(take(kBins * 4));
+  w.counters = reinterpret_cast<unsigned long long*>(take(64));
+  w.zc = reinterpret_cast<float*>(take(static_cast<size_t>(kChunk) * d * 4));
+  w.lc = reinterpret_cast<int32_t*>(take(kChunk * 4));
+  w.rc = reinterpret_cast<float*>(take(kChunk * 4));
+  w.src_c = reinterpret_cast<int64_t*>(take(kChunk * 8));
+  w.dup = reinterpret_cast<int32_t*>(take(kChunk * 4));
+  w.sel = reinterpret_cast<int32_t*>(take(kChunk * 4));
+  w.rel = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(kChunk) * kChunkWords * 4));
+  w.class_count = reinterpret_cast<int32_t*>(take(static_cast<size_t>(n_classes > 0 ? n_classes : 1) * 4));
+  w.mind = reinterpret_cast<double*>(take(static_cast<size_t>(n) * 8));
+  w.pick = reinterpret_cast<int64_t*>(take(8));
+  w.start = reinterpret_cast<int64_t*>(take(8));
+  w.group_count = reinterpret_cast<int*>(take(8));
+  const int64_t kb = (n + 255) / 256;
+  w.part_v = reinterpret_cast<double*>(take(static_cast<size_t>(kb) * 8));
+  w.part_i = reinterpret_cast<int64_t*>(take(static_cast<size_t>(kb) * 8));
+  w.picks = reinterpret_cast<int64_t*>(take(static_cast<size_t>(budget > 0 ? budget : 1) * 8));
+  w.sub_ws = take(sub_bytes);
+  w.sub_bytes = sub_bytes;
+  w.total = off;
+  return w;
+}
+
+}  // namespace lc
+
+using namespace lc;
+
+extern "C" size_t lipcache_construct_workspace_bytes(const lipcache_cache* c, int64_t N, int32_t n_classes,
+                                                     int64_t budget) {
+  if (!c || N < 0 || c->capacity < 0 || c->d < 1) return 0;
+  const int64_t free_rows = c->capacity - c->n;
+  const int64_t b = budget < 0 ? free_rows : budget;
+  return cws_layout(N, c->d, n_classes, b, sub_ws_bytes(c), nullptr).total;
+}
+
+extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z, const int32_t* label,
+                                              const float* r, const int32_t* guard_label, const float* priority,
+                                              int64_t N, int32_t strategy, int64_t budget, int32_t per_class,
+                                              int32_t n_classes, int64_t* selected_out, int64_t* appended,
+                                              void* ws, size_t ws_bytes, lipcache_stream_t stream) {
+  if (!c || N < 0 || N > INT32_MAX) return N > INT32_MAX ? LIPCACHE_EUNSUPPORTED : LIPCACHE_EINVAL;
+  if (c->d < 32 || c->d > 1024 || c->d % 32 != 0) return LIPCACHE_EINVAL;
+  if (c->store_dtype != LIPCACHE_F32 && c->store_dtype != LIPCACHE_BF16) return LIPCACHE_EINVAL;
+  if (c->n < 0 || c->capacity < 0 || c->n > c->capacity) return LIPCACHE_EINVAL;
+  if (c->capacity > 0 && (!c->z || !c->r || !c->label || !c->norm2)) return LIPCACHE_EINVAL;
+  if (strategy != LIPCACHE_SELECT_RADIUS_DEDUP && strategy != LIPCACHE_SELECT_PRIORITY &&
+      strategy != LIPCACHE_SELECT_KCENTER)
+    return LIPCACHE_EINVAL;
+  if (N > 0 && (!z || !label || !r)) return LIPCACHE_EINVAL;
+  if (strategy == LIPCACHE_SELECT_PRIORITY && N > 0 && !priority) return LIPCACHE_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(z) & 15u) != 0) return LIPCACHE_EINVAL;
+  if (per_class < 0) return LIPCACHE_EINVAL;
+  if (per_class > 0 && (n_classes < 1 || n_classes > kMaxClasses)) return LIPCACHE_EINVAL;
+  const int64_t free_rows = c->capacity - c->n;
+  const int64_t bud = budget < 0 ? free_rows : budget;
+  if (bud > free_rows) return LIPCACHE_ECAPACITY;
+  const size_t need = lipcache_construct_workspace_bytes(c, N, n_classes, budget);
+  if (!ws || ws_bytes < need || !aligned256(ws)) return LIPCACHE_EWORKSPACE;
+  if (appended) *appended = 0;
+  if (N == 0 || bud == 0) return LIPCACHE_OK;
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  CWs w = cws_layout(N, c->d, n_classes, bud, sub_ws_bytes(c), static_cast<char*>(ws));
+  const int d = c->d;
+  const int bf16 = c->store_dtype == LIPCACHE_BF16 ? 1 : 0;
+  const int ncls = per_class > 0 ? n_classes : 0;
+  const float* prio = strategy == LIPCACHE_SELECT_PRIORITY ? priority : nullptr;
+
+  // ---- eligibility and visit order (stable radix sort by descending key)
+  hipLaunchKernelGGL(fill_u64_kernel, dim3(1), dim3(64), 0, s, w.counters, 8, 0ull);
+  LC_LAUNCHED();
+  if (ncls > 0) {
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(static_cast<unsigned>((ncls + 255) / 256)), dim3(256), 0, s,
+                       w.class_count, static_cast<int64_t>(ncls), 0);
+    LC_LAUNCHED();
+  }
+  const unsigned g256 = static_cast<unsigned>((N + 255) / 256);
+  hipLaunchKernelGGL(construct_keys_kernel, dim3(g256), dim3(256), 0, s, r, prio, label, guard_label, N, ncls,
+                     w.keys[0], w.vals[0], w.counters);
+  LC_LAUNCHED();
+  const int64_t nb = (N + kSortThreads - 1) / kSortThreads;
+  int cur = 0;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 8 * pass;
+    hipLaunchKernelGGL(radix_hist_kernel, dim3(static_cast<unsigned>(nb)), dim3(kSortThreads), 0, s, w.keys[cur], N,
+                       shift, nb, w.hist);
+    LC_LAUNCHED();
+    hipLaunchKernelGGL(radix_digit_scan_kernel, dim3(kBins), dim3(kSortThreads), 0, s, w.hist, nb, w.dsum);
+    LC_LAUNCHED();
+    hipLaunchKernelGGL(radix_base_kernel, dim3(1), dim3(64), 0, s, w.dsum, w.dbase);
+    LC_LAUNCHED();
+    hipLaunchKernelGGL(radix_scatter_kernel, dim3(static_cast<unsigned>(nb)), dim3(kSortThreads), 0, s, w.keys[cur],
+                       w.vals[cur], N, shift, nb, w.hist, w.dbase, w.keys[cur ^ 1], w.vals[cur ^ 1]);
+    LC_LAUNCHED();
+    cur ^= 1;
+  }
+  const uint32_t* order = w.vals[cur];
+  unsigned long long host_cnt[2] = {0ull, 0ull};
+  LC_HIP(hipMemcpyAsync(host_cnt, w.counters, 16, hipMemcpyDeviceToHost, s));
+  LC_HIP(hipStreamSynchronize(s));
+  const int64_t n_elig = static_cast<int64_t>(host_cnt[0]);
+  if (n_elig == 0) return LIPCACHE_OK;
+  unsigned long long* total_dev = w.counters + 1;
+
+  int64_t added = 0;
+  if (strategy != LIPCACHE_SELECT_KCENTER) {
+    const int dedup = strategy == LIPCACHE_SELECT_RADIUS_DEDUP ? 1 : 0;
+    for (int64_t s0 = 0; s0 < n_elig && added < bud; s0 += kChunk) {
+      const int k = static_cast<int>(n_elig - s0 < kChunk ? n_elig - s0 : kChunk);
+      hipLaunchKernelGGL(construct_gather_kernel, dim3(static_cast<unsigned>((k + 3) / 4)), dim3(256), 0, s, z, label,
+                         r, order + s0, k, d, bf16, w.zc, w.lc, w.rc, w.src_c);
+      LC_LAUNCHED();
+      const int32_t* dup = nullptr;
+      if (dedup) {
+        if (c->n > 0) {
+          const lipcache_status st = lipcache_lookup(c, w.zc, k, LIPCACHE_BF16, w.dup, nullptr, nullptr, nullptr,
+                                                     nullptr, w.sub_ws, w.sub_bytes, stream);
+          if (st != LIPCACHE_OK) return st;
+          dup = w.dup;
+        }
+        const unsigned tiles = static_cast<unsigned>((k + 31) / 32);
+        hipLaunchKernelGGL(construct_relation_kernel, dim3(tiles, tiles), dim3(1024), 0, s, w.zc, w.rc, k, d, w.rel);
+        LC_LAUNCHED();
+      }
+      AcceptParams ap;
+      ap.k = k;
+      ap.dedup = dedup;
+      ap.dup_label = dup;
+      ap.rel = dedup ? w.rel : nullptr;
+      ap.lc = w.lc;
+      ap.src_c = w.src_c;
+      ap.sel = w.sel;
+      ap.class_count = w.class_count;
+      ap.n_classes = ncls;
+      ap.per_class = per_class;
+      ap.total = total_dev;
+      ap.budget = static_cast<unsigned long long>(bud);
+      ap.selected_out = selected_out;
+      hipLaunchKernelGGL(construct_accept_kernel, dim3(1), dim3(1024), 0, s, ap);
+      LC_LAUNCHED();
+      int64_t got = 0;
+      const lipcache_status st = lipcache_insert(c, w.zc, w.lc, w.rc, w.sel, k, &got, w.sub_ws, w.sub_bytes, stream);
+      if (st != LIPCACHE_OK) return st;
+      added += got;
+    }
+  } else {
+    // groups: all eligible candidates, or each payload class in ascending order
+    const int64_t kb = (N + 255) / 256;
+    const int ngroups = per_class > 0 ? n_classes : 1;
+    for (int gi = 0; gi < ngroups; ++gi) {
+      KcParams kp;
+      kp.z = z;
+      kp.r = r;
+      kp.prio = nullptr;
+      kp.label = label;
+      kp.guard = guard_label;
+      kp.n = N;
+      kp.d = d;
+      kp.bf16 = bf16;
+      kp.n_classes = ncls;
+      kp.group = per_class > 0 ? gi : -1;
+      kp.mind = w.mind;
+      kp.pick = w.pick;
+      kp.part_v = w.part_v;
+      kp.part_i = w.part_i;
+      kp.total = total_dev;
+      kp.budget = static_cast<unsigned long long>(bud);
+      kp.picks = w.picks;
+      kp.group_count = w.group_count;
+      const int64_t lim = per_class > 0 ? (per_class < bud ? per_class : bud) : bud;
+      kp.limit = static_cast<int>(lim < INT_MAX ? lim : INT_MAX);
+      hipLaunchKernelGGL(kcenter_start_kernel, dim3(1), dim3(256), 0, s, label, order, n_elig, kp.group, w.start);
+      LC_LAUNCHED();
+      hipLaunchKernelGGL(kcenter_init_kernel, dim3(static_cast<unsigned>(kb)), dim3(256), 0, s, kp, w.start);
+      LC_LAUNCHED();
+      const int64_t steps = (lim < n_elig ? lim : n_elig) - 1;
+      for (int64_t it = 0; it < steps; ++it) {
+        hipLaunchKernelGGL(kcenter_step_kernel, dim3(static_cast<unsigned>(kb)), dim3(256), 0, s, kp);
+        LC_LAUNCHED();
+        hipLaunchKernelGGL(kcenter_pick_kernel, dim3(1), dim3(256), 0, s, kp, static_cast<int>(kb));
+        LC_LAUNCHED();
+      }
+    }
+    LC_HIP(hipMemcpyAsync(host_cnt, w.counters, 16, hipMemcpyDeviceToHost, s));
+    LC_HIP(hipStreamSynchronize(s));
+    const int64_t npick = static_cast<int64_t>(host_cnt[1]);
+    if (selected_out && npick > 0)
+      LC_HIP(hipMemcpyAsync(selected_out, w.picks, static_cast<size_t>(npick) * 8, hipMemcpyDeviceToDevice, s));
+    for (int64_t t0 = 0; t0 < npick; t0 += kChunk) {
+      const int k = static_cast<int>(npick - t0 < kChunk ? npick - t0 : kChunk);
+      hipLaunchKernelGGL(kcenter_gather_kernel, dim3(static_cast<unsigned>((k + 3) / 4)), dim3(256), 0, s, z, label, r,
+                         w.picks, t0, k, d, bf16, w.zc, w.lc, w.rc);
+      LC_LAUNCHED();
+      int64_t got = 0;
+      const lipcache_status st = lipcache_insert(c, w.zc, w.lc, w.rc, nullptr, k, &got, w.sub_ws, w.sub_bytes, stream);
+      if (st != LIPCACHE_OK) return st;
+      added += got;
+    }
+  }
+  if (appended) *appended = added;
+  return LIPCACHE_OK;
+}

@@ -225,6 +225,83 @@ def stream_bench(args, cfg) -> int:
     return 0
 
 
+def construct_bench(args, cfg) -> int:
+    """Offline construction (Alg. 1) of a cache from the workload's N candidates:
+    spectral norm, certify with the tight radius (the paper's default),
+    select with the chosen strategy under a per-class budget.  One step =
+    the whole construction into an emptied cache."""
+    import numpy as np
+    import torch
+
+    from paper_2608_13144_amd import api
+    from paper_2608_13144_amd import workload as wlmod
+
+    dev = torch.device("cuda:0")
+    N, d, C = cfg.n_cache, cfg.d, cfg.C
+    t0 = time.perf_counter()
+    wl = wlmod.make_workload(cfg, seed=0)
+    log(f"workload {cfg.name}: {N} candidates, d={d}, C={C}; drawn in {time.perf_counter() - t0:.1f} s")
+    g = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)  # noqa: E731
+    W, b, z = g(wl.W), g(wl.b), g(wl.z)
+    budget = args.per_class * C
+    cache = api.LipCache(d, budget, store=cfg.store_dtype, device=dev)
+    pri = g(np.random.default_rng(1).random(N).astype(np.float32)) if args.construct == "priority" else None
+
+    def step():
+        cache.n = 0
+        s = api.spectral_norm(W).sigma
+        cert = api.certify(z, W, b, s, store=cfg.store_dtype, radius_mode="tight")
+        return cache.construct(z, cert.label, cert.r, strategy=args.construct, per_class=args.per_class,
+                               n_classes=C, priority=pri)
+
+    for _ in range(max(1, args.warmup)):
+        step()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(args.steps):
+        ts = time.perf_counter()
+        n_app, _sel = step()
+        torch.cuda.synchronize()
+        times.append(time.perf_counter() - ts)
+    t = float(np.median(times))
+    log(f"construct {args.construct}: {n_app} of {N} candidates appended; median {t * 1e3:.2f} ms per construction")
+    out = {
+        "metric": "offline construction (Alg. 1): candidates processed per second",
+        "value": N / t,
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": t * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "N": N, "d": d, "C": C, "strategy": args.construct,
+                   "per_class": args.per_class, "radius": "tight",
+                   "step": "spectral_norm+certify(N, tight)+construct"},
+        "appended": n_app,
+        "roofline": None,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        m = min(N, 4000)
+        ts = time.perf_counter()
+        sig = oracle.spectral_norm(wl.W).sigma
+        cert = oracle.certify(wl.z[:m], wl.W, wl.b, sig, store=cfg.store_dtype, radius_mode="tight")
+        st = oracle.CacheState(d=d, capacity=budget, store=cfg.store_dtype)
+        oracle.construct(st, wl.z[:m], cert.label, cert.r, strategy=args.construct, budget_per_class=args.per_class,
+                         n_classes=C, priority=None if pri is None else pri.cpu().numpy()[:m])
+        tc = time.perf_counter() - ts
+        out["cpu_baseline"] = {"value": m / tc, "unit": "candidates/s", "cores": _blas_threads()[0], "kind": "oracle",
+                               "sample": f"the first {m} candidates (tight certify + oracle.construct)",
+                               "seconds": tc}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -234,6 +311,9 @@ def main() -> int:
     ap.add_argument("--precision", default="bf16", choices=["bf16", "f32"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--construct", default="", choices=["", "radius_dedup", "priority", "kcenter"],
+                    help="time the offline construction (Alg. 1) of a cache from the workload's candidates")
+    ap.add_argument("--per-class", type=int, default=200, help="per-class budget of --construct")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (5 times) to calibrate HBM byte counters")
     args = ap.parse_args()
@@ -261,6 +341,8 @@ def main() -> int:
 
     dev = torch.device("cuda:0")
     cfg = wlmod.CONFIGS[args.workload]
+    if args.construct:
+        return construct_bench(args, cfg)
     if cfg.rounds != 1:
         return stream_bench(args, cfg)
     N, B, d, C = cfg.n_cache, cfg.batch, cfg.d, cfg.C

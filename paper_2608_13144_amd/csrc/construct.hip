@@ -262,50 +262,119 @@ struct AcceptParams {
 };
 
 // One workgroup decides the chunk in visit order.  All threads stage the
-// relation and the class counts in LDS; wave 0 then walks the chunk: lane l
-// keeps bits 32 l .. 32 l + 31 of the accepted set, so "inside an accepted
-// earlier ball" is one AND per lane and one ballot.
+// relation, the chunk's labels, the lookup verdicts, a per-row "has any
+// relation bit" flag and the class counts in LDS; wave 0 then walks the
+// chunk: lane l keeps bits 32 l .. 32 l + 31 of the accepted set, so
+// "inside an accepted earlier ball" is one AND per lane and one ballot,
+// needed only for rows that have a relation bit at all.
 __global__ __launch_bounds__(1024) void construct_accept_kernel(const AcceptParams p) {
   __shared__ uint32_t srel[kChunk * kChunkWords];  // 128 KiB
-  __shared__ int32_t scount[kMaxClasses / 16];      // first 1024 classes cached; the rest from global
+  __shared__ int32_t scount[kMaxClasses / 16];      // the first 1024 classes; the rest from global
+  __shared__ int32_t slab[kChunk];
+  __shared__ uint8_t sfree[kChunk];                 // not inside a cached ball
+  __shared__ uint8_t srow[kChunk];                  // relation row j has a bit
   const int t = static_cast<int>(threadIdx.x);
   if (p.dedup) {
     for (int e = t; e < p.k * kChunkWords; e += 1024) srel[e] = p.rel[e];
+  }
+  if (t < p.k) {
+    slab[t] = p.lc[t];
+    sfree[t] = p.dup_label ? (p.dup_label[t] == LIPCACHE_MISS ? 1 : 0) : 1;
   }
   const int cached = p.n_classes < kMaxClasses / 16 ? p.n_classes : kMaxClasses / 16;
   if (p.per_class > 0)
     for (int c = t; c < cached; c += 1024) scount[c] = p.class_count[c];
   __syncthreads();
+  if (t < p.k) {
+    uint32_t any = 0u;
+    if (p.dedup) {
+      const int words = (t + 31) / 32;  // only a < t can be set
+      for (int w = 0; w < words; ++w) any |= srel[t * kChunkWords + w];
+    }
+    srow[t] = any != 0u ? 1 : 0;
+  }
+  __syncthreads();
   if (t >= kWave) return;
   const int lane = t;
+  const unsigned long long lt = (1ull << lane) - 1ull;
   uint32_t acc_bits = 0u;  // lane's word of the accepted set (lanes >= kChunkWords stay 0)
   unsigned long long total = *p.total;
-  for (int j = 0; j < p.k; ++j) {
-    bool take = total < p.budget;
-    if (take && p.dup_label) take = p.dup_label[j] == LIPCACHE_MISS;
-    const int c = p.lc[j];
-    if (take && p.per_class > 0) {
-      const int cnt = c < cached ? scount[c] : p.class_count[c];
-      take = cnt < p.per_class;
-    }
-    if (take && p.dedup) {
-      const uint32_t row = lane < kChunkWords ? srel[j * kChunkWords + lane] : 0u;
-      take = __ballot((row & acc_bits) != 0u) == 0ull;
-    }
-    if (lane == 0) p.sel[j] = take ? LIPCACHE_MISS : 0;
-    if (take) {
-      if (lane == j / 32) acc_bits |= 1u << (j % 32);
-      if (lane == 0) {
-        if (p.per_class > 0) {
+  // Windows of 64 candidates.  Without relation rows a window is decided at
+  // once: the k-th free candidate of class c in the window passes its class
+  // test iff count[c] + k < per_class, and the passers are taken in order up
+  // to the total budget - exactly what the one-by-one visit does.  A window
+  // with a relation row is walked one candidate at a time.
+  for (int w0 = 0; w0 < p.k; w0 += kWave) {
+    const int j = w0 + lane;
+    const bool in = j < p.k;
+    const int c = in ? slab[j] : 0;
+    const bool fr = in && sfree[j] != 0;
+    const bool rel = __ballot(in && srow[j] != 0) != 0ull;
+    if (!rel) {
+      bool pass = fr;
+      unsigned long long same = 0ull;
+      if (p.per_class > 0) {
+        same = __ballot(fr);
+#pragma unroll
+        for (int b = 0; b < 14; ++b) {
+          const bool bit = (c >> b) & 1;
+          const unsigned long long bal = __ballot(bit);
+          same &= bit ? bal : ~bal;
+        }
+        const int rank = __builtin_popcountll(same & lt);
+        if (fr) {
+          const int cnt = c < cached ? scount[c] : p.class_count[c];
+          pass = cnt + rank < p.per_class;
+        }
+      }
+      const unsigned long long pm = __ballot(pass);
+      const unsigned long long grank = static_cast<unsigned long long>(__builtin_popcountll(pm & lt));
+      const bool take = pass && total + grank < p.budget;
+      const unsigned long long tm = __ballot(take);
+      if (in) p.sel[j] = take ? LIPCACHE_MISS : 0;
+      if (take && p.selected_out) p.selected_out[total + grank] = p.src_c[j];
+      if (p.per_class > 0 && fr && __builtin_popcountll(same & lt) == 0) {
+        const int add = __builtin_popcountll(same & tm);  // taken members of this lane's class group
+        if (add) {
           if (c < cached) {
-            scount[c] += 1;
+            scount[c] += add;
           } else {
-            p.class_count[c] += 1;
+            p.class_count[c] += add;
           }
         }
-        if (p.selected_out) p.selected_out[total] = p.src_c[j];
       }
-      total += 1;
+      if (lane == (w0 >> 5)) acc_bits |= static_cast<uint32_t>(tm);
+      if (lane == (w0 >> 5) + 1) acc_bits |= static_cast<uint32_t>(tm >> 32);
+      total += static_cast<unsigned long long>(__builtin_popcountll(tm));
+      continue;
+    }
+    const int jend = w0 + kWave < p.k ? w0 + kWave : p.k;
+    for (int jj = w0; jj < jend; ++jj) {
+      const int cj = slab[jj];
+      bool take = total < p.budget && sfree[jj] != 0;
+      if (take && p.per_class > 0) {
+        const int cnt = cj < cached ? scount[cj] : p.class_count[cj];
+        take = cnt < p.per_class;
+      }
+      if (take && srow[jj] != 0) {
+        const uint32_t row = lane < kChunkWords ? srel[jj * kChunkWords + lane] : 0u;
+        take = __ballot((row & acc_bits) != 0u) == 0ull;
+      }
+      if (lane == 0) p.sel[jj] = take ? LIPCACHE_MISS : 0;
+      if (take) {
+        if (lane == jj / 32) acc_bits |= 1u << (jj % 32);
+        if (lane == 0) {
+          if (p.per_class > 0) {
+            if (cj < cached) {
+              scount[cj] += 1;
+            } else {
+              p.class_count[cj] += 1;
+            }
+          }
+          if (p.selected_out) p.selected_out[total] = p.src_c[jj];
+        }
+        total += 1;
+      }
     }
   }
   if (lane == 0) *p.total = total;

@@ -7,4 +7,5 @@ from .lipcache_oracle import *  # noqa: F401,F403
 from .lipcache_oracle import (MISS, BAND_REL, DegenerateHead, CapacityError,  # noqa: F401
                               bf16_round, stored_values, spectral_norm, certify,
                               logits_of, lookup, lookup_rows, lookup_blocked, insert,
-                              CacheState, construct, SELECT_STRATEGIES)
+                              CacheState, construct, SELECT_STRATEGIES,
+                              boundary_radius, consistency, BOUNDARY_MODES)

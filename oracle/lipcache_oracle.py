@@ -28,6 +28,10 @@ bfloat16 cache), with float64 as the stand-in for exact arithmetic:
                          Alg. 1): eligibility, budgets and the selection
                          strategies (radius-prioritised de-duplication,
                          caller priority / random, K-center).
+  * ``boundary_radius``, ``consistency`` - the reuse boundaries compared in
+                         Sec. 6 (scaled certified radius, global threshold,
+                         inter-class empirical radius) and the
+                         certified-consistency count.
   * ``bf16_round``     - round-to-nearest-even float32 -> bfloat16 (storage).
 
 Pins: every function is checked in ``tests/`` against closed forms, brute
@@ -549,3 +553,53 @@ def construct(state: CacheState, z, label, r, strategy: str = "radius_dedup", bu
         state.label = np.concatenate([state.label, lab[sel]])
         state.norm2 = np.concatenate([state.norm2, np.sum(zs[sel].astype(np.float64) ** 2, axis=1)])
     return sel
+
+
+# ------------------------------------------------- reuse boundaries, metric
+BOUNDARY_MODES = ("scaled", "global", "interclass")
+
+
+def boundary_radius(state: CacheState, mode: str, factor: float) -> np.ndarray:
+    """Per-entry reuse radii for the boundary comparisons of Sec. 6 (float32).
+
+    * ``scaled``     - factor * r_i: radius tightening for factor <= 1, which
+                       keeps every hit inside its certified ball.
+    * ``global``     - factor for every entry: one global nearest-neighbour
+                       threshold tau (the nearest entry within tau is reused).
+    * ``interclass`` - an empirical radius from inter-class distance
+                       statistics: factor * 1/2 * min_{c != y_i} ||mu_{y_i} -
+                       mu_c||, where mu_c is the mean of the cached features
+                       of label c (float64); +inf when no other label is
+                       cached.
+    Entries with r_i <= 0 keep radius 0 (never hit).
+    """
+    r = state.r.astype(np.float64)
+    live = state.r > 0
+    if mode == "scaled":
+        out = factor * r
+    elif mode == "global":
+        out = np.full(state.n, float(factor))
+    elif mode == "interclass":
+        lab = state.label
+        classes = np.unique(lab[live])
+        z = state.z.astype(np.float64)
+        mu = {int(c): z[live & (lab == c)].mean(axis=0) for c in classes}
+        half = {}
+        for c in classes:
+            others = [np.linalg.norm(mu[int(c)] - mu[int(o)]) for o in classes if o != c]
+            half[int(c)] = 0.5 * min(others) if others else np.inf
+        out = np.array([factor * half.get(int(l), 0.0) for l in lab])
+    else:
+        raise ValueError(f"unknown boundary mode {mode!r}")
+    out = np.where(live, out, 0.0)
+    return out.astype(np.float32)
+
+
+def consistency(lookup_label, head_label):
+    """Certified-consistency bookkeeping (Sec. 6): among the hits (lookup
+    label != MISS), how many return the head's own argmax at the query.
+    Returns (hits, consistent)."""
+    lk = np.asarray(lookup_label, dtype=np.int64)
+    hd = np.asarray(head_label, dtype=np.int64)
+    hit = lk != MISS
+    return int(hit.sum()), int((hit & (lk == hd)).sum())

@@ -302,6 +302,71 @@ def construct_bench(args, cfg) -> int:
     return 0
 
 
+def boundaries_bench(args, cfg) -> int:
+    """The reuse-boundary comparison of the paper's Sec. 6 on a synthetic workload:
+    for each boundary, the hit rate, the certified-consistency rate (hits
+    returning the head's own argmax at the query) and the lookup time."""
+    import numpy as np
+    import torch
+
+    from paper_2608_13144_amd import api
+    from paper_2608_13144_amd import workload as wlmod
+
+    dev = torch.device("cuda:0")
+    N, B, d, C = cfg.n_cache, cfg.batch, cfg.d, cfg.C
+    wl = wlmod.make_workload(cfg, seed=0)
+    g = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)  # noqa: E731
+    W, b, zc = g(wl.W), g(wl.b), g(wl.z)
+    sig = api.spectral_norm(W).sigma
+    cert = api.certify(zc, W, b, sig, store=cfg.store_dtype)
+    tight = api.certify(zc, W, b, sig, store=cfg.store_dtype, radius_mode="tight")
+    cache = api.LipCache(d, N, store=cfg.store_dtype, device=dev)
+    cache.insert(zc, cert.label, cert.r)
+    draws = wlmod.draw_queries(wl, 0)
+    idx = torch.from_numpy(wlmod.near_indices(draws, cache.n)).to(dev)
+    zq = g(wlmod.compose_queries(draws, cache.z[idx].float().cpu().numpy(), cache.r[idx].cpu().numpy()))
+    head = api.certify(zq, W, b, sig, store=cfg.store_dtype).label
+    r_med = float(cache.r[: cache.n].median().item())
+    boundaries = [("certified conservative (Eq. 21)", cache.r[: cache.n]),
+                  ("certified tight (Remark 5.1)", tight.r[: cache.n]),
+                  ("tightened 0.5 x conservative", cache.boundary_radius("scaled", 0.5)),
+                  (f"global threshold tau = 2 x median r = {2 * r_med:.4f}", cache.boundary_radius("global", 2 * r_med)),
+                  ("inter-class empirical (half the nearest class-mean gap)",
+                   cache.boundary_radius("interclass", 1.0, n_classes=C))]
+    rows = []
+    for name, r in boundaries:
+        view = cache.with_radii(r.contiguous())
+        for _ in range(max(1, args.warmup)):
+            res = view.lookup(zq)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            res = view.lookup(zq)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        hits, cons = api.consistency(res.label, head)
+        rows.append({"boundary": name, "hit_rate": hits / B, "consistency_rate": (cons / hits) if hits else None,
+                     "hits": hits, "consistent": cons, "lookup_ms": ms,
+                     "rechecked_pairs": int(res.stats[1].item())})
+        log(f"{name}: hit rate {hits / B:.4f}, consistency {cons}/{hits}, lookup {ms:.2f} ms")
+    out = {
+        "metric": "reuse boundaries: hit rate and certified-consistency rate",
+        "value": B / (rows[0]["lookup_ms"] * 1e-3),
+        "unit": "lookups/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": rows[0]["lookup_ms"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": args.precision, "data": "synthetic",
+        "config": {"workload": cfg.name, "N": N, "B": B, "d": d, "C": C, "step": "lookup per boundary"},
+        "boundaries": rows,
+        "roofline": None, "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -314,6 +379,8 @@ def main() -> int:
     ap.add_argument("--construct", default="", choices=["", "radius_dedup", "priority", "kcenter"],
                     help="time the offline construction (Alg. 1) of a cache from the workload's candidates")
     ap.add_argument("--per-class", type=int, default=200, help="per-class budget of --construct")
+    ap.add_argument("--boundaries", action="store_true",
+                    help="compare reuse boundaries (hit rate, certified-consistency rate) on the workload")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (5 times) to calibrate HBM byte counters")
     args = ap.parse_args()
@@ -343,6 +410,8 @@ def main() -> int:
     cfg = wlmod.CONFIGS[args.workload]
     if args.construct:
         return construct_bench(args, cfg)
+    if args.boundaries:
+        return boundaries_bench(args, cfg)
     if cfg.rounds != 1:
         return stream_bench(args, cfg)
     N, B, d, C = cfg.n_cache, cfg.batch, cfg.d, cfg.C

@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define LIPCACHE_ABI_VERSION 3
+#define LIPCACHE_ABI_VERSION 4
 
 /* Same type as hipStream_t. */
 typedef struct ihipStream_t* lipcache_stream_t;
@@ -59,6 +59,13 @@ enum { LIPCACHE_F32 = 0, LIPCACHE_BF16 = 1 };
 /* Radius modes (policy component rho, Sec. 4.3): the conservative radius of
  * Eq. (21) or the tight per-pair radius of Remark 5.1, Eq. (29). */
 enum { LIPCACHE_RADIUS_CONSERVATIVE = 0 /* Eq. (21) */, LIPCACHE_RADIUS_TIGHT = 1 /* Remark 5.1 */ };
+
+/* Reuse boundaries compared with the certified radius (Sec. 6). */
+enum {
+  LIPCACHE_BOUNDARY_SCALED = 0,     /* factor * r_i (radius tightening)               */
+  LIPCACHE_BOUNDARY_GLOBAL = 1,     /* one nearest-neighbour threshold for all        */
+  LIPCACHE_BOUNDARY_INTERCLASS = 2  /* empirical: half the nearest class-mean gap     */
+};
 
 /* Cache selection strategies S of the offline construction (Alg. 1). */
 enum {
@@ -259,6 +266,42 @@ lipcache_status lipcache_construct(lipcache_cache* c, const float* z, const int3
                                    void* ws, size_t ws_bytes, lipcache_stream_t stream);
 size_t lipcache_construct_workspace_bytes(const lipcache_cache* c, int64_t N, int32_t n_classes,
                                           int64_t budget);
+
+/*
+ * Reuse boundaries for the comparison of Sec. 6: a radius per cache entry,
+ * written to r_out [c->n] float, for use with lipcache_lookup on a copy of
+ * the cache descriptor whose `r` points at r_out (features, labels and
+ * norms are shared).  Entries whose certified radius c->r[i] is not
+ * positive get 0.
+ *  mode LIPCACHE_BOUNDARY_SCALED: factor * r_i (0 <= factor; factor <= 1 is
+ *       the paper's radius tightening and keeps every hit certified)
+ *       LIPCACHE_BOUNDARY_GLOBAL: factor for every live entry (a global
+ *       nearest-neighbour threshold tau: the nearest entry within tau is
+ *       reused)
+ *       LIPCACHE_BOUNDARY_INTERCLASS: factor * 1/2 * min over other labels o
+ *       of ||mu_{y_i} - mu_o||, mu_c = mean of the live cached features of
+ *       label c (float64); +inf when no other label is cached.  Labels must
+ *       lie in [0, n_classes) (1 <= n_classes <= 65536); an entry outside
+ *       gets 0 and is left out of the means.
+ *  ws   lipcache_boundary_radius_workspace_bytes(c->d, n_classes) bytes
+ *       (INTERCLASS only; may be NULL otherwise)
+ * (async)
+ */
+lipcache_status lipcache_boundary_radius(const lipcache_cache* c, int32_t mode, double factor,
+                                         int32_t n_classes, float* r_out, void* ws, size_t ws_bytes,
+                                         lipcache_stream_t stream);
+size_t lipcache_boundary_radius_workspace_bytes(int32_t d, int32_t n_classes);
+
+/*
+ * Certified-consistency count (Sec. 6): counts[0] = hits (lookup_label !=
+ * LIPCACHE_MISS), counts[1] = hits whose label equals head_label, the
+ * head's argmax at the same query (e.g. lipcache_certify's label_out for
+ * the queries).  The consistency rate is counts[1] / counts[0].
+ *  lookup_label [B], head_label [B] int32; counts [2] uint64 (device)
+ * (async)
+ */
+lipcache_status lipcache_consistency(const int32_t* lookup_label, const int32_t* head_label, int64_t B,
+                                     uint64_t* counts, lipcache_stream_t stream);
 
 /*
  * Diagnostic view of the lookup's distance filter for small problems.  For

@@ -14,6 +14,7 @@ OK, EINVAL, EDEGENERATE, ENOCONV, ECAPACITY, EUNSUPPORTED, EWORKSPACE, EHIP = ra
 F32, BF16 = 0, 1
 RADIUS_CONSERVATIVE, RADIUS_TIGHT = 0, 1
 SELECT_RADIUS_DEDUP, SELECT_PRIORITY, SELECT_KCENTER = 0, 1, 2
+BOUNDARY_SCALED, BOUNDARY_GLOBAL, BOUNDARY_INTERCLASS = 0, 1, 2
 MISS = -1
 STAT_HITS, STAT_RECHECKED, STAT_BAND_PAIRS, STAT_BAND_QUERIES = range(4)
 
@@ -54,6 +55,9 @@ SIGNATURES = {
     "lipcache_construct": (_i32, [_PCACHE, _vp, _vp, _vp, _vp, _vp, _i64, _i32, _i64, _i32, _i32, _vp,
                                   ctypes.POINTER(_i64), _vp, _sz, _vp]),
     "lipcache_construct_workspace_bytes": (_sz, [_PCACHE, _i64, _i32, _i64]),
+    "lipcache_boundary_radius": (_i32, [_PCACHE, _i32, _f64, _i32, _vp, _vp, _sz, _vp]),
+    "lipcache_boundary_radius_workspace_bytes": (_sz, [_i32, _i32]),
+    "lipcache_consistency": (_i32, [_vp, _vp, _i64, _vp, _vp]),
     "lipcache_status_string": (ctypes.c_char_p, [_i32]),
     "lipcache_abi_version": (_i32, []),
 }

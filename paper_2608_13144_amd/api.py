@@ -17,6 +17,7 @@ _STORE = {"f32": L.F32, "bf16": L.BF16}
 _PRECISION = {"f32": L.F32, "bf16": L.BF16}
 _RADIUS = {"conservative": L.RADIUS_CONSERVATIVE, "tight": L.RADIUS_TIGHT}
 _SELECT = {"radius_dedup": L.SELECT_RADIUS_DEDUP, "priority": L.SELECT_PRIORITY, "kcenter": L.SELECT_KCENTER}
+_BOUNDARY = {"scaled": L.BOUNDARY_SCALED, "global": L.BOUNDARY_GLOBAL, "interclass": L.BOUNDARY_INTERCLASS}
 
 
 def _p(t: torch.Tensor | None):
@@ -226,6 +227,29 @@ class LipCache:
         self.n = int(cs.n)
         return int(got.value), sel[: got.value]
 
+    def boundary_radius(self, mode: str, factor: float, n_classes: int = 0) -> torch.Tensor:
+        """lipcache_boundary_radius: per-entry radii of a reuse boundary (async)."""
+        lib = L.load()
+        out = torch.empty(max(self.n, 1), dtype=torch.float32, device=self.device)
+        ws = workspace(lib.lipcache_boundary_radius_workspace_bytes(self.d, int(n_classes)), self.device)
+        cs = self.cstruct()
+        st = lib.lipcache_boundary_radius(ctypes.byref(cs), _BOUNDARY[mode], float(factor), int(n_classes),
+                                          _p(out), _p(ws), ws.numel(), _stream(self.device))
+        L.check("lipcache_boundary_radius", st)
+        return out[: self.n]
+
+    def with_radii(self, r: torch.Tensor) -> "LipCache":
+        """A lookup-only view of this cache whose radii are ``r`` (features,
+        labels and norms shared)."""
+        _need_cuda(r, "r", torch.float32, 1)
+        if r.shape[0] < self.n:
+            raise ValueError("with_radii: one radius per live entry")
+        v = LipCache.__new__(LipCache)
+        v.__dict__.update(self.__dict__)
+        v.r = r
+        v._ws = None
+        return v
+
     def filter_dump(self, zq: torch.Tensor, precision: str = "bf16"):
         """lipcache_lookup_filter_dump: matrix-core dot products and filter decisions (small sizes)."""
         _need_cuda(zq, "zq", torch.float32, 2)
@@ -240,3 +264,18 @@ class LipCache:
                                              ws.numel(), _stream(self.device))
         L.check("lipcache_lookup_filter_dump", st)
         return g_hat, cand
+
+
+def consistency(lookup_label: torch.Tensor, head_label: torch.Tensor) -> tuple[int, int]:
+    """lipcache_consistency: (hits, hits returning the head's own label) (sync)."""
+    _need_cuda(lookup_label, "lookup_label", torch.int32, 1)
+    _need_cuda(head_label, "head_label", torch.int32, 1)
+    if lookup_label.shape != head_label.shape:
+        raise ValueError("consistency: shapes differ")
+    lib = L.load()
+    counts = torch.empty(2, dtype=torch.int64, device=lookup_label.device)
+    st = lib.lipcache_consistency(_p(lookup_label), _p(head_label), lookup_label.shape[0], _p(counts),
+                                  _stream(lookup_label.device))
+    L.check("lipcache_consistency", st)
+    h, c = counts.cpu().tolist()
+    return int(h), int(c)

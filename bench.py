@@ -367,6 +367,89 @@ def boundaries_bench(args, cfg) -> int:
     return 0
 
 
+def indexed_bench(args, cfg) -> int:
+    """The exact cluster-pruned lookup (an index of K clusters over the cache)
+    against the dense lookup on the same cache and batch: one step = one
+    indexed lookup of the batch (query plan, pruned scan, finalize; one
+    host read-back).  The index build is timed once and reported."""
+    import numpy as np
+    import torch
+
+    from paper_2608_13144_amd import api
+    from paper_2608_13144_amd import workload as wlmod
+
+    dev = torch.device("cuda:0")
+    N, B, d, C = cfg.n_cache, cfg.batch, cfg.d, cfg.C
+    wl = wlmod.make_workload(cfg, seed=0)
+    g = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)  # noqa: E731
+    W, b, zc = g(wl.W), g(wl.b), g(wl.z)
+    sig = api.spectral_norm(W).sigma
+    cert = api.certify(zc, W, b, sig, store=cfg.store_dtype)
+    cache = api.LipCache(d, N, store=cfg.store_dtype, device=dev)
+    cache.insert(zc, cert.label, cert.r)
+    draws = wlmod.draw_queries(wl, 0)
+    idx = torch.from_numpy(wlmod.near_indices(draws, cache.n)).to(dev)
+    zq = g(wlmod.compose_queries(draws, cache.z[idx].float().cpu().numpy(), cache.r[idx].cpu().numpy()))
+    K = args.indexed
+    ix = cache.build_index(K, args.index_iters)  # warm-up build
+    torch.cuda.synchronize()
+    tb = time.perf_counter()
+    ix = cache.build_index(K, args.index_iters)
+    torch.cuda.synchronize()
+    build_ms = (time.perf_counter() - tb) * 1e3
+    sizes = np.diff(ix.offsets.cpu().numpy())
+    log(f"index K={K} iters={args.index_iters}: built in {build_ms:.1f} ms; cluster sizes "
+        f"min {sizes.min()} median {int(np.median(sizes))} max {sizes.max()}; "
+        f"dead {int((ix.bound.cpu().numpy() == -np.inf).sum())}")
+    for _ in range(max(1, args.warmup)):
+        res_d = cache.lookup(zq, precision=args.precision)
+        res_i, pairs = cache.lookup_indexed(ix, zq, precision=args.precision)
+    torch.cuda.synchronize()
+    same = bool(torch.equal(res_i.label, res_d.label) and torch.equal(res_i.index, res_d.index))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        cache.lookup(zq, precision=args.precision, out=res_d)
+    e1.record()
+    torch.cuda.synchronize()
+    dense_ms = e0.elapsed_time(e1) / args.steps
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        res_i, pairs = cache.lookup_indexed(ix, zq, precision=args.precision, out=res_i)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / args.steps * 1e3
+    frac = pairs / (B * cache.n)
+    log(f"indexed lookup {ms:.3f} ms vs dense {dense_ms:.3f} ms ({dense_ms / ms:.1f}x); pairs scanned "
+        f"{pairs} = {frac:.4f} of B*N; same answers as dense: {same}")
+    flops = 2.0 * pairs * d
+    achieved = flops / (ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[args.precision]
+    out = {
+        "metric": "indexed certified lookups per second (exact cluster-pruned lookup)",
+        "value": B / (ms * 1e-3),
+        "unit": "lookups/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": args.precision, "data": "synthetic",
+        "config": {"workload": cfg.name, "N": cache.n, "B": B, "d": d, "C": C, "K": K,
+                   "index_iters": args.index_iters, "step": "lookup_indexed (plan + pruned scan + finalize)"},
+        "dense_lookup_ms": dense_ms,
+        "speedup_vs_dense": dense_ms / ms,
+        "pairs_scanned": pairs,
+        "pairs_fraction": frac,
+        "index_build_ms": build_ms,
+        "same_answers_as_dense": same,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None,
+                     "kernel": "whole indexed lookup (plan + scan + finalize)",
+                     "algorithmic": f"2*pairs*d = {flops:.4e} flop per lookup"},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -379,6 +462,9 @@ def main() -> int:
     ap.add_argument("--construct", default="", choices=["", "radius_dedup", "priority", "kcenter"],
                     help="time the offline construction (Alg. 1) of a cache from the workload's candidates")
     ap.add_argument("--per-class", type=int, default=200, help="per-class budget of --construct")
+    ap.add_argument("--indexed", type=int, default=0, metavar="K",
+                    help="time the exact cluster-pruned lookup with K clusters against the dense lookup")
+    ap.add_argument("--index-iters", type=int, default=4, help="Lloyd iterations of the index build")
     ap.add_argument("--boundaries", action="store_true",
                     help="compare reuse boundaries (hit rate, certified-consistency rate) on the workload")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -412,6 +498,8 @@ def main() -> int:
         return construct_bench(args, cfg)
     if args.boundaries:
         return boundaries_bench(args, cfg)
+    if args.indexed:
+        return indexed_bench(args, cfg)
     if cfg.rounds != 1:
         return stream_bench(args, cfg)
     N, B, d, C = cfg.n_cache, cfg.batch, cfg.d, cfg.C

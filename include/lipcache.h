@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define LIPCACHE_ABI_VERSION 4
+#define LIPCACHE_ABI_VERSION 5
 
 /* Same type as hipStream_t. */
 typedef struct ihipStream_t* lipcache_stream_t;
@@ -266,6 +266,57 @@ lipcache_status lipcache_construct(lipcache_cache* c, const float* z, const int3
                                    void* ws, size_t ws_bytes, lipcache_stream_t stream);
 size_t lipcache_construct_workspace_bytes(const lipcache_cache* c, int64_t N, int32_t n_classes,
                                           int64_t budget);
+
+/*
+ * Exact cluster index for a sublinear lookup (the paper points to an exact
+ * sublinear index for large caches).  Rows 0 .. n_indexed-1 of a cache are
+ * partitioned into K clusters (a few Lloyd iterations of k-means from
+ * evenly spaced rows); entry i of cluster c can contain a query q only if
+ * ||q - mu_c|| < R_c with R_c >= max over its live members of
+ * (||z_i - mu_c|| + r_i) (triangle inequality), so the indexed lookup scans
+ * only the clusters a query may need and returns exactly what
+ * lipcache_lookup returns.  Rows appended after the build are scanned in
+ * full.  All arrays are caller-owned device memory.
+ */
+typedef struct lipcache_index {
+  lipcache_cache sorted; /* the indexed rows in cluster order (same d and store_dtype as the
+                            cache, capacity >= n_indexed; zimg as for a cache)               */
+  int64_t* perm;         /* [n_indexed] cache row held by sorted row j                       */
+  int64_t* offsets;      /* [K + 1] cluster c = sorted rows [offsets[c], offsets[c + 1])     */
+  float* centers;        /* [K][d] cluster centres mu_c                                      */
+  float* bound;          /* [K] R_c, rounded up; -inf when no member can be hit              */
+  int32_t K;
+  int64_t n_indexed;     /* rows of the cache covered (the cache's n at build time)          */
+} lipcache_index;
+
+/*
+ * Build an index over rows 0 .. c->n-1 (K clusters, `iters` Lloyd
+ * iterations; 1 <= K <= 65536, K <= c->n).  Sets idx->K, idx->n_indexed and
+ * idx->sorted.n; the arrays of idx must be allocated by the caller.
+ *  ws lipcache_index_build_workspace_bytes(c->n, c->d, K) bytes
+ * (async)
+ */
+lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t K, int32_t iters,
+                                     lipcache_index* idx, void* ws, size_t ws_bytes,
+                                     lipcache_stream_t stream);
+size_t lipcache_index_build_workspace_bytes(int64_t n, int32_t d, int32_t K);
+
+/*
+ * lipcache_lookup through an index built on this cache: the same outputs
+ * (label, index into the cache, d^2, stats, band flags) as lipcache_lookup
+ * on the same cache.  pairs (host, nullable) out: query-entry pairs the
+ * filter scanned (B * c->n for the dense lookup).
+ *  ws lipcache_lookup_indexed_workspace_bytes(B, c->n, c->d, idx->K,
+ *     idx->n_indexed) bytes
+ * (sync: one read-back of the work-list size)
+ */
+lipcache_status lipcache_lookup_indexed(const lipcache_cache* c, const lipcache_index* idx,
+                                        const float* zq, int64_t B, int32_t precision,
+                                        int32_t* label_out, int64_t* index_out, float* dist2_out,
+                                        uint64_t* stats, uint8_t* band_flag, int64_t* pairs,
+                                        void* ws, size_t ws_bytes, lipcache_stream_t stream);
+size_t lipcache_lookup_indexed_workspace_bytes(int64_t B, int64_t n, int32_t d, int32_t K,
+                                               int64_t n_indexed);
 
 /*
  * Reuse boundaries for the comparison of Sec. 6: a radius per cache entry,

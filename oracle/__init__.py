@@ -8,4 +8,5 @@ from .lipcache_oracle import (MISS, BAND_REL, DegenerateHead, CapacityError,  # 
                               bf16_round, stored_values, spectral_norm, certify,
                               logits_of, lookup, lookup_rows, lookup_blocked, insert,
                               CacheState, construct, SELECT_STRATEGIES,
-                              boundary_radius, consistency, BOUNDARY_MODES)
+                              boundary_radius, consistency, BOUNDARY_MODES,
+                              cluster_pruned_lookup)

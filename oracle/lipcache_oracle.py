@@ -28,6 +28,10 @@ bfloat16 cache), with float64 as the stand-in for exact arithmetic:
                          Alg. 1): eligibility, budgets and the selection
                          strategies (radius-prioritised de-duplication,
                          caller priority / random, K-center).
+  * ``cluster_pruned_lookup`` - ``lookup`` through a partition of the rows,
+                         pruning clusters by the triangle inequality (the
+                         exact sublinear index of Sec. 4.4); pinned equal to
+                         ``lookup`` on every partition.
   * ``boundary_radius``, ``consistency`` - the reuse boundaries compared in
                          Sec. 6 (scaled certified radius, global threshold,
                          inter-class empirical radius) and the
@@ -593,6 +597,56 @@ def boundary_radius(state: CacheState, mode: str, factor: float) -> np.ndarray:
         raise ValueError(f"unknown boundary mode {mode!r}")
     out = np.where(live, out, 0.0)
     return out.astype(np.float32)
+
+
+def cluster_pruned_lookup(zq, cache_z, cache_r, cache_label, assign, centres=None):
+    """``lookup`` through a partition of the cache rows (the exact sublinear
+    index the paper points to in Sec. 4.4 for large caches).
+
+    ``assign[i]`` is the cluster of row i; the centre mu_c of a cluster is
+    ``centres[c]`` when given, else the float64 mean of its rows.  Its bound
+    is R_c = max over its live rows (r_i > 0) of ||z_i - mu_c|| + r_i; by the
+    triangle inequality a query z with ||z - mu_c|| >= R_c lies outside every
+    ball of the cluster, so only the rows of clusters with ||z - mu_c|| < R_c
+    are tested.  Returns (``LookupResult`` with indices into the whole cache,
+    number of (query, row) pairs tested).  The label, index, d^2 and hit
+    count equal ``lookup``'s for every partition; the band counts cover the
+    tested rows only.
+    """
+    Q = np.asarray(zq, dtype=np.float64)
+    Z = np.asarray(cache_z)
+    Z64 = Z.astype(np.float64)
+    r = np.asarray(cache_r, dtype=np.float32).astype(np.float64)
+    lab = np.asarray(cache_label, dtype=np.int32)
+    a = np.asarray(assign, dtype=np.int64)
+    K = int(a.max()) + 1 if a.size else 0
+    members = [np.flatnonzero(a == c) for c in range(K)]
+    mu = np.zeros((K, Z.shape[1]))
+    R = np.full(K, -np.inf)
+    for c, rows in enumerate(members):
+        if centres is not None:
+            mu[c] = np.asarray(centres[c], dtype=np.float64)
+        elif rows.size:
+            mu[c] = Z64[rows].mean(axis=0)
+        live = rows[r[rows] > 0]
+        if live.size:
+            R[c] = np.max(np.sqrt(np.sum((Z64[live] - mu[c]) ** 2, axis=1)) + r[live])
+    B = Q.shape[0]
+    parts = []
+    pairs = 0
+    for qi in range(B):
+        dc = np.sqrt(np.sum((mu - Q[qi]) ** 2, axis=1))
+        cand = [members[c] for c in range(K) if dc[c] < R[c]]
+        rows = np.sort(np.concatenate(cand)) if cand else np.zeros(0, np.int64)
+        pairs += rows.size
+        res = lookup(Q[qi:qi + 1], Z[rows], r[rows].astype(np.float32), lab[rows])
+        if res.index[0] >= 0:
+            res.index[0] = rows[res.index[0]]
+        parts.append(res)
+    cat = lambda f: np.concatenate([getattr(p, f) for p in parts]) if parts else np.zeros(0)  # noqa: E731
+    out = LookupResult(cat("label").astype(np.int32), cat("index").astype(np.int64), cat("dist2"),
+                       cat("n_hits").astype(np.int64), cat("n_band").astype(np.int64), cat("flagged").astype(bool))
+    return out, pairs
 
 
 def consistency(lookup_label, head_label):

@@ -40,6 +40,23 @@ class LipcacheCache(ctypes.Structure):
 
 _PCACHE = ctypes.POINTER(LipcacheCache)
 
+
+class LipcacheIndex(ctypes.Structure):
+    """Mirror of ``lipcache_index``."""
+
+    _fields_ = [
+        ("sorted", LipcacheCache),
+        ("perm", ctypes.c_void_p),
+        ("offsets", ctypes.c_void_p),
+        ("centers", ctypes.c_void_p),
+        ("bound", ctypes.c_void_p),
+        ("K", ctypes.c_int32),
+        ("n_indexed", ctypes.c_int64),
+    ]
+
+
+_PINDEX = ctypes.POINTER(LipcacheIndex)
+
 SIGNATURES = {
     "lipcache_spectral_norm": (_i32, [_vp, _i32, _i32, _i32, _f64, ctypes.POINTER(_f64), ctypes.POINTER(_i32),
                                       _vp, _sz, _vp]),
@@ -58,6 +75,11 @@ SIGNATURES = {
     "lipcache_boundary_radius": (_i32, [_PCACHE, _i32, _f64, _i32, _vp, _vp, _sz, _vp]),
     "lipcache_boundary_radius_workspace_bytes": (_sz, [_i32, _i32]),
     "lipcache_consistency": (_i32, [_vp, _vp, _i64, _vp, _vp]),
+    "lipcache_index_build": (_i32, [_PCACHE, _i32, _i32, _PINDEX, _vp, _sz, _vp]),
+    "lipcache_index_build_workspace_bytes": (_sz, [_i64, _i32, _i32]),
+    "lipcache_lookup_indexed": (_i32, [_PCACHE, _PINDEX, _vp, _i64, _i32, _vp, _vp, _vp, _vp, _vp,
+                                       ctypes.POINTER(_i64), _vp, _sz, _vp]),
+    "lipcache_lookup_indexed_workspace_bytes": (_sz, [_i64, _i64, _i32, _i32, _i64]),
     "lipcache_status_string": (ctypes.c_char_p, [_i32]),
     "lipcache_abi_version": (_i32, []),
 }

@@ -250,6 +250,57 @@ class LipCache:
         v._ws = None
         return v
 
+    def build_index(self, K: int, iters: int = 4) -> "ClusterIndex":
+        """lipcache_index_build over the current rows (async; the index owns its arrays)."""
+        lib = L.load()
+        n, d = self.n, self.d
+        if n < 1:
+            raise ValueError("build_index: the cache is empty")
+        ix = ClusterIndex.__new__(ClusterIndex)
+        ix.sorted = LipCache(d, n, store=self.store, device=self.device, image=self.zimg is not None)
+        ix.perm = torch.empty(n, dtype=torch.int64, device=self.device)
+        ix.offsets = torch.empty(int(K) + 1, dtype=torch.int64, device=self.device)
+        ix.centers = torch.empty((int(K), d), dtype=torch.float32, device=self.device)
+        ix.bound = torch.empty(int(K), dtype=torch.float32, device=self.device)
+        ix.K, ix.n_indexed = int(K), 0
+        ws = workspace(lib.lipcache_index_build_workspace_bytes(n, d, int(K)), self.device)
+        cs = self.cstruct()
+        st_ = ix.cstruct()
+        st = lib.lipcache_index_build(ctypes.byref(cs), int(K), int(iters), ctypes.byref(st_), _p(ws), ws.numel(),
+                                      _stream(self.device))
+        L.check("lipcache_index_build", st)
+        ix.n_indexed = int(st_.n_indexed)
+        ix.sorted.n = int(st_.sorted.n)
+        ix._build_ws = ws  # kept alive until the build has run
+        return ix
+
+    def lookup_indexed(self, index: "ClusterIndex", zq: torch.Tensor, precision: str = "bf16",
+                       out: LookupResult | None = None) -> tuple[LookupResult, int]:
+        """lipcache_lookup_indexed: the lookup's outputs through a cluster index
+        (sync).  Returns (result, query-entry pairs the filter scanned)."""
+        _need_cuda(zq, "zq", torch.float32, 2)
+        if zq.shape[1] != self.d:
+            raise ValueError("lookup_indexed: query width differs from the cache's d")
+        lib = L.load()
+        B = zq.shape[0]
+        dev = self.device
+        if out is None:
+            out = LookupResult(torch.empty(B, dtype=torch.int32, device=dev),
+                               torch.empty(B, dtype=torch.int64, device=dev),
+                               torch.empty(B, dtype=torch.float32, device=dev),
+                               torch.zeros(4, dtype=torch.int64, device=dev),
+                               torch.empty(B, dtype=torch.uint8, device=dev))
+        prec = _PRECISION[precision]
+        ws = self._workspace(lib.lipcache_lookup_indexed_workspace_bytes(B, self.n, self.d, index.K, index.n_indexed))
+        cs = self.cstruct()
+        ic = index.cstruct()
+        pairs = ctypes.c_int64(0)
+        st = lib.lipcache_lookup_indexed(ctypes.byref(cs), ctypes.byref(ic), _p(zq), B, prec, _p(out.label),
+                                         _p(out.index), _p(out.dist2), _p(out.stats), _p(out.band),
+                                         ctypes.byref(pairs), _p(ws), ws.numel(), _stream(dev))
+        L.check("lipcache_lookup_indexed", st)
+        return out, int(pairs.value)
+
     def filter_dump(self, zq: torch.Tensor, precision: str = "bf16"):
         """lipcache_lookup_filter_dump: matrix-core dot products and filter decisions (small sizes)."""
         _need_cuda(zq, "zq", torch.float32, 2)
@@ -264,6 +315,23 @@ class LipCache:
                                              ws.numel(), _stream(self.device))
         L.check("lipcache_lookup_filter_dump", st)
         return g_hat, cand
+
+
+class ClusterIndex:
+    """Exact cluster index of a LipCache (lipcache_index): the indexed rows in
+    cluster order, the cluster offsets, centres and bounds R_c."""
+
+    sorted: LipCache
+    perm: torch.Tensor      # int64 [n_indexed]: cache row of sorted row j
+    offsets: torch.Tensor   # int64 [K + 1]
+    centers: torch.Tensor   # float32 [K, d]
+    bound: torch.Tensor     # float32 [K]
+    K: int
+    n_indexed: int
+
+    def cstruct(self) -> L.LipcacheIndex:
+        return L.LipcacheIndex(self.sorted.cstruct(), self.perm.data_ptr(), self.offsets.data_ptr(),
+                               self.centers.data_ptr(), self.bound.data_ptr(), self.K, self.n_indexed)
 
 
 def consistency(lookup_label: torch.Tensor, head_label: torch.Tensor) -> tuple[int, int]:

@@ -28,12 +28,10 @@
 #include <limits.h>
 
 #include "lc_common.hpp"
+#include "lc_sort.hpp"
 
 namespace lc {
 
-constexpr int kSortThreads = 1024;  // one item per thread
-constexpr int kSortWaves = kSortThreads / kWave;
-constexpr int kBins = 256;
 constexpr int kChunk = 1024;              // candidates per greedy step
 constexpr int kChunkWords = kChunk / 32;  // relation row length in 32-bit words
 constexpr int kMaxClasses = 16384;        // class counts live in LDS
@@ -78,105 +76,6 @@ __global__ void construct_keys_kernel(const float* __restrict__ r, const float* 
   }
   const unsigned long long bal = __ballot(e);
   if (lane_id() == 0 && bal != 0ull) atomicAdd(n_elig, static_cast<unsigned long long>(__builtin_popcountll(bal)));
-}
-
-// hist[d * nb + b] = number of items of block b whose digit is d.
-__global__ __launch_bounds__(kSortThreads) void radix_hist_kernel(const uint32_t* __restrict__ keys, int64_t n,
-                                                                  int shift, int64_t nb, uint32_t* __restrict__ hist) {
-  __shared__ uint32_t h[kBins];
-  if (threadIdx.x < kBins) h[threadIdx.x] = 0u;
-  __syncthreads();
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * kSortThreads + threadIdx.x;
-  if (i < n) atomicAdd(&h[(keys[i] >> shift) & (kBins - 1)], 1u);
-  __syncthreads();
-  if (threadIdx.x < kBins) hist[static_cast<int64_t>(threadIdx.x) * nb + blockIdx.x] = h[threadIdx.x];
-}
-
-// Inclusive prefix sum over the 1024 threads of the block (wave shuffles,
-// then the 16 wave totals).
-__device__ __forceinline__ uint32_t block_inclusive_scan(uint32_t v, uint32_t* wave_tot, uint32_t& block_total) {
-  const int lane = lane_id();
-  const int wave = static_cast<int>(threadIdx.x) / kWave;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const uint32_t o = static_cast<uint32_t>(__shfl_up(static_cast<int>(v), off, kWave));
-    if (lane >= off) v += o;
-  }
-  if (lane == kWave - 1) wave_tot[wave] = v;
-  __syncthreads();
-  uint32_t before = 0, total = 0;
-  for (int w = 0; w < kSortWaves; ++w) {
-    const uint32_t t = wave_tot[w];
-    before += w < wave ? t : 0u;
-    total += t;
-  }
-  __syncthreads();
-  block_total = total;
-  return before + v;
-}
-
-// Block d: exclusive scan of hist[d * nb .. d * nb + nb) in place; the digit
-// total goes to dsum[d].
-__global__ __launch_bounds__(kSortThreads) void radix_digit_scan_kernel(uint32_t* __restrict__ hist, int64_t nb,
-                                                                        uint32_t* __restrict__ dsum) {
-  __shared__ uint32_t wave_tot[kSortWaves];
-  uint32_t* row = hist + static_cast<int64_t>(blockIdx.x) * nb;
-  uint32_t running = 0;
-  for (int64_t base = 0; base < nb; base += kSortThreads) {
-    const int64_t j = base + threadIdx.x;
-    const uint32_t v = j < nb ? row[j] : 0u;
-    uint32_t tot = 0;
-    const uint32_t incl = block_inclusive_scan(v, wave_tot, tot);
-    if (j < nb) row[j] = running + incl - v;
-    running += tot;
-  }
-  if (threadIdx.x == 0) dsum[blockIdx.x] = running;
-}
-
-// dbase[d] = sum of dsum[0 .. d) (one block of 256 threads, serial is fine).
-__global__ void radix_base_kernel(const uint32_t* __restrict__ dsum, uint32_t* __restrict__ dbase) {
-  if (threadIdx.x == 0) {
-    uint32_t s = 0;
-    for (int d = 0; d < kBins; ++d) {
-      dbase[d] = s;
-      s += dsum[d];
-    }
-  }
-}
-
-// Stable scatter: within a block, items keep their order among equal digits
-// (rank inside the wave from eight digit-bit ballots, then the counts of the
-// same digit in the block's earlier waves).
-__global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
-    const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in, int64_t n, int shift, int64_t nb,
-    const uint32_t* __restrict__ hist, const uint32_t* __restrict__ dbase, uint32_t* __restrict__ keys_out,
-    uint32_t* __restrict__ vals_out) {
-  __shared__ uint32_t wcount[kSortWaves][kBins];
-  for (int t = threadIdx.x; t < kSortWaves * kBins; t += kSortThreads) (&wcount[0][0])[t] = 0u;
-  __syncthreads();
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * kSortThreads + threadIdx.x;
-  const bool valid = i < n;
-  const uint32_t key = valid ? keys_in[i] : 0u;
-  const int dig = static_cast<int>((key >> shift) & (kBins - 1));
-  const int lane = lane_id();
-  const int wave = static_cast<int>(threadIdx.x) / kWave;
-  unsigned long long same = __ballot(valid);
-#pragma unroll
-  for (int b = 0; b < 8; ++b) {
-    const bool bit = (dig >> b) & 1;
-    const unsigned long long bal = __ballot(bit);
-    same &= bit ? bal : ~bal;
-  }
-  const int rank = __builtin_popcountll(same & ((1ull << lane) - 1ull));
-  if (valid && rank == 0) wcount[wave][dig] = static_cast<uint32_t>(__builtin_popcountll(same));
-  __syncthreads();
-  if (valid) {
-    uint32_t before = 0;
-    for (int w = 0; w < wave; ++w) before += wcount[w][dig];
-    const uint32_t pos = dbase[dig] + hist[static_cast<int64_t>(dig) * nb + blockIdx.x] + before + rank;
-    keys_out[pos] = key;
-    vals_out[pos] = vals_in[i];
-  }
 }
 
 // Chunk rows in visit order: the stored values (bf16-rounded for a bf16
@@ -687,22 +586,8 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
   hipLaunchKernelGGL(construct_keys_kernel, dim3(g256), dim3(256), 0, s, r, prio, label, guard_label, N, ncls,
                      w.keys[0], w.vals[0], w.counters);
   LC_LAUNCHED();
-  const int64_t nb = (N + kSortThreads - 1) / kSortThreads;
   int cur = 0;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 8 * pass;
-    hipLaunchKernelGGL(radix_hist_kernel, dim3(static_cast<unsigned>(nb)), dim3(kSortThreads), 0, s, w.keys[cur], N,
-                       shift, nb, w.hist);
-    LC_LAUNCHED();
-    hipLaunchKernelGGL(radix_digit_scan_kernel, dim3(kBins), dim3(kSortThreads), 0, s, w.hist, nb, w.dsum);
-    LC_LAUNCHED();
-    hipLaunchKernelGGL(radix_base_kernel, dim3(1), dim3(64), 0, s, w.dsum, w.dbase);
-    LC_LAUNCHED();
-    hipLaunchKernelGGL(radix_scatter_kernel, dim3(static_cast<unsigned>(nb)), dim3(kSortThreads), 0, s, w.keys[cur],
-                       w.vals[cur], N, shift, nb, w.hist, w.dbase, w.keys[cur ^ 1], w.vals[cur ^ 1]);
-    LC_LAUNCHED();
-    cur ^= 1;
-  }
+  LC_HIP(radix_sort_u32(w.keys, w.vals, N, 4, w.hist, w.dsum, w.dbase, cur, s));
   const uint32_t* order = w.vals[cur];
   unsigned long long host_cnt[2] = {0ull, 0ull};
   LC_HIP(hipMemcpyAsync(host_cnt, w.counters, 16, hipMemcpyDeviceToHost, s));

@@ -17,21 +17,25 @@
 // distance and then by index, independent of scheduling.
 //
 // Kernel layout (gfx950, wave64):
-//  - workgroup = 4 waves; wave w holds RT*16 queries as MFMA A operands in
-//    registers for the whole sweep (bf16 or float32, converted once);
-//  - the workgroup streams its slice of the cache through LDS in tiles of 64
-//    entries (converted to the MFMA element type on the way in; rows padded
-//    by 16 bytes so the B-operand reads are free of bank conflicts);
+//  - workgroup = 8 waves (two per SIMD); wave w holds RT*16 queries as MFMA
+//    A operands in registers for the whole sweep (bf16 or float32, converted
+//    once);
+//  - the workgroup streams its slice of the cache through LDS in tiles of
+//    128 entries (64 KiB, double-buffered), copied global -> LDS without
+//    registers (lookup_dma_kernel), or, when the rows need a conversion,
+//    register-staged tiles of 64 (lookup_kernel);
 //  - per 16-entry column tile: KS k-steps of v_mfma_f32_16x16x32_bf16 (or 4x
-//    v_mfma_f32_16x16x4_f32), then the one-subtract-one-compare filter on the
-//    accumulators; a wave ballot skips the re-check path unless a pair passed;
+//    v_mfma_f32_16x16x4_f32), then the filter on the accumulators; a wave
+//    ballot skips the re-check path unless a pair passed;
 //  - grid = query blocks x cache slices; blocks are numbered so that the
-//    blocks a given XCD runs (block id mod 8) share cache slices, so the 64
+//    blocks a given XCD runs (block id mod 8) share cache slices, so the
 //    resident workgroups of an XCD read each cache tile from its L2 at about
-//    the same time.
+//    the same time.  The indexed lookup instead gives each block one item of
+//    a work list: a query block against the rows of one cache cluster.
 #include <limits.h>
 
 #include "lc_common.hpp"
+#include "lc_index.hpp"
 
 namespace lc {
 
@@ -63,6 +67,12 @@ struct LookupParams {
   int64_t slice_len;
   float* g_hat;          // dump mode only
   uint8_t* cand;         // dump mode only
+  // Work-list mode (indexed lookup): block b takes query block items[3b]
+  // against cache rows [items[3b+1], items[3b+2]) instead of a slice.
+  const int64_t* items;
+  // Index written into a hit's key: (emap ? emap[e] : e) + eoff.
+  const int64_t* emap;
+  int64_t eoff;
 };
 
 // ------------------------------------------------------------- prep
@@ -102,17 +112,20 @@ __global__ void lookup_athr_kernel(const float* __restrict__ cr, const float* __
 }
 
 // ------------------------------------------------------------- finalize
+// Query q of the internal order answers original query qmap[q] (or q).
 __global__ void lookup_finalize_kernel(int64_t B, const unsigned long long* __restrict__ best,
                                        const unsigned int* __restrict__ bflag,
                                        const int32_t* __restrict__ clabel, int32_t* __restrict__ label_out,
                                        int64_t* __restrict__ index_out, float* __restrict__ dist2_out,
-                                       uint8_t* __restrict__ band_out, unsigned long long* __restrict__ stats) {
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+                                       uint8_t* __restrict__ band_out, unsigned long long* __restrict__ stats,
+                                       const int64_t* __restrict__ qmap) {
+  const int64_t qi = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   bool hit = false, band = false;
-  if (q < B) {
-    const unsigned long long key = best[q];
+  if (qi < B) {
+    const int64_t q = qmap ? qmap[qi] : qi;
+    const unsigned long long key = best[qi];
     hit = key != kNoHit;
-    band = bflag[q] != 0u;
+    band = bflag[qi] != 0u;
     const int64_t i = hit ? static_cast<int64_t>(key & 0xffffffffull) : -1;
     label_out[q] = hit ? clabel[i] : LIPCACHE_MISS;
     if (index_out) index_out[q] = i;
@@ -128,6 +141,27 @@ __global__ void lookup_finalize_kernel(int64_t B, const unsigned long long* __re
 }
 
 // ------------------------------------------------------------- main kernel
+// Block -> (query block, cache rows).  Slice mode: consecutive blocks of one
+// XCD (same id mod 8) take consecutive query blocks of one slice, so they
+// read each tile from that XCD's L2 at about the same time.  Work-list mode:
+// the block's item.
+__device__ __forceinline__ void block_work(const LookupParams& p, int& qb, int64_t& e_begin, int64_t& e_end) {
+  const int bid = static_cast<int>(blockIdx.x);
+  if (p.items) {
+    const int64_t* it = p.items + 3 * static_cast<int64_t>(bid);
+    qb = static_cast<int>(it[0]);
+    e_begin = it[1];
+    e_end = it[2] < p.n ? it[2] : p.n;
+    return;
+  }
+  const int xcd = bid % kXcds;
+  const int local = bid / kXcds;
+  const int slice = xcd + kXcds * (local / p.n_qblocks);
+  qb = local % p.n_qblocks;
+  e_begin = static_cast<int64_t>(slice) * p.slice_len;
+  e_end = e_begin + p.slice_len < p.n ? e_begin + p.slice_len : p.n;
+}
+
 template <int MODE>
 struct ModeTraits;
 template <>
@@ -213,10 +247,12 @@ struct RecheckArgs {
   int64_t B;
   int64_t n;
   int d;
+  const int64_t* emap;
+  int64_t eoff;
 };
 
 __device__ __forceinline__ RecheckArgs recheck_args(const LookupParams& p) {
-  return RecheckArgs{p.zq, p.cz, p.cr, p.best, p.bflag, p.stats, p.B, p.n, p.d};
+  return RecheckArgs{p.zq, p.cz, p.cr, p.best, p.bflag, p.stats, p.B, p.n, p.d, p.emap, p.eoff};
 }
 
 // Exact re-check of the pairs whose bits are set in `mask` (bit rt*4+i of a
@@ -254,9 +290,10 @@ __device__ __noinline__ void recheck_pairs(const RecheckArgs p, uint32_t mask, i
       }
       if (hit) {
         const float d2f = static_cast<float>(d2);
+        const int64_t ek = (p.emap ? p.emap[e] : e) + p.eoff;
         const unsigned long long key =
             (static_cast<unsigned long long>(__builtin_bit_cast(uint32_t, d2f)) << 32) |
-            static_cast<unsigned long long>(static_cast<uint32_t>(e));
+            static_cast<unsigned long long>(static_cast<uint32_t>(ek));
         atomicMin(&p.best[q], key);
       }
     }
@@ -303,13 +340,9 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_kernel(const LookupParam
   __shared__ __attribute__((aligned(16))) unsigned char tile[kTileN * kRowBytes];
   __shared__ float athr[kTileN];
 
-  // Block -> (query block, cache slice).  Consecutive blocks of one XCD
-  // (same id mod 8) take consecutive query blocks of one slice.
-  const int bid = static_cast<int>(blockIdx.x);
-  const int xcd = bid % kXcds;
-  const int local = bid / kXcds;
-  const int slice = xcd + kXcds * (local / p.n_qblocks);
-  const int qb = local % p.n_qblocks;
+  int qb;
+  int64_t e_begin, e_end;
+  block_work(p, qb, e_begin, e_end);
 
   const int lane = lane_id();
   const int wave = uniform(static_cast<int>(threadIdx.x) / kWave);
@@ -321,8 +354,6 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_kernel(const LookupParam
   float qt[RT][4];
   load_queries<MODE, KS, RT>(p, qwave, m16, g, a, qt);
 
-  const int64_t e_begin = static_cast<int64_t>(slice) * p.slice_len;
-  const int64_t e_end = e_begin + p.slice_len < p.n ? e_begin + p.slice_len : p.n;
   for (int64_t t0 = e_begin; t0 < e_end; t0 += kTileN) {
     __syncthreads();
     for (int c = threadIdx.x; c < kTileN * kChunksPerRow; c += kLkThreads) {
@@ -627,7 +658,9 @@ __device__ __forceinline__ void compute_tile(const unsigned char* buf, const flo
 #pragma unroll
   for (int sub = 0; sub < kRows / kColTile; ++sub) {
     if (sub >= nsub) break;
-    const float an = athr_buf[sub * kColTile + m16];
+    // rows past the range end (real rows of the next range in work-list
+    // mode) never pass
+    const float an = t0 + sub * kColTile + m16 < e_end ? athr_buf[sub * kColTile + m16] : __builtin_inff();
     f32x4 acc[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -701,11 +734,9 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
   __shared__ __attribute__((aligned(16))) float ath0[kRows];
   __shared__ __attribute__((aligned(16))) float ath1[kRows];
 
-  const int bid = static_cast<int>(blockIdx.x);
-  const int xcd = bid % kXcds;
-  const int local = bid / kXcds;
-  const int slice = xcd + kXcds * (local / p.n_qblocks);
-  const int qb = local % p.n_qblocks;
+  int qb;
+  int64_t e_begin, e_end;
+  block_work(p, qb, e_begin, e_end);
 
   const int lane = lane_id();
   const int wave = uniform(static_cast<int>(threadIdx.x) / kWave);
@@ -713,8 +744,6 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
   const int g = lane >> 4;
   const int64_t qwave = static_cast<int64_t>(qb) * (kLkWaves * RT * 16) + wave * (RT * 16);
 
-  const int64_t e_begin = static_cast<int64_t>(slice) * p.slice_len;
-  const int64_t e_end = e_begin + p.slice_len < p.n ? e_begin + p.slice_len : p.n;
   if (e_begin >= e_end) return;  // whole workgroup: an empty slice
   issue_tile<MODE, KS>(buf0, ath0, p, e_begin, e_end, wave);
 
@@ -874,6 +903,104 @@ inline bool cache_ok(const lipcache_cache* c) {
   return true;
 }
 
+// Filter constants of one lookup (depend on precision, store and d).
+struct FilterConsts {
+  Plan pl;
+  double kappa;
+  double kappa_c;
+};
+
+lipcache_status lookup_consts(const lipcache_cache* c, int32_t precision, FilterConsts& fc) {
+  if (!make_plan(precision, c, fc.pl)) return LIPCACHE_EUNSUPPORTED;
+  if (precision == LIPCACHE_F32 && (fc.pl.ks > 32 || c->d > 512)) return LIPCACHE_EUNSUPPORTED;
+  fc.kappa = filter_kappa(precision, c->store_dtype, fc.pl.d_pad);
+  const double u32 = 1.0 / 16777216.0;
+  fc.kappa_c = 1.0 - fc.kappa - 4.0 * u32;
+  return LIPCACHE_OK;
+}
+
+// Stage 1: Q_q, and the reset of best / band flags / counters.
+lipcache_status lookup_stage_prep(const float* zq, int64_t B, int d, const FilterConsts& fc, float* qthr,
+                                  unsigned long long* best, unsigned int* bflag, unsigned long long* stats,
+                                  hipStream_t s) {
+  const unsigned prep_grid = static_cast<unsigned>(B > 0 ? (B + kLkWaves - 1) / kLkWaves : 1);
+  hipLaunchKernelGGL(lookup_prep_kernel, dim3(prep_grid), dim3(kLkThreads), 0, s, zq, B, d, 1.0 - fc.kappa, qthr,
+                     best, bflag, stats);
+  LC_LAUNCHED();
+  return LIPCACHE_OK;
+}
+
+// Stage 2: the filter + re-check kernel of `view` (its n rows) against the
+// B queries, over cache slices or, with `items`, over a work list of
+// n_items (query block, row range) items.  Hits are keyed by
+// (emap ? emap[e] : e) + eoff.  athr needs athr_len(view->n) floats.
+lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision, const FilterConsts& fc,
+                                  const float* zq, int64_t B, const float* qthr, unsigned long long* best,
+                                  unsigned int* bflag, unsigned long long* stats, float* athr,
+                                  const int64_t* items, int64_t n_items, const int64_t* emap, int64_t eoff,
+                                  bool dump, float* g_hat, uint8_t* cand, hipStream_t s) {
+  if (B <= 0 || view->n <= 0) return LIPCACHE_OK;
+  if (items && n_items <= 0) return LIPCACHE_OK;
+  const int64_t n_pad = athr_len(view->n);
+  hipLaunchKernelGGL(lookup_athr_kernel, dim3(static_cast<unsigned>((n_pad + 255) / 256)), dim3(256), 0, s, view->r,
+                     view->norm2, view->n, n_pad, fc.kappa_c, athr);
+  LC_LAUNCHED();
+  const Plan& pl = fc.pl;
+  LookupParams p;
+  p.zq = zq;
+  p.B = B;
+  p.cz = view->z;
+  p.cr = view->r;
+  p.cnorm2 = view->norm2;
+  p.n = view->n;
+  p.d = view->d;
+  p.qthr = qthr;
+  p.best = best;
+  p.bflag = bflag;
+  p.stats = stats;
+  p.kappa_c = fc.kappa_c;
+  p.athr = athr;
+  p.cimg = (precision == LIPCACHE_BF16 && view->store_dtype == LIPCACHE_F32) ? view->zimg : view->z;
+  p.n_qblocks = static_cast<int>((B + pl.qblock - 1) / pl.qblock);
+  p.g_hat = g_hat;
+  p.cand = cand;
+  p.items = items;
+  p.emap = emap;
+  p.eoff = eoff;
+  int64_t grid = n_items;
+  p.slice_len = 0;
+  if (!items) {
+    // Cache slices: a multiple of 8 (one set per XCD), enough blocks to fill
+    // the chip (~1024), but at least 4 tiles per slice.
+    const int64_t tiles = (view->n + pl.tile_rows - 1) / pl.tile_rows;
+    int64_t s8 = (1024 + kXcds * p.n_qblocks - 1) / (kXcds * static_cast<int64_t>(p.n_qblocks));
+    int64_t s8_max = tiles / (kXcds * 4);
+    if (s8_max < 1) s8_max = 1;
+    if (s8 > s8_max) s8 = s8_max;
+    if (s8 < 1) s8 = 1;
+    const int64_t slices = kXcds * s8;
+    p.slice_len = ((tiles + slices - 1) / slices) * pl.tile_rows;
+    grid = slices * p.n_qblocks;
+  }
+  if (grid > INT_MAX) return LIPCACHE_EUNSUPPORTED;
+  const hipError_t e = dump ? launch_lookup<true>(precision, view->store_dtype, pl, p, static_cast<unsigned>(grid), s)
+                            : launch_lookup<false>(precision, view->store_dtype, pl, p, static_cast<unsigned>(grid), s);
+  return e == hipSuccess ? LIPCACHE_OK : LIPCACHE_EHIP;
+}
+
+// Stage 3: per query (internal order, mapped through qmap), label / index /
+// d^2 / band flag, and the hit and band counts.
+lipcache_status lookup_stage_finalize(int64_t B, const unsigned long long* best, const unsigned int* bflag,
+                                      const int32_t* clabel, int32_t* label_out, int64_t* index_out,
+                                      float* dist2_out, uint8_t* band_flag, unsigned long long* stats,
+                                      const int64_t* qmap, hipStream_t s) {
+  if (B <= 0) return LIPCACHE_OK;
+  hipLaunchKernelGGL(lookup_finalize_kernel, dim3(static_cast<unsigned>((B + 255) / 256)), dim3(256), 0, s, B, best,
+                     bflag, clabel, label_out, index_out, dist2_out, band_flag, stats, qmap);
+  LC_LAUNCHED();
+  return LIPCACHE_OK;
+}
+
 lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, int32_t precision,
                            int32_t* label_out, int64_t* index_out, float* dist2_out, uint64_t* stats,
                            uint8_t* band_flag, void* ws, size_t ws_bytes, hipStream_t s, bool dump,
@@ -884,74 +1011,115 @@ lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, 
   if ((reinterpret_cast<uintptr_t>(zq) & 15u) != 0) return LIPCACHE_EINVAL;
   if (B > static_cast<int64_t>(INT_MAX) / 2) return LIPCACHE_EINVAL;
   if (dump && (!g_hat || !cand || B * c->n > (1ll << 26))) return LIPCACHE_EINVAL;
-  Plan pl;
-  if (!make_plan(precision, c, pl)) return LIPCACHE_EUNSUPPORTED;
-  if (precision == LIPCACHE_F32 && pl.ks > 32) return LIPCACHE_EUNSUPPORTED;
-  if (precision == LIPCACHE_F32 && c->d > 512) return LIPCACHE_EUNSUPPORTED;
+  FilterConsts fc;
+  const lipcache_status cs = lookup_consts(c, precision, fc);
+  if (cs != LIPCACHE_OK) return cs;
   const size_t need = ws_layout(B, c->n, nullptr, nullptr);
   if (!ws || ws_bytes < need || !aligned256(ws)) return LIPCACHE_EWORKSPACE;
   Workspace w;
   ws_layout(B, c->n, &w, ws);
   unsigned long long* st = stats ? reinterpret_cast<unsigned long long*>(stats) : w.stats;
+  lipcache_status r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s);
+  if (r != LIPCACHE_OK) return r;
+  r = lookup_stage_scan(c, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr, 0, dump,
+                        g_hat, cand, s);
+  if (r != LIPCACHE_OK) return r;
+  if (dump) return LIPCACHE_OK;
+  return lookup_stage_finalize(B, w.best, w.bflag, c->label, label_out, index_out, dist2_out, band_flag, st,
+                               nullptr, s);
+}
 
-  const double kappa = filter_kappa(precision, c->store_dtype, pl.d_pad);
-  const double u32 = 1.0 / 16777216.0;
-  const double kappa_c = 1.0 - kappa - 4.0 * u32;
-  const unsigned prep_grid = static_cast<unsigned>(B > 0 ? (B + kLkWaves - 1) / kLkWaves : 1);
-  hipLaunchKernelGGL(lookup_prep_kernel, dim3(prep_grid), dim3(kLkThreads), 0, s, zq, B, c->d, 1.0 - kappa,
-                     w.qthr, w.best, w.bflag, st);
-  LC_LAUNCHED();
+// Workspace of an indexed lookup: the dense lookup's buffers (thresholds
+// sized for the larger of the indexed part and the tail) and the plan's.
+// The work-list capacity is sized for the smallest query block of any plan.
+inline size_t indexed_ws_layout(int64_t B, int64_t n, int d, int K, int64_t n_indexed, Workspace* w,
+                                IndexPlanWs* pw, void* base) {
+  const int64_t tail = n - n_indexed;
+  const size_t lk = ws_layout(B, n_indexed > tail ? n_indexed : tail, w, base);
+  char* pb = base ? static_cast<char*>(base) + lk : nullptr;
+  return lk + index_plan_layout(B, d, K, n_indexed, kLkWaves * 16, pw, pb);
+}
 
-  if (B > 0 && c->n > 0) {
-    const int64_t n_pad = athr_len(c->n);
-    hipLaunchKernelGGL(lookup_athr_kernel, dim3(static_cast<unsigned>((n_pad + 255) / 256)), dim3(256), 0, s, c->r,
-                       c->norm2, c->n, n_pad, kappa_c, w.athr);
-    LC_LAUNCHED();
-    LookupParams p;
-    p.zq = zq;
-    p.B = B;
-    p.cz = c->z;
-    p.cr = c->r;
-    p.cnorm2 = c->norm2;
-    p.n = c->n;
-    p.d = c->d;
-    p.qthr = w.qthr;
-    p.best = w.best;
-    p.bflag = w.bflag;
-    p.stats = st;
-    p.kappa_c = kappa_c;
-    p.athr = w.athr;
-    p.cimg = (precision == LIPCACHE_BF16 && c->store_dtype == LIPCACHE_F32) ? c->zimg : c->z;
-    p.n_qblocks = static_cast<int>((B + pl.qblock - 1) / pl.qblock);
-    p.g_hat = g_hat;
-    p.cand = cand;
-    // Cache slices: a multiple of 8 (one set per XCD), enough blocks to fill
-    // the chip (~1024), but at least 4 tiles per slice.
-    const int64_t tiles = (c->n + pl.tile_rows - 1) / pl.tile_rows;
-    int64_t s8 = (1024 + kXcds * p.n_qblocks - 1) / (kXcds * static_cast<int64_t>(p.n_qblocks));
-    int64_t s8_max = tiles / (kXcds * 4);
-    if (s8_max < 1) s8_max = 1;
-    if (s8 > s8_max) s8 = s8_max;
-    if (s8 < 1) s8 = 1;
-    const int64_t slices = kXcds * s8;
-    p.slice_len = ((tiles + slices - 1) / slices) * pl.tile_rows;
-    const int64_t grid = slices * p.n_qblocks;
-    if (grid > INT_MAX) return LIPCACHE_EUNSUPPORTED;
-    const hipError_t e = dump ? launch_lookup<true>(precision, c->store_dtype, pl, p, static_cast<unsigned>(grid), s)
-                              : launch_lookup<false>(precision, c->store_dtype, pl, p, static_cast<unsigned>(grid), s);
-    if (e != hipSuccess) return LIPCACHE_EHIP;
+lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index* idx, const float* zq, int64_t B,
+                                   int32_t precision, int32_t* label_out, int64_t* index_out, float* dist2_out,
+                                   uint64_t* stats, uint8_t* band_flag, int64_t* pairs, void* ws, size_t ws_bytes,
+                                   hipStream_t s) {
+  if (!cache_ok(c) || !idx || B < 0) return LIPCACHE_EINVAL;
+  if (precision != LIPCACHE_BF16 && precision != LIPCACHE_F32) return LIPCACHE_EINVAL;
+  if (B > 0 && (!zq || !label_out)) return LIPCACHE_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(zq) & 15u) != 0) return LIPCACHE_EINVAL;
+  if (B > static_cast<int64_t>(INT_MAX) / 2) return LIPCACHE_EINVAL;
+  const lipcache_cache& so = idx->sorted;
+  if (idx->K < 1 || idx->K > 65536 || idx->n_indexed < 1 || idx->n_indexed > c->n) return LIPCACHE_EINVAL;
+  if (so.n != idx->n_indexed || so.d != c->d || so.store_dtype != c->store_dtype || !cache_ok(&so))
+    return LIPCACHE_EINVAL;
+  if (!idx->perm || !idx->offsets || !idx->centers || !idx->bound) return LIPCACHE_EINVAL;
+  // the bf16 filter streams the bf16 image of float32 rows when the cache has one
+  if (precision == LIPCACHE_BF16 && c->store_dtype == LIPCACHE_F32 && (c->zimg == nullptr) != (so.zimg == nullptr))
+    return LIPCACHE_EINVAL;
+  FilterConsts fc;
+  const lipcache_status cs = lookup_consts(c, precision, fc);
+  if (cs != LIPCACHE_OK) return cs;
+  const size_t need = indexed_ws_layout(B, c->n, c->d, idx->K, idx->n_indexed, nullptr, nullptr, nullptr);
+  if (!ws || ws_bytes < need || !aligned256(ws)) return LIPCACHE_EWORKSPACE;
+  Workspace w;
+  IndexPlanWs pw;
+  indexed_ws_layout(B, c->n, c->d, idx->K, idx->n_indexed, &w, &pw, ws);
+  unsigned long long* st = stats ? reinterpret_cast<unsigned long long*>(stats) : w.stats;
+  if (B == 0) {
+    lipcache_status r = lookup_stage_prep(zq, 0, c->d, fc, w.qthr, w.best, w.bflag, st, s);
+    if (r == LIPCACHE_OK && pairs) *pairs = 0;
+    return r;
   }
-  if (!dump && B > 0) {
-    hipLaunchKernelGGL(lookup_finalize_kernel, dim3(static_cast<unsigned>((B + 255) / 256)), dim3(256), 0, s, B,
-                       w.best, w.bflag, c->label, label_out, index_out, dist2_out, band_flag, st);
-    LC_LAUNCHED();
+  int64_t n_items = 0, idx_pairs = 0;
+  lipcache_status r = index_query_plan(idx, zq, B, c->d, fc.pl.qblock, pw, n_items, idx_pairs, s);
+  if (r != LIPCACHE_OK) return r;
+  const float* zs = pw.zq_sorted;
+  r = lookup_stage_prep(zs, B, c->d, fc, w.qthr, w.best, w.bflag, st, s);
+  if (r != LIPCACHE_OK) return r;
+  r = lookup_stage_scan(&so, precision, fc, zs, B, w.qthr, w.best, w.bflag, st, w.athr, pw.items, n_items, idx->perm,
+                        0, false, nullptr, nullptr, s);
+  if (r != LIPCACHE_OK) return r;
+  const int64_t tail = c->n - idx->n_indexed;
+  if (tail > 0) {
+    // rows appended after the build: a dense scan of the cache's tail
+    lipcache_cache view = *c;
+    const size_t esz = c->store_dtype == LIPCACHE_BF16 ? 2 : 4;
+    const size_t off = static_cast<size_t>(idx->n_indexed) * c->d;
+    view.z = static_cast<char*>(c->z) + off * esz;
+    view.zimg = c->zimg ? static_cast<char*>(c->zimg) + off * 2 : nullptr;
+    view.r = c->r + idx->n_indexed;
+    view.label = c->label + idx->n_indexed;
+    view.norm2 = c->norm2 + idx->n_indexed;
+    view.n = tail;
+    view.capacity = tail;
+    r = lookup_stage_scan(&view, precision, fc, zs, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr,
+                          idx->n_indexed, false, nullptr, nullptr, s);
+    if (r != LIPCACHE_OK) return r;
   }
-  return LIPCACHE_OK;
+  if (pairs) *pairs = idx_pairs + B * tail;
+  return lookup_stage_finalize(B, w.best, w.bflag, c->label, label_out, index_out, dist2_out, band_flag, st, pw.qmap,
+                               s);
 }
 
 }  // namespace lc
 
 using namespace lc;
+
+extern "C" size_t lipcache_lookup_indexed_workspace_bytes(int64_t B, int64_t n, int32_t d, int32_t K,
+                                                          int64_t n_indexed) {
+  if (B < 0 || n < 1 || d < 1 || K < 1 || n_indexed < 1 || n_indexed > n) return 0;
+  return indexed_ws_layout(B, n, d, K, n_indexed, nullptr, nullptr, nullptr);
+}
+
+extern "C" lipcache_status lipcache_lookup_indexed(const lipcache_cache* c, const lipcache_index* idx,
+                                                   const float* zq, int64_t B, int32_t precision,
+                                                   int32_t* label_out, int64_t* index_out, float* dist2_out,
+                                                   uint64_t* stats, uint8_t* band_flag, int64_t* pairs, void* ws,
+                                                   size_t ws_bytes, lipcache_stream_t stream) {
+  return run_lookup_indexed(c, idx, zq, B, precision, label_out, index_out, dist2_out, stats, band_flag, pairs, ws,
+                            ws_bytes, reinterpret_cast<hipStream_t>(stream));
+}
 
 extern "C" size_t lipcache_lookup_workspace_bytes(int64_t B, int64_t N, int32_t d, int32_t precision) {
   (void)d;

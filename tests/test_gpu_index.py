@@ -1,0 +1,190 @@
+"""The exact cluster index on the device (lipcache_index_build,
+lipcache_lookup_indexed), against the brute-force oracle.
+
+Index invariants, checked on the host in float64 from the device's arrays:
+perm is a permutation, the offsets cover [0, n), sorted rows are the cache
+rows perm[j] bit for bit, and every live row lies within its cluster's
+bound: ||z_i - mu_c|| + r_i <= R_c (clusters without a live row have
+R_c = -inf).
+
+The indexed lookup returns the oracle's answers query by query and the
+dense device lookup's outputs bit for bit (label, index, d^2, band flags,
+hit and band counters), for both stores and filters, K from 1 to n,
+rows appended after the build, dead rows, duplicated rows (empty
+clusters), a ragged batch, non-finite queries, and the full-size mixture.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_13144_amd import api
+from paper_2608_13144_amd import workload as wlmod
+from gpu_helpers import DEV, build_cache, compare_lookup, gpu, host, oracle_cache, say
+
+pytestmark = pytest.mark.gpu
+
+
+def check_index(c, ix, what):
+    n, K = c.n, ix.K
+    assert ix.n_indexed == n and ix.sorted.n == n, what
+    perm = host(ix.perm)
+    off = host(ix.offsets)
+    assert np.array_equal(np.sort(perm), np.arange(n)), f"{what}: perm"
+    assert off[0] == 0 and off[K] == n and np.all(np.diff(off) >= 0), f"{what}: offsets"
+    z = host(c.z[:n].view(torch.int16 if c.store == "bf16" else torch.int32))
+    zs = host(ix.sorted.z[:n].view(torch.int16 if c.store == "bf16" else torch.int32))
+    assert np.array_equal(zs, z[perm]), f"{what}: sorted rows"
+    if c.zimg is not None:
+        assert np.array_equal(host(ix.sorted.zimg[:n].view(torch.int16)),
+                              host(c.zimg[:n].view(torch.int16))[perm]), f"{what}: image"
+    r = host(c.r[:n])
+    for name in ("r", "label", "norm2"):
+        a = host(getattr(ix.sorted, name)[:n])
+        b = host(getattr(c, name)[:n])[perm]
+        assert np.array_equal(a.view(np.int32), b.view(np.int32)), f"{what}: {name}"
+    zf = host(c.z[:n].float()).astype(np.float64)
+    mu = host(ix.centers).astype(np.float64)
+    R = host(ix.bound).astype(np.float64)
+    for cl in range(K):
+        rows = perm[off[cl]:off[cl + 1]]
+        live = rows[r[rows] > 0]
+        if live.size == 0:
+            assert R[cl] == -np.inf, f"{what}: cluster {cl} has no live row but R = {R[cl]}"
+            continue
+        reach = np.sqrt(np.sum((zf[live] - mu[cl]) ** 2, axis=1)) + r[live].astype(np.float64)
+        assert reach.max() <= R[cl], f"{what}: cluster {cl} bound {R[cl]} < reach {reach.max()}"
+
+
+def same_as_dense(res_i, res_d, what):
+    for f in ("label", "index", "band"):
+        assert torch.equal(getattr(res_i, f), getattr(res_d, f)), f"{what}: {f}"
+    assert torch.equal(res_i.dist2.view(torch.int32), res_d.dist2.view(torch.int32)), f"{what}: dist2"
+    si, sd = host(res_i.stats), host(res_d.stats)
+    for k in (0, 2, 3):
+        assert si[k] == sd[k], f"{what}: stats[{k}] {si} vs {sd}"
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    wl = wlmod.make_workload("tiny-d64-c10", seed=0)
+    sig = oracle.spectral_norm(wl.W).sigma
+    out = {}
+    for store in ("f32", "bf16"):
+        cert = oracle.certify(wl.z, wl.W, wl.b, sig, store=store)
+        st = oracle_cache(wl.z, cert.label, cert.r, 64, store=store)
+        draws = wlmod.draw_queries(wl, 0, batch=1000)
+        idx = wlmod.near_indices(draws, st.n)
+        zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
+        out[store] = (wl, st, zq, oracle.lookup_blocked(zq, st.z, st.r, st.label))
+    return out
+
+
+CASES = [("f32", "bf16", True), ("f32", "bf16", False), ("bf16", "bf16", True), ("f32", "f32", True),
+         ("bf16", "f32", True)]
+
+
+@pytest.mark.parametrize("store,prec,image", CASES)
+@pytest.mark.parametrize("K,iters", [(1, 0), (16, 3), (256, 4), (4096, 1)])
+def test_indexed_matches_oracle_and_dense(tiny, store, prec, image, K, iters):
+    wl, st, zq, ref = tiny[store]
+    what = f"{store}/{prec}/image={image}/K={K}/it={iters}"
+    say("index", what)
+    c = build_cache(st, image=image)
+    ix = c.build_index(K, iters)
+    check_index(c, ix, what)
+    q = gpu(zq)
+    res_i, pairs = c.lookup_indexed(ix, q, precision=prec)
+    compare_lookup(res_i, ref, what)
+    res_d = c.lookup(q, precision=prec)
+    same_as_dense(res_i, res_d, what)
+    assert 0 < pairs <= zq.shape[0] * st.n
+    say("index", what, "pairs", pairs, "of", zq.shape[0] * st.n)
+
+
+def test_rows_appended_after_build(tiny):
+    wl, st, zq, ref = tiny["f32"]
+    say("index appended rows")
+    c = build_cache(st, capacity=st.n + zq.shape[0])
+    ix = c.build_index(64, 3)
+    q = gpu(zq)
+    sig = oracle.spectral_norm(wl.W).sigma
+    cq = oracle.certify(zq, wl.W, wl.b, sig)
+    c.insert(q, gpu(cq.label), gpu(cq.r))
+    st2 = oracle_cache(np.concatenate([st.z, zq]), np.concatenate([st.label, cq.label]),
+                       np.concatenate([st.r, cq.r]), 64)
+    draws = wlmod.draw_queries(wl, 1, batch=777)
+    idx = wlmod.near_indices(draws, st2.n)
+    zq2 = wlmod.compose_queries(draws, st2.z[idx], st2.r[idx])
+    ref2 = oracle.lookup_blocked(zq2, st2.z, st2.r, st2.label)
+    res_i, pairs = c.lookup_indexed(ix, gpu(zq2))
+    compare_lookup(res_i, ref2, "appended")
+    same_as_dense(res_i, c.lookup(gpu(zq2)), "appended")
+    assert host(res_i.index).max() >= st.n, "some hits should land in the appended rows"
+    assert pairs >= zq2.shape[0] * zq.shape[0]
+
+
+def test_dead_rows_and_duplicates(tiny):
+    wl, st, zq, ref = tiny["f32"]
+    say("index dead rows and duplicates")
+    # every row twice (duplicates give empty clusters), one class dead
+    z = np.repeat(st.z, 2, axis=0)
+    lab = np.repeat(st.label, 2)
+    r = np.repeat(st.r, 2)
+    r = np.where(lab == 2, np.float32(0.0), r)
+    st2 = oracle_cache(z, lab, r, 64)
+    c = build_cache(st2)
+    ix = c.build_index(1024, 2)
+    check_index(c, ix, "dup")
+    off = host(ix.offsets)
+    say("empty clusters", int(np.sum(np.diff(off) == 0)), "dead", int(np.sum(host(ix.bound) == -np.inf)))
+    ref2 = oracle.lookup_blocked(zq, st2.z, st2.r, st2.label)
+    res_i, _ = c.lookup_indexed(ix, gpu(zq))
+    compare_lookup(res_i, ref2, "dup")
+    same_as_dense(res_i, c.lookup(gpu(zq)), "dup")
+
+
+def test_edge_batches(tiny):
+    wl, st, zq, ref = tiny["bf16"]
+    say("index edge batches")
+    c = build_cache(st)
+    ix = c.build_index(32, 2)
+    res, pairs = c.lookup_indexed(ix, gpu(zq[:0]))
+    assert pairs == 0 and host(res.stats)[0] == 0
+    bad = zq[:70].copy()
+    bad[3, 5] = np.nan
+    bad[9, 0] = np.inf
+    bad[11] = 0.0
+    res_i, _ = c.lookup_indexed(ix, gpu(bad))
+    res_d = c.lookup(gpu(bad))
+    same_as_dense(res_i, res_d, "non-finite")
+    lab = host(res_i.label)
+    assert lab[3] == oracle.MISS and lab[9] == oracle.MISS
+    one, _ = c.lookup_indexed(ix, gpu(zq[:1]))
+    assert host(one.label)[0] == ref.label[0] or ref.flagged[0]
+
+
+@pytest.mark.slow
+def test_full_size_mixture():
+    cfg = wlmod.CONFIGS["mix-d256-c200"]
+    say("index full size", cfg.name, "N", cfg.n_cache, "B", cfg.batch)
+    wl = wlmod.make_workload(cfg, seed=0)
+    sig_o = oracle.spectral_norm(wl.W).sigma
+    cert_o = oracle.certify(wl.z, wl.W, wl.b, sig_o, store=cfg.store_dtype)
+    st = oracle_cache(wl.z, cert_o.label, cert_o.r, cfg.d, store=cfg.store_dtype)
+    draws = wlmod.draw_queries(wl, 0)
+    idx = wlmod.near_indices(draws, st.n)
+    zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
+    c = build_cache(st)
+    ix = c.build_index(1024, 4)
+    torch.cuda.synchronize()
+    say("index built")
+    check_index(c, ix, "full")
+    q = gpu(zq)
+    res_i, pairs = c.lookup_indexed(ix, q)
+    res_d = c.lookup(q)
+    same_as_dense(res_i, res_d, "full")
+    rows = np.sort(np.random.default_rng(7).choice(zq.shape[0], 2048, replace=False))
+    compare_lookup(res_i, oracle.lookup_blocked(zq[rows], st.z, st.r, st.label), "full sample", rows=rows)
+    say("index full size pairs", pairs, "fraction", pairs / (zq.shape[0] * st.n))
+    assert pairs < 0.5 * zq.shape[0] * st.n

@@ -283,7 +283,7 @@ typedef struct lipcache_index {
                             cache, capacity >= n_indexed; zimg as for a cache)               */
   int64_t* perm;         /* [n_indexed] cache row held by sorted row j                       */
   int64_t* offsets;      /* [K + 1] cluster c = sorted rows [offsets[c], offsets[c + 1])     */
-  float* centers;        /* [K][d] cluster centres mu_c                                      */
+  float* centers;        /* [K][d] cluster centres mu_c (16-byte aligned)                    */
   float* bound;          /* [K] R_c, rounded up; -inf when no member can be hit              */
   int32_t K;
   int64_t n_indexed;     /* rows of the cache covered (the cache's n at build time)          */

@@ -22,109 +22,145 @@
 
 namespace lc {
 
-constexpr int kTq = 64;   // queries (or rows) per distance tile
-constexpr int kTc = 64;   // centres per distance tile
-constexpr int kTd = 32;   // feature columns per LDS stage
+constexpr int kCr = 64;              // rows per block (4 waves x 16)
+constexpr int kCc = 64;              // centres per chunk (4 column tiles of 16)
+constexpr int kCk = 64;              // features per LDS stage
+constexpr int kCs = kCk + 4;         // floats per LDS row (padding spreads the banks)
 
 __device__ __forceinline__ float stored_value(const void* z, int store, int64_t i, int d, int k) {
   if (store == LIPCACHE_BF16) return bf16_to_f32(static_cast<const uint16_t*>(z)[i * d + k]);
   return static_cast<const float*>(z)[i * d + k];
 }
 
-// Rows `rows` (n of them, float32 or bf16 storage) against K centres: the
-// nearest centre (ties: lower index) among those with usable[c] != 0 (all
-// when usable is null), and optionally the candidate mask
-// mask[r][c / 32] |= bit for ||x_r - mu_c||^2 < R_c^2 (1 + slack_rel).
-// Block: 256 threads, kTq rows; loops over all centre tiles.  Thread t
-// owns rows 4 (t / 16) .. +3 and centres 4 (t % 16) .. +3 of each tile.
-__global__ __launch_bounds__(256) void nearest_centre_kernel(const void* __restrict__ rows, int store, int64_t n,
-                                                             int d, const float* __restrict__ centres, int K,
-                                                             const float* __restrict__ bound, double slack_rel,
-                                                             uint32_t* __restrict__ mask,
-                                                             uint32_t* __restrict__ nearest) {
-  __shared__ float xs[kTq][kTd + 1];
-  __shared__ float cs[kTc][kTd + 1];
-  __shared__ float bestv[kTq][16];
-  __shared__ int besti[kTq][16];
+__device__ __forceinline__ f32x4 stored_x4(const void* z, int store, int64_t i, int d, int k) {
+  if (store == LIPCACHE_BF16) {
+    const uint2 h = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(z) + i * d + k);
+    return f32x4{bf16_to_f32(static_cast<uint16_t>(h.x & 0xffffu)), bf16_to_f32(static_cast<uint16_t>(h.x >> 16)),
+                 bf16_to_f32(static_cast<uint16_t>(h.y & 0xffffu)), bf16_to_f32(static_cast<uint16_t>(h.y >> 16))};
+  }
+  return *reinterpret_cast<const f32x4*>(static_cast<const float*>(z) + i * d + k);
+}
+
+// ||x||^2 in float64 of n rows (one wave per row).
+__global__ void row_norm_kernel(const void* __restrict__ x, int store, int64_t n, int d, double* __restrict__ out) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
+  if (i >= n) return;
+  double s = 0.0;
+  for (int k = lane_id(); k < d; k += kWave) {
+    const double v = static_cast<double>(stored_value(x, store, i, d, k));
+    s = __builtin_fma(v, v, s);
+  }
+  s = wave_sum(s);
+  if (lane_id() == 0) out[i] = s;
+}
+
+// Rows x (n of them, float32 or bf16 storage) against K centres mu_c, on the
+// matrix cores: g = x . mu_c by v_mfma_f32_16x16x4_f32 (float32 products
+// and sums), then in float64 the score ||mu_c||^2 - 2 g, which orders the
+// centres like ||x - mu_c||^2.
+//  - nearest[r] (optional): the centre of least score (ties: lower index)
+//    among the usable ones (bound[c] > 0; all when bound is null);
+//  - mask (optional): bit c of row r when ||x||^2 + score < R_c^2 + slack.
+//    The float32 dot product is off by at most about (d + 1) 2^-24 ||x|| ||mu||
+//    <= (d + 1) 2^-24 (||x||^2 + ||mu||^2) / 2, so with
+//    slack = slack_rel (||x||^2 + ||mu||^2), slack_rel = 2 (d + 2) 2^-24, and a
+//    2^-50 R_c^2 term for the rounding of R_c^2, every cluster with
+//    ||x - mu_c|| < R_c sets its bit.
+// Block: 4 waves, 64 rows; each wave owns 16 rows and all 64 centres of a
+// chunk (4 accumulator tiles); rows and centres pass through LDS in stages
+// of 64 features.
+__global__ __launch_bounds__(256) void centre_mfma_kernel(const void* __restrict__ rows, int store, int64_t n, int d,
+                                                          const float* __restrict__ centres,
+                                                          const double* __restrict__ cnorm, int K,
+                                                          const double* __restrict__ rnorm,
+                                                          const float* __restrict__ bound, double slack_rel,
+                                                          uint32_t* __restrict__ mask,
+                                                          uint32_t* __restrict__ nearest) {
+  __shared__ __attribute__((aligned(16))) float xs[kCr * kCs];
+  __shared__ __attribute__((aligned(16))) float cs[kCc * kCs];
   const int t = static_cast<int>(threadIdx.x);
-  const int tr = t / 16, tc = t % 16;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kTq;
+  const int lane = lane_id(), w = t / kWave;
+  const int m16 = lane & 15, g = lane >> 4;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kCr;
   const int words = (K + 31) / 32;
-  float bv[4];
+  double bs[4], qn[4];
   int bi[4];
 #pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    bv[a] = __builtin_inff();
-    bi[a] = INT_MAX;
+  for (int v = 0; v < 4; ++v) {
+    const int64_t row = r0 + w * 16 + 4 * g + v;
+    bs[v] = __builtin_inf();
+    bi[v] = INT_MAX;
+    qn[v] = (rnorm && row < n) ? rnorm[row] : 0.0;
   }
-  for (int c0 = 0; c0 < K; c0 += kTc) {
-    float acc[4][4];
+  for (int c0 = 0; c0 < K; c0 += kCc) {
+    f32x4 acc[4];
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int b = 0; b < 4; ++b) acc[a][b] = 0.0f;
-    for (int k0 = 0; k0 < d; k0 += kTd) {
+    for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < d; k0 += kCk) {
       __syncthreads();
-      for (int e = t; e < kTq * kTd; e += 256) {
-        const int rr = e / kTd, kk = e % kTd;
+      for (int e = t; e < kCr * kCk / 4; e += 256) {
+        const int rr = e / (kCk / 4), k4 = 4 * (e % (kCk / 4));
+        const bool kin = k0 + k4 < d;
         const int64_t row = r0 + rr;
         const int c = c0 + rr;
-        xs[rr][kk] = row < n ? stored_value(rows, store, row, d, k0 + kk) : 0.0f;
-        cs[rr][kk] = c < K ? centres[static_cast<int64_t>(c) * d + k0 + kk] : 0.0f;
+        f32x4 xv = f32x4{0.f, 0.f, 0.f, 0.f}, cv = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (kin && row < n) xv = stored_x4(rows, store, row, d, k0 + k4);
+        if (kin && c < K) cv = *reinterpret_cast<const f32x4*>(centres + static_cast<int64_t>(c) * d + k0 + k4);
+        *reinterpret_cast<f32x4*>(&xs[rr * kCs + k4]) = xv;
+        *reinterpret_cast<f32x4*>(&cs[rr * kCs + k4]) = cv;
       }
       __syncthreads();
-#pragma unroll 4
-      for (int kk = 0; kk < kTd; ++kk) {
-        float xv[4], cv[4];
 #pragma unroll
-        for (int a = 0; a < 4; ++a) xv[a] = xs[4 * tr + a][kk];
+      for (int kk = 0; kk < kCk; kk += 16) {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(&xs[(w * 16 + m16) * kCs + kk + 4 * g]);
 #pragma unroll
-        for (int b = 0; b < 4; ++b) cv[b] = cs[4 * tc + b][kk];
-#pragma unroll
-        for (int a = 0; a < 4; ++a)
-#pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            const float df = xv[a] - cv[b];
-            acc[a][b] = __builtin_fmaf(df, df, acc[a][b]);
-          }
+        for (int j = 0; j < 4; ++j) {
+          const f32x4 b = *reinterpret_cast<const f32x4*>(&cs[(j * 16 + m16) * kCs + kk + 4 * g]);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], acc[j], 0, 0, 0);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], acc[j], 0, 0, 0);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], acc[j], 0, 0, 0);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], acc[j], 0, 0, 0);
+        }
       }
     }
+    // lane (m16, g) holds rows 4g + v of the wave's 16 and centre 16 j + m16
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      const int64_t row = r0 + 4 * tr + a;
+    for (int j = 0; j < 4; ++j) {
+      const int c = c0 + 16 * j + m16;
+      if (c >= K) continue;
+      const float R = bound ? bound[c] : 1.0f;
+      if (!(R > 0.0f)) continue;
+      const double cn = cnorm[c];
+      const double R2 = static_cast<double>(R) * static_cast<double>(R);
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int c = c0 + 4 * tc + b;
-        if (c >= K || row >= n) continue;
-        const bool use = bound == nullptr || bound[c] > 0.0f;
-        if (use && (acc[a][b] < bv[a] || (acc[a][b] == bv[a] && c < bi[a]))) {
-          bv[a] = acc[a][b];
-          bi[a] = c;
+      for (int v = 0; v < 4; ++v) {
+        const double score = cn - 2.0 * static_cast<double>(acc[j][v]);
+        if (score < bs[v] || (score == bs[v] && c < bi[v])) {
+          bs[v] = score;
+          bi[v] = c;
         }
-        if (mask && use) {
-          const double R = static_cast<double>(bound[c]);
-          if (static_cast<double>(acc[a][b]) < R * R * (1.0 + slack_rel))
+        if (mask) {
+          const int64_t row = r0 + w * 16 + 4 * g + v;
+          if (row < n && qn[v] + score < R2 * (1.0 + 0x1p-50) + slack_rel * (qn[v] + cn))
             atomicOr(&mask[row * words + c / 32], 1u << (c % 32));
         }
       }
     }
   }
+  // least score over the 16 lanes that share g (same rows)
 #pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    bestv[4 * tr + a][tc] = bv[a];
-    besti[4 * tr + a][tc] = bi[a];
-  }
-  __syncthreads();
-  if (t < kTq && r0 + t < n) {
-    float v = bestv[t][0];
-    int i = besti[t][0];
-    for (int j = 1; j < 16; ++j) {
-      if (bestv[t][j] < v || (bestv[t][j] == v && besti[t][j] < i)) {
-        v = bestv[t][j];
-        i = besti[t][j];
+  for (int v = 0; v < 4; ++v) {
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) {
+      const double os = __shfl_xor(bs[v], off, kWave);
+      const int oi = __shfl_xor(bi[v], off, kWave);
+      if (os < bs[v] || (os == bs[v] && oi < bi[v])) {
+        bs[v] = os;
+        bi[v] = oi;
       }
     }
-    nearest[r0 + t] = i == INT_MAX ? 0u : static_cast<uint32_t>(i);
+    const int64_t row = r0 + w * 16 + 4 * g + v;
+    if (nearest && m16 == 0 && row < n) nearest[row] = bi[v] == INT_MAX ? 0u : static_cast<uint32_t>(bi[v]);
   }
 }
 
@@ -269,6 +305,7 @@ struct BuildWs {
   double* sum;
   unsigned long long* cnt;
   unsigned long long* rbits;
+  double* cnorm;
   uint32_t* keys[2];
   uint32_t* vals[2];
   uint32_t* hist;
@@ -289,6 +326,7 @@ inline BuildWs build_layout(int64_t n, int d, int K, char* base) {
   w.sum = reinterpret_cast<double*>(take(static_cast<size_t>(K) * d * 8));
   w.cnt = reinterpret_cast<unsigned long long*>(take(static_cast<size_t>(K) * 8));
   w.rbits = reinterpret_cast<unsigned long long*>(take(static_cast<size_t>(K) * 8));
+  w.cnorm = reinterpret_cast<double*>(take(static_cast<size_t>(K) * 8));
   for (int s = 0; s < 2; ++s) {
     w.keys[s] = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(n) * 4));
     w.vals[s] = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(n) * 4));
@@ -307,63 +345,114 @@ inline int sort_passes(int K) {
 }
 
 // ---------------------------------------------------------------- query plan
-__global__ void plan_keys_kernel(const uint32_t* __restrict__ nearest, int64_t B, uint32_t* __restrict__ keys,
-                                 uint32_t* __restrict__ vals) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= B) return;
-  keys[i] = nearest[i];
-  vals[i] = static_cast<uint32_t>(i);
-}
-
-// Internal query j = original query order[j]: copy its row, record the map.
-__global__ void plan_gather_kernel(const float* __restrict__ zq, const uint32_t* __restrict__ order, int64_t B,
-                                   int d, float* __restrict__ zs, int64_t* __restrict__ qmap) {
-  const int64_t j = static_cast<int64_t>(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
-  if (j >= B) return;
-  const int64_t src = order[j];
-  for (int k = lane_id(); k < d; k += kWave) zs[j * d + k] = zq[src * d + k];
-  if (lane_id() == 0) qmap[j] = src;
-}
-
-// One block per query block: union of the candidate clusters of its
-// queries, then one item per (needed cluster, chunk of <= kItemRows rows).
-__global__ __launch_bounds__(256) void plan_items_kernel(const uint32_t* __restrict__ mask, int words,
-                                                         const int64_t* __restrict__ qmap, int64_t B, int qblock,
-                                                         const int64_t* __restrict__ offsets, int64_t* __restrict__ items,
-                                                         int64_t capacity, unsigned long long* __restrict__ counters) {
-  extern __shared__ uint32_t un[];  // [words]
-  const int qb = static_cast<int>(blockIdx.x);
-  for (int w = threadIdx.x; w < words; w += 256) un[w] = 0u;
-  __syncthreads();
-  const int64_t q0 = static_cast<int64_t>(qb) * qblock;
-  const int64_t q1 = q0 + qblock < B ? q0 + qblock : B;
-  for (int64_t q = q0 + threadIdx.x / 8; q < q1; q += 256 / 8) {
-    const uint32_t* row = mask + qmap[q] * words;
-    for (int w = threadIdx.x % 8; w < words; w += 8) {
-      const uint32_t v = row[w];
-      if (v) atomicOr(&un[w], v);
-    }
+// One wave per query: its candidate count (lanes read the mask words in
+// parallel); list K when above kMaxCand, else one count for each candidate
+// cluster.
+__global__ void plan_count_kernel(const uint32_t* __restrict__ mask, int words, int64_t B, int K,
+                                  uint32_t* __restrict__ ccount) {
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
+  if (q >= B) return;
+  const int lane = lane_id();
+  const uint32_t* row = mask + q * words;
+  int cand = 0;
+  for (int wd = lane; wd < words; wd += kWave) cand += __builtin_popcount(row[wd]);
+  for (int off = 32; off >= 1; off >>= 1) cand += __shfl_xor(cand, off, kWave);
+  if (cand > kMaxCand) {
+    if (lane == 0) atomicAdd(&ccount[K], 1u);
+    return;
   }
-  __syncthreads();
-  const unsigned long long nq = static_cast<unsigned long long>(q1 - q0);
-  for (int w = threadIdx.x; w < words; w += 256) {
-    uint32_t v = un[w];
+  for (int wd = lane; wd < words; wd += kWave) {
+    uint32_t v = row[wd];
     while (v) {
       const int b = __builtin_ctz(v);
       v &= v - 1u;
-      const int c = 32 * w + b;
-      const int64_t e0 = offsets[c], e1 = offsets[c + 1];
-      for (int64_t s = e0; s < e1; s += kItemRows) {
-        const int64_t e = s + kItemRows < e1 ? s + kItemRows : e1;
-        const unsigned long long slot = atomicAdd(&counters[0], 1ull);
-        atomicAdd(&counters[1], nq * static_cast<unsigned long long>(e - s));
-        if (static_cast<int64_t>(slot) < capacity) {
-          items[3 * slot] = qb;
-          items[3 * slot + 1] = s;
-          items[3 * slot + 2] = e;
-        } else {
-          atomicOr(&counters[2], 1ull);
-        }
+      atomicAdd(&ccount[32 * wd + b], 1u);
+    }
+  }
+}
+
+// coff[c] = sum of ccount below c, for c = 0 .. m (one block of 1024).
+__global__ __launch_bounds__(1024) void plan_scan_kernel(const uint32_t* __restrict__ ccount, int m,
+                                                         int64_t* __restrict__ coff) {
+  __shared__ int64_t part[1024];
+  const int t = static_cast<int>(threadIdx.x);
+  const int per = (m + 1023) / 1024;
+  const int b0 = t * per, b1 = b0 + per < m ? b0 + per : m;
+  int64_t sum = 0;
+  for (int i = b0; i < b1; ++i) sum += ccount[i];
+  part[t] = sum;
+  __syncthreads();
+  if (t == 0) {
+    int64_t run = 0;
+    for (int i = 0; i < 1024; ++i) {
+      const int64_t v = part[i];
+      part[i] = run;
+      run += v;
+    }
+    coff[m] = run;
+  }
+  __syncthreads();
+  int64_t run = part[t];
+  for (int i = b0; i < b1; ++i) {
+    coff[i] = run;
+    run += ccount[i];
+  }
+}
+
+// Each query writes itself into the lists of its candidate clusters (or
+// list K); one wave per query, as in plan_count_kernel.
+__global__ void plan_fill_kernel(const uint32_t* __restrict__ mask, int words, int64_t B, int K,
+                                 const int64_t* __restrict__ coff, uint32_t* __restrict__ cfill,
+                                 int32_t* __restrict__ qlist) {
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
+  if (q >= B) return;
+  const int lane = lane_id();
+  const uint32_t* row = mask + q * words;
+  int cand = 0;
+  for (int wd = lane; wd < words; wd += kWave) cand += __builtin_popcount(row[wd]);
+  for (int off = 32; off >= 1; off >>= 1) cand += __shfl_xor(cand, off, kWave);
+  if (cand > kMaxCand) {
+    if (lane == 0) qlist[coff[K] + atomicAdd(&cfill[K], 1u)] = static_cast<int32_t>(q);
+    return;
+  }
+  for (int wd = lane; wd < words; wd += kWave) {
+    uint32_t v = row[wd];
+    while (v) {
+      const int c = 32 * wd + __builtin_ctz(v);
+      v &= v - 1u;
+      qlist[coff[c] + atomicAdd(&cfill[c], 1u)] = static_cast<int32_t>(q);
+    }
+  }
+}
+
+// One thread per list c = 0 .. K: items (query positions of c's list in
+// blocks of qblock) x (c's rows, list K: all rows, in nearly equal chunks of
+// at most kItemRows, which keeps the items of a launch alike in size).
+__global__ void plan_items_kernel(const int64_t* __restrict__ coff, const int64_t* __restrict__ offsets, int K,
+                                  int64_t n_indexed, int qblock, int64_t* __restrict__ items, int64_t capacity,
+                                  unsigned long long* __restrict__ counters) {
+  const int c = static_cast<int>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (c > K) return;
+  const int64_t q0 = coff[c], q1 = coff[c + 1];
+  const int64_t e0 = c < K ? offsets[c] : 0, e1 = c < K ? offsets[c + 1] : n_indexed;
+  if (q0 >= q1 || e0 >= e1) return;
+  // rows in nearly equal chunks of at most kItemRows
+  const int64_t chunks = (e1 - e0 + kItemRows - 1) / kItemRows;
+  const int64_t step = (e1 - e0 + chunks - 1) / chunks;
+  for (int64_t qa = q0; qa < q1; qa += qblock) {
+    const int64_t qb = qa + qblock < q1 ? qa + qblock : q1;
+    for (int64_t ea = e0; ea < e1; ea += step) {
+      const int64_t eb = ea + step < e1 ? ea + step : e1;
+      const unsigned long long slot = atomicAdd(&counters[0], 1ull);
+      atomicAdd(&counters[1], static_cast<unsigned long long>((qb - qa) * (eb - ea)));
+      if (static_cast<int64_t>(slot) < capacity) {
+        int64_t* it = items + 4 * static_cast<int64_t>(slot);
+        it[0] = qa;
+        it[1] = qb;
+        it[2] = ea;
+        it[3] = eb;
+      } else {
+        atomicOr(&counters[2], 1ull);
       }
     }
   }
@@ -375,7 +464,10 @@ using namespace lc;
 
 namespace lc {
 
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
 size_t index_plan_layout(int64_t B, int d, int K, int64_t n_indexed, int qblock, IndexPlanWs* w, char* base) {
+  (void)d;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     char* p = base ? base + off : nullptr;
@@ -383,21 +475,23 @@ size_t index_plan_layout(int64_t B, int d, int K, int64_t n_indexed, int qblock,
     return p;
   };
   const int words = (K + 31) / 32;
-  const int64_t nqb = (B + qblock - 1) / qblock;
+  const int64_t maxc = K < kMaxCand ? K : kMaxCand;
   IndexPlanWs t{};
   t.mask = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(B) * words * 4));
-  for (int s = 0; s < 2; ++s) {
-    t.keys[s] = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(B) * 4));
-    t.vals[s] = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(B) * 4));
-  }
-  t.hist = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(radix_blocks(B)) * kBins * 4));
-  t.dsum = reinterpret_cast<uint32_t*>(take(kBins * 4));
-  t.dbase = reinterpret_cast<uint32_t*>(take(kBins * 4));
-  t.qmap = reinterpret_cast<int64_t*>(take(static_cast<size_t>(B) * 8));
-  t.zq_sorted = reinterpret_cast<float*>(take(static_cast<size_t>(B) * d * 4));
-  t.capacity = nqb * (K + n_indexed / kItemRows + 1);
-  t.items = reinterpret_cast<int64_t*>(take(static_cast<size_t>(t.capacity) * 3 * 8));
+  t.ccount = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(K + 1) * 4));
+  t.cfill = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(K + 1) * 4));
+  t.coff = reinterpret_cast<int64_t*>(take(static_cast<size_t>(K + 2) * 8));
+  // every query sits in at most maxc lists, or in list K alone
+  t.qcap = B * maxc;
+  t.qlist = reinterpret_cast<int32_t*>(take(static_cast<size_t>(t.qcap > 0 ? t.qcap : 1) * 4));
+  // sum over lists c of ceil(cnt_c / qblock) ceil(rows_c / R), with
+  // sum cnt_c <= B maxc, cnt_c <= B, sum rows_c <= 2 n (list K holds all n)
+  const int64_t R = kItemRows;
+  t.capacity = cdiv(2 * B, qblock) * cdiv(n_indexed, R) + cdiv(B * maxc, qblock) + 2 * cdiv(n_indexed, R) + K + 4;
+  t.items = reinterpret_cast<int64_t*>(take(static_cast<size_t>(t.capacity) * 4 * 8));
   t.counters = reinterpret_cast<unsigned long long*>(take(64));
+  t.qnorm = reinterpret_cast<double*>(take(static_cast<size_t>(B) * 8));
+  t.cnorm = reinterpret_cast<double*>(take(static_cast<size_t>(K) * 8));
   if (w) *w = t;
   return off;
 }
@@ -412,25 +506,31 @@ lipcache_status index_query_plan(const lipcache_index* idx, const float* zq, int
   hipLaunchKernelGGL(fill_u32_kernel, dim3(static_cast<unsigned>((mwords + 255) / 256)), dim3(256), 0, s, w.mask,
                      mwords);
   LC_LAUNCHED();
-  // rigorous slack of the float32 squared distance: 4 (d + 3) u, relative
-  const double slack = 4.0 * (d + 3) / 16777216.0;
-  hipLaunchKernelGGL(nearest_centre_kernel, dim3(static_cast<unsigned>((B + kTq - 1) / kTq)), dim3(256), 0, s, zq,
-                     LIPCACHE_F32, B, d, idx->centers, K, idx->bound, slack, w.mask, w.keys[1]);
+  hipLaunchKernelGGL(fill_u32_kernel, dim3(static_cast<unsigned>((K + 1 + 255) / 256)), dim3(256), 0, s, w.ccount,
+                     static_cast<int64_t>(K + 1));
   LC_LAUNCHED();
-  hipLaunchKernelGGL(plan_keys_kernel, dim3(static_cast<unsigned>((B + 255) / 256)), dim3(256), 0, s, w.keys[1], B,
-                     w.keys[0], w.vals[0]);
+  hipLaunchKernelGGL(fill_u32_kernel, dim3(static_cast<unsigned>((K + 1 + 255) / 256)), dim3(256), 0, s, w.cfill,
+                     static_cast<int64_t>(K + 1));
   LC_LAUNCHED();
-  uint32_t* keys[2] = {w.keys[0], w.keys[1]};
-  uint32_t* vals[2] = {w.vals[0], w.vals[1]};
-  int cur = 0;
-  LC_HIP(radix_sort_u32(keys, vals, B, sort_passes(K), w.hist, w.dsum, w.dbase, cur, s));
-  hipLaunchKernelGGL(plan_gather_kernel, dim3(static_cast<unsigned>((B + 3) / 4)), dim3(256), 0, s, zq, vals[cur], B,
-                     d, w.zq_sorted, w.qmap);
+  hipLaunchKernelGGL(row_norm_kernel, dim3(static_cast<unsigned>((B + 3) / 4)), dim3(256), 0, s, zq, LIPCACHE_F32, B,
+                     d, w.qnorm);
   LC_LAUNCHED();
-  const int64_t nqb = (B + qblock - 1) / qblock;
-  hipLaunchKernelGGL(plan_items_kernel, dim3(static_cast<unsigned>(nqb)), dim3(256),
-                     static_cast<size_t>(words) * 4, s, w.mask, words, w.qmap, B, qblock, idx->offsets, w.items,
-                     w.capacity, w.counters);
+  hipLaunchKernelGGL(row_norm_kernel, dim3(static_cast<unsigned>((K + 3) / 4)), dim3(256), 0, s, idx->centers,
+                     LIPCACHE_F32, static_cast<int64_t>(K), d, w.cnorm);
+  LC_LAUNCHED();
+  const double slack = 2.0 * (d + 2) / 16777216.0;
+  hipLaunchKernelGGL(centre_mfma_kernel, dim3(static_cast<unsigned>((B + kCr - 1) / kCr)), dim3(256), 0, s, zq,
+                     LIPCACHE_F32, B, d, idx->centers, w.cnorm, K, w.qnorm, idx->bound, slack, w.mask, nullptr);
+  LC_LAUNCHED();
+  const unsigned gw = static_cast<unsigned>((B + 3) / 4);
+  hipLaunchKernelGGL(plan_count_kernel, dim3(gw), dim3(256), 0, s, w.mask, words, B, K, w.ccount);
+  LC_LAUNCHED();
+  hipLaunchKernelGGL(plan_scan_kernel, dim3(1), dim3(1024), 0, s, w.ccount, K + 1, w.coff);
+  LC_LAUNCHED();
+  hipLaunchKernelGGL(plan_fill_kernel, dim3(gw), dim3(256), 0, s, w.mask, words, B, K, w.coff, w.cfill, w.qlist);
+  LC_LAUNCHED();
+  hipLaunchKernelGGL(plan_items_kernel, dim3(static_cast<unsigned>((K + 1 + 255) / 256)), dim3(256), 0, s, w.coff,
+                     idx->offsets, K, idx->n_indexed, qblock, w.items, w.capacity, w.counters);
   LC_LAUNCHED();
   unsigned long long host[3] = {0ull, 0ull, 0ull};
   LC_HIP(hipMemcpyAsync(host, w.counters, sizeof(host), hipMemcpyDeviceToHost, s));
@@ -461,7 +561,8 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
   if (so.d != c->d || so.store_dtype != c->store_dtype || so.capacity < c->n) return LIPCACHE_EINVAL;
   if (!so.z || !so.r || !so.label || !so.norm2 || !idx->perm || !idx->offsets || !idx->centers || !idx->bound)
     return LIPCACHE_EINVAL;
-  if ((reinterpret_cast<uintptr_t>(so.z) & 15u) != 0 || (reinterpret_cast<uintptr_t>(so.zimg) & 15u) != 0)
+  if ((reinterpret_cast<uintptr_t>(so.z) & 15u) != 0 || (reinterpret_cast<uintptr_t>(so.zimg) & 15u) != 0 ||
+      (reinterpret_cast<uintptr_t>(c->z) & 15u) != 0 || (reinterpret_cast<uintptr_t>(idx->centers) & 15u) != 0)
     return LIPCACHE_EINVAL;
   const size_t need = lipcache_index_build_workspace_bytes(c->n, c->d, K);
   if (!ws || ws_bytes < need || !aligned256(ws)) return LIPCACHE_EWORKSPACE;
@@ -474,10 +575,14 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
   hipLaunchKernelGGL(centre_init_kernel, dim3(static_cast<unsigned>((kd + 255) / 256)), dim3(256), 0, s, c->z,
                      c->store_dtype, n, d, K, idx->centers);
   LC_LAUNCHED();
-  const unsigned gq = static_cast<unsigned>((n + kTq - 1) / kTq);
+  const unsigned gq = static_cast<unsigned>((n + kCr - 1) / kCr);
+  const unsigned gk = static_cast<unsigned>((K + 3) / 4);
   for (int it = 0; it < iters; ++it) {
-    hipLaunchKernelGGL(nearest_centre_kernel, dim3(gq), dim3(256), 0, s, c->z, c->store_dtype, n, d, idx->centers,
-                       K, nullptr, 0.0, nullptr, w.assign);
+    hipLaunchKernelGGL(row_norm_kernel, dim3(gk), dim3(256), 0, s, idx->centers, LIPCACHE_F32,
+                       static_cast<int64_t>(K), d, w.cnorm);
+    LC_LAUNCHED();
+    hipLaunchKernelGGL(centre_mfma_kernel, dim3(gq), dim3(256), 0, s, c->z, c->store_dtype, n, d, idx->centers,
+                       w.cnorm, K, nullptr, nullptr, 0.0, nullptr, w.assign);
     LC_LAUNCHED();
     hipLaunchKernelGGL(fill_f64_kernel, dim3(static_cast<unsigned>((kd + 255) / 256)), dim3(256), 0, s, w.sum, kd,
                        0.0);
@@ -493,8 +598,11 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
                        w.cnt, K, d, idx->centers);
     LC_LAUNCHED();
   }
-  hipLaunchKernelGGL(nearest_centre_kernel, dim3(gq), dim3(256), 0, s, c->z, c->store_dtype, n, d, idx->centers, K,
-                     nullptr, 0.0, nullptr, w.assign);
+  hipLaunchKernelGGL(row_norm_kernel, dim3(gk), dim3(256), 0, s, idx->centers, LIPCACHE_F32, static_cast<int64_t>(K),
+                     d, w.cnorm);
+  LC_LAUNCHED();
+  hipLaunchKernelGGL(centre_mfma_kernel, dim3(gq), dim3(256), 0, s, c->z, c->store_dtype, n, d, idx->centers,
+                     w.cnorm, K, nullptr, nullptr, 0.0, nullptr, w.assign);
   LC_LAUNCHED();
   hipLaunchKernelGGL(row_keys_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, s, w.assign, n,
                      w.keys[0], w.vals[0]);

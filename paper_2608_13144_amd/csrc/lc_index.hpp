@@ -6,28 +6,30 @@
 
 namespace lc {
 
-constexpr int64_t kItemRows = 8192;  // cluster rows per work item at most
+constexpr int64_t kItemRows = 1024;  // cluster rows per work item at most
+constexpr int kMaxCand = 256;        // a query with more candidate clusters scans every indexed row
 
 struct IndexPlanWs {
   uint32_t* mask;                  // [B][ceil(K / 32)] candidate clusters per query
-  uint32_t* keys[2];               // primary-cluster sort
-  uint32_t* vals[2];
-  uint32_t* hist;
-  uint32_t* dsum;
-  uint32_t* dbase;
-  int64_t* qmap;                   // [B] internal query order -> original query
-  float* zq_sorted;                // [B][d] queries in internal order
-  int64_t* items;                  // [capacity][3]
+  uint32_t* ccount;                // [K + 1] queries per cluster list (list K: queries scanned densely)
+  uint32_t* cfill;                 // [K + 1] fill cursors
+  int64_t* coff;                   // [K + 2] list offsets into qlist
+  int32_t* qlist;                  // [qcap] the lists, concatenated
+  int64_t qcap;
+  int64_t* items;                  // [capacity][4]: query positions [0], [1); rows [2], [3)
   int64_t capacity;
   unsigned long long* counters;    // [0] items, [1] pairs, [2] overflow
+  double* qnorm;                   // [B] ||q||^2
+  double* cnorm;                   // [K] ||mu_c||^2
 };
 
 size_t index_plan_layout(int64_t B, int d, int K, int64_t n_indexed, int qblock, IndexPlanWs* w, char* base);
 
 // Candidate clusters of every query (||q - mu_c|| < R_c, tested with a
-// rigorous float32 slack), queries sorted by their nearest cluster, and the
-// work list: for every block of `qblock` sorted queries, the rows of each
-// cluster any of its queries needs (split into items of <= kItemRows rows).
+// rigorous float32 slack), the list of queries of every cluster, and the
+// work list: for every cluster, its queries in blocks of `qblock` against
+// its rows in items of <= kItemRows rows.  A query with more than kMaxCand
+// candidates joins list K, which is scanned against all indexed rows.
 // Reads back the item and pair counts (sync).
 lipcache_status index_query_plan(const lipcache_index* idx, const float* zq, int64_t B, int d, int qblock,
                                  const IndexPlanWs& w, int64_t& n_items, int64_t& pairs, hipStream_t s);

@@ -67,9 +67,12 @@ struct LookupParams {
   int64_t slice_len;
   float* g_hat;          // dump mode only
   uint8_t* cand;         // dump mode only
-  // Work-list mode (indexed lookup): block b takes query block items[3b]
-  // against cache rows [items[3b+1], items[3b+2]) instead of a slice.
+  // Work-list mode (indexed lookup): block b takes the query positions
+  // [items[4b], items[4b+1]) against cache rows [items[4b+2], items[4b+3])
+  // instead of a slice; position j means query qlist[j] (j itself when
+  // qlist is null).
   const int64_t* items;
+  const int32_t* qlist;
   // Index written into a hit's key: (emap ? emap[e] : e) + eoff.
   const int64_t* emap;
   int64_t eoff;
@@ -112,20 +115,17 @@ __global__ void lookup_athr_kernel(const float* __restrict__ cr, const float* __
 }
 
 // ------------------------------------------------------------- finalize
-// Query q of the internal order answers original query qmap[q] (or q).
 __global__ void lookup_finalize_kernel(int64_t B, const unsigned long long* __restrict__ best,
                                        const unsigned int* __restrict__ bflag,
                                        const int32_t* __restrict__ clabel, int32_t* __restrict__ label_out,
                                        int64_t* __restrict__ index_out, float* __restrict__ dist2_out,
-                                       uint8_t* __restrict__ band_out, unsigned long long* __restrict__ stats,
-                                       const int64_t* __restrict__ qmap) {
-  const int64_t qi = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+                                       uint8_t* __restrict__ band_out, unsigned long long* __restrict__ stats) {
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   bool hit = false, band = false;
-  if (qi < B) {
-    const int64_t q = qmap ? qmap[qi] : qi;
-    const unsigned long long key = best[qi];
+  if (q < B) {
+    const unsigned long long key = best[q];
     hit = key != kNoHit;
-    band = bflag[qi] != 0u;
+    band = bflag[q] != 0u;
     const int64_t i = hit ? static_cast<int64_t>(key & 0xffffffffull) : -1;
     label_out[q] = hit ? clabel[i] : LIPCACHE_MISS;
     if (index_out) index_out[q] = i;
@@ -141,26 +141,32 @@ __global__ void lookup_finalize_kernel(int64_t B, const unsigned long long* __re
 }
 
 // ------------------------------------------------------------- main kernel
-// Block -> (query block, cache rows).  Slice mode: consecutive blocks of one
-// XCD (same id mod 8) take consecutive query blocks of one slice, so they
-// read each tile from that XCD's L2 at about the same time.  Work-list mode:
-// the block's item.
-__device__ __forceinline__ void block_work(const LookupParams& p, int& qb, int64_t& e_begin, int64_t& e_end) {
+// Block -> (query positions [q0, qend), cache rows).  Slice mode: consecutive
+// blocks of one XCD (same id mod 8) take consecutive query blocks of one
+// slice, so they read each tile from that XCD's L2 at about the same time.
+// Work-list mode: the block's item.
+__device__ __forceinline__ void block_work(const LookupParams& p, int64_t qblock, int64_t& q0, int64_t& qend,
+                                           int64_t& e_begin, int64_t& e_end) {
   const int bid = static_cast<int>(blockIdx.x);
   if (p.items) {
-    const int64_t* it = p.items + 3 * static_cast<int64_t>(bid);
-    qb = static_cast<int>(it[0]);
-    e_begin = it[1];
-    e_end = it[2] < p.n ? it[2] : p.n;
+    const int64_t* it = p.items + 4 * static_cast<int64_t>(bid);
+    q0 = it[0];
+    qend = it[1];
+    e_begin = it[2];
+    e_end = it[3] < p.n ? it[3] : p.n;
     return;
   }
   const int xcd = bid % kXcds;
   const int local = bid / kXcds;
   const int slice = xcd + kXcds * (local / p.n_qblocks);
-  qb = local % p.n_qblocks;
+  q0 = static_cast<int64_t>(local % p.n_qblocks) * qblock;
+  qend = p.B;
   e_begin = static_cast<int64_t>(slice) * p.slice_len;
   e_end = e_begin + p.slice_len < p.n ? e_begin + p.slice_len : p.n;
 }
+
+// The query at position j of the block's range.
+__device__ __forceinline__ int64_t query_at(const int32_t* qlist, int64_t j) { return qlist ? qlist[j] : j; }
 
 template <int MODE>
 struct ModeTraits;
@@ -244,15 +250,16 @@ struct RecheckArgs {
   unsigned long long* best;
   unsigned int* bflag;
   unsigned long long* stats;
-  int64_t B;
+  int64_t qend;          // query positions at or past qend are padding
   int64_t n;
   int d;
   const int64_t* emap;
   int64_t eoff;
+  const int32_t* qlist;
 };
 
-__device__ __forceinline__ RecheckArgs recheck_args(const LookupParams& p) {
-  return RecheckArgs{p.zq, p.cz, p.cr, p.best, p.bflag, p.stats, p.B, p.n, p.d, p.emap, p.eoff};
+__device__ __forceinline__ RecheckArgs recheck_args(const LookupParams& p, int64_t qend, const int32_t* qlist) {
+  return RecheckArgs{p.zq, p.cz, p.cr, p.best, p.bflag, p.stats, qend, p.n, p.d, p.emap, p.eoff, qlist};
 }
 
 // Exact re-check of the pairs whose bits are set in `mask` (bit rt*4+i of a
@@ -270,9 +277,10 @@ __device__ __noinline__ void recheck_pairs(const RecheckArgs p, uint32_t mask, i
     const int bit = __builtin_ctz(msrc);
     if (lane == src) mask &= mask - 1u;
     const int rt = bit >> 2, i = bit & 3;
-    const int64_t q = qwave + rt * 16 + 4 * (src >> 4) + i;
+    const int64_t qpos = qwave + rt * 16 + 4 * (src >> 4) + i;
     const int64_t e = ebase + (src & 15);
-    if (q >= p.B || e >= p.n) continue;  // padded rows never pass; kept as a guard
+    if (qpos >= p.qend || e >= p.n) continue;  // padded rows never pass; kept as a guard
+    const int64_t q = query_at(p.qlist, qpos);
     const float* qr = p.zq + q * p.d;
     double part = 0.0;
     for (int k = lane; k < p.d; k += kWave) {
@@ -302,36 +310,37 @@ __device__ __noinline__ void recheck_pairs(const RecheckArgs p, uint32_t mask, i
 
 // Queries as MFMA A operands: lane holds row m16 of each row tile and k-chunk
 // g of each k-step (the cache operand uses the same (k-step, chunk) -> k map,
-// so the contraction covers every k exactly once).  Rows past B load row
-// B - 1 (any finite values do): their thresholds are +inf.
+// so the contraction covers every k exactly once).  Positions past qend load
+// the last query (any finite values do): their thresholds are +inf.
 template <int MODE, int KS, int RT>
-__device__ __forceinline__ void load_query_operands(const LookupParams& p, int64_t qwave, int m16, int g,
-                                                    u32x4 (&a)[RT][KS]) {
+__device__ __forceinline__ void load_query_operands(const LookupParams& p, const int32_t* qlist, int64_t qwave,
+                                                    int64_t qend, int m16, int g, u32x4 (&a)[RT][KS]) {
   using T = ModeTraits<MODE>;
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
-    int64_t row = qwave + rt * 16 + m16;
-    row = row < p.B ? row : p.B - 1;
+    int64_t pos = qwave + rt * 16 + m16;
+    pos = pos < qend ? pos : qend - 1;
+    const int64_t row = query_at(qlist, pos);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) a[rt][ks] = load_chunk<MODE, LIPCACHE_F32>(p.zq, row, p.d, ks * T::kPerStep + g * T::kPerChunk);
   }
 }
 
 template <int MODE, int KS, int RT>
-__device__ __forceinline__ void load_queries(const LookupParams& p, int64_t qwave, int m16, int g, u32x4 (&a)[RT][KS],
-                                             float (&qt)[RT][4]) {
-  load_query_operands<MODE, KS, RT>(p, qwave, m16, g, a);
+__device__ __forceinline__ void load_queries(const LookupParams& p, const int32_t* qlist, int64_t qwave, int64_t qend,
+                                             int m16, int g, u32x4 (&a)[RT][KS], float (&qt)[RT][4]) {
+  load_query_operands<MODE, KS, RT>(p, qlist, qwave, qend, m16, g, a);
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int64_t qr = qwave + rt * 16 + 4 * g + i;
-      qt[rt][i] = qr < p.B ? p.qthr[qr] : __builtin_inff();
+      qt[rt][i] = qr < qend ? p.qthr[query_at(qlist, qr)] : __builtin_inff();
     }
   }
 }
 
-template <int MODE, int SRC, int KS, int RT, bool DUMP>
+template <int MODE, int SRC, int KS, int RT, bool DUMP, bool LIST>
 __global__ __launch_bounds__(kLkThreads, 2) void lookup_kernel(const LookupParams p) {
   using T = ModeTraits<MODE>;
   constexpr int kDPad = KS * T::kPerStep;
@@ -340,19 +349,20 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_kernel(const LookupParam
   __shared__ __attribute__((aligned(16))) unsigned char tile[kTileN * kRowBytes];
   __shared__ float athr[kTileN];
 
-  int qb;
-  int64_t e_begin, e_end;
-  block_work(p, qb, e_begin, e_end);
+  int64_t q0, qend, e_begin, e_end;
+  block_work(p, kLkWaves * RT * 16, q0, qend, e_begin, e_end);
+  const int32_t* qlist = LIST ? p.qlist : nullptr;
+  if constexpr (!LIST) qend = p.B;
 
   const int lane = lane_id();
   const int wave = uniform(static_cast<int>(threadIdx.x) / kWave);
   const int m16 = lane & 15;
   const int g = lane >> 4;
-  const int64_t qwave = static_cast<int64_t>(qb) * (kLkWaves * RT * 16) + wave * (RT * 16);
+  const int64_t qwave = q0 + wave * (RT * 16);
 
   u32x4 a[RT][KS];
   float qt[RT][4];
-  load_queries<MODE, KS, RT>(p, qwave, m16, g, a, qt);
+  load_queries<MODE, KS, RT>(p, qlist, qwave, qend, m16, g, a, qt);
 
   for (int64_t t0 = e_begin; t0 < e_end; t0 += kTileN) {
     __syncthreads();
@@ -430,7 +440,7 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_kernel(const LookupParam
 #pragma unroll
             for (int i = 0; i < 4; ++i) mask |= static_cast<uint32_t>((acc[rt][i] - qt[rt][i]) >= an) << (rt * 4 + i);
           }
-          recheck_pairs<SRC>(recheck_args(p), mask, qwave, ebase);
+          recheck_pairs<SRC>(recheck_args(p, qend, qlist), mask, qwave, ebase);
         }
       }
     }
@@ -555,14 +565,15 @@ __device__ __forceinline__ u32x4 lds_operand(const unsigned char* buf, int sub, 
 // Rare path of one column tile: rebuild the exact per-pair mask and re-check.
 template <int STORE, int RT>
 __device__ __forceinline__ void filter_and_recheck(const LookupParams& p, const f32x4 (&acc)[RT], const f32x4 (&qt)[RT],
-                                                   float an, int64_t qwave, int64_t ebase) {
+                                                   float an, int64_t qwave, int64_t qend, const int32_t* qlist,
+                                                   int64_t ebase) {
   uint32_t mask = 0u;
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) mask |= static_cast<uint32_t>((acc[rt][i] - qt[rt][i]) >= an) << (rt * 4 + i);
   }
-  recheck_pairs<STORE>(recheck_args(p), mask, qwave, ebase);
+  recheck_pairs<STORE>(recheck_args(p, qend, qlist), mask, qwave, ebase);
 }
 
 // A full LDS tile, software-pipelined: while the MFMAs of column tile s run,
@@ -571,7 +582,8 @@ __device__ __forceinline__ void filter_and_recheck(const LookupParams& p, const 
 // pipe's shadow instead of following it.
 template <int MODE, int STORE, int KS, int RT>
 __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, const float* athr_buf,
-                                                  const LookupParams& p, int64_t t0, int64_t qwave, int m16, int g,
+                                                  const LookupParams& p, int64_t t0, int64_t qwave, int64_t qend,
+                                                  const int32_t* qlist, int m16, int g,
                                                   const u32x4 (&a)[RT][KS], const f32x4 (&qv)[RT]) {
   constexpr int kSubs = DmaTraits<KS>::kRows / kColTile;
   constexpr int kE = RT * 4;                      // accumulators per lane
@@ -627,7 +639,7 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
     }
     if (cur && KS == 1 && sub + 1 < kSubs) b0 = lds_operand<KS>(buf, sub + 1, 0, m16, g);
     if (prev) {
-      if (__ballot(mx >= anp) != 0ull) filter_and_recheck<STORE, RT>(p, accp, qt, anp, qwave, t0 + (sub - 1) * kColTile);
+      if (__ballot(mx >= anp) != 0ull) filter_and_recheck<STORE, RT>(p, accp, qt, anp, qwave, qend, qlist, t0 + (sub - 1) * kColTile);
     }
     if (cur) {
 #pragma unroll
@@ -639,13 +651,14 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
 
 template <int MODE, int STORE, int KS, int RT, bool DUMP>
 __device__ __forceinline__ void compute_tile(const unsigned char* buf, const float* athr_buf, const LookupParams& p,
-                                             int64_t t0, int64_t e_end, int64_t qwave, int m16, int g,
-                                             const u32x4 (&a)[RT][KS], const f32x4 (&qv)[RT]) {
+                                             int64_t t0, int64_t e_end, int64_t qwave, int64_t qend,
+                                             const int32_t* qlist, int m16, int g, const u32x4 (&a)[RT][KS],
+                                             const f32x4 (&qv)[RT]) {
   constexpr int kRows = DmaTraits<KS>::kRows;
   const int64_t left = e_end - t0;
   if constexpr (!DUMP) {
     if (left >= kRows) {
-      compute_full_tile<MODE, STORE, KS, RT>(buf, athr_buf, p, t0, qwave, m16, g, a, qv);
+      compute_full_tile<MODE, STORE, KS, RT>(buf, athr_buf, p, t0, qwave, qend, qlist, m16, g, a, qv);
       return;
     }
   }
@@ -717,13 +730,13 @@ __device__ __forceinline__ void compute_tile(const unsigned char* buf, const flo
 #pragma unroll
           for (int i = 0; i < 4; ++i) mask |= static_cast<uint32_t>((acc[rt][i] - qt[rt][i]) >= an) << (rt * 4 + i);
         }
-        recheck_pairs<STORE>(recheck_args(p), mask, qwave, ebase);
+        recheck_pairs<STORE>(recheck_args(p, qend, qlist), mask, qwave, ebase);
       }
     }
   }
 }
 
-template <int MODE, int STORE, int KS, int RT, bool DUMP>
+template <int MODE, int STORE, int KS, int RT, bool DUMP, bool LIST>
 __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupParams p) {
   using T = ModeTraits<MODE>;
   constexpr int kCPR = 4 * KS;
@@ -734,21 +747,22 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
   __shared__ __attribute__((aligned(16))) float ath0[kRows];
   __shared__ __attribute__((aligned(16))) float ath1[kRows];
 
-  int qb;
-  int64_t e_begin, e_end;
-  block_work(p, qb, e_begin, e_end);
+  int64_t q0, qend, e_begin, e_end;
+  block_work(p, kLkWaves * RT * 16, q0, qend, e_begin, e_end);
+  const int32_t* qlist = LIST ? p.qlist : nullptr;
+  if constexpr (!LIST) qend = p.B;
 
   const int lane = lane_id();
   const int wave = uniform(static_cast<int>(threadIdx.x) / kWave);
   const int m16 = lane & 15;
   const int g = lane >> 4;
-  const int64_t qwave = static_cast<int64_t>(qb) * (kLkWaves * RT * 16) + wave * (RT * 16);
+  const int64_t qwave = q0 + wave * (RT * 16);
 
   if (e_begin >= e_end) return;  // whole workgroup: an empty slice
   issue_tile<MODE, KS>(buf0, ath0, p, e_begin, e_end, wave);
 
   u32x4 a[RT][KS];
-  load_query_operands<MODE, KS, RT>(p, qwave, m16, g, a);
+  load_query_operands<MODE, KS, RT>(p, qlist, qwave, qend, m16, g, a);
   // Q_q of this lane's accumulator rows 4g .. 4g + 3 of each row tile, kept
   // in registers for the whole slice (reading them from LDS per column tile
   // costs a third of the operand traffic); +inf past B.
@@ -758,7 +772,7 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int64_t q = qwave + rt * 16 + 4 * g + i;
-      qv[rt][i] = q < p.B ? p.qthr[q] : __builtin_inff();
+      qv[rt][i] = q < qend ? p.qthr[query_at(qlist, q)] : __builtin_inff();
     }
   }
 
@@ -767,13 +781,13 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
     __syncthreads();
     const bool more1 = t0 + kRows < e_end;
     if (more1) issue_tile<MODE, KS>(buf1, ath1, p, t0 + kRows, e_end, wave);
-    compute_tile<MODE, STORE, KS, RT, DUMP>(buf0, ath0, p, t0, e_end, qwave, m16, g, a, qv);
+    compute_tile<MODE, STORE, KS, RT, DUMP>(buf0, ath0, p, t0, e_end, qwave, qend, qlist, m16, g, a, qv);
     if (!more1) break;
     wait_copies();
     __syncthreads();
     const bool more2 = t0 + 2 * kRows < e_end;
     if (more2) issue_tile<MODE, KS>(buf0, ath0, p, t0 + 2 * kRows, e_end, wave);
-    compute_tile<MODE, STORE, KS, RT, DUMP>(buf1, ath1, p, t0 + kRows, e_end, qwave, m16, g, a, qv);
+    compute_tile<MODE, STORE, KS, RT, DUMP>(buf1, ath1, p, t0 + kRows, e_end, qwave, qend, qlist, m16, g, a, qv);
     if (!more2) break;
   }
 }
@@ -808,29 +822,34 @@ inline bool make_plan(int precision, const lipcache_cache* c, Plan& pl) {
   return true;
 }
 
-template <int MODE, int SRC, int KS, bool DUMP>
+// Kernel variants: the lookup, the filter dump, and the work-list lookup of
+// the cluster index.
+enum { kVarLookup = 0, kVarDump = 1, kVarList = 2 };
+
+template <int MODE, int SRC, int KS, int VAR>
 hipError_t launch_v1(const LookupParams& p, unsigned grid, hipStream_t s) {
-  hipLaunchKernelGGL((lookup_kernel<MODE, SRC, KS, (KS <= 8 ? 4 : (KS == 16 ? 2 : 1)), DUMP>), dim3(grid),
-                     dim3(kLkThreads), 0, s, p);
+  hipLaunchKernelGGL((lookup_kernel<MODE, SRC, KS, (KS <= 8 ? 4 : (KS == 16 ? 2 : 1)), VAR == kVarDump,
+                                    VAR == kVarList>),
+                     dim3(grid), dim3(kLkThreads), 0, s, p);
   return hipGetLastError();
 }
 
-template <int MODE, int STORE, int KS, bool DUMP>
+template <int MODE, int STORE, int KS, int VAR>
 hipError_t launch_dma(const LookupParams& p, unsigned grid, hipStream_t s) {
   if constexpr (KS <= 16) {
-    hipLaunchKernelGGL((lookup_dma_kernel<MODE, STORE, KS, (KS <= 8 ? 4 : 2), DUMP>), dim3(grid), dim3(kLkThreads),
-                       0, s, p);
+    hipLaunchKernelGGL((lookup_dma_kernel<MODE, STORE, KS, (KS <= 8 ? 4 : 2), VAR == kVarDump, VAR == kVarList>),
+                       dim3(grid), dim3(kLkThreads), 0, s, p);
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;
   }
 }
 
-template <int MODE, int SRC, bool DUMP>
+template <int MODE, int SRC, int VAR>
 hipError_t launch_ks(const Plan& pl, const LookupParams& p, unsigned grid, hipStream_t s) {
   switch (pl.ks) {
 #define LC_CASE(K) \
-  case K: return pl.dma ? launch_dma<MODE, SRC, K, DUMP>(p, grid, s) : launch_v1<MODE, SRC, K, DUMP>(p, grid, s);
+  case K: return pl.dma ? launch_dma<MODE, SRC, K, VAR>(p, grid, s) : launch_v1<MODE, SRC, K, VAR>(p, grid, s);
     LC_CASE(1)
     LC_CASE(2)
     LC_CASE(4)
@@ -842,15 +861,15 @@ hipError_t launch_ks(const Plan& pl, const LookupParams& p, unsigned grid, hipSt
   }
 }
 
-template <bool DUMP>
+template <int VAR>
 hipError_t launch_lookup(int precision, int store, const Plan& pl, const LookupParams& p, unsigned grid,
                          hipStream_t s) {
   if (precision == LIPCACHE_BF16) {
-    return store == LIPCACHE_F32 ? launch_ks<kModeBF16, LIPCACHE_F32, DUMP>(pl, p, grid, s)
-                                 : launch_ks<kModeBF16, LIPCACHE_BF16, DUMP>(pl, p, grid, s);
+    return store == LIPCACHE_F32 ? launch_ks<kModeBF16, LIPCACHE_F32, VAR>(pl, p, grid, s)
+                                 : launch_ks<kModeBF16, LIPCACHE_BF16, VAR>(pl, p, grid, s);
   }
-  return store == LIPCACHE_F32 ? launch_ks<kModeF32, LIPCACHE_F32, DUMP>(pl, p, grid, s)
-                               : launch_ks<kModeF32, LIPCACHE_BF16, DUMP>(pl, p, grid, s);
+  return store == LIPCACHE_F32 ? launch_ks<kModeF32, LIPCACHE_F32, VAR>(pl, p, grid, s)
+                               : launch_ks<kModeF32, LIPCACHE_BF16, VAR>(pl, p, grid, s);
 }
 
 struct Workspace {
@@ -932,13 +951,14 @@ lipcache_status lookup_stage_prep(const float* zq, int64_t B, int d, const Filte
 
 // Stage 2: the filter + re-check kernel of `view` (its n rows) against the
 // B queries, over cache slices or, with `items`, over a work list of
-// n_items (query block, row range) items.  Hits are keyed by
-// (emap ? emap[e] : e) + eoff.  athr needs athr_len(view->n) floats.
+// n_items (query positions, row range) items whose positions index qlist.
+// Hits are keyed by (emap ? emap[e] : e) + eoff.  athr needs
+// athr_len(view->n) floats.
 lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision, const FilterConsts& fc,
                                   const float* zq, int64_t B, const float* qthr, unsigned long long* best,
                                   unsigned int* bflag, unsigned long long* stats, float* athr,
-                                  const int64_t* items, int64_t n_items, const int64_t* emap, int64_t eoff,
-                                  bool dump, float* g_hat, uint8_t* cand, hipStream_t s) {
+                                  const int64_t* items, int64_t n_items, const int32_t* qlist, const int64_t* emap,
+                                  int64_t eoff, bool dump, float* g_hat, uint8_t* cand, hipStream_t s) {
   if (B <= 0 || view->n <= 0) return LIPCACHE_OK;
   if (items && n_items <= 0) return LIPCACHE_OK;
   const int64_t n_pad = athr_len(view->n);
@@ -965,6 +985,7 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
   p.g_hat = g_hat;
   p.cand = cand;
   p.items = items;
+  p.qlist = qlist;
   p.emap = emap;
   p.eoff = eoff;
   int64_t grid = n_items;
@@ -983,20 +1004,22 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
     grid = slices * p.n_qblocks;
   }
   if (grid > INT_MAX) return LIPCACHE_EUNSUPPORTED;
-  const hipError_t e = dump ? launch_lookup<true>(precision, view->store_dtype, pl, p, static_cast<unsigned>(grid), s)
-                            : launch_lookup<false>(precision, view->store_dtype, pl, p, static_cast<unsigned>(grid), s);
+  const unsigned gu = static_cast<unsigned>(grid);
+  const hipError_t e = dump    ? launch_lookup<kVarDump>(precision, view->store_dtype, pl, p, gu, s)
+                       : items ? launch_lookup<kVarList>(precision, view->store_dtype, pl, p, gu, s)
+                               : launch_lookup<kVarLookup>(precision, view->store_dtype, pl, p, gu, s);
   return e == hipSuccess ? LIPCACHE_OK : LIPCACHE_EHIP;
 }
 
-// Stage 3: per query (internal order, mapped through qmap), label / index /
-// d^2 / band flag, and the hit and band counts.
+// Stage 3: per query, label / index / d^2 / band flag, and the hit and band
+// counts.
 lipcache_status lookup_stage_finalize(int64_t B, const unsigned long long* best, const unsigned int* bflag,
                                       const int32_t* clabel, int32_t* label_out, int64_t* index_out,
                                       float* dist2_out, uint8_t* band_flag, unsigned long long* stats,
-                                      const int64_t* qmap, hipStream_t s) {
+                                      hipStream_t s) {
   if (B <= 0) return LIPCACHE_OK;
   hipLaunchKernelGGL(lookup_finalize_kernel, dim3(static_cast<unsigned>((B + 255) / 256)), dim3(256), 0, s, B, best,
-                     bflag, clabel, label_out, index_out, dist2_out, band_flag, stats, qmap);
+                     bflag, clabel, label_out, index_out, dist2_out, band_flag, stats);
   LC_LAUNCHED();
   return LIPCACHE_OK;
 }
@@ -1021,12 +1044,11 @@ lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, 
   unsigned long long* st = stats ? reinterpret_cast<unsigned long long*>(stats) : w.stats;
   lipcache_status r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s);
   if (r != LIPCACHE_OK) return r;
-  r = lookup_stage_scan(c, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr, 0, dump,
-                        g_hat, cand, s);
+  r = lookup_stage_scan(c, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr, nullptr, 0,
+                        dump, g_hat, cand, s);
   if (r != LIPCACHE_OK) return r;
   if (dump) return LIPCACHE_OK;
-  return lookup_stage_finalize(B, w.best, w.bflag, c->label, label_out, index_out, dist2_out, band_flag, st,
-                               nullptr, s);
+  return lookup_stage_finalize(B, w.best, w.bflag, c->label, label_out, index_out, dist2_out, band_flag, st, s);
 }
 
 // Workspace of an indexed lookup: the dense lookup's buffers (thresholds
@@ -1054,6 +1076,7 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
   if (so.n != idx->n_indexed || so.d != c->d || so.store_dtype != c->store_dtype || !cache_ok(&so))
     return LIPCACHE_EINVAL;
   if (!idx->perm || !idx->offsets || !idx->centers || !idx->bound) return LIPCACHE_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(idx->centers) & 15u) != 0) return LIPCACHE_EINVAL;
   // the bf16 filter streams the bf16 image of float32 rows when the cache has one
   if (precision == LIPCACHE_BF16 && c->store_dtype == LIPCACHE_F32 && (c->zimg == nullptr) != (so.zimg == nullptr))
     return LIPCACHE_EINVAL;
@@ -1074,11 +1097,10 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
   int64_t n_items = 0, idx_pairs = 0;
   lipcache_status r = index_query_plan(idx, zq, B, c->d, fc.pl.qblock, pw, n_items, idx_pairs, s);
   if (r != LIPCACHE_OK) return r;
-  const float* zs = pw.zq_sorted;
-  r = lookup_stage_prep(zs, B, c->d, fc, w.qthr, w.best, w.bflag, st, s);
+  r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s);
   if (r != LIPCACHE_OK) return r;
-  r = lookup_stage_scan(&so, precision, fc, zs, B, w.qthr, w.best, w.bflag, st, w.athr, pw.items, n_items, idx->perm,
-                        0, false, nullptr, nullptr, s);
+  r = lookup_stage_scan(&so, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, pw.items, n_items, pw.qlist,
+                        idx->perm, 0, false, nullptr, nullptr, s);
   if (r != LIPCACHE_OK) return r;
   const int64_t tail = c->n - idx->n_indexed;
   if (tail > 0) {
@@ -1093,13 +1115,12 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
     view.norm2 = c->norm2 + idx->n_indexed;
     view.n = tail;
     view.capacity = tail;
-    r = lookup_stage_scan(&view, precision, fc, zs, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr,
-                          idx->n_indexed, false, nullptr, nullptr, s);
+    r = lookup_stage_scan(&view, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr,
+                          nullptr, idx->n_indexed, false, nullptr, nullptr, s);
     if (r != LIPCACHE_OK) return r;
   }
   if (pairs) *pairs = idx_pairs + B * tail;
-  return lookup_stage_finalize(B, w.best, w.bflag, c->label, label_out, index_out, dist2_out, band_flag, st, pw.qmap,
-                               s);
+  return lookup_stage_finalize(B, w.best, w.bflag, c->label, label_out, index_out, dist2_out, band_flag, st, s);
 }
 
 }  // namespace lc

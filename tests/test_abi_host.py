@@ -139,6 +139,65 @@ def test_insert_validation():
     assert st == L.OK and n == 0
 
 
+def _index(K=4, n_indexed=10, **kw):
+    srt = _cache(n=n_indexed, capacity=16)
+    ix = L.LipcacheIndex(srt, FAKE.value, FAKE.value, FAKE.value, FAKE.value, K, n_indexed)
+    for k, v in kw.items():
+        setattr(ix, k, v)
+    return ix
+
+
+def test_index_build_validation():
+    lib = L.load()
+
+    def call(c, K=4, iters=2, ix="default", ws=FAKE, wsb=1 << 30):
+        ix = _index() if ix == "default" else ix
+        return lib.lipcache_index_build(ctypes.byref(c) if c is not None else None, K, iters,
+                                        ctypes.byref(ix) if ix is not None else None, ws, wsb, None)
+    assert call(None) == L.EINVAL
+    assert call(_cache(n=10), ix=None) == L.EINVAL
+    assert call(_cache(n=0)) == L.EINVAL                     # nothing to index
+    assert call(_cache(n=10), K=0) == L.EINVAL
+    assert call(_cache(n=10), K=11) == L.EINVAL              # K > n
+    assert call(_cache(n=10), iters=-1) == L.EINVAL
+    assert call(_cache(n=10, d=40)) == L.EINVAL
+    small = _index()
+    small.sorted.capacity = 8
+    assert call(_cache(n=10), ix=small) == L.EINVAL          # sorted copy cannot hold the rows
+    assert call(_cache(n=10), ix=_index(centers=0x100004)) == L.EINVAL
+    assert call(_cache(n=10), ix=_index(perm=None)) == L.EINVAL
+    assert call(_cache(n=10), ws=None) == L.EWORKSPACE
+    assert call(_cache(n=10), wsb=64) == L.EWORKSPACE
+    assert lib.lipcache_index_build_workspace_bytes(1 << 20, 256, 1024) >= (1 << 20) * 4 + 1024 * 256 * 8
+
+
+def test_lookup_indexed_validation():
+    lib = L.load()
+
+    def call(c, ix, B=8, prec=L.BF16, ws=FAKE, wsb=1 << 30):
+        pairs = ctypes.c_int64(-1)
+        st = lib.lipcache_lookup_indexed(ctypes.byref(c), ctypes.byref(ix) if ix is not None else None, FAKE, B,
+                                         prec, FAKE, None, None, None, None, ctypes.byref(pairs), ws, wsb, None)
+        return st
+    c = _cache(n=12)
+    assert call(c, None) == L.EINVAL
+    assert call(c, _index(K=0)) == L.EINVAL
+    assert call(c, _index(n_indexed=13)) == L.EINVAL         # more rows indexed than the cache holds
+    bad = _index()
+    bad.sorted.n = 9
+    assert call(c, bad) == L.EINVAL                          # sorted copy out of step with the index
+    bad = _index()
+    bad.sorted.d = 128
+    assert call(c, bad) == L.EINVAL
+    assert call(c, _index(centers=0x100004)) == L.EINVAL
+    assert call(_cache(n=12, zimg=FAKE.value), _index()) == L.EINVAL   # image on one side only
+    assert call(c, _index(), B=-1) == L.EINVAL
+    assert call(c, _index(), prec=7) == L.EINVAL
+    assert call(c, _index(), ws=None) == L.EWORKSPACE
+    assert call(c, _index(), wsb=64) == L.EWORKSPACE
+    assert lib.lipcache_lookup_indexed_workspace_bytes(32768, 1 << 20, 256, 1024, 1 << 20) >= 32768 * 1024 // 8
+
+
 def test_binding_refuses_without_library(tmp_path):
     saved = L._LIB
     try:

@@ -11,7 +11,8 @@ The indexed lookup returns the oracle's answers query by query and the
 dense device lookup's outputs bit for bit (label, index, d^2, band flags,
 hit and band counters), for both stores and filters, K from 1 to n,
 rows appended after the build, dead rows, duplicated rows (empty
-clusters), a ragged batch, non-finite queries, and the full-size mixture.
+clusters), queries with more candidate clusters than a list takes, a
+ragged batch, non-finite queries, and the full-size mixture.
 """
 import numpy as np
 import pytest
@@ -142,6 +143,24 @@ def test_dead_rows_and_duplicates(tiny):
     res_i, _ = c.lookup_indexed(ix, gpu(zq))
     compare_lookup(res_i, ref2, "dup")
     same_as_dense(res_i, c.lookup(gpu(zq)), "dup")
+
+
+def test_queries_with_many_candidates(tiny):
+    """Entries of one class get radius 15 and the index has 512 clusters:
+    queries near that class have more than 256 candidate clusters and are
+    scanned against every indexed row; the rest go through cluster lists."""
+    wl, st, zq, ref = tiny["f32"]
+    say("index many candidates")
+    r = np.where(st.label == 0, np.float32(15.0), st.r).astype(np.float32)
+    st2 = oracle_cache(st.z, st.label, r, 64)
+    c = build_cache(st2)
+    ix = c.build_index(512, 2)
+    check_index(c, ix, "many")
+    ref2 = oracle.lookup_blocked(zq, st2.z, st2.r, st2.label)
+    res_i, pairs = c.lookup_indexed(ix, gpu(zq))
+    compare_lookup(res_i, ref2, "many")
+    same_as_dense(res_i, c.lookup(gpu(zq)), "many")
+    say("many candidates: pairs", pairs, "of", zq.shape[0] * st.n)
 
 
 def test_edge_batches(tiny):

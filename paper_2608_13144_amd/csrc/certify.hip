@@ -229,6 +229,208 @@ __global__ __launch_bounds__(kCertThreads) void certify_kernel(
   if (norm2_out) norm2_out[i] = static_cast<float>(nrm);
 }
 
+// ------------------------------------------------------------ matrix cores
+// The same certification with the logits on the matrix cores (d <= 512):
+// s = Z W^T by v_mfma_f64_16x16x4_f64 (float64 products of float32 values
+// are exact; sums in float64).  A workgroup of four waves owns 64 features,
+// 16 per wave, held as A operands in registers (lane (m, g) keeps feature m's
+// k = 16 kq + 4 g + j); the head's rows pass through LDS 32 classes at a
+// time (two 16-class B tiles, shared by the four waves).  Lane (m, g) ends a
+// tile holding s for features g + 4 v of its wave and class c0 + m (the
+// float64 instruction interleaves its output rows); it keeps
+// a running (top-1, class, top-2) per feature over its classes in increasing
+// order, and a butterfly over the 16 lanes of its row group merges them (the
+// larger top-1 wins, the lower class on equal values, the rest competes for
+// top-2): the same result as one pass over the classes in order.
+constexpr int kCmThreads = 256;
+constexpr int kCmRows = 64;        // features per workgroup
+constexpr int kCmClasses = 32;     // head rows per LDS stage
+
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void top2_merge(double w1, int j1, double w2, double& v1, int& i1, double& v2) {
+  if (w1 > v1 || (w1 == v1 && j1 < i1)) {
+    v2 = v1 > v2 ? v1 : v2;
+    v1 = w1;
+    i1 = j1;
+  } else {
+    v2 = w1 > v2 ? w1 : v2;
+  }
+  v2 = w2 > v2 ? w2 : v2;
+}
+
+// Features past d are zero on both sides (registers and LDS), so every
+// k-group runs and adds exact zeros there.
+template <int KQ>
+__device__ __forceinline__ void tile_logits(const f32x4 (&za)[KQ], const float* wl, int stride, int m16, int g,
+                                            f64x4& acc0, f64x4& acc1) {
+  acc0 = f64x4{0.0, 0.0, 0.0, 0.0};
+  acc1 = f64x4{0.0, 0.0, 0.0, 0.0};
+  const float* r0 = wl + m16 * stride + 4 * g;
+  const float* r1 = wl + (16 + m16) * stride + 4 * g;
+#pragma unroll
+  for (int kq = 0; kq < KQ; ++kq) {
+    const f32x4 b0 = *reinterpret_cast<const f32x4*>(r0 + 16 * kq);
+    const f32x4 b1 = *reinterpret_cast<const f32x4*>(r1 + 16 * kq);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const double a = static_cast<double>(za[kq][j]);
+      acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(a, static_cast<double>(b0[j]), acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(a, static_cast<double>(b1[j]), acc1, 0, 0, 0);
+    }
+  }
+}
+
+// Head rows c0 .. c0 + 31 into LDS, float32 as given; zeros past C and in
+// the columns from d to the padded width `width`.
+__device__ __forceinline__ void stage_head(const float* __restrict__ W, int C, int d, int width, int c0, float* wl,
+                                           int stride) {
+  const int q4 = width / 4;
+  for (int t = static_cast<int>(threadIdx.x); t < kCmClasses * q4; t += kCmThreads) {
+    const int row = t / q4, col = 4 * (t % q4);
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (c0 + row < C && col < d) v = *reinterpret_cast<const f32x4*>(W + static_cast<int64_t>(c0 + row) * d + col);
+    *reinterpret_cast<f32x4*>(wl + row * stride + col) = v;
+  }
+}
+
+template <bool BF16_STORE, bool TIGHT, int KQ>
+__global__ __launch_bounds__(kCmThreads) void certify_mfma_kernel(
+    const float* __restrict__ z, int64_t N, int d, const float* __restrict__ W, const float* __restrict__ b, int C,
+    double sigma, const double* __restrict__ row_dist, int32_t* __restrict__ label_out, float* __restrict__ r_out,
+    float* __restrict__ margin_out, float* __restrict__ norm2_out) {
+  extern __shared__ float wl[];  // kCmClasses rows of stride 16 KQ + 4 floats
+  constexpr int kWidth = 16 * KQ;
+  constexpr int stride = kWidth + 4;
+  const int lane = lane_id();
+  const int wave = uniform(static_cast<int>(threadIdx.x) / kWave);
+  const int m16 = lane & 15, g = lane >> 4;
+  const int nk = d / 16;
+  const int64_t row0 = static_cast<int64_t>(blockIdx.x) * kCmRows + wave * 16;
+
+  // A operands: feature row0 + m16, k = 16 kq + 4 g + j (stored values)
+  f32x4 za[KQ];
+  double nrm = 0.0;
+  {
+    const int64_t e = row0 + m16;
+#pragma unroll
+    for (int kq = 0; kq < KQ; ++kq) {
+      f32x4 v = {0.f, 0.f, 0.f, 0.f};
+      if (kq < nk && e < N) v = *reinterpret_cast<const f32x4*>(z + e * d + 16 * kq + 4 * g);
+      if constexpr (BF16_STORE) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = bf16_round_f32(v[j]);
+      }
+      za[kq] = v;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) nrm = __builtin_fma(static_cast<double>(v[j]), static_cast<double>(v[j]), nrm);
+    }
+  }
+  // ||z||^2 of feature m16: the four lanes g = 0..3 hold a quarter each
+  nrm += __shfl_xor(nrm, 16, kWave);
+  nrm += __shfl_xor(nrm, 32, kWave);
+
+  double v1[4], v2[4];
+  int i1[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    v1[v] = -__builtin_inf();
+    v2[v] = -__builtin_inf();
+    i1[v] = INT_MAX;
+  }
+  for (int c0 = 0; c0 < C; c0 += kCmClasses) {
+    __syncthreads();
+    stage_head(W, C, d, kWidth, c0, wl, stride);
+    __syncthreads();
+    f64x4 acc[2];
+    tile_logits<KQ>(za, wl, stride, m16, g, acc[0], acc[1]);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int c = c0 + 16 * t + m16;
+      if (c < C) {
+        const double bc = b ? static_cast<double>(b[c]) : 0.0;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) top2_push(acc[t][v] + bc, c, v1[v], i1[v], v2[v]);
+      }
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      const double w1 = __shfl_xor(v1[v], off, kWave);
+      const int j1 = __shfl_xor(i1[v], off, kWave);
+      const double w2 = __shfl_xor(v2[v], off, kWave);
+      top2_merge(w1, j1, w2, v1[v], i1[v], v2[v]);
+    }
+  }
+
+  double r[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) r[v] = (v1[v] - v2[v]) / (sigma * kSqrt2);
+  if constexpr (TIGHT) {
+    double best[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) best[v] = __builtin_inf();
+    for (int c0 = 0; c0 < C; c0 += kCmClasses) {
+      __syncthreads();
+      stage_head(W, C, d, kWidth, c0, wl, stride);
+      __syncthreads();
+      f64x4 acc[2];
+      tile_logits<KQ>(za, wl, stride, m16, g, acc[0], acc[1]);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int c = c0 + 16 * t + m16;
+        if (c < C) {
+          const double bc = b ? static_cast<double>(b[c]) : 0.0;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int y = i1[v];
+            if (y >= 0 && y < C && c != y) {
+              const double den = row_dist[static_cast<int64_t>(y) * C + c];
+              if (den > 0.0) {
+                const double rij = (v1[v] - (acc[t][v] + bc)) / den;
+                best[v] = rij < best[v] ? rij : best[v];
+              }
+            }
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) {
+        const double o = __shfl_xor(best[v], off, kWave);
+        best[v] = o < best[v] ? o : best[v];
+      }
+      // no label when the feature is not finite
+      r[v] = (i1[v] >= 0 && i1[v] < C) ? best[v] : __builtin_nan("");
+    }
+  }
+  // lane (m16 < 4, g) writes feature g + 4 m16 of the wave (its v = m16)
+  const double n_out = __shfl(nrm, g + 4 * (m16 & 3), kWave);
+  if (m16 < 4) {
+    const int64_t i = row0 + g + 4 * m16;
+    if (i < N) {
+      double rv = r[0], mv = v1[0] - v2[0];
+      int lab = i1[0];
+#pragma unroll
+      for (int v = 1; v < 4; ++v) {
+        if (m16 == v) {
+          rv = r[v];
+          mv = v1[v] - v2[v];
+          lab = i1[v];
+        }
+      }
+      label_out[i] = lab;
+      r_out[i] = static_cast<float>(rv);
+      if (margin_out) margin_out[i] = static_cast<float>(mv);
+      if (norm2_out) norm2_out[i] = static_cast<float>(n_out);
+    }
+  }
+}
+
 }  // namespace lc
 
 using namespace lc;
@@ -247,6 +449,59 @@ hipError_t launch_certify(unsigned grid, size_t lds, hipStream_t s, const float*
   hipLaunchKernelGGL((certify_kernel<BF16_STORE, TIGHT>), dim3(grid), dim3(kCertThreads), lds, s, z, N, d, E, W64, b,
                      C, sigma, row_dist, label_out, r_out, margin_out, norm2_out);
   return hipGetLastError();
+}
+
+template <bool BF16_STORE, bool TIGHT, int KQ>
+hipError_t launch_mfma_kq(unsigned grid, size_t lds, hipStream_t s, const float* z, int64_t N, int d, const float* W,
+                          const float* b, int C, double sigma, const double* row_dist, int32_t* label_out,
+                          float* r_out, float* margin_out, float* norm2_out) {
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(certify_mfma_kernel<BF16_STORE, TIGHT, KQ>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((certify_mfma_kernel<BF16_STORE, TIGHT, KQ>), dim3(grid), dim3(kCmThreads), lds, s, z, N, d, W,
+                     b, C, sigma, row_dist, label_out, r_out, margin_out, norm2_out);
+  return hipGetLastError();
+}
+
+template <bool BF16_STORE, bool TIGHT>
+hipError_t launch_mfma_d(int d, unsigned grid, size_t lds, hipStream_t s, const float* z, int64_t N, const float* W,
+                         const float* b, int C, double sigma, const double* row_dist, int32_t* label_out,
+                         float* r_out, float* margin_out, float* norm2_out) {
+  // registers for d / 16 k-groups, rounded up to a power of two
+  const int nk = d / 16;
+  if (nk <= 2)
+    return launch_mfma_kq<BF16_STORE, TIGHT, 2>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, label_out, r_out,
+                                                margin_out, norm2_out);
+  if (nk <= 4)
+    return launch_mfma_kq<BF16_STORE, TIGHT, 4>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, label_out, r_out,
+                                                margin_out, norm2_out);
+  if (nk <= 8)
+    return launch_mfma_kq<BF16_STORE, TIGHT, 8>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, label_out, r_out,
+                                                margin_out, norm2_out);
+  if (nk <= 16)
+    return launch_mfma_kq<BF16_STORE, TIGHT, 16>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, label_out, r_out,
+                                                 margin_out, norm2_out);
+  return launch_mfma_kq<BF16_STORE, TIGHT, 32>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, label_out, r_out,
+                                               margin_out, norm2_out);
+}
+
+hipError_t launch_certify_mfma(bool bf16, bool tight, int d, unsigned grid, size_t lds, hipStream_t s, const float* z,
+                               int64_t N, const float* W, const float* b, int C, double sigma,
+                               const double* row_dist, int32_t* label_out, float* r_out, float* margin_out,
+                               float* norm2_out) {
+  if (bf16 && tight)
+    return launch_mfma_d<true, true>(d, grid, lds, s, z, N, W, b, C, sigma, row_dist, label_out, r_out, margin_out,
+                                     norm2_out);
+  if (bf16)
+    return launch_mfma_d<true, false>(d, grid, lds, s, z, N, W, b, C, sigma, row_dist, label_out, r_out, margin_out,
+                                      norm2_out);
+  if (tight)
+    return launch_mfma_d<false, true>(d, grid, lds, s, z, N, W, b, C, sigma, row_dist, label_out, r_out, margin_out,
+                                      norm2_out);
+  return launch_mfma_d<false, false>(d, grid, lds, s, z, N, W, b, C, sigma, row_dist, label_out, r_out, margin_out,
+                                     norm2_out);
 }
 
 }  // namespace
@@ -290,6 +545,16 @@ extern "C" lipcache_status lipcache_certify(const float* z, int64_t N, int32_t d
     LC_LAUNCHED();
   }
 
+  if (d <= 512) {
+    int kq = 2;
+    while (16 * kq < d) kq *= 2;
+    const size_t lds_m = static_cast<size_t>(kCmClasses) * (16 * kq + 4) * sizeof(float);
+    const unsigned grid_m = static_cast<unsigned>((N + kCmRows - 1) / kCmRows);
+    const hipError_t em = launch_certify_mfma(store_dtype == LIPCACHE_BF16, radius_mode == LIPCACHE_RADIUS_TIGHT, d,
+                                              grid_m, lds_m, s, z, N, W, b, C, sigma, row_dist, label_out, r_out,
+                                              margin_out, norm2_out);
+    return em == hipSuccess ? LIPCACHE_OK : LIPCACHE_EHIP;
+  }
   const int E = d <= 512 ? 64 : 32;
   const size_t lds = static_cast<size_t>(E) * (d + 4) * sizeof(float);
   const unsigned grid = static_cast<unsigned>((N + E - 1) / E);

@@ -9,11 +9,13 @@
 // in float64; float32 accumulation would move a large share of the radii by
 // more than 1e-5 relative.
 //
-// Layout: a workgroup of four waves owns a tile of E features (E = 64 for
-// d <= 512, else 32), staged once in LDS.  Lane e of every wave works on
-// feature e; wave w runs over the class chunks w, w+4, w+8, ... (eight classes
-// per chunk), so the head row it reads is the same in all 64 lanes and comes
-// through scalar loads of a float64 copy of W.  Each lane keeps a running
+// Two kernels.  For d <= 512 the logits run on the float64 matrix cores
+// (certify_mfma_kernel, below).  For wider features a vector kernel is used:
+// a workgroup of four waves owns a tile of E = 32 features, staged once in
+// LDS.  Lane e of every wave works on feature e; wave w runs over the class
+// chunks w, w+4, w+8, ... (eight classes per chunk), so the head row it
+// reads is the same in all 64 lanes and comes through scalar loads of a
+// float64 copy of W.  Each lane keeps a running
 // (top-1 value, top-1 class, top-2 value); the four waves' candidates are
 // merged in wave order through LDS.  For the tight radius the label is
 // broadcast back to the four waves, which recompute their classes' logits
@@ -533,9 +535,12 @@ extern "C" lipcache_status lipcache_certify(const float* z, int64_t N, int32_t d
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   double* W64 = static_cast<double*>(ws);
   const int64_t cd = static_cast<int64_t>(C) * d;
-  hipLaunchKernelGGL(widen_kernel, dim3(static_cast<unsigned>((cd + 255) / 256)), dim3(256), 0, s, W, cd, W64);
-  LC_LAUNCHED();
   const bool tight = radius_mode == LIPCACHE_RADIUS_TIGHT;
+  // the float64 copy of W feeds the row distances and the vector kernel
+  if (tight || d > 512) {
+    hipLaunchKernelGGL(widen_kernel, dim3(static_cast<unsigned>((cd + 255) / 256)), dim3(256), 0, s, W, cd, W64);
+    LC_LAUNCHED();
+  }
   double* row_dist = nullptr;
   if (tight) {
     row_dist = reinterpret_cast<double*>(static_cast<unsigned char*>(ws) + head_bytes(C, d));
@@ -555,7 +560,7 @@ extern "C" lipcache_status lipcache_certify(const float* z, int64_t N, int32_t d
                                               margin_out, norm2_out);
     return em == hipSuccess ? LIPCACHE_OK : LIPCACHE_EHIP;
   }
-  const int E = d <= 512 ? 64 : 32;
+  const int E = 32;  // features per workgroup of the vector kernel (d > 512)
   const size_t lds = static_cast<size_t>(E) * (d + 4) * sizeof(float);
   const unsigned grid = static_cast<unsigned>((N + E - 1) / E);
   const bool bf16 = store_dtype == LIPCACHE_BF16;

@@ -26,26 +26,56 @@ constexpr int kPowMaxM = 1024;
 constexpr int kPowRegMaxM = 208;                            // matrix held in registers up to here
 constexpr int kSquarings = 6;                               // P = (G 2^-e)^(2^6)
 
-// G[a][b] = sum over the long side of W of products of W's entries.
-__global__ void gram_kernel(const float* __restrict__ W, int C, int d, int side,
-                            double* __restrict__ G) {
-  const int m = side == 0 ? C : d;
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (idx >= static_cast<int64_t>(m) * m) return;
-  const int a = static_cast<int>(idx / m);
-  const int b = static_cast<int>(idx % m);
-  double s = 0.0;
-  if (side == 0) {  // (W W^T)_ab = sum_k W_ak W_bk
-    const float* wa = W + static_cast<int64_t>(a) * d;
-    const float* wb = W + static_cast<int64_t>(b) * d;
-    for (int k = 0; k < d; ++k) s = __builtin_fma(static_cast<double>(wa[k]), static_cast<double>(wb[k]), s);
-  } else {          // (W^T W)_ab = sum_c W_ca W_cb
-    for (int c = 0; c < C; ++c) {
-      const float* wc = W + static_cast<int64_t>(c) * d;
-      s = __builtin_fma(static_cast<double>(wc[a]), static_cast<double>(wc[b]), s);
-    }
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+enum { kGramRows = 0, kGramCols = 1, kGramSym = 2 };
+
+// Entry (a, k) of the factor X in Out = X X^T: W's row a (W W^T), W's column
+// a (W^T W), or row a of a symmetric float64 matrix times an exact power of
+// two; zero outside the m x L range.
+template <int MODE>
+__device__ __forceinline__ double gram_x(const void* __restrict__ X, int ld, int m, int L, int a, int k, double s) {
+  if (a >= m || k >= L) return 0.0;
+  if constexpr (MODE == kGramRows) return static_cast<double>(static_cast<const float*>(X)[static_cast<int64_t>(a) * ld + k]);
+  if constexpr (MODE == kGramCols) return static_cast<double>(static_cast<const float*>(X)[static_cast<int64_t>(k) * ld + a]);
+  return static_cast<const double*>(X)[static_cast<int64_t>(a) * ld + k] * s;
+}
+
+// Out[a][b] = sum_k X(a, k) X(b, k) for a, b < m on the float64 matrix cores
+// (v_mfma_f64_16x16x4_f64; products of floats are exact, sums in float64):
+// one workgroup per 16 x 16 output tile.  Wave w takes the k-steps w, w + 4,
+// w + 8, ... (so each dependent chain is a quarter of the k range and the
+// four waves' loads overlap); lane (r, q) feeds X(i0 + r, k + q) and
+// X(j0 + r, k + q) and ends holding rows i0 + q + 4v of column j0 + r.  The
+// four partial tiles are added in wave order through LDS.
+template <int MODE>
+__global__ __launch_bounds__(256) void gram_mfma_kernel(const void* __restrict__ X, int ld, int m, int L,
+                                                        const double* __restrict__ scale, double* __restrict__ Out) {
+  __shared__ double part[4][4][kWave];
+  const int lane = lane_id();
+  const int w = static_cast<int>(threadIdx.x) / kWave;
+  const int r = lane & 15, q = lane >> 4;
+  const int tiles = (m + 15) / 16;
+  const int t = static_cast<int>(blockIdx.x);
+  const int i0 = (t / tiles) * 16, j0 = (t % tiles) * 16;
+  const double s = (MODE == kGramSym && scale) ? scale[0] : 1.0;
+  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 4
+  for (int k0 = 4 * w; k0 < L; k0 += 16) {
+    const double a = gram_x<MODE>(X, ld, m, L, i0 + r, k0 + q, s);
+    const double b = gram_x<MODE>(X, ld, m, L, j0 + r, k0 + q, s);
+    acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
   }
-  G[idx] = s;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) part[w][v][lane] = acc[v];
+  __syncthreads();
+  if (w != 0) return;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const double sum = ((part[0][v][lane] + part[1][v][lane]) + part[2][v][lane]) + part[3][v][lane];
+    const int row = i0 + q + 4 * v, col = j0 + r;
+    if (row < m && col < m) Out[static_cast<int64_t>(row) * m + col] = sum;
+  }
 }
 
 // scale[0] = 2^-e with 2^e > trace(A) >= lambda_max (0 for a zero trace):
@@ -64,27 +94,6 @@ __global__ __launch_bounds__(256) void gram_scale_kernel(const double* __restric
     for (int w = 0; w < 256 / kWave; ++w) t += part[w];
     scale[0] = t > 0.0 ? ldexp(1.0, -(ilogb(t) + 1)) : 0.0;
   }
-}
-
-// Out = (s A)(s A) for a symmetric m x m A (so row b of A is also its
-// column b), s = scale[0] when given, else 1.
-__global__ void gram_square_kernel(const double* __restrict__ A, int m, const double* __restrict__ scale,
-                                   double* __restrict__ Out) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (idx >= static_cast<int64_t>(m) * m) return;
-  const int a = static_cast<int>(idx / m);
-  const int b = static_cast<int>(idx % m);
-  const double sc = scale ? scale[0] : 1.0;
-  const double* ra = A + static_cast<int64_t>(a) * m;
-  const double* rb = A + static_cast<int64_t>(b) * m;
-  double s0 = 0.0, s1 = 0.0;
-  int k = 0;
-  for (; k + 1 < m; k += 2) {
-    s0 = __builtin_fma(ra[k], rb[k], s0);
-    s1 = __builtin_fma(ra[k + 1], rb[k + 1], s1);
-  }
-  if (k < m) s0 = __builtin_fma(ra[k], rb[k], s0);
-  Out[idx] = (s0 + s1) * (sc * sc);
 }
 
 // Start vector: SplitMix64 of the component index mapped to [-1, 1).
@@ -316,17 +325,22 @@ extern "C" lipcache_status lipcache_spectral_norm(const float* W, int32_t C, int
                   reinterpret_cast<double*>(static_cast<char*>(ws) + 2 * mat)};
   double* out = reinterpret_cast<double*>(static_cast<char*>(ws) + 3 * mat);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const int64_t cells = static_cast<int64_t>(m) * m;
-  const dim3 cgrid(static_cast<unsigned>((cells + 255) / 256));
-  hipLaunchKernelGGL(gram_kernel, cgrid, dim3(256), 0, s, W, C, d, side, G);
+  const int tiles = (m + 15) / 16;
+  const dim3 tgrid(static_cast<unsigned>(tiles * tiles));
+  if (side == 0) {
+    hipLaunchKernelGGL(gram_mfma_kernel<kGramRows>, tgrid, dim3(256), 0, s, W, d, m, d, nullptr, G);
+  } else {
+    hipLaunchKernelGGL(gram_mfma_kernel<kGramCols>, tgrid, dim3(256), 0, s, W, d, m, C, nullptr, G);
+  }
   LC_LAUNCHED();
   double* scale = out + 4;
   hipLaunchKernelGGL(gram_scale_kernel, dim3(1), dim3(256), 0, s, G, m, scale);
   LC_LAUNCHED();
-  hipLaunchKernelGGL(gram_square_kernel, cgrid, dim3(256), 0, s, G, m, scale, P[0]);
+  // P_1 = (s G)(s G), then P_{i+1} = P_i P_i (G and its powers are symmetric)
+  hipLaunchKernelGGL(gram_mfma_kernel<kGramSym>, tgrid, dim3(256), 0, s, G, m, m, m, scale, P[0]);
   LC_LAUNCHED();
   for (int i = 1; i < kSquarings; ++i) {
-    hipLaunchKernelGGL(gram_square_kernel, cgrid, dim3(256), 0, s, P[(i + 1) & 1], m, nullptr, P[i & 1]);
+    hipLaunchKernelGGL(gram_mfma_kernel<kGramSym>, tgrid, dim3(256), 0, s, P[(i + 1) & 1], m, m, m, nullptr, P[i & 1]);
     LC_LAUNCHED();
   }
   const double* M = P[(kSquarings + 1) & 1];

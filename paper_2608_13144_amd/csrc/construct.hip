@@ -438,6 +438,191 @@ __global__ __launch_bounds__(256) void kcenter_pick_kernel(const KcParams p, int
   }
 }
 
+// ------------------------------------------------- per-class K-center
+// With a per-class budget every class is traversed on its own, so the
+// classes run side by side: their eligible candidates are sorted by class
+// (stably, so each class list keeps the visit order and starts at its
+// largest radius), one workgroup walks one class, and the total budget is
+// applied afterwards in ascending class order (a traversal's first k picks
+// do not depend on how many follow).
+
+// keys / vals of the class sort: label and candidate of visit position q.
+__global__ void class_keys_kernel(const int32_t* __restrict__ label, const uint32_t* __restrict__ order,
+                                  int64_t n_elig, uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
+                                  uint32_t* __restrict__ ccount) {
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (q >= n_elig) return;
+  const uint32_t i = order[q];
+  const uint32_t c = static_cast<uint32_t>(label[i]);  // in [0, n_classes): eligibility
+  keys[q] = c;
+  vals[q] = i;
+  atomicAdd(&ccount[c], 1u);
+}
+
+constexpr int kKcThreads = 1024;
+
+// Farthest-first traversal of class blockIdx.x over its list
+// list[coff[c] .. coff[c + 1]): up to min(per_class, budget, size) picks into
+// cpicks[coff[c] ..], their number into ccount[c].  mind[coff[c] + j] holds
+// candidate j's squared distance to the chosen set (-1 once chosen).  Each
+// wave measures four candidates at a time (16 lanes each, float64 sums of the
+// stored values against the newest pick, kept in LDS); the block arg-max
+// takes the larger distance, then the lower candidate index.  U = row chunks
+// of 64 features per lane (d <= 64 U); wide rows run 512 threads, so each
+// lane may keep two rows of chunks in registers.
+template <int U, int THREADS>
+__global__ __launch_bounds__(THREADS) void kcenter_class_kernel(const float* __restrict__ z, int d, int bf16,
+                                                                   const uint32_t* __restrict__ list,
+                                                                   const int64_t* __restrict__ coff, int per_class,
+                                                                   int64_t budget, double* __restrict__ mind,
+                                                                   int64_t* __restrict__ cpicks,
+                                                                   uint32_t* __restrict__ ccount) {
+  __shared__ __attribute__((aligned(16))) float prow[1024];
+  constexpr int kWaves = THREADS / kWave;
+  __shared__ double sv[kWaves];
+  __shared__ int64_t si[kWaves];
+  __shared__ int64_t s_pick;
+  const int c = static_cast<int>(blockIdx.x);
+  const int t = static_cast<int>(threadIdx.x);
+  const int lane = lane_id(), wave = t / kWave;
+  const int grp = lane >> 4, lr = lane & 15;
+  const int64_t j0 = coff[c];
+  const int64_t nc = coff[c + 1] - j0;
+  int64_t lim = per_class < nc ? per_class : nc;
+  lim = budget < lim ? budget : lim;
+  if (lim <= 0) {
+    if (t == 0) ccount[c] = 0u;
+    return;
+  }
+  int64_t pick = list[j0];
+  if (t == 0) cpicks[j0] = pick;
+  int64_t cnt = 1;
+  for (int pass = 0; cnt < lim; ++pass) {
+    __syncthreads();
+    for (int k = t; k < d; k += THREADS) {
+      const float v = z[pick * d + k];
+      prow[k] = bf16 ? bf16_round_f32(v) : v;
+    }
+    __syncthreads();
+    double bv = -1.0;
+    int64_t bi = -1;
+    // Software pipeline: while the distances of batch b are summed, the rows
+    // of batch b + 1 and the candidate and distance of batch b + 2 are in
+    // flight.  Every load is unconditional (indices clamped into range,
+    // validity applied where the value is used), so no wait comes early.
+    const int64_t step = 4 * kWaves;
+    auto clamp = [&](int64_t j) { return j < nc ? j : nc - 1; };
+    int64_t j = 4 * static_cast<int64_t>(wave) + grp;
+    uint32_t cand_raw = list[j0 + clamp(j)];
+    double m_raw = mind[j0 + clamp(j)];
+    uint32_t cand_raw2 = list[j0 + clamp(j + step)];
+    double m_raw2 = mind[j0 + clamp(j + step)];
+    f32x4 v[U];
+    {
+      const int64_t row = j < nc ? static_cast<int64_t>(cand_raw) : pick;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int k = 4 * lr + 64 * u;
+        v[u] = *reinterpret_cast<const f32x4*>(z + row * d + (k < d ? k : 0));
+      }
+    }
+    for (int64_t jb = 4 * static_cast<int64_t>(wave); jb < nc; jb += step, j += step) {
+      const bool in = j < nc;
+      const int64_t cand = in ? static_cast<int64_t>(cand_raw) : -1;
+      double m = in ? (pass == 0 ? __builtin_inf() : m_raw) : -1.0;
+      // next batch: its rows now, the one after: its candidate and distance
+      const int64_t j1 = j + step;
+      const int64_t row1 = j1 < nc ? static_cast<int64_t>(cand_raw2) : pick;
+      f32x4 vn[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int k = 4 * lr + 64 * u;
+        vn[u] = *reinterpret_cast<const f32x4*>(z + row1 * d + (k < d ? k : 0));
+      }
+      cand_raw = cand_raw2;
+      m_raw = m_raw2;
+      cand_raw2 = list[j0 + clamp(j1 + step)];
+      m_raw2 = mind[j0 + clamp(j1 + step)];
+      double part = 0.0;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int k = 4 * lr + 64 * u;
+        if (k < d) {
+          const f32x4 p = *reinterpret_cast<const f32x4*>(prow + k);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float sv_ = bf16 ? bf16_round_f32(v[u][e]) : v[u][e];
+            const double diff = static_cast<double>(sv_) - static_cast<double>(p[e]);
+            part = __builtin_fma(diff, diff, part);
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = vn[u];
+      // sum over the 16 lanes of the group (fixed butterfly)
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) part += __shfl_xor(part, off, kWave);
+      if (m >= 0.0) {
+        m = cand == pick ? -1.0 : (part < m ? part : m);
+        if (lr == 0) mind[j0 + j] = m;
+      }
+      double gv = m >= 0.0 ? m : -1.0;
+      int64_t gi = m >= 0.0 ? cand : -1;
+      better(bv, bi, gv, gi);
+    }
+    // wave: merge the four groups; block: merge the waves
+#pragma unroll
+    for (int off = 16; off < 64; off <<= 1) {
+      const double ov = __shfl_xor(bv, off, kWave);
+      const int64_t oi = __shfl_xor(bi, off, kWave);
+      better(bv, bi, ov, oi);
+    }
+    if (lane == 0) {
+      sv[wave] = bv;
+      si[wave] = bi;
+    }
+    __syncthreads();
+    if (t == 0) {
+      double v = -1.0;
+      int64_t i = -1;
+      for (int w = 0; w < kWaves; ++w) better(v, i, sv[w], si[w]);
+      s_pick = (i >= 0 && v >= 0.0) ? i : -1;
+      if (s_pick >= 0) cpicks[j0 + cnt] = s_pick;
+    }
+    __syncthreads();
+    pick = s_pick;
+    if (pick < 0) break;
+    ++cnt;
+  }
+  if (t == 0) ccount[c] = static_cast<uint32_t>(cnt);
+}
+
+// The total budget over the classes in ascending order: class c appends
+// min(ccount[c], what is left) of its picks, in pick order, to picks[];
+// total = the number appended.  One block; thread 0 takes the prefix.
+__global__ __launch_bounds__(1024) void kcenter_budget_kernel(const uint32_t* __restrict__ ccount,
+                                                              const int64_t* __restrict__ coff, int n_classes,
+                                                              int64_t budget, const int64_t* __restrict__ cpicks,
+                                                              int64_t* __restrict__ picks, int64_t* __restrict__ dst,
+                                                              unsigned long long* __restrict__ total) {
+  if (threadIdx.x == 0) {
+    int64_t run = 0;
+    for (int c = 0; c < n_classes; ++c) {
+      int64_t take = ccount[c];
+      if (take > budget - run) take = budget - run;
+      dst[2 * c] = run;
+      dst[2 * c + 1] = take;
+      run += take;
+    }
+    *total = static_cast<unsigned long long>(run);
+  }
+  __syncthreads();
+  for (int c = 0; c < n_classes; ++c) {
+    const int64_t base = dst[2 * c], take = dst[2 * c + 1];
+    for (int64_t q = threadIdx.x; q < take; q += blockDim.x) picks[base + q] = cpicks[coff[c] + q];
+  }
+}
+
 // Rows of the picks [t0, t0 + k) as float32 stored values, with their
 // payload and radius (for the append).
 __global__ void kcenter_gather_kernel(const float* __restrict__ z, const int32_t* __restrict__ label,
@@ -479,6 +664,10 @@ struct CWs {
   double* part_v;
   int64_t* part_i;
   int64_t* picks;
+  int64_t* cpicks;      // [n] per-class picks (per-class K-center)
+  uint32_t* ccount;     // [n_classes] candidates, then picks, per class
+  int64_t* coff;        // [n_classes + 1] class list offsets
+  int64_t* cdst;        // [2 n_classes] output offset and count per class
   void* sub_ws;  // lookup / insert workspace
   size_t sub_bytes;
   size_t total;
@@ -523,6 +712,11 @@ inline CWs cws_layout(int64_t n, int d, int n_classes, int64_t budget, size_t su
   w.part_v = reinterpret_cast<double*>(take(static_cast<size_t>(kb) * 8));
   w.part_i = reinterpret_cast<int64_t*>(take(static_cast<size_t>(kb) * 8));
   w.picks = reinterpret_cast<int64_t*>(take(static_cast<size_t>(budget > 0 ? budget : 1) * 8));
+  const size_t nc = static_cast<size_t>(n_classes > 0 ? n_classes : 1);
+  w.cpicks = reinterpret_cast<int64_t*>(take(static_cast<size_t>(n > 0 ? n : 1) * 8));
+  w.ccount = reinterpret_cast<uint32_t*>(take(nc * 4));
+  w.coff = reinterpret_cast<int64_t*>(take((nc + 1) * 8));
+  w.cdst = reinterpret_cast<int64_t*>(take(2 * nc * 8));
   w.sub_ws = take(sub_bytes);
   w.sub_bytes = sub_bytes;
   w.total = off;
@@ -638,10 +832,43 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
       added += got;
     }
   } else {
-    // groups: all eligible candidates, or each payload class in ascending order
-    const int64_t kb = (N + 255) / 256;
-    const int ngroups = per_class > 0 ? n_classes : 1;
-    for (int gi = 0; gi < ngroups; ++gi) {
+    if (per_class > 0) {
+      // every class on its own workgroup, then the total budget in class order
+      hipLaunchKernelGGL(fill_i32_kernel, dim3(static_cast<unsigned>((ncls + 255) / 256)), dim3(256), 0, s,
+                         reinterpret_cast<int32_t*>(w.ccount), static_cast<int64_t>(ncls), 0);
+      LC_LAUNCHED();
+      const int other = cur ^ 1;
+      hipLaunchKernelGGL(class_keys_kernel, dim3(static_cast<unsigned>((n_elig + 255) / 256)), dim3(256), 0, s, label,
+                         order, n_elig, w.keys[other], w.vals[other], w.ccount);
+      LC_LAUNCHED();
+      int ccur = other;
+      LC_HIP(radix_sort_u32(w.keys, w.vals, n_elig, ncls <= 256 ? 1 : 2, w.hist, w.dsum, w.dbase, ccur, s));
+      hipLaunchKernelGGL(exclusive_scan_kernel, dim3(1), dim3(1024), 0, s, w.ccount, ncls, w.coff);
+      LC_LAUNCHED();
+      const dim3 kgrid(static_cast<unsigned>(ncls));
+      const uint32_t* clist = w.vals[ccur];
+      if (d <= 64)
+        hipLaunchKernelGGL((kcenter_class_kernel<1, kKcThreads>), kgrid, dim3(kKcThreads), 0, s, z, d, bf16, clist, w.coff,
+                           per_class, bud, w.mind, w.cpicks, w.ccount);
+      else if (d <= 128)
+        hipLaunchKernelGGL((kcenter_class_kernel<2, kKcThreads>), kgrid, dim3(kKcThreads), 0, s, z, d, bf16, clist, w.coff,
+                           per_class, bud, w.mind, w.cpicks, w.ccount);
+      else if (d <= 256)
+        hipLaunchKernelGGL((kcenter_class_kernel<4, kKcThreads>), kgrid, dim3(kKcThreads), 0, s, z, d, bf16, clist, w.coff,
+                           per_class, bud, w.mind, w.cpicks, w.ccount);
+      else if (d <= 512)
+        hipLaunchKernelGGL((kcenter_class_kernel<8, 512>), kgrid, dim3(512), 0, s, z, d, bf16, clist, w.coff,
+                           per_class, bud, w.mind, w.cpicks, w.ccount);
+      else
+        hipLaunchKernelGGL((kcenter_class_kernel<16, 512>), kgrid, dim3(512), 0, s, z, d, bf16, clist, w.coff,
+                           per_class, bud, w.mind, w.cpicks, w.ccount);
+      LC_LAUNCHED();
+      hipLaunchKernelGGL(kcenter_budget_kernel, dim3(1), dim3(1024), 0, s, w.ccount, w.coff, ncls, bud, w.cpicks,
+                         w.picks, w.cdst, total_dev);
+      LC_LAUNCHED();
+    } else {
+      // one traversal over all eligible candidates
+      const int64_t kb = (N + 255) / 256;
       KcParams kp;
       kp.z = z;
       kp.r = r;
@@ -652,7 +879,7 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
       kp.d = d;
       kp.bf16 = bf16;
       kp.n_classes = ncls;
-      kp.group = per_class > 0 ? gi : -1;
+      kp.group = -1;
       kp.mind = w.mind;
       kp.pick = w.pick;
       kp.part_v = w.part_v;
@@ -661,13 +888,12 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
       kp.budget = static_cast<unsigned long long>(bud);
       kp.picks = w.picks;
       kp.group_count = w.group_count;
-      const int64_t lim = per_class > 0 ? (per_class < bud ? per_class : bud) : bud;
-      kp.limit = static_cast<int>(lim < INT_MAX ? lim : INT_MAX);
+      kp.limit = static_cast<int>(bud < INT_MAX ? bud : INT_MAX);
       hipLaunchKernelGGL(kcenter_start_kernel, dim3(1), dim3(256), 0, s, label, order, n_elig, kp.group, w.start);
       LC_LAUNCHED();
       hipLaunchKernelGGL(kcenter_init_kernel, dim3(static_cast<unsigned>(kb)), dim3(256), 0, s, kp, w.start);
       LC_LAUNCHED();
-      const int64_t steps = (lim < n_elig ? lim : n_elig) - 1;
+      const int64_t steps = (bud < n_elig ? bud : n_elig) - 1;
       for (int64_t it = 0; it < steps; ++it) {
         hipLaunchKernelGGL(kcenter_step_kernel, dim3(static_cast<unsigned>(kb)), dim3(256), 0, s, kp);
         LC_LAUNCHED();

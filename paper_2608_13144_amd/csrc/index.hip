@@ -371,34 +371,6 @@ __global__ void plan_count_kernel(const uint32_t* __restrict__ mask, int words, 
   }
 }
 
-// coff[c] = sum of ccount below c, for c = 0 .. m (one block of 1024).
-__global__ __launch_bounds__(1024) void plan_scan_kernel(const uint32_t* __restrict__ ccount, int m,
-                                                         int64_t* __restrict__ coff) {
-  __shared__ int64_t part[1024];
-  const int t = static_cast<int>(threadIdx.x);
-  const int per = (m + 1023) / 1024;
-  const int b0 = t * per, b1 = b0 + per < m ? b0 + per : m;
-  int64_t sum = 0;
-  for (int i = b0; i < b1; ++i) sum += ccount[i];
-  part[t] = sum;
-  __syncthreads();
-  if (t == 0) {
-    int64_t run = 0;
-    for (int i = 0; i < 1024; ++i) {
-      const int64_t v = part[i];
-      part[i] = run;
-      run += v;
-    }
-    coff[m] = run;
-  }
-  __syncthreads();
-  int64_t run = part[t];
-  for (int i = b0; i < b1; ++i) {
-    coff[i] = run;
-    run += ccount[i];
-  }
-}
-
 // Each query writes itself into the lists of its candidate clusters (or
 // list K); one wave per query, as in plan_count_kernel.
 __global__ void plan_fill_kernel(const uint32_t* __restrict__ mask, int words, int64_t B, int K,
@@ -525,7 +497,7 @@ lipcache_status index_query_plan(const lipcache_index* idx, const float* zq, int
   const unsigned gw = static_cast<unsigned>((B + 3) / 4);
   hipLaunchKernelGGL(plan_count_kernel, dim3(gw), dim3(256), 0, s, w.mask, words, B, K, w.ccount);
   LC_LAUNCHED();
-  hipLaunchKernelGGL(plan_scan_kernel, dim3(1), dim3(1024), 0, s, w.ccount, K + 1, w.coff);
+  hipLaunchKernelGGL(exclusive_scan_kernel, dim3(1), dim3(1024), 0, s, w.ccount, K + 1, w.coff);
   LC_LAUNCHED();
   hipLaunchKernelGGL(plan_fill_kernel, dim3(gw), dim3(256), 0, s, w.mask, words, B, K, w.coff, w.cfill, w.qlist);
   LC_LAUNCHED();

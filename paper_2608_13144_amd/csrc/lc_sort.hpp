@@ -2,8 +2,9 @@
 // pass: per-block digit histograms, a per-digit scan over blocks, digit
 // bases, and a scatter that keeps the order of equal digits inside a block
 // (rank in the wave from eight digit-bit ballots, then the counts of the
-// same digit in the block's earlier waves).  The kernels are file-local so
-// that every translation unit that sorts carries its own copy.
+// same digit in the block's earlier waves); and a one-block exclusive scan of
+// counts.  The kernels are file-local so that every translation unit that
+// uses them carries its own copy.
 #pragma once
 
 #include "lc_common.hpp"
@@ -111,6 +112,35 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
     const uint32_t pos = dbase[dig] + hist[static_cast<int64_t>(dig) * nb + blockIdx.x] + before + rank;
     keys_out[pos] = key;
     vals_out[pos] = vals_in[i];
+  }
+}
+
+// out[i] = sum of cnt below i for i = 0 .. m (out[m] is the total); one
+// block of 1024 threads, each owning a contiguous run of counts.
+__global__ __launch_bounds__(1024) void exclusive_scan_kernel(const uint32_t* __restrict__ cnt, int m,
+                                                              int64_t* __restrict__ out) {
+  __shared__ int64_t part[1024];
+  const int t = static_cast<int>(threadIdx.x);
+  const int per = (m + 1023) / 1024;
+  const int b0 = t * per, b1 = b0 + per < m ? b0 + per : m;
+  int64_t sum = 0;
+  for (int i = b0; i < b1; ++i) sum += cnt[i];
+  part[t] = sum;
+  __syncthreads();
+  if (t == 0) {
+    int64_t run = 0;
+    for (int i = 0; i < 1024; ++i) {
+      const int64_t v = part[i];
+      part[i] = run;
+      run += v;
+    }
+    out[m] = run;
+  }
+  __syncthreads();
+  int64_t run = part[t];
+  for (int i = b0; i < b1; ++i) {
+    out[i] = run;
+    run += cnt[i];
   }
 }
 

@@ -113,6 +113,29 @@ def test_construct_matches_oracle_on_mixtures(strategy, per_class, budget, store
     say("construct", strategy, "selected", sel.size, "of", n)
 
 
+@pytest.mark.parametrize("per_class,budget,store,d", [(30, -1, "f32", 64), (30, 170, "f32", 64),
+                                                      (500, -1, "f32", 64), (7, 40, "bf16", 64),
+                                                      (20, -1, "f32", 288), (9, -1, "bf16", 640)])
+def test_kcenter_per_class(per_class, budget, store, d):
+    """Per-class farthest-first traversal: classes that fill, a total budget
+    that ends inside a class, classes smaller than their budget, an empty
+    class (label 9 never occurs) and the label-consistency flag."""
+    say("kcenter per class", per_class, budget, store, d)
+    C = 10
+    W, z, rng = mixture(1200, d, C, seed=per_class + max(budget, 0))
+    sig = oracle.spectral_norm(W).sigma
+    cert = oracle.certify(z, W, None, sig, store=store)
+    lab = cert.label.copy()
+    lab[lab == 9] = 8                              # class 9 has no candidate
+    guard = lab.copy()
+    guard[::13] = (guard[::13] + 1) % C           # inconsistent payloads are not eligible
+    c, st, sel = run_both(z, lab, cert.r, d, strategy="kcenter", budget=budget, per_class=per_class,
+                          n_classes=C, guard=guard, store=store)
+    counts = np.bincount(st.label, minlength=C)
+    assert counts[9] == 0 and counts.max() <= per_class
+    say("kcenter per class selected", sel.size, "counts", counts.tolist())
+
+
 def test_construct_chain_then_lookup():
     """Alg. 1 end to end on the device (tight radius, de-dup, 40 per class), then Alg. 2's lookup."""
     say("construct chain")

@@ -465,6 +465,8 @@ def main() -> int:
     ap.add_argument("--indexed", type=int, default=0, metavar="K",
                     help="time the exact cluster-pruned lookup with K clusters against the dense lookup")
     ap.add_argument("--index-iters", type=int, default=4, help="Lloyd iterations of the index build")
+    ap.add_argument("--index-k", type=int, default=256, metavar="K",
+                    help="also run the batch through a K-cluster index after the timed steps (0: skip)")
     ap.add_argument("--boundaries", action="store_true",
                     help="compare reuse boundaries (hit rate, certified-consistency rate) on the workload")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -614,10 +616,42 @@ def main() -> int:
         out["roofline"]["traffic_unit"] = "bytes per launch (FETCH_SIZE x %.4f + WRITE_SIZE x %.4f)" % (
             tr["fetch_scale"], tr["write_scale"])
         out["roofline"]["hbm_gbs"] = tr["traffic_bytes"] / (lk * 1e-3) / 1e9
+    if args.index_k > 0:
+        out["indexed_lookup"] = indexed_context(cache, zq, res, args)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, zq_host, args.cpu_seconds)
     print(json.dumps(out), flush=True)
     return 0
+
+
+def indexed_context(cache, zq, res, args) -> dict:
+    """The same batch through the exact cluster index (outside the timed
+    steps): build time, lookup time and whether the answers equal the dense
+    lookup's.  Context for the headline, which stays the dense scan."""
+    import numpy as np
+    import torch
+
+    ix = cache.build_index(args.index_k, 4)
+    torch.cuda.synchronize()
+    tb = time.perf_counter()
+    ix = cache.build_index(args.index_k, 4)
+    torch.cuda.synchronize()
+    build_ms = (time.perf_counter() - tb) * 1e3
+    out_i, pairs = cache.lookup_indexed(ix, zq, precision=args.precision)
+    same = bool(torch.equal(out_i.label, res.label) and torch.equal(out_i.index, res.index))
+    ts = []
+    for _ in range(5):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        cache.lookup_indexed(ix, zq, precision=args.precision, out=out_i)
+        torch.cuda.synchronize()
+        ts.append((time.perf_counter() - t0) * 1e3)
+    ms = float(np.median(ts))
+    B = zq.shape[0]
+    log(f"indexed lookup (K={args.index_k}): {ms:.3f} ms, {pairs / (B * cache.n):.4f} of the pairs, "
+        f"same answers as the dense lookup: {same}")
+    return {"K": args.index_k, "build_ms": build_ms, "lookup_ms": ms, "lookups_per_s": B / (ms * 1e-3),
+            "pairs_fraction": pairs / (B * cache.n), "same_answers_as_dense": same}
 
 
 if __name__ == "__main__":

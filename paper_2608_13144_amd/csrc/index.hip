@@ -345,87 +345,152 @@ inline int sort_passes(int K) {
 }
 
 // ---------------------------------------------------------------- query plan
-// One wave per query: its candidate count (lanes read the mask words in
-// parallel); list K when above kMaxCand, else one count for each candidate
-// cluster.
-__global__ void plan_count_kernel(const uint32_t* __restrict__ mask, int words, int64_t B, int K,
-                                  uint32_t* __restrict__ ccount) {
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
-  if (q >= B) return;
-  const int lane = lane_id();
-  const uint32_t* row = mask + q * words;
+// The per-cluster query lists.  A workgroup takes 256 queries (a thread
+// each); a query with more than kMaxCand candidate clusters joins list K,
+// otherwise every candidate cluster's list.  Counts are gathered in LDS and
+// flushed with one global atomic per list and workgroup (lists above
+// kPlanLds fall back to global atomics).
+constexpr int kPlanLds = 4096;
+
+__device__ __forceinline__ int query_candidates(const uint32_t* row, int words) {
   int cand = 0;
-  for (int wd = lane; wd < words; wd += kWave) cand += __builtin_popcount(row[wd]);
-  for (int off = 32; off >= 1; off >>= 1) cand += __shfl_xor(cand, off, kWave);
-  if (cand > kMaxCand) {
-    if (lane == 0) atomicAdd(&ccount[K], 1u);
+  for (int wd = 0; wd < words; ++wd) cand += __builtin_popcount(row[wd]);
+  return cand;
+}
+
+__global__ __launch_bounds__(256) void plan_count_kernel(const uint32_t* __restrict__ mask, int words, int64_t B,
+                                                         int K, uint32_t* __restrict__ ccount) {
+  __shared__ uint32_t h[kPlanLds];
+  const int lists = K + 1;
+  for (int c = threadIdx.x; c < lists && c < kPlanLds; c += 256) h[c] = 0u;
+  __syncthreads();
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (q < B) {
+    const uint32_t* row = mask + q * words;
+    auto count = [&](int c) {
+      if (c < kPlanLds) {
+        atomicAdd(&h[c], 1u);
+      } else {
+        atomicAdd(&ccount[c], 1u);
+      }
+    };
+    if (query_candidates(row, words) > kMaxCand) {
+      count(K);
+    } else {
+      for (int wd = 0; wd < words; ++wd) {
+        uint32_t v = row[wd];
+        while (v) {
+          count(32 * wd + __builtin_ctz(v));
+          v &= v - 1u;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < lists && c < kPlanLds; c += 256)
+    if (h[c]) atomicAdd(&ccount[c], h[c]);
+}
+
+// Each workgroup reserves, per list, a range for its queries (one global
+// atomic per list) and places them with LDS cursors.
+__global__ __launch_bounds__(256) void plan_fill_kernel(const uint32_t* __restrict__ mask, int words, int64_t B,
+                                                        int K, const int64_t* __restrict__ coff,
+                                                        uint32_t* __restrict__ cfill, int32_t* __restrict__ qlist) {
+  __shared__ uint32_t h[kPlanLds];
+  __shared__ uint32_t base[kPlanLds];
+  const int lists = K + 1;
+  for (int c = threadIdx.x; c < lists && c < kPlanLds; c += 256) h[c] = 0u;
+  __syncthreads();
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const uint32_t* row = mask + (q < B ? q : 0) * words;
+  const bool dense = q < B && query_candidates(row, words) > kMaxCand;
+  if (q < B) {
+    if (dense) {
+      if (K < kPlanLds) atomicAdd(&h[K], 1u);
+    } else {
+      for (int wd = 0; wd < words; ++wd) {
+        uint32_t v = row[wd];
+        while (v) {
+          const int c = 32 * wd + __builtin_ctz(v);
+          v &= v - 1u;
+          if (c < kPlanLds) atomicAdd(&h[c], 1u);
+        }
+      }
+    }
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < lists && c < kPlanLds; c += 256) {
+    base[c] = h[c] ? atomicAdd(&cfill[c], h[c]) : 0u;
+    h[c] = 0u;  // becomes the workgroup's cursor
+  }
+  __syncthreads();
+  if (q >= B) return;
+  auto place = [&](int c) {
+    const uint32_t slot = c < kPlanLds ? base[c] + atomicAdd(&h[c], 1u) : atomicAdd(&cfill[c], 1u);
+    qlist[coff[c] + slot] = static_cast<int32_t>(q);
+  };
+  if (dense) {
+    place(K);
     return;
   }
-  for (int wd = lane; wd < words; wd += kWave) {
+  for (int wd = 0; wd < words; ++wd) {
     uint32_t v = row[wd];
     while (v) {
-      const int b = __builtin_ctz(v);
+      place(32 * wd + __builtin_ctz(v));
       v &= v - 1u;
-      atomicAdd(&ccount[32 * wd + b], 1u);
     }
   }
 }
 
-// Each query writes itself into the lists of its candidate clusters (or
-// list K); one wave per query, as in plan_count_kernel.
-__global__ void plan_fill_kernel(const uint32_t* __restrict__ mask, int words, int64_t B, int K,
-                                 const int64_t* __restrict__ coff, uint32_t* __restrict__ cfill,
-                                 int32_t* __restrict__ qlist) {
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
-  if (q >= B) return;
-  const int lane = lane_id();
-  const uint32_t* row = mask + q * words;
-  int cand = 0;
-  for (int wd = lane; wd < words; wd += kWave) cand += __builtin_popcount(row[wd]);
-  for (int off = 32; off >= 1; off >>= 1) cand += __shfl_xor(cand, off, kWave);
-  if (cand > kMaxCand) {
-    if (lane == 0) qlist[coff[K] + atomicAdd(&cfill[K], 1u)] = static_cast<int32_t>(q);
-    return;
-  }
-  for (int wd = lane; wd < words; wd += kWave) {
-    uint32_t v = row[wd];
-    while (v) {
-      const int c = 32 * wd + __builtin_ctz(v);
-      v &= v - 1u;
-      qlist[coff[c] + atomicAdd(&cfill[c], 1u)] = static_cast<int32_t>(q);
-    }
-  }
+// Rows of list c: cluster c, or every indexed row for list K; cut into
+// nearly equal chunks of at most kItemRows.
+__device__ __forceinline__ void list_rows(const int64_t* offsets, int K, int64_t n_indexed, int c, int64_t& e0,
+                                          int64_t& e1, int64_t& chunks, int64_t& step) {
+  e0 = c < K ? offsets[c] : 0;
+  e1 = c < K ? offsets[c + 1] : n_indexed;
+  chunks = e1 > e0 ? (e1 - e0 + kItemRows - 1) / kItemRows : 0;
+  step = chunks ? (e1 - e0 + chunks - 1) / chunks : 1;
 }
 
-// One thread per list c = 0 .. K: items (query positions of c's list in
-// blocks of qblock) x (c's rows, list K: all rows, in nearly equal chunks of
-// at most kItemRows, which keeps the items of a launch alike in size).
+// Items per list: (query blocks of qblock) x (row chunks); one thread per list.
+__global__ void plan_item_count_kernel(const int64_t* __restrict__ coff, const int64_t* __restrict__ offsets, int K,
+                                       int64_t n_indexed, int qblock, uint32_t* __restrict__ icount,
+                                       unsigned long long* __restrict__ counters) {
+  const int c = static_cast<int>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (c > K) return;
+  const int64_t nq = coff[c + 1] - coff[c];
+  int64_t e0, e1, chunks, step;
+  list_rows(offsets, K, n_indexed, c, e0, e1, chunks, step);
+  const int64_t qb = (nq + qblock - 1) / qblock;
+  icount[c] = static_cast<uint32_t>(qb * chunks);
+  if (nq > 0 && e1 > e0) atomicAdd(&counters[1], static_cast<unsigned long long>(nq * (e1 - e0)));
+}
+
+// The items of list c at ioff[c] (in list order); counters[0] = the total.
 __global__ void plan_items_kernel(const int64_t* __restrict__ coff, const int64_t* __restrict__ offsets, int K,
-                                  int64_t n_indexed, int qblock, int64_t* __restrict__ items, int64_t capacity,
+                                  int64_t n_indexed, int qblock, const int64_t* __restrict__ ioff,
+                                  int64_t* __restrict__ items, int64_t capacity,
                                   unsigned long long* __restrict__ counters) {
   const int c = static_cast<int>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (c > K) return;
+  if (c == 0) {
+    counters[0] = static_cast<unsigned long long>(ioff[K + 1]);
+    if (ioff[K + 1] > capacity) counters[2] = 1ull;
+  }
+  if (ioff[K + 1] > capacity) return;
   const int64_t q0 = coff[c], q1 = coff[c + 1];
-  const int64_t e0 = c < K ? offsets[c] : 0, e1 = c < K ? offsets[c + 1] : n_indexed;
+  int64_t e0, e1, chunks, step;
+  list_rows(offsets, K, n_indexed, c, e0, e1, chunks, step);
   if (q0 >= q1 || e0 >= e1) return;
-  // rows in nearly equal chunks of at most kItemRows
-  const int64_t chunks = (e1 - e0 + kItemRows - 1) / kItemRows;
-  const int64_t step = (e1 - e0 + chunks - 1) / chunks;
+  int64_t slot = ioff[c];
   for (int64_t qa = q0; qa < q1; qa += qblock) {
     const int64_t qb = qa + qblock < q1 ? qa + qblock : q1;
     for (int64_t ea = e0; ea < e1; ea += step) {
-      const int64_t eb = ea + step < e1 ? ea + step : e1;
-      const unsigned long long slot = atomicAdd(&counters[0], 1ull);
-      atomicAdd(&counters[1], static_cast<unsigned long long>((qb - qa) * (eb - ea)));
-      if (static_cast<int64_t>(slot) < capacity) {
-        int64_t* it = items + 4 * static_cast<int64_t>(slot);
-        it[0] = qa;
-        it[1] = qb;
-        it[2] = ea;
-        it[3] = eb;
-      } else {
-        atomicOr(&counters[2], 1ull);
-      }
+      int64_t* it = items + 4 * slot++;
+      it[0] = qa;
+      it[1] = qb;
+      it[2] = ea;
+      it[3] = ea + step < e1 ? ea + step : e1;
     }
   }
 }
@@ -461,6 +526,8 @@ size_t index_plan_layout(int64_t B, int d, int K, int64_t n_indexed, int qblock,
   const int64_t R = kItemRows;
   t.capacity = cdiv(2 * B, qblock) * cdiv(n_indexed, R) + cdiv(B * maxc, qblock) + 2 * cdiv(n_indexed, R) + K + 4;
   t.items = reinterpret_cast<int64_t*>(take(static_cast<size_t>(t.capacity) * 4 * 8));
+  t.icount = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(K + 1) * 4));
+  t.ioff = reinterpret_cast<int64_t*>(take(static_cast<size_t>(K + 2) * 8));
   t.counters = reinterpret_cast<unsigned long long*>(take(64));
   t.qnorm = reinterpret_cast<double*>(take(static_cast<size_t>(B) * 8));
   t.cnorm = reinterpret_cast<double*>(take(static_cast<size_t>(K) * 8));
@@ -494,15 +561,21 @@ lipcache_status index_query_plan(const lipcache_index* idx, const float* zq, int
   hipLaunchKernelGGL(centre_mfma_kernel, dim3(static_cast<unsigned>((B + kCr - 1) / kCr)), dim3(256), 0, s, zq,
                      LIPCACHE_F32, B, d, idx->centers, w.cnorm, K, w.qnorm, idx->bound, slack, w.mask, nullptr);
   LC_LAUNCHED();
-  const unsigned gw = static_cast<unsigned>((B + 3) / 4);
-  hipLaunchKernelGGL(plan_count_kernel, dim3(gw), dim3(256), 0, s, w.mask, words, B, K, w.ccount);
+  const unsigned gq = static_cast<unsigned>((B + 255) / 256);
+  const unsigned gl = static_cast<unsigned>((K + 1 + 255) / 256);
+  hipLaunchKernelGGL(plan_count_kernel, dim3(gq), dim3(256), 0, s, w.mask, words, B, K, w.ccount);
   LC_LAUNCHED();
   hipLaunchKernelGGL(exclusive_scan_kernel, dim3(1), dim3(1024), 0, s, w.ccount, K + 1, w.coff);
   LC_LAUNCHED();
-  hipLaunchKernelGGL(plan_fill_kernel, dim3(gw), dim3(256), 0, s, w.mask, words, B, K, w.coff, w.cfill, w.qlist);
+  hipLaunchKernelGGL(plan_fill_kernel, dim3(gq), dim3(256), 0, s, w.mask, words, B, K, w.coff, w.cfill, w.qlist);
   LC_LAUNCHED();
-  hipLaunchKernelGGL(plan_items_kernel, dim3(static_cast<unsigned>((K + 1 + 255) / 256)), dim3(256), 0, s, w.coff,
-                     idx->offsets, K, idx->n_indexed, qblock, w.items, w.capacity, w.counters);
+  hipLaunchKernelGGL(plan_item_count_kernel, dim3(gl), dim3(256), 0, s, w.coff, idx->offsets, K, idx->n_indexed,
+                     qblock, w.icount, w.counters);
+  LC_LAUNCHED();
+  hipLaunchKernelGGL(exclusive_scan_kernel, dim3(1), dim3(1024), 0, s, w.icount, K + 1, w.ioff);
+  LC_LAUNCHED();
+  hipLaunchKernelGGL(plan_items_kernel, dim3(gl), dim3(256), 0, s, w.coff, idx->offsets, K, idx->n_indexed, qblock,
+                     w.ioff, w.items, w.capacity, w.counters);
   LC_LAUNCHED();
   unsigned long long host[3] = {0ull, 0ull, 0ull};
   LC_HIP(hipMemcpyAsync(host, w.counters, sizeof(host), hipMemcpyDeviceToHost, s));

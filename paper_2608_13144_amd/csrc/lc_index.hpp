@@ -18,6 +18,8 @@ struct IndexPlanWs {
   int64_t qcap;
   int64_t* items;                  // [capacity][4]: query positions [0], [1); rows [2], [3)
   int64_t capacity;
+  uint32_t* icount;                // [K + 1] work items per list
+  int64_t* ioff;                   // [K + 2] first item of each list
   unsigned long long* counters;    // [0] items, [1] pairs, [2] overflow
   double* qnorm;                   // [B] ||q||^2
   double* cnorm;                   // [K] ||mu_c||^2

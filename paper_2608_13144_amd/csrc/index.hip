@@ -1,19 +1,21 @@
 // Exact cluster index for a sublinear lookup.
 //
 // Build: K centres start at evenly spaced cache rows; `iters` Lloyd
-// iterations assign every live row to its nearest centre (float32 tiles in
-// LDS) and move each centre to the float64 mean of its rows.  After the
-// final assignment a stable radix sort by cluster gives the row order, the
-// cluster offsets come from the counts, and R_c = max over live members of
-// ||z_i - mu_c|| + r_i is taken in float64 and rounded up to float32.  The
-// indexed rows are copied into a cluster-ordered cache.  Any partition
-// gives exact answers; the iterations only make the clusters tight.
+// iterations assign every row to its nearest centre (x . mu_c on the matrix
+// cores, centre_mfma_kernel) and move each centre to the float64 mean of its
+// live rows.  After the final assignment a stable radix sort by cluster
+// gives the row order, the cluster offsets come from the counts, and
+// R_c = max over live members of ||z_i - mu_c|| + r_i (widened so that the
+// re-check's boundary band is covered) is taken in float64 and rounded up to
+// float32.  The indexed rows are copied into a cluster-ordered cache.  Any
+// partition gives exact answers; the iterations only make the clusters
+// tight.
 //
-// Query plan: for every query the clusters with ||q - mu_c|| < R_c (the
-// float32 distance keeps a cluster whenever its rounding error could hide
-// one), and the nearest cluster; queries are sorted by nearest cluster so
-// that a block of them shares few clusters; each block's union of needed
-// clusters becomes work items for the fused lookup kernel.
+// Query plan: for every query the clusters with ||q - mu_c|| < R_c (tested
+// on the matrix cores with a rigorous float32 slack, so no such cluster is
+// missed); for every cluster the list of queries that need it; and work
+// items pairing a block of a cluster's list with a chunk of its rows, which
+// the fused lookup kernel scans through the list.
 #include <limits.h>
 
 #include "lc_common.hpp"

@@ -302,10 +302,13 @@ lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t K, int32_t
 size_t lipcache_index_build_workspace_bytes(int64_t n, int32_t d, int32_t K);
 
 /*
- * lipcache_lookup through an index built on this cache: the same outputs
- * (label, index into the cache, d^2, stats, band flags) as lipcache_lookup
- * on the same cache.  pairs (host, nullable) out: query-entry pairs the
- * filter scanned (B * c->n for the dense lookup).
+ * lipcache_lookup through an index built on this cache: the same label,
+ * index into the cache, d^2 and band flags as lipcache_lookup on the same
+ * cache, and the same stats except LIPCACHE_STAT_RECHECKED, which counts the
+ * indexed scan's re-checks.  pairs (host, nullable) out: query-entry pairs
+ * the filter scanned (B * c->n for the dense lookup).  Rows 0 .. n_indexed-1
+ * of the cache must be the ones the index was built on; rows appended since
+ * are scanned in full.  zq 16-byte aligned.
  *  ws lipcache_lookup_indexed_workspace_bytes(B, c->n, c->d, idx->K,
  *     idx->n_indexed) bytes
  * (sync: one read-back of the work-list size)

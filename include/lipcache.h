@@ -271,7 +271,9 @@ size_t lipcache_construct_workspace_bytes(const lipcache_cache* c, int64_t N, in
  * Exact cluster index for a sublinear lookup (the paper points to an exact
  * sublinear index for large caches).  Rows 0 .. n_indexed-1 of a cache are
  * partitioned into K clusters (a few Lloyd iterations of k-means from
- * evenly spaced rows); entry i of cluster c can contain a query q only if
+ * evenly spaced rows, on an evenly strided sample of about 512 rows per
+ * cluster, then one assignment of every row); entry i of cluster c can
+ * contain a query q only if
  * ||q - mu_c|| < R_c with R_c >= max over its live members of
  * (||z_i - mu_c|| + r_i) (triangle inequality), so the indexed lookup scans
  * only the clusters a query may need and returns exactly what

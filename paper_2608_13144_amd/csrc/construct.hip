@@ -446,17 +446,27 @@ __global__ __launch_bounds__(256) void kcenter_pick_kernel(const KcParams p, int
 // applied afterwards in ascending class order (a traversal's first k picks
 // do not depend on how many follow).
 
-// keys / vals of the class sort: label and candidate of visit position q.
-__global__ void class_keys_kernel(const int32_t* __restrict__ label, const uint32_t* __restrict__ order,
-                                  int64_t n_elig, uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
-                                  uint32_t* __restrict__ ccount) {
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (q >= n_elig) return;
-  const uint32_t i = order[q];
-  const uint32_t c = static_cast<uint32_t>(label[i]);  // in [0, n_classes): eligibility
-  keys[q] = c;
-  vals[q] = i;
-  atomicAdd(&ccount[c], 1u);
+// keys / vals of the class sort: label and candidate of visit position q;
+// class sizes counted per workgroup of 4096 positions in LDS (n_classes <=
+// kMaxClasses), one atomic per class it saw.
+__global__ __launch_bounds__(256) void class_keys_kernel(const int32_t* __restrict__ label,
+                                                         const uint32_t* __restrict__ order, int64_t n_elig,
+                                                         int n_classes, uint32_t* __restrict__ keys,
+                                                         uint32_t* __restrict__ vals, uint32_t* __restrict__ ccount) {
+  __shared__ uint32_t h[kMaxClasses];
+  for (int c = threadIdx.x; c < n_classes; c += 256) h[c] = 0u;
+  __syncthreads();
+  const int64_t q0 = static_cast<int64_t>(blockIdx.x) * 4096;
+  for (int64_t q = q0 + threadIdx.x; q < q0 + 4096 && q < n_elig; q += 256) {
+    const uint32_t i = order[q];
+    const uint32_t c = static_cast<uint32_t>(label[i]);  // in [0, n_classes): eligibility
+    keys[q] = c;
+    vals[q] = i;
+    atomicAdd(&h[c], 1u);
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < n_classes; c += 256)
+    if (h[c]) atomicAdd(&ccount[c], h[c]);
 }
 
 constexpr int kKcThreads = 1024;
@@ -838,8 +848,8 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
                          reinterpret_cast<int32_t*>(w.ccount), static_cast<int64_t>(ncls), 0);
       LC_LAUNCHED();
       const int other = cur ^ 1;
-      hipLaunchKernelGGL(class_keys_kernel, dim3(static_cast<unsigned>((n_elig + 255) / 256)), dim3(256), 0, s, label,
-                         order, n_elig, w.keys[other], w.vals[other], w.ccount);
+      hipLaunchKernelGGL(class_keys_kernel, dim3(static_cast<unsigned>((n_elig + 4095) / 4096)), dim3(256), 0, s,
+                         label, order, n_elig, ncls, w.keys[other], w.vals[other], w.ccount);
       LC_LAUNCHED();
       int ccur = other;
       LC_HIP(radix_sort_u32(w.keys, w.vals, n_elig, ncls <= 256 ? 1 : 2, w.hist, w.dsum, w.dbase, ccur, s));

@@ -1,9 +1,10 @@
 // Exact cluster index for a sublinear lookup.
 //
 // Build: K centres start at evenly spaced cache rows; `iters` Lloyd
-// iterations assign every row to its nearest centre (x . mu_c on the matrix
-// cores, centre_mfma_kernel) and move each centre to the float64 mean of its
-// live rows.  After the final assignment a stable radix sort by cluster
+// iterations over an evenly strided sample of the rows (about 512 per
+// cluster) assign each sampled row to its nearest centre (x . mu_c on the
+// matrix cores, centre_mfma_kernel) and move each centre to the float64
+// mean of its live sampled rows; the final assignment covers every row.  After the final assignment a stable radix sort by cluster
 // gives the row order, the cluster offsets come from the counts, and
 // R_c = max over live members of ||z_i - mu_c|| + r_i (widened so that the
 // re-check's boundary band is covered) is taken in float64 and rounded up to
@@ -25,6 +26,7 @@
 namespace lc {
 
 constexpr int kCr = 64;              // rows per block (4 waves x 16)
+constexpr int64_t kSampleRows = 512; // rows per cluster the Lloyd iterations sample
 constexpr int kCc = 64;              // centres per chunk (4 column tiles of 16)
 constexpr int kCk = 64;              // features per LDS stage
 constexpr int kCs = kCk + 4;         // floats per LDS row (padding spreads the banks)
@@ -56,7 +58,8 @@ __global__ void row_norm_kernel(const void* __restrict__ x, int store, int64_t n
   if (lane_id() == 0) out[i] = s;
 }
 
-// Rows x (n of them, float32 or bf16 storage) against K centres mu_c, on the
+// Rows x (n of them: rows j * stride of the array, float32 or bf16 storage)
+// against K centres mu_c, on the
 // matrix cores: g = x . mu_c by v_mfma_f32_16x16x4_f32 (float32 products
 // and sums), then in float64 the score ||mu_c||^2 - 2 g, which orders the
 // centres like ||x - mu_c||^2.
@@ -71,7 +74,8 @@ __global__ void row_norm_kernel(const void* __restrict__ x, int store, int64_t n
 // Block: 4 waves, 64 rows; each wave owns 16 rows and all 64 centres of a
 // chunk (4 accumulator tiles); rows and centres pass through LDS in stages
 // of 64 features.
-__global__ __launch_bounds__(256) void centre_mfma_kernel(const void* __restrict__ rows, int store, int64_t n, int d,
+__global__ __launch_bounds__(256) void centre_mfma_kernel(const void* __restrict__ rows, int store, int64_t n,
+                                                          int64_t stride, int d,
                                                           const float* __restrict__ centres,
                                                           const double* __restrict__ cnorm, int K,
                                                           const double* __restrict__ rnorm,
@@ -106,7 +110,7 @@ __global__ __launch_bounds__(256) void centre_mfma_kernel(const void* __restrict
         const int64_t row = r0 + rr;
         const int c = c0 + rr;
         f32x4 xv = f32x4{0.f, 0.f, 0.f, 0.f}, cv = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (kin && row < n) xv = stored_x4(rows, store, row, d, k0 + k4);
+        if (kin && row < n) xv = stored_x4(rows, store, row * stride, d, k0 + k4);
         if (kin && c < K) cv = *reinterpret_cast<const f32x4*>(centres + static_cast<int64_t>(c) * d + k0 + k4);
         *reinterpret_cast<f32x4*>(&xs[rr * kCs + k4]) = xv;
         *reinterpret_cast<f32x4*>(&cs[rr * kCs + k4]) = cv;
@@ -191,16 +195,18 @@ __global__ void centre_init_kernel(const void* __restrict__ z, int store, int64_
   centres[t] = stored_value(z, store, row, d, k);
 }
 
-// sum[c][k] += z_ik, cnt[c] += 1 over live rows (thread per (row, column)).
-__global__ void centre_sum_kernel(const void* __restrict__ z, int store, const float* __restrict__ r, int64_t n,
-                                  int d, const uint32_t* __restrict__ assign, double* __restrict__ sum,
-                                  unsigned long long* __restrict__ cnt) {
+// sum[c][k] += z_ik, cnt[c] += 1 over the live rows i = j * stride of the
+// sample (thread per (sample row, column); assign[j] is row j's cluster).
+__global__ void centre_sum_kernel(const void* __restrict__ z, int store, const float* __restrict__ r, int64_t ns,
+                                  int d, int64_t stride, const uint32_t* __restrict__ assign,
+                                  double* __restrict__ sum, unsigned long long* __restrict__ cnt) {
   const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (t >= n * d) return;
-  const int64_t i = t / d;
+  if (t >= ns * d) return;
+  const int64_t j = t / d;
+  const int64_t i = j * stride;
   const int k = static_cast<int>(t % d);
   if (!(r[i] > 0.0f)) return;
-  const uint32_t c = assign[i];
+  const uint32_t c = assign[j];
   atomicAdd(&sum[static_cast<int64_t>(c) * d + k], static_cast<double>(stored_value(z, store, i, d, k)));
   if (k == 0) atomicAdd(&cnt[c], 1ull);
 }
@@ -223,9 +229,27 @@ __global__ void row_keys_kernel(const uint32_t* __restrict__ assign, int64_t n, 
   vals[i] = static_cast<uint32_t>(i);
 }
 
-__global__ void count_kernel(const uint32_t* __restrict__ assign, int64_t n, unsigned long long* __restrict__ cnt) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < n) atomicAdd(&cnt[assign[i]], 1ull);
+// Rows per cluster: a workgroup counts 4096 rows in LDS and flushes one
+// atomic per cluster it saw (clusters from kCountLds on count globally).
+constexpr int kCountLds = 4096;
+
+__global__ __launch_bounds__(256) void count_kernel(const uint32_t* __restrict__ assign, int64_t n, int K,
+                                                    unsigned long long* __restrict__ cnt) {
+  __shared__ uint32_t h[kCountLds];
+  for (int c = threadIdx.x; c < K && c < kCountLds; c += 256) h[c] = 0u;
+  __syncthreads();
+  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * 4096;
+  for (int64_t i = i0 + threadIdx.x; i < i0 + 4096 && i < n; i += 256) {
+    const uint32_t c = assign[i];
+    if (c < static_cast<uint32_t>(kCountLds)) {
+      atomicAdd(&h[c], 1u);
+    } else {
+      atomicAdd(&cnt[c], 1ull);
+    }
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < K && c < kCountLds; c += 256)
+    if (h[c]) atomicAdd(&cnt[c], static_cast<unsigned long long>(h[c]));
 }
 
 // offsets[c] = sum of counts below c (one block, serial chunks).
@@ -561,7 +585,8 @@ lipcache_status index_query_plan(const lipcache_index* idx, const float* zq, int
   LC_LAUNCHED();
   const double slack = 2.0 * (d + 2) / 16777216.0;
   hipLaunchKernelGGL(centre_mfma_kernel, dim3(static_cast<unsigned>((B + kCr - 1) / kCr)), dim3(256), 0, s, zq,
-                     LIPCACHE_F32, B, d, idx->centers, w.cnorm, K, w.qnorm, idx->bound, slack, w.mask, nullptr);
+                     LIPCACHE_F32, B, static_cast<int64_t>(1), d, idx->centers, w.cnorm, K, w.qnorm, idx->bound,
+                     slack, w.mask, nullptr);
   LC_LAUNCHED();
   const unsigned gq = static_cast<unsigned>((B + 255) / 256);
   const unsigned gl = static_cast<unsigned>((K + 1 + 255) / 256);
@@ -624,12 +649,18 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
   LC_LAUNCHED();
   const unsigned gq = static_cast<unsigned>((n + kCr - 1) / kCr);
   const unsigned gk = static_cast<unsigned>((K + 3) / 4);
+  // The iterations see every stride-th row (about kSampleRows per cluster);
+  // the final assignment sees every row.
+  const int64_t stride = n / (static_cast<int64_t>(K) * kSampleRows) > 1 ? n / (static_cast<int64_t>(K) * kSampleRows) : 1;
+  const int64_t ns = (n + stride - 1) / stride;
+  const int64_t sd = ns * d;
+  const unsigned gs = static_cast<unsigned>((ns + kCr - 1) / kCr);
   for (int it = 0; it < iters; ++it) {
     hipLaunchKernelGGL(row_norm_kernel, dim3(gk), dim3(256), 0, s, idx->centers, LIPCACHE_F32,
                        static_cast<int64_t>(K), d, w.cnorm);
     LC_LAUNCHED();
-    hipLaunchKernelGGL(centre_mfma_kernel, dim3(gq), dim3(256), 0, s, c->z, c->store_dtype, n, d, idx->centers,
-                       w.cnorm, K, nullptr, nullptr, 0.0, nullptr, w.assign);
+    hipLaunchKernelGGL(centre_mfma_kernel, dim3(gs), dim3(256), 0, s, c->z, c->store_dtype, ns, stride, d,
+                       idx->centers, w.cnorm, K, nullptr, nullptr, 0.0, nullptr, w.assign);
     LC_LAUNCHED();
     hipLaunchKernelGGL(fill_f64_kernel, dim3(static_cast<unsigned>((kd + 255) / 256)), dim3(256), 0, s, w.sum, kd,
                        0.0);
@@ -637,9 +668,8 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
     hipLaunchKernelGGL(fill_u64x_kernel, dim3(static_cast<unsigned>((K + 255) / 256)), dim3(256), 0, s, w.cnt,
                        static_cast<int64_t>(K), 0ull);
     LC_LAUNCHED();
-    const int64_t nd = n * d;
-    hipLaunchKernelGGL(centre_sum_kernel, dim3(static_cast<unsigned>((nd + 255) / 256)), dim3(256), 0, s, c->z,
-                       c->store_dtype, c->r, n, d, w.assign, w.sum, w.cnt);
+    hipLaunchKernelGGL(centre_sum_kernel, dim3(static_cast<unsigned>((sd + 255) / 256)), dim3(256), 0, s, c->z,
+                       c->store_dtype, c->r, ns, d, stride, w.assign, w.sum, w.cnt);
     LC_LAUNCHED();
     hipLaunchKernelGGL(centre_update_kernel, dim3(static_cast<unsigned>((kd + 255) / 256)), dim3(256), 0, s, w.sum,
                        w.cnt, K, d, idx->centers);
@@ -648,8 +678,8 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
   hipLaunchKernelGGL(row_norm_kernel, dim3(gk), dim3(256), 0, s, idx->centers, LIPCACHE_F32, static_cast<int64_t>(K),
                      d, w.cnorm);
   LC_LAUNCHED();
-  hipLaunchKernelGGL(centre_mfma_kernel, dim3(gq), dim3(256), 0, s, c->z, c->store_dtype, n, d, idx->centers,
-                     w.cnorm, K, nullptr, nullptr, 0.0, nullptr, w.assign);
+  hipLaunchKernelGGL(centre_mfma_kernel, dim3(gq), dim3(256), 0, s, c->z, c->store_dtype, n, static_cast<int64_t>(1),
+                     d, idx->centers, w.cnorm, K, nullptr, nullptr, 0.0, nullptr, w.assign);
   LC_LAUNCHED();
   hipLaunchKernelGGL(row_keys_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, s, w.assign, n,
                      w.keys[0], w.vals[0]);
@@ -659,7 +689,8 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
   hipLaunchKernelGGL(fill_u64x_kernel, dim3(static_cast<unsigned>((K + 255) / 256)), dim3(256), 0, s, w.cnt,
                      static_cast<int64_t>(K), 0ull);
   LC_LAUNCHED();
-  hipLaunchKernelGGL(count_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, s, w.assign, n, w.cnt);
+  hipLaunchKernelGGL(count_kernel, dim3(static_cast<unsigned>((n + 4095) / 4096)), dim3(256), 0, s, w.assign, n, K,
+                     w.cnt);
   LC_LAUNCHED();
   hipLaunchKernelGGL(offsets_kernel, dim3(1), dim3(64), 0, s, w.cnt, K, idx->offsets);
   LC_LAUNCHED();

@@ -31,7 +31,9 @@
 //    blocks a given XCD runs (block id mod 8) share cache slices, so the
 //    resident workgroups of an XCD read each cache tile from its L2 at about
 //    the same time.  The indexed lookup instead gives each block one item of
-//    a work list: a query block against the rows of one cache cluster.
+//    a work list: up to 512 queries of one cluster's query list (read through
+//    the list, in a separate instantiation) against a chunk of that cluster's
+//    rows.
 #include <limits.h>
 
 #include "lc_common.hpp"

@@ -19,11 +19,14 @@
 // The greedy visit then runs in chunks of kChunk candidates: the chunk is
 // looked up against the cache (lipcache_lookup: a hit means a duplicate),
 // an exact float64 relation "b lies in the ball of a" is formed for all
-// pairs a < b of the chunk (bit matrix), one wave decides the chunk in order
-// (AND of the relation row with the bits of the candidates accepted so far,
-// class counts in LDS), and lipcache_insert appends the accepted rows in
-// visit order.  K-center keeps every candidate's squared distance to the
-// chosen set in float64 and alternates a fused update/arg-max kernel with a
+// pairs a < b of the chunk (bit matrix), one workgroup decides the chunk in
+// order (64 candidates at a time where no relation row is set, else one by
+// one with the AND of the relation row and the accepted bits; class counts in
+// LDS), and lipcache_insert appends the accepted rows in visit order.
+// K-center keeps every candidate's squared distance to the chosen set in
+// float64.  With a per-class budget each class is traversed by one workgroup
+// (candidates sorted by class), and the total budget is applied in class
+// order afterwards; otherwise a fused update/arg-max kernel alternates with a
 // one-block reduction, with no host round trip per pick.
 #include <limits.h>
 

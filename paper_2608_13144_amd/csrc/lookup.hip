@@ -75,6 +75,10 @@ struct LookupParams {
   // qlist is null).
   const int64_t* items;
   const int32_t* qlist;
+  // bf16 copy of the queries (round to nearest even, as the in-kernel
+  // conversion): the bf16 A operands of the work-list kernel, half the bytes
+  // of the float32 rows every item would otherwise gather.
+  const uint16_t* zq16;
   // Index written into a hit's key: (emap ? emap[e] : e) + eoff.
   const int64_t* emap;
   int64_t eoff;
@@ -114,6 +118,12 @@ __global__ void lookup_athr_kernel(const float* __restrict__ cr, const float* __
     }
   }
   athr[i] = at;
+}
+
+// bf16 copy of the queries (round to nearest even), for the work-list kernel.
+__global__ void query_bf16_kernel(const float* __restrict__ zq, int64_t n, uint16_t* __restrict__ zq16) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) zq16[i] = bf16_bits(zq[i]);
 }
 
 // ------------------------------------------------------------- finalize
@@ -314,7 +324,7 @@ __device__ __noinline__ void recheck_pairs(const RecheckArgs p, uint32_t mask, i
 // g of each k-step (the cache operand uses the same (k-step, chunk) -> k map,
 // so the contraction covers every k exactly once).  Positions past qend load
 // the last query (any finite values do): their thresholds are +inf.
-template <int MODE, int KS, int RT>
+template <int MODE, int KS, int RT, bool Q16 = false>
 __device__ __forceinline__ void load_query_operands(const LookupParams& p, const int32_t* qlist, int64_t qwave,
                                                     int64_t qend, int m16, int g, u32x4 (&a)[RT][KS]) {
   using T = ModeTraits<MODE>;
@@ -324,14 +334,21 @@ __device__ __forceinline__ void load_query_operands(const LookupParams& p, const
     pos = pos < qend ? pos : qend - 1;
     const int64_t row = query_at(qlist, pos);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) a[rt][ks] = load_chunk<MODE, LIPCACHE_F32>(p.zq, row, p.d, ks * T::kPerStep + g * T::kPerChunk);
+    for (int ks = 0; ks < KS; ++ks) {
+      const int k0 = ks * T::kPerStep + g * T::kPerChunk;
+      if constexpr (Q16) {
+        a[rt][ks] = load_chunk<MODE, LIPCACHE_BF16>(p.zq16, row, p.d, k0);
+      } else {
+        a[rt][ks] = load_chunk<MODE, LIPCACHE_F32>(p.zq, row, p.d, k0);
+      }
+    }
   }
 }
 
-template <int MODE, int KS, int RT>
+template <int MODE, int KS, int RT, bool Q16>
 __device__ __forceinline__ void load_queries(const LookupParams& p, const int32_t* qlist, int64_t qwave, int64_t qend,
                                              int m16, int g, u32x4 (&a)[RT][KS], float (&qt)[RT][4]) {
-  load_query_operands<MODE, KS, RT>(p, qlist, qwave, qend, m16, g, a);
+  load_query_operands<MODE, KS, RT, Q16>(p, qlist, qwave, qend, m16, g, a);
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
@@ -364,7 +381,7 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_kernel(const LookupParam
 
   u32x4 a[RT][KS];
   float qt[RT][4];
-  load_queries<MODE, KS, RT>(p, qlist, qwave, qend, m16, g, a, qt);
+  load_queries<MODE, KS, RT, LIST && MODE == kModeBF16>(p, qlist, qwave, qend, m16, g, a, qt);
 
   for (int64_t t0 = e_begin; t0 < e_end; t0 += kTileN) {
     __syncthreads();
@@ -764,7 +781,7 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
   issue_tile<MODE, KS>(buf0, ath0, p, e_begin, e_end, wave);
 
   u32x4 a[RT][KS];
-  load_query_operands<MODE, KS, RT>(p, qlist, qwave, qend, m16, g, a);
+  load_query_operands<MODE, KS, RT, LIST && MODE == kModeBF16>(p, qlist, qwave, qend, m16, g, a);
   // Q_q of this lane's accumulator rows 4g .. 4g + 3 of each row tile, kept
   // in registers for the whole slice (reading them from LDS per column tile
   // costs a third of the operand traffic); +inf past B.
@@ -959,8 +976,9 @@ lipcache_status lookup_stage_prep(const float* zq, int64_t B, int d, const Filte
 lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision, const FilterConsts& fc,
                                   const float* zq, int64_t B, const float* qthr, unsigned long long* best,
                                   unsigned int* bflag, unsigned long long* stats, float* athr,
-                                  const int64_t* items, int64_t n_items, const int32_t* qlist, const int64_t* emap,
-                                  int64_t eoff, bool dump, float* g_hat, uint8_t* cand, hipStream_t s) {
+                                  const int64_t* items, int64_t n_items, const int32_t* qlist, const uint16_t* zq16,
+                                  const int64_t* emap, int64_t eoff, bool dump, float* g_hat, uint8_t* cand,
+                                  hipStream_t s) {
   if (B <= 0 || view->n <= 0) return LIPCACHE_OK;
   if (items && n_items <= 0) return LIPCACHE_OK;
   const int64_t n_pad = athr_len(view->n);
@@ -988,6 +1006,7 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
   p.cand = cand;
   p.items = items;
   p.qlist = qlist;
+  p.zq16 = zq16;
   p.emap = emap;
   p.eoff = eoff;
   int64_t grid = n_items;
@@ -1046,8 +1065,8 @@ lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, 
   unsigned long long* st = stats ? reinterpret_cast<unsigned long long*>(stats) : w.stats;
   lipcache_status r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s);
   if (r != LIPCACHE_OK) return r;
-  r = lookup_stage_scan(c, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr, nullptr, 0,
-                        dump, g_hat, cand, s);
+  r = lookup_stage_scan(c, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr, nullptr,
+                        nullptr, 0, dump, g_hat, cand, s);
   if (r != LIPCACHE_OK) return r;
   if (dump) return LIPCACHE_OK;
   return lookup_stage_finalize(B, w.best, w.bflag, c->label, label_out, index_out, dist2_out, band_flag, st, s);
@@ -1056,12 +1075,15 @@ lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, 
 // Workspace of an indexed lookup: the dense lookup's buffers (thresholds
 // sized for the larger of the indexed part and the tail) and the plan's.
 // The work-list capacity is sized for the smallest query block of any plan.
+// with_q16: include the bf16 copy of the queries (at the returned offset of
+// the layout without it).
 inline size_t indexed_ws_layout(int64_t B, int64_t n, int d, int K, int64_t n_indexed, Workspace* w,
-                                IndexPlanWs* pw, void* base) {
+                                IndexPlanWs* pw, void* base, bool with_q16 = true) {
   const int64_t tail = n - n_indexed;
   const size_t lk = ws_layout(B, n_indexed > tail ? n_indexed : tail, w, base);
   char* pb = base ? static_cast<char*>(base) + lk : nullptr;
-  return lk + index_plan_layout(B, d, K, n_indexed, kLkWaves * 16, pw, pb);
+  const size_t plan = lk + index_plan_layout(B, d, K, n_indexed, kLkWaves * 16, pw, pb);
+  return with_q16 ? plan + align_up(static_cast<size_t>(B) * d * 2, 256) : plan;
 }
 
 lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index* idx, const float* zq, int64_t B,
@@ -1101,8 +1123,16 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
   if (r != LIPCACHE_OK) return r;
   r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s);
   if (r != LIPCACHE_OK) return r;
+  uint16_t* zq16 = nullptr;
+  if (precision == LIPCACHE_BF16) {
+    zq16 = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + indexed_ws_layout(B, c->n, c->d, idx->K, idx->n_indexed,
+                                                                                   nullptr, nullptr, nullptr, false));
+    const int64_t nq = B * c->d;
+    hipLaunchKernelGGL(query_bf16_kernel, dim3(static_cast<unsigned>((nq + 255) / 256)), dim3(256), 0, s, zq, nq, zq16);
+    LC_LAUNCHED();
+  }
   r = lookup_stage_scan(&so, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, pw.items, n_items, pw.qlist,
-                        idx->perm, 0, false, nullptr, nullptr, s);
+                        zq16, idx->perm, 0, false, nullptr, nullptr, s);
   if (r != LIPCACHE_OK) return r;
   const int64_t tail = c->n - idx->n_indexed;
   if (tail > 0) {
@@ -1118,7 +1148,7 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
     view.n = tail;
     view.capacity = tail;
     r = lookup_stage_scan(&view, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr,
-                          nullptr, idx->n_indexed, false, nullptr, nullptr, s);
+                          nullptr, nullptr, idx->n_indexed, false, nullptr, nullptr, s);
     if (r != LIPCACHE_OK) return r;
   }
   if (pairs) *pairs = idx_pairs + B * tail;

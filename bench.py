@@ -617,7 +617,11 @@ def main() -> int:
             tr["fetch_scale"], tr["write_scale"])
         out["roofline"]["hbm_gbs"] = tr["traffic_bytes"] / (lk * 1e-3) / 1e9
     if args.index_k > 0:
-        out["indexed_lookup"] = indexed_context(cache, zq, res, args)
+        try:
+            out["indexed_lookup"] = indexed_context(cache, zq, res, args)
+        except Exception as e:  # context only: report it, keep the headline line
+            log(f"indexed lookup context failed: {e}")
+            out["indexed_lookup"] = {"K": args.index_k, "error": str(e)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, zq_host, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -295,6 +295,8 @@ typedef struct lipcache_index {
  * Build an index over rows 0 .. c->n-1 (K clusters, `iters` Lloyd
  * iterations; 1 <= K <= 65536, K <= c->n).  Sets idx->K, idx->n_indexed and
  * idx->sorted.n; the arrays of idx must be allocated by the caller.
+ * c->z, idx->sorted.z, idx->sorted.zimg and idx->centers must be 16-byte
+ * aligned and c->zimg 8-byte aligned (LIPCACHE_EINVAL otherwise).
  *  ws lipcache_index_build_workspace_bytes(c->n, c->d, K) bytes
  * (async)
  */

@@ -263,48 +263,137 @@ __global__ void offsets_kernel(const unsigned long long* __restrict__ cnt, int K
   offsets[K] = s;
 }
 
-// Sorted row j: copy cache row perm[j]; R_c candidates from live rows.
-__global__ void reorder_kernel(const lipcache_cache c, lipcache_cache out, const uint32_t* __restrict__ order,
-                               int64_t n, int64_t* __restrict__ perm, const uint32_t* __restrict__ assign,
-                               const float* __restrict__ centres, unsigned long long* __restrict__ rbits) {
-  const int64_t j = static_cast<int64_t>(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
-  if (j >= n) return;
+// Sorted rows j0 .. j0+7 (one wave): copy cache rows perm[j] and raise R_c.
+// Lanes 0..7 move the per-row scalars; the feature rows move as 16-byte
+// (f32) or 8-byte (bf16, image) vectors, the eight rows' loads issued
+// before their stores.  The rows are in cluster order, so the wave keeps a
+// running max of ||z_j - mu_c|| + r_j and flushes one atomic per cluster
+// it covers instead of one per row.
+constexpr int kReorderRows = 8;
+
+__device__ __forceinline__ double diff2_4(float4 v, float4 m) {
+  double p = static_cast<double>(v.x) - static_cast<double>(m.x);
+  double acc = p * p;
+  p = static_cast<double>(v.y) - static_cast<double>(m.y);
+  acc = __builtin_fma(p, p, acc);
+  p = static_cast<double>(v.z) - static_cast<double>(m.z);
+  acc = __builtin_fma(p, p, acc);
+  p = static_cast<double>(v.w) - static_cast<double>(m.w);
+  return __builtin_fma(p, p, acc);
+}
+
+__device__ __forceinline__ float4 bf16x4_to_f32(uint2 h) {
+  return make_float4(bf16_to_f32(static_cast<uint16_t>(h.x)), bf16_to_f32(static_cast<uint16_t>(h.x >> 16)),
+                     bf16_to_f32(static_cast<uint16_t>(h.y)), bf16_to_f32(static_cast<uint16_t>(h.y >> 16)));
+}
+
+__device__ __forceinline__ uint2 f32x4_to_bf16(float4 v) {
+  return make_uint2(static_cast<uint32_t>(bf16_bits(v.x)) | (static_cast<uint32_t>(bf16_bits(v.y)) << 16),
+                    static_cast<uint32_t>(bf16_bits(v.z)) | (static_cast<uint32_t>(bf16_bits(v.w)) << 16));
+}
+
+__global__ __launch_bounds__(256) void reorder_kernel(const lipcache_cache c, lipcache_cache out,
+                                                      const uint32_t* __restrict__ order, int64_t n,
+                                                      int64_t* __restrict__ perm,
+                                                      const uint32_t* __restrict__ assign,
+                                                      const float* __restrict__ centres,
+                                                      unsigned long long* __restrict__ rbits) {
+  constexpr int R = kReorderRows;
+  const int64_t j0 = (static_cast<int64_t>(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave) * R;
+  if (j0 >= n) return;
   const int lane = lane_id();
-  const int64_t src = order[j];
+  const int rows = n - j0 < R ? static_cast<int>(n - j0) : R;
+  int64_t src_l = 0;
+  uint32_t cl_l = 0;
+  float r_l = 0.0f;
+  if (lane < rows) {
+    src_l = order[j0 + lane];
+    cl_l = assign[src_l];
+    r_l = c.r[src_l];
+    perm[j0 + lane] = src_l;
+    out.r[j0 + lane] = r_l;
+    out.label[j0 + lane] = c.label[src_l];
+    out.norm2[j0 + lane] = c.norm2[src_l];
+  }
+  int64_t src[R];
+  uint32_t cl[R];
+#pragma unroll
+  for (int t = 0; t < R; ++t) {
+    // rows past the end repeat the last row's loads; their stores are skipped
+    const int u = t < rows ? t : rows - 1;
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(src_l)), u);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(src_l >> 32)), u);
+    src[t] = static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+    cl[t] = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(cl_l), u));
+  }
   const int d = c.d;
-  const uint32_t cl = assign[src];
-  double part = 0.0;
-  for (int k = lane; k < d; k += kWave) {
+  const int d4 = d >> 2;
+  const float4* __restrict__ mu4 = reinterpret_cast<const float4*>(centres);
+  double part[R];
+#pragma unroll
+  for (int t = 0; t < R; ++t) part[t] = 0.0;
+  for (int k4 = lane; k4 < d4; k4 += kWave) {
     if (c.store_dtype == LIPCACHE_BF16) {
-      const uint16_t h = static_cast<const uint16_t*>(c.z)[src * d + k];
-      static_cast<uint16_t*>(out.z)[j * d + k] = h;
-      const double diff = static_cast<double>(bf16_to_f32(h)) - static_cast<double>(centres[static_cast<int64_t>(cl) * d + k]);
-      part = __builtin_fma(diff, diff, part);
-    } else {
-      const float v = static_cast<const float*>(c.z)[src * d + k];
-      static_cast<float*>(out.z)[j * d + k] = v;
-      if (out.zimg) {
-        static_cast<uint16_t*>(out.zimg)[j * d + k] =
-            c.zimg ? static_cast<const uint16_t*>(c.zimg)[src * d + k] : bf16_bits(v);
+      const uint2* __restrict__ zs = static_cast<const uint2*>(c.z);
+      uint2* __restrict__ zo = static_cast<uint2*>(out.z);
+      uint2 v[R];
+#pragma unroll
+      for (int t = 0; t < R; ++t) v[t] = zs[src[t] * d4 + k4];
+#pragma unroll
+      for (int t = 0; t < R; ++t) {
+        if (t < rows) {
+          zo[(j0 + t) * d4 + k4] = v[t];
+          part[t] += diff2_4(bf16x4_to_f32(v[t]), mu4[static_cast<int64_t>(cl[t]) * d4 + k4]);
+        }
       }
-      const double diff = static_cast<double>(v) - static_cast<double>(centres[static_cast<int64_t>(cl) * d + k]);
-      part = __builtin_fma(diff, diff, part);
+    } else {
+      const float4* __restrict__ zs = static_cast<const float4*>(c.z);
+      float4* __restrict__ zo = static_cast<float4*>(out.z);
+      const uint2* __restrict__ is = static_cast<const uint2*>(c.zimg);
+      uint2* __restrict__ io = static_cast<uint2*>(out.zimg);
+      float4 v[R];
+      uint2 im[R];
+#pragma unroll
+      for (int t = 0; t < R; ++t) v[t] = zs[src[t] * d4 + k4];
+      if (io && is) {
+#pragma unroll
+        for (int t = 0; t < R; ++t) im[t] = is[src[t] * d4 + k4];
+      } else {
+#pragma unroll
+        for (int t = 0; t < R; ++t) im[t] = f32x4_to_bf16(v[t]);
+      }
+#pragma unroll
+      for (int t = 0; t < R; ++t) {
+        if (t < rows) {
+          zo[(j0 + t) * d4 + k4] = v[t];
+          if (io) io[(j0 + t) * d4 + k4] = im[t];
+          part[t] += diff2_4(v[t], mu4[static_cast<int64_t>(cl[t]) * d4 + k4]);
+        }
+      }
     }
   }
-  const double d2 = wave_sum(part);
-  if (lane == 0) {
-    perm[j] = src;
-    const float rr = c.r[src];
-    out.r[j] = rr;
-    out.label[j] = c.label[src];
-    out.norm2[j] = c.norm2[src];
-    if (rr > 0.0f) {
-      // the ball widened by 2^-16 r, so every pair inside the 1e-5 r band of
-      // the re-check is also reached
-      const double reach = __builtin_sqrt(d2) + static_cast<double>(rr) * (1.0 + 0x1p-16);
-      atomicMax(&rbits[cl], __builtin_bit_cast(unsigned long long, reach));
+  // per-row reach, folded into a running max per cluster (negative: none yet)
+  double run = -1.0;
+  uint32_t run_cl = cl[0];
+#pragma unroll
+  for (int t = 0; t < R; ++t) {
+    if (t < rows) {
+      const double d2 = wave_sum_dpp(part[t]);
+      const float rr = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, r_l), t));
+      if (cl[t] != run_cl) {
+        if (run >= 0.0 && lane == 0) atomicMax(&rbits[run_cl], __builtin_bit_cast(unsigned long long, run));
+        run = -1.0;
+        run_cl = cl[t];
+      }
+      if (rr > 0.0f) {
+        // the ball widened by 2^-16 r, so every pair inside the 1e-5 r band
+        // of the re-check is also reached
+        const double reach = __builtin_sqrt(d2) + static_cast<double>(rr) * (1.0 + 0x1p-16);
+        run = reach > run ? reach : run;
+      }
     }
   }
+  if (run >= 0.0 && lane == 0) atomicMax(&rbits[run_cl], __builtin_bit_cast(unsigned long long, run));
 }
 
 // R_c rounded up to float32; -inf when no live member.  The reach values are
@@ -634,7 +723,8 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
   if (!so.z || !so.r || !so.label || !so.norm2 || !idx->perm || !idx->offsets || !idx->centers || !idx->bound)
     return LIPCACHE_EINVAL;
   if ((reinterpret_cast<uintptr_t>(so.z) & 15u) != 0 || (reinterpret_cast<uintptr_t>(so.zimg) & 15u) != 0 ||
-      (reinterpret_cast<uintptr_t>(c->z) & 15u) != 0 || (reinterpret_cast<uintptr_t>(idx->centers) & 15u) != 0)
+      (reinterpret_cast<uintptr_t>(c->z) & 15u) != 0 || (reinterpret_cast<uintptr_t>(c->zimg) & 7u) != 0 ||
+      (reinterpret_cast<uintptr_t>(idx->centers) & 15u) != 0)
     return LIPCACHE_EINVAL;
   const size_t need = lipcache_index_build_workspace_bytes(c->n, c->d, K);
   if (!ws || ws_bytes < need || !aligned256(ws)) return LIPCACHE_EWORKSPACE;
@@ -698,8 +788,9 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
                      static_cast<int64_t>(K), 0ull);
   LC_LAUNCHED();
   lipcache_cache out = idx->sorted;
-  hipLaunchKernelGGL(reorder_kernel, dim3(static_cast<unsigned>((n + 3) / 4)), dim3(256), 0, s, *c, out, w.vals[cur],
-                     n, idx->perm, w.assign, idx->centers, w.rbits);
+  const int64_t rpb = 4 * kReorderRows;  // rows per 256-thread workgroup
+  hipLaunchKernelGGL(reorder_kernel, dim3(static_cast<unsigned>((n + rpb - 1) / rpb)), dim3(256), 0, s, *c, out,
+                     w.vals[cur], n, idx->perm, w.assign, idx->centers, w.rbits);
   LC_LAUNCHED();
   hipLaunchKernelGGL(bound_kernel, dim3(static_cast<unsigned>((K + 255) / 256)), dim3(256), 0, s, w.rbits, K,
                      idx->bound);

@@ -274,10 +274,41 @@ __device__ __forceinline__ RecheckArgs recheck_args(const LookupParams& p, int64
   return RecheckArgs{p.zq, p.cz, p.cr, p.best, p.bflag, p.stats, qend, p.n, p.d, p.emap, p.eoff, qlist};
 }
 
+// ||q - z_e||^2 of query row q and cache row e in float64 over the whole
+// wave: lane-strided partial sums, then a fixed butterfly, so the value does
+// not depend on scheduling or on which path evaluates the pair.
+template <int SRC>
+__device__ __forceinline__ double wave_dist2(const RecheckArgs& p, int64_t q, int64_t e) {
+  const float* qr = p.zq + q * p.d;
+  double part = 0.0;
+  for (int k = lane_id(); k < p.d; k += kWave) {
+    const double diff = static_cast<double>(qr[k]) - cache_value<SRC>(p.cz, e, p.d, k);
+    part = __builtin_fma(diff, diff, part);
+  }
+  return wave_sum(part);
+}
+
+// Outcome of one re-checked pair (one lane): counters, band flag, and the
+// packed (d^2, entry) key of a hit into the query's minimum.
+__device__ __forceinline__ void record_pair(const RecheckArgs& p, int64_t q, int64_t e, double d2) {
+  atomicAdd(&p.stats[LIPCACHE_STAT_RECHECKED], 1ull);
+  const double r = static_cast<double>(p.cr[e]);
+  const bool hit = d2 < r * r;
+  if (__builtin_fabs(__builtin_sqrt(d2) - r) <= 1e-5 * r) {
+    atomicAdd(&p.stats[LIPCACHE_STAT_BAND_PAIRS], 1ull);
+    atomicOr(&p.bflag[q], 1u);
+  }
+  if (hit) {
+    const float d2f = static_cast<float>(d2);
+    const int64_t ek = (p.emap ? p.emap[e] : e) + p.eoff;
+    const unsigned long long key = (static_cast<unsigned long long>(__builtin_bit_cast(uint32_t, d2f)) << 32) |
+                                   static_cast<unsigned long long>(static_cast<uint32_t>(ek));
+    atomicMin(&p.best[q], key);
+  }
+}
+
 // Exact re-check of the pairs whose bits are set in `mask` (bit rt*4+i of a
-// lane = accumulator i of row tile rt).  The whole wave evaluates one pair
-// at a time: sum_k (q_k - z_ik)^2 in float64, lane-strided then a fixed
-// butterfly, so the result does not depend on scheduling.
+// lane = accumulator i of row tile rt), one pair at a time by the whole wave.
 template <int SRC>
 __device__ __noinline__ void recheck_pairs(const RecheckArgs p, uint32_t mask, int64_t qwave, int64_t ebase) {
   const int lane = lane_id();
@@ -293,31 +324,137 @@ __device__ __noinline__ void recheck_pairs(const RecheckArgs p, uint32_t mask, i
     const int64_t e = ebase + (src & 15);
     if (qpos >= p.qend || e >= p.n) continue;  // padded rows never pass; kept as a guard
     const int64_t q = query_at(p.qlist, qpos);
-    const float* qr = p.zq + q * p.d;
-    double part = 0.0;
-    for (int k = lane; k < p.d; k += kWave) {
-      const double diff = static_cast<double>(qr[k]) - cache_value<SRC>(p.cz, e, p.d, k);
-      part = __builtin_fma(diff, diff, part);
-    }
-    const double d2 = wave_sum(part);
-    if (lane == 0) {
-      atomicAdd(&p.stats[LIPCACHE_STAT_RECHECKED], 1ull);
-      const double r = static_cast<double>(p.cr[e]);
-      const bool hit = d2 < r * r;
-      if (__builtin_fabs(__builtin_sqrt(d2) - r) <= 1e-5 * r) {
-        atomicAdd(&p.stats[LIPCACHE_STAT_BAND_PAIRS], 1ull);
-        atomicOr(&p.bflag[q], 1u);
+    const double d2 = wave_dist2<SRC>(p, q, e);
+    if (lane == 0) record_pair(p, q, e, d2);
+  }
+}
+
+// Work-list mode defers the re-check: a wave queues its passing pairs in
+// LDS while it scans the item's tiles and settles them after its last tile
+// (or when the queue is full), so a pair costs no barrier-coupled stall of
+// the whole workgroup.
+constexpr int kRq = 64;  // queued pairs per wave
+
+struct RecheckQueue {
+  int32_t* q;  // LDS: kRq query positions, relative to the wave's first
+  int64_t* e;  // LDS: kRq cache rows
+  int n;       // queued pairs (wave-uniform)
+};
+
+// Up to four queued pairs per pass: lanes 0..3 fetch the pairs' query ids,
+// radii and entry map first, then every lane loads its features of all four
+// rows before the sums (each pair keeps the lane-strided order of
+// wave_dist2, so results equal the immediate path's bit for bit).
+template <int SRC>
+__device__ __noinline__ void settle_queue(const RecheckArgs p, const int32_t* rq_q, const int64_t* rq_e, int n,
+                                          int64_t qwave) {
+  constexpr int P = 4;
+  const int lane = lane_id();
+  for (int b = 0; b < n; b += P) {
+    // lane j < P: pair b + j
+    int64_t mq = -1, me = 0, mk = 0;
+    float mr = 0.0f;
+    if (lane < P && b + lane < n) {
+      const int64_t qpos = qwave + rq_q[b + lane];
+      const int64_t e = rq_e[b + lane];
+      if (qpos < p.qend && e < p.n) {
+        mq = query_at(p.qlist, qpos);
+        me = e;
+        mr = p.cr[e];
+        mk = (p.emap ? p.emap[e] : e) + p.eoff;
       }
-      if (hit) {
-        const float d2f = static_cast<float>(d2);
-        const int64_t ek = (p.emap ? p.emap[e] : e) + p.eoff;
-        const unsigned long long key =
-            (static_cast<unsigned long long>(__builtin_bit_cast(uint32_t, d2f)) << 32) |
-            static_cast<unsigned long long>(static_cast<uint32_t>(ek));
-        atomicMin(&p.best[q], key);
+    }
+    int64_t q[P], e[P];
+    bool v[P];
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(mq)), j);
+      const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(mq >> 32)), j);
+      const int64_t qj = static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+      const uint32_t elo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(me)), j);
+      const uint32_t ehi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(me >> 32)), j);
+      v[j] = qj >= 0;
+      q[j] = v[j] ? qj : 0;
+      e[j] = static_cast<int64_t>((static_cast<uint64_t>(ehi) << 32) | elo);
+    }
+    double acc[P];
+#pragma unroll
+    for (int j = 0; j < P; ++j) acc[j] = 0.0;
+#pragma unroll 4
+    for (int k = lane; k < p.d; k += kWave) {
+      float qa[P];
+      double za[P];
+#pragma unroll
+      for (int j = 0; j < P; ++j) {
+        qa[j] = p.zq[q[j] * p.d + k];
+        za[j] = cache_value<SRC>(p.cz, e[j], p.d, k);
+      }
+#pragma unroll
+      for (int j = 0; j < P; ++j) {
+        const double diff = static_cast<double>(qa[j]) - za[j];
+        acc[j] = __builtin_fma(diff, diff, acc[j]);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const double d2 = wave_sum(acc[j]);
+      if (lane == j && v[j]) {
+        // record_pair with the radius and key fetched above
+        atomicAdd(&p.stats[LIPCACHE_STAT_RECHECKED], 1ull);
+        const double r = static_cast<double>(mr);
+        if (__builtin_fabs(__builtin_sqrt(d2) - r) <= 1e-5 * r) {
+          atomicAdd(&p.stats[LIPCACHE_STAT_BAND_PAIRS], 1ull);
+          atomicOr(&p.bflag[mq], 1u);
+        }
+        if (d2 < r * r) {
+          const float d2f = static_cast<float>(d2);
+          const unsigned long long key = (static_cast<unsigned long long>(__builtin_bit_cast(uint32_t, d2f)) << 32) |
+                                         static_cast<unsigned long long>(static_cast<uint32_t>(mk));
+          atomicMin(&p.best[mq], key);
+        }
       }
     }
   }
+}
+
+// Queues the pairs of `mask` (same bit layout as recheck_pairs: lane (m16, g)
+// holds entry ebase + m16 and query rows 4g + i of each row tile).  Pairs
+// that do not fit are re-checked at once.
+template <int SRC>
+__device__ __forceinline__ void queue_pairs(const RecheckArgs& p, RecheckQueue& rq, uint32_t mask, int64_t qwave,
+                                            int64_t ebase) {
+  const int lane = lane_id();
+  while (true) {
+    const bool has = mask != 0u;
+    const unsigned long long bal = __ballot(has);
+    if (bal == 0ull) break;
+    const int fresh = __popcll(bal);
+    if (rq.n + fresh > kRq) {
+      recheck_pairs<SRC>(p, mask, qwave, ebase);
+      break;
+    }
+    if (has) {
+      const int bit = __builtin_ctz(mask);
+      const int slot = rq.n + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                                  static_cast<uint32_t>(bal >> 32),
+                                  __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(bal), 0u)));
+      rq.q[slot] = (bit >> 2) * 16 + 4 * (lane >> 4) + (bit & 3);
+      rq.e[slot] = ebase + (lane & 15);
+      mask &= mask - 1u;
+    }
+    rq.n += fresh;
+  }
+}
+
+// Settles the queue after the wave's last tile; the queue was written by
+// other lanes of this wave.
+template <int SRC>
+__device__ __forceinline__ void flush_queue(const RecheckArgs& p, RecheckQueue& rq, int64_t qwave) {
+  if (rq.n == 0) return;
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_wave_barrier();
+  settle_queue<SRC>(p, rq.q, rq.e, rq.n, qwave);
+  rq.n = 0;
 }
 
 // Queries as MFMA A operands: lane holds row m16 of each row tile and k-chunk
@@ -582,28 +719,33 @@ __device__ __forceinline__ u32x4 lds_operand(const unsigned char* buf, int sub, 
 // and compares once against A_i; the exact per-pair mask is only rebuilt on
 // the rare path.
 // Rare path of one column tile: rebuild the exact per-pair mask and re-check.
-template <int STORE, int RT>
+template <int STORE, int RT, bool LIST>
 __device__ __forceinline__ void filter_and_recheck(const LookupParams& p, const f32x4 (&acc)[RT], const f32x4 (&qt)[RT],
                                                    float an, int64_t qwave, int64_t qend, const int32_t* qlist,
-                                                   int64_t ebase) {
+                                                   int64_t ebase, RecheckQueue& rq) {
   uint32_t mask = 0u;
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) mask |= static_cast<uint32_t>((acc[rt][i] - qt[rt][i]) >= an) << (rt * 4 + i);
   }
-  recheck_pairs<STORE>(recheck_args(p, qend, qlist), mask, qwave, ebase);
+  if constexpr (LIST) {
+    queue_pairs<STORE>(recheck_args(p, qend, qlist), rq, mask, qwave, ebase);
+  } else {
+    recheck_pairs<STORE>(recheck_args(p, qend, qlist), mask, qwave, ebase);
+  }
 }
 
 // A full LDS tile, software-pipelined: while the MFMAs of column tile s run,
 // the same wave evaluates the filter of column tile s - 1 (its accumulators
 // are kept one step longer), so the filter's VALU work fills the matrix
 // pipe's shadow instead of following it.
-template <int MODE, int STORE, int KS, int RT>
+template <int MODE, int STORE, int KS, int RT, bool LIST>
 __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, const float* athr_buf,
                                                   const LookupParams& p, int64_t t0, int64_t qwave, int64_t qend,
                                                   const int32_t* qlist, int m16, int g,
-                                                  const u32x4 (&a)[RT][KS], const f32x4 (&qv)[RT]) {
+                                                  const u32x4 (&a)[RT][KS], const f32x4 (&qv)[RT],
+                                                  RecheckQueue& rq) {
   constexpr int kSubs = DmaTraits<KS>::kRows / kColTile;
   constexpr int kE = RT * 4;                      // accumulators per lane
   constexpr int kPer = (kE + KS - 1) / KS;        // filter terms folded into each k-step
@@ -658,7 +800,8 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
     }
     if (cur && KS == 1 && sub + 1 < kSubs) b0 = lds_operand<KS>(buf, sub + 1, 0, m16, g);
     if (prev) {
-      if (__ballot(mx >= anp) != 0ull) filter_and_recheck<STORE, RT>(p, accp, qt, anp, qwave, qend, qlist, t0 + (sub - 1) * kColTile);
+      if (__ballot(mx >= anp) != 0ull)
+        filter_and_recheck<STORE, RT, LIST>(p, accp, qt, anp, qwave, qend, qlist, t0 + (sub - 1) * kColTile, rq);
     }
     if (cur) {
 #pragma unroll
@@ -668,16 +811,16 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
   }
 }
 
-template <int MODE, int STORE, int KS, int RT, bool DUMP>
+template <int MODE, int STORE, int KS, int RT, bool DUMP, bool LIST>
 __device__ __forceinline__ void compute_tile(const unsigned char* buf, const float* athr_buf, const LookupParams& p,
                                              int64_t t0, int64_t e_end, int64_t qwave, int64_t qend,
                                              const int32_t* qlist, int m16, int g, const u32x4 (&a)[RT][KS],
-                                             const f32x4 (&qv)[RT]) {
+                                             const f32x4 (&qv)[RT], RecheckQueue& rq) {
   constexpr int kRows = DmaTraits<KS>::kRows;
   const int64_t left = e_end - t0;
   if constexpr (!DUMP) {
     if (left >= kRows) {
-      compute_full_tile<MODE, STORE, KS, RT>(buf, athr_buf, p, t0, qwave, qend, qlist, m16, g, a, qv);
+      compute_full_tile<MODE, STORE, KS, RT, LIST>(buf, athr_buf, p, t0, qwave, qend, qlist, m16, g, a, qv, rq);
       return;
     }
   }
@@ -749,7 +892,11 @@ __device__ __forceinline__ void compute_tile(const unsigned char* buf, const flo
 #pragma unroll
           for (int i = 0; i < 4; ++i) mask |= static_cast<uint32_t>((acc[rt][i] - qt[rt][i]) >= an) << (rt * 4 + i);
         }
-        recheck_pairs<STORE>(recheck_args(p, qend, qlist), mask, qwave, ebase);
+        if constexpr (LIST) {
+          queue_pairs<STORE>(recheck_args(p, qend, qlist), rq, mask, qwave, ebase);
+        } else {
+          recheck_pairs<STORE>(recheck_args(p, qend, qlist), mask, qwave, ebase);
+        }
       }
     }
   }
@@ -765,6 +912,8 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
   __shared__ __attribute__((aligned(16))) unsigned char buf1[kTileBytes];
   __shared__ __attribute__((aligned(16))) float ath0[kRows];
   __shared__ __attribute__((aligned(16))) float ath1[kRows];
+  __shared__ int64_t rq_e[LIST ? kLkWaves * kRq : 1];
+  __shared__ int32_t rq_q[LIST ? kLkWaves * kRq : 1];
 
   int64_t q0, qend, e_begin, e_end;
   block_work(p, kLkWaves * RT * 16, q0, qend, e_begin, e_end);
@@ -778,10 +927,14 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
   const int64_t qwave = q0 + wave * (RT * 16);
 
   if (e_begin >= e_end) return;  // whole workgroup: an empty slice
+  // Work-list mode: a wave whose queries all lie past the list's end only
+  // moves its share of each tile (the copies and barriers are the block's).
+  const bool active = !LIST || qwave < qend;
   issue_tile<MODE, KS>(buf0, ath0, p, e_begin, e_end, wave);
 
   u32x4 a[RT][KS];
-  load_query_operands<MODE, KS, RT, LIST && MODE == kModeBF16>(p, qlist, qwave, qend, m16, g, a);
+  if (active) load_query_operands<MODE, KS, RT, LIST && MODE == kModeBF16>(p, qlist, qwave, qend, m16, g, a);
+  RecheckQueue rq{rq_q + (LIST ? wave * kRq : 0), rq_e + (LIST ? wave * kRq : 0), 0};
   // Q_q of this lane's accumulator rows 4g .. 4g + 3 of each row tile, kept
   // in registers for the whole slice (reading them from LDS per column tile
   // costs a third of the operand traffic); +inf past B.
@@ -800,14 +953,17 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
     __syncthreads();
     const bool more1 = t0 + kRows < e_end;
     if (more1) issue_tile<MODE, KS>(buf1, ath1, p, t0 + kRows, e_end, wave);
-    compute_tile<MODE, STORE, KS, RT, DUMP>(buf0, ath0, p, t0, e_end, qwave, qend, qlist, m16, g, a, qv);
+    if (active) compute_tile<MODE, STORE, KS, RT, DUMP, LIST>(buf0, ath0, p, t0, e_end, qwave, qend, qlist, m16, g, a, qv, rq);
     if (!more1) break;
     wait_copies();
     __syncthreads();
     const bool more2 = t0 + 2 * kRows < e_end;
     if (more2) issue_tile<MODE, KS>(buf0, ath0, p, t0 + 2 * kRows, e_end, wave);
-    compute_tile<MODE, STORE, KS, RT, DUMP>(buf1, ath1, p, t0 + kRows, e_end, qwave, qend, qlist, m16, g, a, qv);
+    if (active) compute_tile<MODE, STORE, KS, RT, DUMP, LIST>(buf1, ath1, p, t0 + kRows, e_end, qwave, qend, qlist, m16, g, a, qv, rq);
     if (!more2) break;
+  }
+  if constexpr (LIST) {
+    if (active) flush_queue<STORE>(recheck_args(p, qend, qlist), rq, qwave);
   }
 }
 

@@ -119,25 +119,34 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
 // block of 1024 threads, each owning a contiguous run of counts.
 __global__ __launch_bounds__(1024) void exclusive_scan_kernel(const uint32_t* __restrict__ cnt, int m,
                                                               int64_t* __restrict__ out) {
-  __shared__ int64_t part[1024];
+  __shared__ int64_t wsum[16];
   const int t = static_cast<int>(threadIdx.x);
+  const int lane = t & 63, w = t >> 6;
   const int per = (m + 1023) / 1024;
   const int b0 = t * per, b1 = b0 + per < m ? b0 + per : m;
   int64_t sum = 0;
   for (int i = b0; i < b1; ++i) sum += cnt[i];
-  part[t] = sum;
+  // inclusive scan of the thread sums inside each wave, then of the wave totals
+  int64_t x = sum;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[w] = x;
   __syncthreads();
-  if (t == 0) {
-    int64_t run = 0;
-    for (int i = 0; i < 1024; ++i) {
-      const int64_t v = part[i];
-      part[i] = run;
-      run += v;
+  if (w == 0) {
+    int64_t v = lane < 16 ? wsum[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      const int64_t y = __shfl_up(v, o, 64);
+      if (lane >= o) v += y;
     }
-    out[m] = run;
+    if (lane < 16) wsum[lane] = v;
   }
   __syncthreads();
-  int64_t run = part[t];
+  int64_t run = x - sum + (w > 0 ? wsum[w - 1] : 0);
+  if (t == 1023) out[m] = run + sum;
   for (int i = b0; i < b1; ++i) {
     out[i] = run;
     run += cnt[i];

@@ -73,7 +73,8 @@ __global__ void row_norm_kernel(const void* __restrict__ x, int store, int64_t n
 //    ||x - mu_c|| < R_c sets its bit.
 // Block: 4 waves, 64 rows; each wave owns 16 rows and all 64 centres of a
 // chunk (4 accumulator tiles); rows and centres pass through LDS in stages
-// of 64 features.
+// of 64 features.  blockIdx.y splits the chunks into groups (only with
+// nearest == nullptr: the mask bits of different centres are independent).
 __global__ __launch_bounds__(256) void centre_mfma_kernel(const void* __restrict__ rows, int store, int64_t n,
                                                           int64_t stride, int d,
                                                           const float* __restrict__ centres,
@@ -98,7 +99,11 @@ __global__ __launch_bounds__(256) void centre_mfma_kernel(const void* __restrict
     bi[v] = INT_MAX;
     qn[v] = (rnorm && row < n) ? rnorm[row] : 0.0;
   }
-  for (int c0 = 0; c0 < K; c0 += kCc) {
+  const int chunks = (K + kCc - 1) / kCc;
+  const int per = (chunks + static_cast<int>(gridDim.y) - 1) / static_cast<int>(gridDim.y);
+  const int c_begin = static_cast<int>(blockIdx.y) * per * kCc;
+  const int c_end = c_begin + per * kCc < K ? c_begin + per * kCc : K;
+  for (int c0 = c_begin; c0 < c_end; c0 += kCc) {
     f32x4 acc[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -673,8 +678,14 @@ lipcache_status index_query_plan(const lipcache_index* idx, const float* zq, int
                      LIPCACHE_F32, static_cast<int64_t>(K), d, w.cnorm);
   LC_LAUNCHED();
   const double slack = 2.0 * (d + 2) / 16777216.0;
-  hipLaunchKernelGGL(centre_mfma_kernel, dim3(static_cast<unsigned>((B + kCr - 1) / kCr)), dim3(256), 0, s, zq,
-                     LIPCACHE_F32, B, static_cast<int64_t>(1), d, idx->centers, w.cnorm, K, w.qnorm, idx->bound,
+  // query blocks x centre groups, about 2048 workgroups in all
+  const int64_t gx = (B + kCr - 1) / kCr;
+  int64_t gy = (2048 + gx - 1) / gx;
+  const int64_t chunks = (K + kCc - 1) / kCc;
+  if (gy > chunks) gy = chunks;
+  if (gy < 1) gy = 1;
+  hipLaunchKernelGGL(centre_mfma_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy)), dim3(256), 0, s,
+                     zq, LIPCACHE_F32, B, static_cast<int64_t>(1), d, idx->centers, w.cnorm, K, w.qnorm, idx->bound,
                      slack, w.mask, nullptr);
   LC_LAUNCHED();
   const unsigned gq = static_cast<unsigned>((B + 255) / 256);

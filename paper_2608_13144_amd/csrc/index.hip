@@ -4,8 +4,11 @@
 // iterations over an evenly strided sample of the rows (about 512 per
 // cluster) assign each sampled row to its nearest centre (x . mu_c on the
 // matrix cores, centre_mfma_kernel) and move each centre to the float64
-// mean of its live sampled rows; the final assignment covers every row.  After the final assignment a stable radix sort by cluster
-// gives the row order, the cluster offsets come from the counts, and
+// mean of its live sampled rows, summed per cluster in sample order after a
+// stable sort of the sample by cluster (so a build does not depend on
+// scheduling); the final assignment covers every row.  After the final
+// assignment a stable radix sort by cluster gives the row order, the
+// cluster offsets come from the counts, and
 // R_c = max over live members of ||z_i - mu_c|| + r_i (widened so that the
 // re-check's boundary band is covered) is taken in float64 and rounded up to
 // float32.  The indexed rows are copied into a cluster-ordered cache.  Any
@@ -175,11 +178,6 @@ __global__ __launch_bounds__(256) void centre_mfma_kernel(const void* __restrict
   }
 }
 
-__global__ void fill_f64_kernel(double* __restrict__ p, int64_t n, double v) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = v;
-}
-
 __global__ void fill_u32_kernel(uint32_t* __restrict__ p, int64_t n) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i < n) p[i] = 0u;
@@ -200,28 +198,88 @@ __global__ void centre_init_kernel(const void* __restrict__ z, int store, int64_
   centres[t] = stored_value(z, store, row, d, k);
 }
 
-// sum[c][k] += z_ik, cnt[c] += 1 over the live rows i = j * stride of the
-// sample (thread per (sample row, column); assign[j] is row j's cluster).
-__global__ void centre_sum_kernel(const void* __restrict__ z, int store, const float* __restrict__ r, int64_t ns,
-                                  int d, int64_t stride, const uint32_t* __restrict__ assign,
-                                  double* __restrict__ sum, unsigned long long* __restrict__ cnt) {
-  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (t >= ns * d) return;
-  const int64_t j = t / d;
-  const int64_t i = j * stride;
-  const int k = static_cast<int>(t % d);
-  if (!(r[i] > 0.0f)) return;
-  const uint32_t c = assign[j];
-  atomicAdd(&sum[static_cast<int64_t>(c) * d + k], static_cast<double>(stored_value(z, store, i, d, k)));
-  if (k == 0) atomicAdd(&cnt[c], 1ull);
+// Lloyd update of cluster c (one workgroup): mu_c = the float64 mean of the
+// live rows among its sampled rows order[off[c] .. off[c + 1]) (sample
+// index j is row j * stride), added in that order, so the centres do not
+// depend on scheduling; a cluster without a live sampled row keeps its
+// centre.  Thread t owns features t + 256 q, q < Q = ceil(d / 256); rows are
+// taken 64 / Q at a time and their loads are unconditional (a dead or
+// missing row reads row 0, a feature past d reads feature 0), so a batch's
+// loads are all in flight before its sums.
+template <int STORE, int Q>
+__global__ __launch_bounds__(256) void centre_mean_kernel(const void* __restrict__ z, const float* __restrict__ r,
+                                                          int d, int64_t stride, const uint32_t* __restrict__ order,
+                                                          const int64_t* __restrict__ off,
+                                                          float* __restrict__ centres) {
+  constexpr int kBatch = 64 / Q;
+  __shared__ int64_t rows[kBatch];
+  const int c = static_cast<int>(blockIdx.x);
+  const int t = static_cast<int>(threadIdx.x);
+  const int64_t b = off[c], e = off[c + 1];
+  double s[Q];
+  int kq[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    s[q] = 0.0;
+    kq[q] = t + 256 * q < d ? t + 256 * q : 0;
+  }
+  int64_t live = 0;
+  for (int64_t j0 = b; j0 < e; j0 += kBatch) {
+    const int m = e - j0 < kBatch ? static_cast<int>(e - j0) : kBatch;
+    __syncthreads();  // the previous batch's row list is consumed
+    if (t < kBatch) {
+      int64_t i = -1;
+      if (t < m) {
+        i = static_cast<int64_t>(order[j0 + t]) * stride;
+        if (!(r[i] > 0.0f)) i = -1;
+      }
+      rows[t] = i;
+    }
+    __syncthreads();
+    float v[kBatch][Q];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int64_t i = rows[u];
+      const int64_t base = (i >= 0 ? i : 0) * d;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        if constexpr (STORE == LIPCACHE_BF16) {
+          v[u][q] = bf16_to_f32(static_cast<const uint16_t*>(z)[base + kq[q]]);
+        } else {
+          v[u][q] = static_cast<const float*>(z)[base + kq[q]];
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      if (rows[u] >= 0) {
+        ++live;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) s[q] += static_cast<double>(v[u][q]);
+      }
+    }
+  }
+  if (live == 0) return;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int k = t + 256 * q;
+    if (k < d) centres[static_cast<int64_t>(c) * d + k] = static_cast<float>(s[q] / static_cast<double>(live));
+  }
 }
 
-__global__ void centre_update_kernel(const double* __restrict__ sum, const unsigned long long* __restrict__ cnt,
-                                     int K, int d, float* __restrict__ centres) {
-  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (t >= static_cast<int64_t>(K) * d) return;
-  const unsigned long long m = cnt[t / d];
-  if (m > 0) centres[t] = static_cast<float>(sum[t] / static_cast<double>(m));
+template <int STORE>
+inline void launch_centre_mean(int d, unsigned K, hipStream_t s, const void* z, const float* r, int64_t stride,
+                               const uint32_t* order, const int64_t* off, float* centres) {
+  const int q = (d + 255) / 256;
+  if (q <= 1) {
+    hipLaunchKernelGGL((centre_mean_kernel<STORE, 1>), dim3(K), dim3(256), 0, s, z, r, d, stride, order, off, centres);
+  } else if (q == 2) {
+    hipLaunchKernelGGL((centre_mean_kernel<STORE, 2>), dim3(K), dim3(256), 0, s, z, r, d, stride, order, off, centres);
+  } else if (q == 3) {
+    hipLaunchKernelGGL((centre_mean_kernel<STORE, 3>), dim3(K), dim3(256), 0, s, z, r, d, stride, order, off, centres);
+  } else {
+    hipLaunchKernelGGL((centre_mean_kernel<STORE, 4>), dim3(K), dim3(256), 0, s, z, r, d, stride, order, off, centres);
+  }
 }
 
 // Keys for the stable sort of rows by cluster; dead rows go to their cluster
@@ -239,7 +297,7 @@ __global__ void row_keys_kernel(const uint32_t* __restrict__ assign, int64_t n, 
 constexpr int kCountLds = 4096;
 
 __global__ __launch_bounds__(256) void count_kernel(const uint32_t* __restrict__ assign, int64_t n, int K,
-                                                    unsigned long long* __restrict__ cnt) {
+                                                    uint32_t* __restrict__ cnt) {
   __shared__ uint32_t h[kCountLds];
   for (int c = threadIdx.x; c < K && c < kCountLds; c += 256) h[c] = 0u;
   __syncthreads();
@@ -249,23 +307,12 @@ __global__ __launch_bounds__(256) void count_kernel(const uint32_t* __restrict__
     if (c < static_cast<uint32_t>(kCountLds)) {
       atomicAdd(&h[c], 1u);
     } else {
-      atomicAdd(&cnt[c], 1ull);
+      atomicAdd(&cnt[c], 1u);
     }
   }
   __syncthreads();
   for (int c = threadIdx.x; c < K && c < kCountLds; c += 256)
-    if (h[c]) atomicAdd(&cnt[c], static_cast<unsigned long long>(h[c]));
-}
-
-// offsets[c] = sum of counts below c (one block, serial chunks).
-__global__ void offsets_kernel(const unsigned long long* __restrict__ cnt, int K, int64_t* __restrict__ offsets) {
-  if (threadIdx.x != 0) return;
-  int64_t s = 0;
-  for (int c = 0; c < K; ++c) {
-    offsets[c] = s;
-    s += static_cast<int64_t>(cnt[c]);
-  }
-  offsets[K] = s;
+    if (h[c]) atomicAdd(&cnt[c], h[c]);
 }
 
 // Sorted rows j0 .. j0+7 (one wave): copy cache rows perm[j] and raise R_c.
@@ -422,8 +469,8 @@ __global__ void bound_kernel(const unsigned long long* __restrict__ rbits, int K
 
 struct BuildWs {
   uint32_t* assign;
-  double* sum;
-  unsigned long long* cnt;
+  uint32_t* cnt;
+  int64_t* coff;
   unsigned long long* rbits;
   double* cnorm;
   uint32_t* keys[2];
@@ -443,8 +490,8 @@ inline BuildWs build_layout(int64_t n, int d, int K, char* base) {
     return p;
   };
   w.assign = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(n) * 4));
-  w.sum = reinterpret_cast<double*>(take(static_cast<size_t>(K) * d * 8));
-  w.cnt = reinterpret_cast<unsigned long long*>(take(static_cast<size_t>(K) * 8));
+  w.cnt = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(K) * 4));
+  w.coff = reinterpret_cast<int64_t*>(take(static_cast<size_t>(K + 1) * 8));
   w.rbits = reinterpret_cast<unsigned long long*>(take(static_cast<size_t>(K) * 8));
   w.cnorm = reinterpret_cast<double*>(take(static_cast<size_t>(K) * 8));
   for (int s = 0; s < 2; ++s) {
@@ -754,7 +801,6 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
   // the final assignment sees every row.
   const int64_t stride = n / (static_cast<int64_t>(K) * kSampleRows) > 1 ? n / (static_cast<int64_t>(K) * kSampleRows) : 1;
   const int64_t ns = (n + stride - 1) / stride;
-  const int64_t sd = ns * d;
   const unsigned gs = static_cast<unsigned>((ns + kCr - 1) / kCr);
   for (int it = 0; it < iters; ++it) {
     hipLaunchKernelGGL(row_norm_kernel, dim3(gk), dim3(256), 0, s, idx->centers, LIPCACHE_F32,
@@ -763,17 +809,27 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
     hipLaunchKernelGGL(centre_mfma_kernel, dim3(gs), dim3(256), 0, s, c->z, c->store_dtype, ns, stride, d,
                        idx->centers, w.cnorm, K, nullptr, nullptr, 0.0, nullptr, w.assign);
     LC_LAUNCHED();
-    hipLaunchKernelGGL(fill_f64_kernel, dim3(static_cast<unsigned>((kd + 255) / 256)), dim3(256), 0, s, w.sum, kd,
-                       0.0);
+    // the sample in cluster order, then one workgroup per cluster
+    hipLaunchKernelGGL(row_keys_kernel, dim3(static_cast<unsigned>((ns + 255) / 256)), dim3(256), 0, s, w.assign,
+                       ns, w.keys[0], w.vals[0]);
     LC_LAUNCHED();
-    hipLaunchKernelGGL(fill_u64x_kernel, dim3(static_cast<unsigned>((K + 255) / 256)), dim3(256), 0, s, w.cnt,
-                       static_cast<int64_t>(K), 0ull);
+    int scur = 0;
+    LC_HIP(radix_sort_u32(w.keys, w.vals, ns, sort_passes(K), w.hist, w.dsum, w.dbase, scur, s));
+    hipLaunchKernelGGL(fill_u32_kernel, dim3(static_cast<unsigned>((K + 255) / 256)), dim3(256), 0, s, w.cnt,
+                       static_cast<int64_t>(K));
     LC_LAUNCHED();
-    hipLaunchKernelGGL(centre_sum_kernel, dim3(static_cast<unsigned>((sd + 255) / 256)), dim3(256), 0, s, c->z,
-                       c->store_dtype, c->r, ns, d, stride, w.assign, w.sum, w.cnt);
+    hipLaunchKernelGGL(count_kernel, dim3(static_cast<unsigned>((ns + 4095) / 4096)), dim3(256), 0, s, w.assign, ns,
+                       K, w.cnt);
     LC_LAUNCHED();
-    hipLaunchKernelGGL(centre_update_kernel, dim3(static_cast<unsigned>((kd + 255) / 256)), dim3(256), 0, s, w.sum,
-                       w.cnt, K, d, idx->centers);
+    hipLaunchKernelGGL(exclusive_scan_kernel, dim3(1), dim3(1024), 0, s, w.cnt, K, w.coff);
+    LC_LAUNCHED();
+    if (c->store_dtype == LIPCACHE_BF16) {
+      launch_centre_mean<LIPCACHE_BF16>(d, static_cast<unsigned>(K), s, c->z, c->r, stride, w.vals[scur], w.coff,
+                                        idx->centers);
+    } else {
+      launch_centre_mean<LIPCACHE_F32>(d, static_cast<unsigned>(K), s, c->z, c->r, stride, w.vals[scur], w.coff,
+                                       idx->centers);
+    }
     LC_LAUNCHED();
   }
   hipLaunchKernelGGL(row_norm_kernel, dim3(gk), dim3(256), 0, s, idx->centers, LIPCACHE_F32, static_cast<int64_t>(K),
@@ -787,13 +843,13 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
   LC_LAUNCHED();
   int cur = 0;
   LC_HIP(radix_sort_u32(w.keys, w.vals, n, sort_passes(K), w.hist, w.dsum, w.dbase, cur, s));
-  hipLaunchKernelGGL(fill_u64x_kernel, dim3(static_cast<unsigned>((K + 255) / 256)), dim3(256), 0, s, w.cnt,
-                     static_cast<int64_t>(K), 0ull);
+  hipLaunchKernelGGL(fill_u32_kernel, dim3(static_cast<unsigned>((K + 255) / 256)), dim3(256), 0, s, w.cnt,
+                     static_cast<int64_t>(K));
   LC_LAUNCHED();
   hipLaunchKernelGGL(count_kernel, dim3(static_cast<unsigned>((n + 4095) / 4096)), dim3(256), 0, s, w.assign, n, K,
                      w.cnt);
   LC_LAUNCHED();
-  hipLaunchKernelGGL(offsets_kernel, dim3(1), dim3(64), 0, s, w.cnt, K, idx->offsets);
+  hipLaunchKernelGGL(exclusive_scan_kernel, dim3(1), dim3(1024), 0, s, w.cnt, K, idx->offsets);
   LC_LAUNCHED();
   hipLaunchKernelGGL(fill_u64x_kernel, dim3(static_cast<unsigned>((K + 255) / 256)), dim3(256), 0, s, w.rbits,
                      static_cast<int64_t>(K), 0ull);

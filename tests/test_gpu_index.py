@@ -7,6 +7,8 @@ rows perm[j] bit for bit, and every live row lies within its cluster's
 bound: ||z_i - mu_c|| + r_i <= R_c (clusters without a live row have
 R_c = -inf).
 
+Two builds of one cache are identical bit for bit.
+
 The indexed lookup returns the oracle's answers query by query and the
 dense device lookup's outputs bit for bit (label, index, d^2, band flags,
 hit and band counters), for both stores and filters, K from 1 to n,
@@ -101,6 +103,23 @@ def test_indexed_matches_oracle_and_dense(tiny, store, prec, image, K, iters):
     same_as_dense(res_i, res_d, what)
     assert 0 < pairs <= zq.shape[0] * st.n
     say("index", what, "pairs", pairs, "of", zq.shape[0] * st.n)
+
+
+@pytest.mark.parametrize("K,iters", [(4, 3), (64, 2)])
+def test_build_is_deterministic(tiny, K, iters):
+    """Two builds of one cache give the same index bit for bit: each Lloyd
+    update sums a cluster's sampled rows in sample order (K = 4 samples every
+    other row of the 4,096; K = 64 takes them all)."""
+    wl, st, zq, ref = tiny["f32"]
+    say("index determinism", K, iters)
+    c = build_cache(st)
+    a = c.build_index(K, iters)
+    b = c.build_index(K, iters)
+    for name in ("perm", "offsets"):
+        assert torch.equal(getattr(a, name), getattr(b, name)), name
+    for name in ("centers", "bound"):
+        assert torch.equal(getattr(a, name).view(torch.int32), getattr(b, name).view(torch.int32)), name
+    check_index(c, a, f"determinism K={K}")
 
 
 def test_rows_appended_after_build(tiny):

@@ -14,7 +14,8 @@ dense device lookup's outputs bit for bit (label, index, d^2, band flags,
 hit and band counters), for both stores and filters, K from 1 to n,
 rows appended after the build, dead rows, duplicated rows (empty
 clusters), queries with more candidate clusters than a list takes, a
-ragged batch, non-finite queries, and the full-size mixture.
+ragged batch, non-finite queries, wide features (d = 512, 1024), and the
+full-size mixture.
 """
 import numpy as np
 import pytest
@@ -200,6 +201,35 @@ def test_edge_batches(tiny):
     assert lab[3] == oracle.MISS and lab[9] == oracle.MISS
     one, _ = c.lookup_indexed(ix, gpu(zq[:1]))
     assert host(one.label)[0] == ref.label[0] or ref.flagged[0]
+
+
+@pytest.mark.parametrize("store", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [512, 1024])
+def test_wide_features(store, d):
+    """d > 256: the Lloyd update takes two or four features per thread, the
+    reorder several vectors per lane, and at d = 1024 the bf16 lookup scans
+    the work list with the register-staged kernel.  K = 2 samples every
+    other row of the 2,048; K = 16 takes them all."""
+    cfg = wlmod.WorkloadConfig(f"wide-d{d}", d=d, C=10, n_cache=2048, batch=512, sigma=0.5)
+    wl = wlmod.make_workload(cfg, seed=3)
+    sig = oracle.spectral_norm(wl.W).sigma
+    cert = oracle.certify(wl.z, wl.W, wl.b, sig, store=store)
+    st = oracle_cache(wl.z, cert.label, cert.r, d, store=store)
+    draws = wlmod.draw_queries(wl, 0, batch=cfg.batch)
+    idx = wlmod.near_indices(draws, st.n)
+    zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
+    ref = oracle.lookup_blocked(zq, st.z, st.r, st.label)
+    c = build_cache(st)
+    q = gpu(zq)
+    for K in (2, 16):
+        what = f"wide d={d} {store} K={K}"
+        say("index", what)
+        ix = c.build_index(K, 3)
+        check_index(c, ix, what)
+        res_i, pairs = c.lookup_indexed(ix, q)
+        compare_lookup(res_i, ref, what)
+        same_as_dense(res_i, c.lookup(q), what)
+        assert 0 < pairs <= zq.shape[0] * st.n
 
 
 @pytest.mark.slow

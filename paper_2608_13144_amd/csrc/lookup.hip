@@ -33,7 +33,12 @@
 //    the same time.  The indexed lookup instead gives each block one item of
 //    a work list: up to 512 queries of one cluster's query list (read through
 //    the list, in a separate instantiation) against a chunk of that cluster's
-//    rows.
+//    rows.  There a query meets its own cluster's rows, so pairs pass the
+//    filter often: each wave queues them in LDS instead of re-checking at
+//    once (which stalls the whole workgroup at the next tile barrier), hands
+//    the queue to a global queue after its last tile, and a separate kernel
+//    re-checks the queued pairs chip-wide; waves past the list end only
+//    copy.
 #include <limits.h>
 
 #include "lc_common.hpp"
@@ -82,6 +87,14 @@ struct LookupParams {
   // Index written into a hit's key: (emap ? emap[e] : e) + eoff.
   const int64_t* emap;
   int64_t eoff;
+  // Work-list mode: after its last tile a wave moves its queued re-checks to
+  // this queue (list position, cache row) when it has room; gq_count counts
+  // reserved slots, and a slot a wave reserved but settled itself holds
+  // position -1.  Null: every wave settles its own queue.
+  int64_t* gq_pos;
+  int64_t* gq_e;
+  unsigned long long* gq_count;
+  int64_t gq_cap;
 };
 
 // ------------------------------------------------------------- prep
@@ -341,80 +354,119 @@ struct RecheckQueue {
   int n;       // queued pairs (wave-uniform)
 };
 
-// Up to four queued pairs per pass: lanes 0..3 fetch the pairs' query ids,
-// radii and entry map first, then every lane loads its features of all four
-// rows before the sums (each pair keeps the lane-strided order of
-// wave_dist2, so results equal the immediate path's bit for bit).
+// Re-check of up to four pairs per pass: lane j < 4 brings pair j (valid,
+// list position, cache row), fetches its query id, radius and key first,
+// then every lane loads its features of all four rows before the sums (each
+// pair keeps the lane-strided order of wave_dist2, so results equal the
+// immediate path's bit for bit).  All 64 lanes call it; it returns the
+// number of pairs re-checked (the caller adds it to the counter once, since
+// thousands of waves settling at the same time would serialise on it).
 template <int SRC>
-__device__ __noinline__ void settle_queue(const RecheckArgs p, const int32_t* rq_q, const int64_t* rq_e, int n,
-                                          int64_t qwave) {
+__device__ __forceinline__ int settle_four(const RecheckArgs& p, bool valid, int64_t qpos, int64_t e) {
   constexpr int P = 4;
   const int lane = lane_id();
-  for (int b = 0; b < n; b += P) {
-    // lane j < P: pair b + j
-    int64_t mq = -1, me = 0, mk = 0;
-    float mr = 0.0f;
-    if (lane < P && b + lane < n) {
-      const int64_t qpos = qwave + rq_q[b + lane];
-      const int64_t e = rq_e[b + lane];
-      if (qpos < p.qend && e < p.n) {
-        mq = query_at(p.qlist, qpos);
-        me = e;
-        mr = p.cr[e];
-        mk = (p.emap ? p.emap[e] : e) + p.eoff;
-      }
-    }
-    int64_t q[P], e[P];
-    bool v[P];
+  int64_t mq = -1, me = 0, mk = 0;
+  float mr = 0.0f;
+  if (lane < P && valid && qpos < p.qend && e < p.n) {
+    mq = query_at(p.qlist, qpos);
+    me = e;
+    mr = p.cr[e];
+    mk = (p.emap ? p.emap[e] : e) + p.eoff;
+  }
+  int64_t q[P], ee[P];
+  bool v[P];
 #pragma unroll
-    for (int j = 0; j < P; ++j) {
-      const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(mq)), j);
-      const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(mq >> 32)), j);
-      const int64_t qj = static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
-      const uint32_t elo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(me)), j);
-      const uint32_t ehi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(me >> 32)), j);
-      v[j] = qj >= 0;
-      q[j] = v[j] ? qj : 0;
-      e[j] = static_cast<int64_t>((static_cast<uint64_t>(ehi) << 32) | elo);
-    }
-    double acc[P];
+  for (int j = 0; j < P; ++j) {
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(mq)), j);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(mq >> 32)), j);
+    const int64_t qj = static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+    const uint32_t elo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(me)), j);
+    const uint32_t ehi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(me >> 32)), j);
+    v[j] = qj >= 0;
+    q[j] = v[j] ? qj : 0;
+    ee[j] = static_cast<int64_t>((static_cast<uint64_t>(ehi) << 32) | elo);
+  }
+  double acc[P];
 #pragma unroll
-    for (int j = 0; j < P; ++j) acc[j] = 0.0;
+  for (int j = 0; j < P; ++j) acc[j] = 0.0;
 #pragma unroll 4
-    for (int k = lane; k < p.d; k += kWave) {
-      float qa[P];
-      double za[P];
+  for (int k = lane; k < p.d; k += kWave) {
+    float qa[P];
+    double za[P];
 #pragma unroll
-      for (int j = 0; j < P; ++j) {
-        qa[j] = p.zq[q[j] * p.d + k];
-        za[j] = cache_value<SRC>(p.cz, e[j], p.d, k);
-      }
-#pragma unroll
-      for (int j = 0; j < P; ++j) {
-        const double diff = static_cast<double>(qa[j]) - za[j];
-        acc[j] = __builtin_fma(diff, diff, acc[j]);
-      }
+    for (int j = 0; j < P; ++j) {
+      qa[j] = p.zq[q[j] * p.d + k];
+      za[j] = cache_value<SRC>(p.cz, ee[j], p.d, k);
     }
 #pragma unroll
     for (int j = 0; j < P; ++j) {
-      const double d2 = wave_sum(acc[j]);
-      if (lane == j && v[j]) {
-        // record_pair with the radius and key fetched above
-        atomicAdd(&p.stats[LIPCACHE_STAT_RECHECKED], 1ull);
-        const double r = static_cast<double>(mr);
-        if (__builtin_fabs(__builtin_sqrt(d2) - r) <= 1e-5 * r) {
-          atomicAdd(&p.stats[LIPCACHE_STAT_BAND_PAIRS], 1ull);
-          atomicOr(&p.bflag[mq], 1u);
-        }
-        if (d2 < r * r) {
-          const float d2f = static_cast<float>(d2);
-          const unsigned long long key = (static_cast<unsigned long long>(__builtin_bit_cast(uint32_t, d2f)) << 32) |
-                                         static_cast<unsigned long long>(static_cast<uint32_t>(mk));
-          atomicMin(&p.best[mq], key);
-        }
+      const double diff = static_cast<double>(qa[j]) - za[j];
+      acc[j] = __builtin_fma(diff, diff, acc[j]);
+    }
+  }
+  int done = 0;
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    done += v[j] ? 1 : 0;
+    const double d2 = wave_sum(acc[j]);
+    if (lane == j && v[j]) {
+      // record_pair with the radius and key fetched above (the re-check
+      // count is the caller's)
+      const double r = static_cast<double>(mr);
+      if (__builtin_fabs(__builtin_sqrt(d2) - r) <= 1e-5 * r) {
+        atomicAdd(&p.stats[LIPCACHE_STAT_BAND_PAIRS], 1ull);
+        atomicOr(&p.bflag[mq], 1u);
+      }
+      if (d2 < r * r) {
+        const float d2f = static_cast<float>(d2);
+        const unsigned long long key = (static_cast<unsigned long long>(__builtin_bit_cast(uint32_t, d2f)) << 32) |
+                                       static_cast<unsigned long long>(static_cast<uint32_t>(mk));
+        atomicMin(&p.best[mq], key);
       }
     }
   }
+  return done;
+}
+
+template <int SRC>
+__device__ __noinline__ void settle_queue(const RecheckArgs p, const int32_t* rq_q, const int64_t* rq_e, int n,
+                                          int64_t qwave) {
+  const int lane = lane_id();
+  int done = 0;
+  for (int b = 0; b < n; b += 4) {
+    const bool mine = lane < 4 && b + lane < n;
+    done += settle_four<SRC>(p, mine, mine ? qwave + rq_q[b + lane] : 0, mine ? rq_e[b + lane] : 0);
+  }
+  if (lane == 0 && done) atomicAdd(&p.stats[LIPCACHE_STAT_RECHECKED], static_cast<unsigned long long>(done));
+}
+
+// The global re-check queue of a work-list scan: wave w of the grid takes
+// four pairs at a time, w * 4 + i * (4 * waves).  Every wave's loop bound is
+// the same, so the grid drains.
+template <int SRC>
+__global__ __launch_bounds__(256) void recheck_queue_kernel(const RecheckArgs p, const int64_t* __restrict__ gpos,
+                                                            const int64_t* __restrict__ ge,
+                                                            const unsigned long long* __restrict__ gcount,
+                                                            int64_t cap) {
+  __shared__ unsigned int block_done;
+  const int lane = lane_id();
+  if (threadIdx.x == 0) block_done = 0u;
+  __syncthreads();
+  const int64_t reserved = static_cast<int64_t>(*gcount);
+  const int64_t total = reserved < cap ? reserved : cap;
+  const int64_t waves = static_cast<int64_t>(gridDim.x) * (blockDim.x / kWave);
+  const int64_t w = static_cast<int64_t>(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
+  int done = 0;
+  for (int64_t b = w * 4; b < total; b += waves * 4) {
+    const int64_t i = b + lane;
+    const bool mine = lane < 4 && i < total;
+    const int64_t pos = mine ? gpos[i] : -1;
+    done += settle_four<SRC>(p, mine && pos >= 0, pos, mine ? ge[i] : 0);
+  }
+  if (lane == 0 && done) atomicAdd(&block_done, static_cast<unsigned int>(done));
+  __syncthreads();
+  if (threadIdx.x == 0 && block_done)
+    atomicAdd(&p.stats[LIPCACHE_STAT_RECHECKED], static_cast<unsigned long long>(block_done));
 }
 
 // Queues the pairs of `mask` (same bit layout as recheck_pairs: lane (m16, g)
@@ -446,13 +498,35 @@ __device__ __forceinline__ void queue_pairs(const RecheckArgs& p, RecheckQueue& 
   }
 }
 
-// Settles the queue after the wave's last tile; the queue was written by
-// other lanes of this wave.
+// After the wave's last tile: move the queue to the global queue when it has
+// room (one 64-bit atomic reserves the slots), else settle it here.  The
+// queue was written by other lanes of this wave.
 template <int SRC>
-__device__ __forceinline__ void flush_queue(const RecheckArgs& p, RecheckQueue& rq, int64_t qwave) {
+__device__ __forceinline__ void flush_queue(const LookupParams& lp, const RecheckArgs& p, RecheckQueue& rq,
+                                            int64_t qwave) {
   if (rq.n == 0) return;
   __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
   __builtin_amdgcn_wave_barrier();
+  const int lane = lane_id();
+  if (lp.gq_pos) {
+    unsigned long long base = 0;
+    if (lane == 0) base = atomicAdd(lp.gq_count, static_cast<unsigned long long>(rq.n));
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(base)), 0);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(base >> 32)), 0);
+    const uint64_t b0 = (static_cast<uint64_t>(hi) << 32) | lo;
+    const uint64_t cap = static_cast<uint64_t>(lp.gq_cap);
+    if (b0 + static_cast<uint64_t>(rq.n) <= cap) {
+      for (int i = lane; i < rq.n; i += kWave) {
+        lp.gq_pos[b0 + i] = qwave + rq.q[i];
+        lp.gq_e[b0 + i] = rq.e[i];
+      }
+      rq.n = 0;
+      return;
+    }
+    // no room: mark the reserved slots that exist, settle here
+    for (int i = lane; i < rq.n; i += kWave)
+      if (b0 + i < cap) lp.gq_pos[b0 + i] = -1;
+  }
   settle_queue<SRC>(p, rq.q, rq.e, rq.n, qwave);
   rq.n = 0;
 }
@@ -963,7 +1037,7 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
     if (!more2) break;
   }
   if constexpr (LIST) {
-    if (active) flush_queue<STORE>(recheck_args(p, qend, qlist), rq, qwave);
+    if (active) flush_queue<STORE>(p, recheck_args(p, qend, qlist), rq, qwave);
   }
 }
 
@@ -1129,12 +1203,22 @@ lipcache_status lookup_stage_prep(const float* zq, int64_t B, int d, const Filte
 // n_items (query positions, row range) items whose positions index qlist.
 // Hits are keyed by (emap ? emap[e] : e) + eoff.  athr needs
 // athr_len(view->n) floats.
+// The global re-check queue of a work-list scan (workspace memory).
+struct GlobalRecheckWs {
+  int64_t* pos;
+  int64_t* e;
+  unsigned long long* count;
+  int64_t cap;
+};
+
+__global__ void zero_u64_kernel(unsigned long long* __restrict__ p) { *p = 0ull; }
+
 lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision, const FilterConsts& fc,
                                   const float* zq, int64_t B, const float* qthr, unsigned long long* best,
                                   unsigned int* bflag, unsigned long long* stats, float* athr,
                                   const int64_t* items, int64_t n_items, const int32_t* qlist, const uint16_t* zq16,
                                   const int64_t* emap, int64_t eoff, bool dump, float* g_hat, uint8_t* cand,
-                                  hipStream_t s) {
+                                  hipStream_t s, const GlobalRecheckWs* gq = nullptr) {
   if (B <= 0 || view->n <= 0) return LIPCACHE_OK;
   if (items && n_items <= 0) return LIPCACHE_OK;
   const int64_t n_pad = athr_len(view->n);
@@ -1165,6 +1249,15 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
   p.zq16 = zq16;
   p.emap = emap;
   p.eoff = eoff;
+  const bool queued = items && gq && gq->pos && !dump;
+  p.gq_pos = queued ? gq->pos : nullptr;
+  p.gq_e = queued ? gq->e : nullptr;
+  p.gq_count = queued ? gq->count : nullptr;
+  p.gq_cap = queued ? gq->cap : 0;
+  if (queued) {
+    hipLaunchKernelGGL(zero_u64_kernel, dim3(1), dim3(1), 0, s, gq->count);
+    LC_LAUNCHED();
+  }
   int64_t grid = n_items;
   p.slice_len = 0;
   if (!items) {
@@ -1185,7 +1278,23 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
   const hipError_t e = dump    ? launch_lookup<kVarDump>(precision, view->store_dtype, pl, p, gu, s)
                        : items ? launch_lookup<kVarList>(precision, view->store_dtype, pl, p, gu, s)
                                : launch_lookup<kVarLookup>(precision, view->store_dtype, pl, p, gu, s);
-  return e == hipSuccess ? LIPCACHE_OK : LIPCACHE_EHIP;
+  if (e != hipSuccess) return LIPCACHE_EHIP;
+  if (queued) {
+    // the pairs the scan's waves handed off, one chip-wide pass
+    const RecheckArgs ra{zq, view->z, view->r, best, bflag, stats, static_cast<int64_t>(LLONG_MAX), view->n, view->d,
+                         emap, eoff, qlist};
+    int64_t blocks = (gq->cap + 15) / 16;
+    if (blocks > 256) blocks = 256;
+    if (view->store_dtype == LIPCACHE_BF16) {
+      hipLaunchKernelGGL(recheck_queue_kernel<LIPCACHE_BF16>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
+                         ra, gq->pos, gq->e, gq->count, gq->cap);
+    } else {
+      hipLaunchKernelGGL(recheck_queue_kernel<LIPCACHE_F32>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
+                         ra, gq->pos, gq->e, gq->count, gq->cap);
+    }
+    LC_LAUNCHED();
+  }
+  return LIPCACHE_OK;
 }
 
 // Stage 3: per query, label / index / d^2 / band flag, and the hit and band
@@ -1233,13 +1342,31 @@ lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, 
 // The work-list capacity is sized for the smallest query block of any plan.
 // with_q16: include the bf16 copy of the queries (at the returned offset of
 // the layout without it).
-inline size_t indexed_ws_layout(int64_t B, int64_t n, int d, int K, int64_t n_indexed, Workspace* w,
-                                IndexPlanWs* pw, void* base, bool with_q16 = true) {
+// Past the lookup and plan workspaces: the bf16 query copy, then the global
+// re-check queue of the work-list scan (count, positions, rows; 2 B + 65536
+// pairs, more go through the scan's own settle path).
+struct IndexedTail {
+  size_t q16, gq_count, gq_pos, gq_e, total;
+  int64_t gq_cap;
+};
+
+inline IndexedTail indexed_ws_layout(int64_t B, int64_t n, int d, int K, int64_t n_indexed, Workspace* w,
+                                     IndexPlanWs* pw, void* base) {
   const int64_t tail = n - n_indexed;
   const size_t lk = ws_layout(B, n_indexed > tail ? n_indexed : tail, w, base);
   char* pb = base ? static_cast<char*>(base) + lk : nullptr;
-  const size_t plan = lk + index_plan_layout(B, d, K, n_indexed, kLkWaves * 16, pw, pb);
-  return with_q16 ? plan + align_up(static_cast<size_t>(B) * d * 2, 256) : plan;
+  IndexedTail t;
+  t.q16 = lk + index_plan_layout(B, d, K, n_indexed, kLkWaves * 16, pw, pb);
+  size_t off = t.q16 + align_up(static_cast<size_t>(B) * d * 2, 256);
+  t.gq_cap = 2 * B + 65536;
+  t.gq_count = off;
+  off = align_up(off + 8, 256);
+  t.gq_pos = off;
+  off = align_up(off + static_cast<size_t>(t.gq_cap) * 8, 256);
+  t.gq_e = off;
+  off = align_up(off + static_cast<size_t>(t.gq_cap) * 8, 256);
+  t.total = off;
+  return t;
 }
 
 lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index* idx, const float* zq, int64_t B,
@@ -1263,11 +1390,14 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
   FilterConsts fc;
   const lipcache_status cs = lookup_consts(c, precision, fc);
   if (cs != LIPCACHE_OK) return cs;
-  const size_t need = indexed_ws_layout(B, c->n, c->d, idx->K, idx->n_indexed, nullptr, nullptr, nullptr);
+  const size_t need = indexed_ws_layout(B, c->n, c->d, idx->K, idx->n_indexed, nullptr, nullptr, nullptr).total;
   if (!ws || ws_bytes < need || !aligned256(ws)) return LIPCACHE_EWORKSPACE;
   Workspace w;
   IndexPlanWs pw;
-  indexed_ws_layout(B, c->n, c->d, idx->K, idx->n_indexed, &w, &pw, ws);
+  const IndexedTail tl = indexed_ws_layout(B, c->n, c->d, idx->K, idx->n_indexed, &w, &pw, ws);
+  char* wsb = static_cast<char*>(ws);
+  const GlobalRecheckWs gq{reinterpret_cast<int64_t*>(wsb + tl.gq_pos), reinterpret_cast<int64_t*>(wsb + tl.gq_e),
+                           reinterpret_cast<unsigned long long*>(wsb + tl.gq_count), tl.gq_cap};
   unsigned long long* st = stats ? reinterpret_cast<unsigned long long*>(stats) : w.stats;
   if (B == 0) {
     lipcache_status r = lookup_stage_prep(zq, 0, c->d, fc, w.qthr, w.best, w.bflag, st, s);
@@ -1281,14 +1411,13 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
   if (r != LIPCACHE_OK) return r;
   uint16_t* zq16 = nullptr;
   if (precision == LIPCACHE_BF16) {
-    zq16 = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + indexed_ws_layout(B, c->n, c->d, idx->K, idx->n_indexed,
-                                                                                   nullptr, nullptr, nullptr, false));
+    zq16 = reinterpret_cast<uint16_t*>(wsb + tl.q16);
     const int64_t nq = B * c->d;
     hipLaunchKernelGGL(query_bf16_kernel, dim3(static_cast<unsigned>((nq + 255) / 256)), dim3(256), 0, s, zq, nq, zq16);
     LC_LAUNCHED();
   }
   r = lookup_stage_scan(&so, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, pw.items, n_items, pw.qlist,
-                        zq16, idx->perm, 0, false, nullptr, nullptr, s);
+                        zq16, idx->perm, 0, false, nullptr, nullptr, s, &gq);
   if (r != LIPCACHE_OK) return r;
   const int64_t tail = c->n - idx->n_indexed;
   if (tail > 0) {
@@ -1318,7 +1447,7 @@ using namespace lc;
 extern "C" size_t lipcache_lookup_indexed_workspace_bytes(int64_t B, int64_t n, int32_t d, int32_t K,
                                                           int64_t n_indexed) {
   if (B < 0 || n < 1 || d < 1 || K < 1 || n_indexed < 1 || n_indexed > n) return 0;
-  return indexed_ws_layout(B, n, d, K, n_indexed, nullptr, nullptr, nullptr);
+  return indexed_ws_layout(B, n, d, K, n_indexed, nullptr, nullptr, nullptr).total;
 }
 
 extern "C" lipcache_status lipcache_lookup_indexed(const lipcache_cache* c, const lipcache_index* idx,

@@ -178,6 +178,148 @@ __global__ __launch_bounds__(256) void centre_mfma_kernel(const void* __restrict
   }
 }
 
+// Nearest centre of each row for the build, on the bf16 matrix cores: x.mu_c
+// by v_mfma_f32_16x16x32_bf16 from bf16 rows (the image of a float32 store,
+// or a bf16 store itself) and bf16-rounded centres, then ||mu_c||^2 - 2 x.mu_c
+// in float64; ties go to the lower index.  Any assignment keeps the index
+// exact (R_c is taken from the rows a cluster receives), so the rounding only
+// affects how tight the clusters are.  Rows are j * stride, j < n.
+// Block: 4 waves x 16 rows; a wave keeps its rows' A operands for the whole
+// feature range in registers (KS k-steps of 32, features past d read as 0)
+// and sweeps the centres in chunks staged in LDS (rows padded by 16 bytes so
+// the 16 lanes of one k-chunk read distinct banks).  Lane (m16, g) supplies
+// row m16, features 32 s + 8 g .. + 7 of step s, and holds the products of
+// rows 4 g .. 4 g + 3 with centre m16 of each 16-centre tile.
+template <int KS>
+struct AssignTraits {
+  static constexpr int kChunk = KS <= 8 ? 64 : (KS <= 16 ? 32 : 16);  // centres per LDS chunk
+  static constexpr int kRowBytes = KS * 64 + 16;                       // padded bf16 row
+};
+
+__device__ __forceinline__ u32x4 load16_or_zero(const uint16_t* base, bool ok) {
+  return ok ? *reinterpret_cast<const u32x4*>(base) : u32x4{0u, 0u, 0u, 0u};
+}
+
+template <int KS>
+__global__ __launch_bounds__(256) void assign_bf16_kernel(const uint16_t* __restrict__ rows, int64_t n,
+                                                          int64_t stride, int d,
+                                                          const uint16_t* __restrict__ centres16,
+                                                          const double* __restrict__ cnorm, int K,
+                                                          uint32_t* __restrict__ nearest) {
+  using T = AssignTraits<KS>;
+  constexpr int kTiles = T::kChunk / 16;
+  __shared__ __attribute__((aligned(16))) unsigned char cs[T::kChunk * T::kRowBytes];
+  const int t = static_cast<int>(threadIdx.x);
+  const int lane = lane_id(), w = t / kWave;
+  const int m16 = lane & 15, g = lane >> 4;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kCr;
+  // this lane's row of the wave's 16 (clamped; rows past n are never written)
+  int64_t ra = r0 + w * 16 + m16;
+  ra = ra < n ? ra : n - 1;
+  const uint16_t* arow = rows + ra * stride * d;
+  u32x4 a[KS];
+#pragma unroll
+  for (int st = 0; st < KS; ++st) {
+    const int k0 = 32 * st + 8 * g;
+    a[st] = load16_or_zero(arow + k0, k0 < d);
+  }
+  double bs[4];
+  int bi[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    bs[v] = __builtin_inf();
+    bi[v] = INT_MAX;
+  }
+  constexpr int kChunksPerRow = 4 * KS;  // 16-byte chunks of a row (without the padding)
+  for (int c0 = 0; c0 < K; c0 += T::kChunk) {
+    __syncthreads();
+    for (int e = t; e < T::kChunk * kChunksPerRow; e += 256) {
+      const int cr = e / kChunksPerRow, q = e % kChunksPerRow;
+      const int c = c0 + cr, k0 = 8 * q;
+      const u32x4 v = load16_or_zero(centres16 + static_cast<int64_t>(c < K ? c : 0) * d + k0, c < K && k0 < d);
+      *reinterpret_cast<u32x4*>(cs + cr * T::kRowBytes + q * 16) = v;
+    }
+    __syncthreads();
+    f32x4 acc[kTiles];
+#pragma unroll
+    for (int j = 0; j < kTiles; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < KS; ++st) {
+#pragma unroll
+      for (int j = 0; j < kTiles; ++j) {
+        const u32x4 b = *reinterpret_cast<const u32x4*>(cs + (16 * j + m16) * T::kRowBytes + (4 * st + g) * 16);
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[st]),
+                                                         __builtin_bit_cast(bf16x8, b), acc[j], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kTiles; ++j) {
+      const int c = c0 + 16 * j + m16;
+      if (c >= K) continue;
+      const double cn = cnorm[c];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const double score = cn - 2.0 * static_cast<double>(acc[j][v]);
+        if (score < bs[v] || (score == bs[v] && c < bi[v])) {
+          bs[v] = score;
+          bi[v] = c;
+        }
+      }
+    }
+  }
+  // least score over the 16 lanes that share g (same rows)
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) {
+      const double os = __shfl_xor(bs[v], off, kWave);
+      const int oi = __shfl_xor(bi[v], off, kWave);
+      if (os < bs[v] || (os == bs[v] && oi < bi[v])) {
+        bs[v] = os;
+        bi[v] = oi;
+      }
+    }
+    const int64_t row = r0 + w * 16 + 4 * g + v;
+    if (m16 == 0 && row < n) nearest[row] = bi[v] == INT_MAX ? 0u : static_cast<uint32_t>(bi[v]);
+  }
+}
+
+// bf16 (round to nearest even) copy of the float32 centres.
+__global__ void centre_bf16_kernel(const float* __restrict__ c, int64_t n, uint16_t* __restrict__ out) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) out[i] = bf16_bits(c[i]);
+}
+
+// Assignment of rows j * stride (j < n) for the build: the bf16 kernel when
+// bf16 rows exist, else the float32 one.
+inline void launch_assign(const lipcache_cache* c, int64_t n, int64_t stride, int d, const float* centres,
+                          uint16_t* centres16, const double* cnorm, int K, uint32_t* nearest, hipStream_t s) {
+  const uint16_t* rows16 = c->store_dtype == LIPCACHE_BF16 ? static_cast<const uint16_t*>(c->z)
+                                                           : static_cast<const uint16_t*>(c->zimg);
+  const unsigned grid = static_cast<unsigned>((n + kCr - 1) / kCr);
+  if (!rows16) {
+    hipLaunchKernelGGL(centre_mfma_kernel, dim3(grid), dim3(256), 0, s, c->z, c->store_dtype, n, stride, d, centres,
+                       cnorm, K, nullptr, nullptr, 0.0, nullptr, nearest);
+    return;
+  }
+  const int64_t kd = static_cast<int64_t>(K) * d;
+  hipLaunchKernelGGL(centre_bf16_kernel, dim3(static_cast<unsigned>((kd + 255) / 256)), dim3(256), 0, s, centres, kd,
+                     centres16);
+  int ks = 1;
+  while (ks * 32 < d) ks *= 2;
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, rows16, n, stride, d, centres16, cnorm, K, nearest);
+  };
+  switch (ks) {
+    case 1: go(assign_bf16_kernel<1>); break;
+    case 2: go(assign_bf16_kernel<2>); break;
+    case 4: go(assign_bf16_kernel<4>); break;
+    case 8: go(assign_bf16_kernel<8>); break;
+    case 16: go(assign_bf16_kernel<16>); break;
+    default: go(assign_bf16_kernel<32>); break;
+  }
+}
+
 __global__ void fill_u32_kernel(uint32_t* __restrict__ p, int64_t n) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i < n) p[i] = 0u;
@@ -471,6 +613,7 @@ struct BuildWs {
   uint32_t* assign;
   uint32_t* cnt;
   int64_t* coff;
+  uint16_t* c16;  // bf16 copy of the centres (bf16 assignment)
   unsigned long long* rbits;
   double* cnorm;
   uint32_t* keys[2];
@@ -492,6 +635,7 @@ inline BuildWs build_layout(int64_t n, int d, int K, char* base) {
   w.assign = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(n) * 4));
   w.cnt = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(K) * 4));
   w.coff = reinterpret_cast<int64_t*>(take(static_cast<size_t>(K + 1) * 8));
+  w.c16 = reinterpret_cast<uint16_t*>(take(static_cast<size_t>(K) * d * 2));
   w.rbits = reinterpret_cast<unsigned long long*>(take(static_cast<size_t>(K) * 8));
   w.cnorm = reinterpret_cast<double*>(take(static_cast<size_t>(K) * 8));
   for (int s = 0; s < 2; ++s) {
@@ -795,19 +939,16 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
   hipLaunchKernelGGL(centre_init_kernel, dim3(static_cast<unsigned>((kd + 255) / 256)), dim3(256), 0, s, c->z,
                      c->store_dtype, n, d, K, idx->centers);
   LC_LAUNCHED();
-  const unsigned gq = static_cast<unsigned>((n + kCr - 1) / kCr);
   const unsigned gk = static_cast<unsigned>((K + 3) / 4);
   // The iterations see every stride-th row (about kSampleRows per cluster);
   // the final assignment sees every row.
   const int64_t stride = n / (static_cast<int64_t>(K) * kSampleRows) > 1 ? n / (static_cast<int64_t>(K) * kSampleRows) : 1;
   const int64_t ns = (n + stride - 1) / stride;
-  const unsigned gs = static_cast<unsigned>((ns + kCr - 1) / kCr);
   for (int it = 0; it < iters; ++it) {
     hipLaunchKernelGGL(row_norm_kernel, dim3(gk), dim3(256), 0, s, idx->centers, LIPCACHE_F32,
                        static_cast<int64_t>(K), d, w.cnorm);
     LC_LAUNCHED();
-    hipLaunchKernelGGL(centre_mfma_kernel, dim3(gs), dim3(256), 0, s, c->z, c->store_dtype, ns, stride, d,
-                       idx->centers, w.cnorm, K, nullptr, nullptr, 0.0, nullptr, w.assign);
+    launch_assign(c, ns, stride, d, idx->centers, w.c16, w.cnorm, K, w.assign, s);
     LC_LAUNCHED();
     // the sample in cluster order, then one workgroup per cluster
     hipLaunchKernelGGL(row_keys_kernel, dim3(static_cast<unsigned>((ns + 255) / 256)), dim3(256), 0, s, w.assign,
@@ -835,8 +976,7 @@ extern "C" lipcache_status lipcache_index_build(const lipcache_cache* c, int32_t
   hipLaunchKernelGGL(row_norm_kernel, dim3(gk), dim3(256), 0, s, idx->centers, LIPCACHE_F32, static_cast<int64_t>(K),
                      d, w.cnorm);
   LC_LAUNCHED();
-  hipLaunchKernelGGL(centre_mfma_kernel, dim3(gq), dim3(256), 0, s, c->z, c->store_dtype, n, static_cast<int64_t>(1),
-                     d, idx->centers, w.cnorm, K, nullptr, nullptr, 0.0, nullptr, w.assign);
+  launch_assign(c, n, 1, d, idx->centers, w.c16, w.cnorm, K, w.assign, s);
   LC_LAUNCHED();
   hipLaunchKernelGGL(row_keys_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, s, w.assign, n,
                      w.keys[0], w.vals[0]);

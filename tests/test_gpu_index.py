@@ -123,6 +123,31 @@ def test_build_is_deterministic(tiny, K, iters):
     check_index(c, a, f"determinism K={K}")
 
 
+@pytest.mark.parametrize("store,image", [("f32", True), ("bf16", True), ("f32", False)])
+def test_build_assigns_nearest_centres(tiny, store, image):
+    """The final assignment puts every row in a cluster whose centre is the
+    nearest one up to the rounding of the matrix-core distances: bf16 rows and
+    centres (an f32 store with its image, a bf16 store) give
+    d^2(assigned) <= d^2(nearest) + 2^-6 (||x||^2 + max ||mu||^2); float32 (an
+    f32 store without image) 2^-14 of the same."""
+    wl, st, zq, ref = tiny[store]
+    say("index assignment", store, "image", image)
+    c = build_cache(st, image=image)
+    ix = c.build_index(16, 2)
+    perm, off = host(ix.perm), host(ix.offsets)
+    assign = np.empty(c.n, dtype=np.int64)
+    for cl in range(ix.K):
+        assign[perm[off[cl]:off[cl + 1]]] = cl
+    x = host(c.z[:c.n].float()).astype(np.float64)
+    mu = host(ix.centers).astype(np.float64)
+    d2 = ((x[:, None, :] - mu[None, :, :]) ** 2).sum(-1)
+    gap = d2[np.arange(c.n), assign] - d2.min(axis=1)
+    scale = (x ** 2).sum(1) + (mu ** 2).sum(1).max()
+    rel = 2.0 ** -6 if image or store == "bf16" else 2.0 ** -14
+    assert np.all(gap <= rel * scale), float((gap / scale).max())
+    say("assignment gap / scale max", float((gap / scale).max()), "rows not at the nearest", int(np.sum(gap > 0)))
+
+
 def test_rows_appended_after_build(tiny):
     wl, st, zq, ref = tiny["f32"]
     say("index appended rows")

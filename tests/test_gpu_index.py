@@ -67,6 +67,8 @@ def same_as_dense(res_i, res_d, what):
     si, sd = host(res_i.stats), host(res_d.stats)
     for k in (0, 2, 3):
         assert si[k] == sd[k], f"{what}: stats[{k}] {si} vs {sd}"
+    # the indexed scan filters a subset of the dense scan's pairs with the same arithmetic
+    assert si[1] <= sd[1], f"{what}: re-checked {si[1]} > dense {sd[1]}"
 
 
 @pytest.fixture(scope="module")
@@ -146,6 +148,40 @@ def test_build_assigns_nearest_centres(tiny, store, image):
     rel = 2.0 ** -6 if image or store == "bf16" else 2.0 ** -14
     assert np.all(gap <= rel * scale), float((gap / scale).max())
     say("assignment gap / scale max", float((gap / scale).max()), "rows not at the nearest", int(np.sum(gap > 0)))
+
+
+def test_every_pair_rechecked_once_when_queues_fill():
+    """Every radius huge, so every pair is a hit and every cluster a
+    candidate: the indexed scan covers exactly the dense scan's pairs with the
+    same filter arithmetic, so both re-check the same number of pairs.  With
+    256 clusters of about 64 rows and 512 queries, each of the 2,048 waves of
+    the scan meets 4,096 passing pairs: its LDS queue fills (the rest are
+    re-checked at once) and the global queue (2 B + 65,536 slots) overflows
+    (the late waves settle their own queues) -- no pair may be lost or
+    counted twice on any of these paths."""
+    cfg = wlmod.WorkloadConfig("allhit-d64", d=64, C=10, n_cache=16384, batch=512, sigma=0.5)
+    wl = wlmod.make_workload(cfg, seed=5)
+    sig = oracle.spectral_norm(wl.W).sigma
+    cert = oracle.certify(wl.z, wl.W, wl.b, sig)
+    r = np.full(cert.r.shape, 1000.0, dtype=np.float32)
+    st = oracle_cache(wl.z, cert.label, r, cfg.d)
+    draws = wlmod.draw_queries(wl, 0, batch=cfg.batch)
+    idx = wlmod.near_indices(draws, st.n)
+    # queries near the data (composed with the certified radii), so every
+    # cluster is a candidate of every query
+    zq = wlmod.compose_queries(draws, st.z[idx], cert.r[idx])
+    say("index all-hit queues")
+    c = build_cache(st)
+    ix = c.build_index(256, 2)
+    check_index(c, ix, "all-hit")
+    q = gpu(zq)
+    res_i, pairs = c.lookup_indexed(ix, q)
+    res_d = c.lookup(q)
+    same_as_dense(res_i, res_d, "all-hit")
+    si, sd = host(res_i.stats), host(res_d.stats)
+    assert pairs == zq.shape[0] * st.n
+    assert si[1] == sd[1] == zq.shape[0] * st.n, (si, sd)
+    compare_lookup(res_i, oracle.lookup_blocked(zq, st.z, st.r, st.label), "all-hit")
 
 
 def test_rows_appended_after_build(tiny):

@@ -198,6 +198,91 @@ def test_lookup_indexed_validation():
     assert lib.lipcache_lookup_indexed_workspace_bytes(32768, 1 << 20, 256, 1024, 1 << 20) >= 32768 * 1024 // 8
 
 
+
+def test_construct_validation():
+    lib = L.load()
+
+    def call(c, N=4, strategy=L.SELECT_RADIUS_DEDUP, budget=8, per_class=0, n_classes=0, z=FAKE, lab=FAKE,
+             r=FAKE, prio=None, ws=FAKE, wsb=None):
+        if wsb is None:
+            wsb = lib.lipcache_construct_workspace_bytes(ctypes.byref(c), max(N, 0), n_classes, budget) if c else 0
+        appended = ctypes.c_int64(-5)
+        st = lib.lipcache_construct(ctypes.byref(c) if c is not None else None, z, lab, r, None, prio, N,
+                                    strategy, budget, per_class, n_classes, None, ctypes.byref(appended), ws,
+                                    wsb, None)
+        return st, appended.value
+    assert call(None)[0] == L.EINVAL
+    assert call(_cache(), N=-1)[0] == L.EINVAL
+    assert call(_cache(), N=1 << 31)[0] == L.EUNSUPPORTED      # candidate indices are 32-bit
+    assert call(_cache(d=48))[0] == L.EINVAL
+    assert call(_cache(store_dtype=3))[0] == L.EINVAL
+    assert call(_cache(n=17))[0] == L.EINVAL                   # n > capacity
+    assert call(_cache(r=None))[0] == L.EINVAL
+    assert call(_cache(), strategy=7)[0] == L.EINVAL
+    assert call(_cache(), z=None)[0] == L.EINVAL
+    assert call(_cache(), r=None)[0] == L.EINVAL
+    assert call(_cache(), z=ctypes.c_void_p(0x100008))[0] == L.EINVAL  # rows move as 16-byte vectors
+    assert call(_cache(), strategy=L.SELECT_PRIORITY)[0] == L.EINVAL   # priority keys missing
+    assert call(_cache(), per_class=-1)[0] == L.EINVAL
+    assert call(_cache(), per_class=2, n_classes=0)[0] == L.EINVAL
+    assert call(_cache(), per_class=2, n_classes=16385)[0] == L.EINVAL
+    assert call(_cache(n=10), budget=7)[0] == L.ECAPACITY      # only 6 free rows
+    assert call(_cache(), ws=None)[0] == L.EWORKSPACE
+    assert call(_cache(), wsb=64)[0] == L.EWORKSPACE
+    assert call(_cache(), budget=0) == (L.OK, 0)               # nothing to append: no launch
+    assert call(_cache(), N=0) == (L.OK, 0)
+
+
+def test_boundary_radius_validation():
+    lib = L.load()
+
+    def call(c, mode=L.BOUNDARY_SCALED, factor=0.5, n_classes=0, out=FAKE, ws=None, wsb=0):
+        return lib.lipcache_boundary_radius(ctypes.byref(c) if c is not None else None, mode, factor, n_classes,
+                                            out, ws, wsb, None)
+    assert call(None) == L.EINVAL
+    assert call(_cache(n=4), out=None) == L.EINVAL
+    assert call(_cache(n=4, d=48)) == L.EINVAL
+    assert call(_cache(n=4, store_dtype=3)) == L.EINVAL
+    assert call(_cache(n=17)) == L.EINVAL                      # n > capacity
+    assert call(_cache(n=4, label=None)) == L.EINVAL
+    assert call(_cache(n=4), mode=9) == L.EINVAL
+    for bad in (-1.0, float("nan"), float("inf")):
+        assert call(_cache(n=4), factor=bad) == L.EINVAL
+    assert call(_cache(n=4), mode=L.BOUNDARY_INTERCLASS, n_classes=0) == L.EINVAL
+    assert call(_cache(n=4), mode=L.BOUNDARY_INTERCLASS, n_classes=65537) == L.EINVAL
+    assert call(_cache(n=4), mode=L.BOUNDARY_INTERCLASS, n_classes=10) == L.EWORKSPACE
+    need = lib.lipcache_boundary_radius_workspace_bytes(64, 10)
+    assert need >= 10 * 64 * 8
+    assert call(_cache(n=4), mode=L.BOUNDARY_INTERCLASS, n_classes=10, ws=FAKE, wsb=need - 1) == L.EWORKSPACE
+    assert call(_cache(n=0)) == L.OK                           # empty cache: no launch
+    assert call(_cache(n=0), mode=L.BOUNDARY_INTERCLASS, n_classes=10, ws=FAKE, wsb=need) == L.OK
+
+
+def test_consistency_validation():
+    lib = L.load()
+    assert lib.lipcache_consistency(FAKE, FAKE, -1, FAKE, None) == L.EINVAL
+    assert lib.lipcache_consistency(FAKE, FAKE, 8, None, None) == L.EINVAL
+    assert lib.lipcache_consistency(None, FAKE, 8, FAKE, None) == L.EINVAL
+    assert lib.lipcache_consistency(FAKE, None, 8, FAKE, None) == L.EINVAL
+
+
+def test_filter_dump_validation():
+    lib = L.load()
+
+    def call(c, B=8, prec=L.BF16, g=FAKE, cand=FAKE, ws=FAKE, wsb=1 << 30):
+        return lib.lipcache_lookup_filter_dump(ctypes.byref(c) if c is not None else None, FAKE, B, prec, g, cand,
+                                               ws, wsb, None)
+    assert call(None) == L.EINVAL
+    assert call(_cache(n=4, d=48)) == L.EINVAL
+    assert call(_cache(n=4), B=-1) == L.EINVAL
+    assert call(_cache(n=4), prec=5) == L.EINVAL
+    assert call(_cache(n=4), g=None) == L.EINVAL
+    assert call(_cache(n=4), cand=None) == L.EINVAL
+    big = _cache(n=1 << 20, capacity=1 << 20)
+    assert call(big, B=128) == L.EINVAL                        # B * n above 2^26
+    assert call(_cache(n=4), ws=None) == L.EWORKSPACE
+    assert call(_cache(n=4), wsb=64) == L.EWORKSPACE
+
 def test_binding_refuses_without_library(tmp_path):
     saved = L._LIB
     try:

@@ -364,8 +364,11 @@ lipcache_status lipcache_consistency(const int32_t* lookup_label, const int32_t*
 /*
  * Diagnostic view of the lookup's distance filter for small problems.  For
  * every pair (q, i < n) writes the matrix-core dot product g_hat = q . z_i
- * exactly as the lookup kernel computes it, and cand = 1 if the pair passes
- * the filter (and is re-checked by lipcache_lookup), else 0.
+ * as the lookup kernel computes it, and cand = 1 if the pair passes the
+ * filter (and is re-checked by lipcache_lookup), else 0.  Where the bf16
+ * filter starts its accumulators at -Q_q (d <= 128 with a bf16 image or
+ * store), g_hat is that accumulator plus Q_q in float32; cand is always the
+ * kernel's own decision.
  *
  *  g_hat [B][n] float, cand [B][n] uint8 (required); B * n <= 2^26
  *  ws    lipcache_lookup_workspace_bytes(B, n, d, precision) bytes

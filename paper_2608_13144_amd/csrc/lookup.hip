@@ -54,6 +54,15 @@ constexpr int kXcds = 8;
 constexpr unsigned long long kNoHit = ~0ull;
 
 enum { kModeBF16 = 0, kModeF32 = 1 };
+// For d <= 128 the bf16 filter starts each accumulator at -Q_q instead of
+// zero, so the matrix core returns g - Q_q and the filter is one max per
+// accumulator (there the filter's vector work, not the matrix core, is what
+// limits); the extra fp32 rounding is far inside the bf16 slack.  Wider rows
+// keep the subtraction: the extra live registers would spill there.  The
+// fp32 filter, whose slack is tight, always subtracts Q_q after the
+// contraction.
+template <int MODE, int KS>
+constexpr bool kFoldQ = MODE == kModeBF16 && KS <= 4;
 
 struct LookupParams {
   const float* zq;
@@ -836,12 +845,12 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
     f32x4 qt[RT];
     if (prev) {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) qt[rt] = qv[rt];
+      for (int rt = 0; rt < RT; ++rt) qt[rt] = kFoldQ<MODE, KS> ? f32x4{0.f, 0.f, 0.f, 0.f} : qv[rt];
     }
     if (cur) {
       an = athr_buf[sub * kColTile + m16];
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int rt = 0; rt < RT; ++rt) acc[rt] = kFoldQ<MODE, KS> ? qv[rt] : f32x4{0.f, 0.f, 0.f, 0.f};
     }
     float mx = -__builtin_inff();
 #pragma unroll
@@ -865,7 +874,8 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
       }
       if (prev) {
 #pragma unroll
-        for (int e = ks * kPer; e < (ks + 1) * kPer && e < kE; ++e) mx = __builtin_fmaxf(mx, accp[e / 4][e % 4] - qt[e / 4][e % 4]);
+        for (int e = ks * kPer; e < (ks + 1) * kPer && e < kE; ++e)
+          mx = __builtin_fmaxf(mx, kFoldQ<MODE, KS> ? accp[e / 4][e % 4] : accp[e / 4][e % 4] - qt[e / 4][e % 4]);
       }
       // Keep the operand read for k-step ks + 2 in this step: left to
       // itself the scheduler sinks it next to its use and the wave stalls
@@ -912,7 +922,7 @@ __device__ __forceinline__ void compute_tile(const unsigned char* buf, const flo
     const float an = t0 + sub * kColTile + m16 < e_end ? athr_buf[sub * kColTile + m16] : __builtin_inff();
     f32x4 acc[RT];
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int rt = 0; rt < RT; ++rt) acc[rt] = kFoldQ<MODE, KS> ? qv[rt] : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const u32x4 cur = (ks & 1) ? b1 : b0;
@@ -935,10 +945,11 @@ __device__ __forceinline__ void compute_tile(const unsigned char* buf, const flo
       if (sub + 1 < nsub) b0 = lds_operand<KS>(buf, sub + 1, 0, m16, g);
     }
     const int64_t ebase = t0 + sub * kColTile;
-    // Q_q of the four rows 4g..4g+3 of each row tile (this lane's accumulators)
+    // Q_q of the four rows 4g..4g+3 of each row tile (this lane's
+    // accumulators), or zero where the accumulators already hold g - Q_q
     f32x4 qt[RT];
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) qt[rt] = qv[rt];
+    for (int rt = 0; rt < RT; ++rt) qt[rt] = kFoldQ<MODE, KS> ? f32x4{0.f, 0.f, 0.f, 0.f} : qv[rt];
     if constexpr (DUMP) {
       const int64_t e = ebase + m16;
 #pragma unroll
@@ -947,7 +958,7 @@ __device__ __forceinline__ void compute_tile(const unsigned char* buf, const flo
         for (int i = 0; i < 4; ++i) {
           const int64_t q = qwave + rt * 16 + 4 * g + i;
           if (q < p.B && e < e_end) {
-            p.g_hat[q * p.n + e] = acc[rt][i];
+            p.g_hat[q * p.n + e] = kFoldQ<MODE, KS> ? acc[rt][i] - qv[rt][i] : acc[rt][i];
             p.cand[q * p.n + e] = static_cast<uint8_t>((acc[rt][i] - qt[rt][i]) >= an);
           }
         }
@@ -1011,14 +1022,16 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
   RecheckQueue rq{rq_q + (LIST ? wave * kRq : 0), rq_e + (LIST ? wave * kRq : 0), 0};
   // Q_q of this lane's accumulator rows 4g .. 4g + 3 of each row tile, kept
   // in registers for the whole slice (reading them from LDS per column tile
-  // costs a third of the operand traffic); +inf past B.
+  // costs a third of the operand traffic); +inf past B.  Negated where the
+  // accumulators start at -Q_q.
   f32x4 qv[RT];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int64_t q = qwave + rt * 16 + 4 * g + i;
-      qv[rt][i] = q < qend ? p.qthr[query_at(qlist, q)] : __builtin_inff();
+      const float qq = q < qend ? p.qthr[query_at(qlist, q)] : __builtin_inff();
+      qv[rt][i] = kFoldQ<MODE, KS> ? -qq : qq;
     }
   }
 

@@ -353,7 +353,12 @@ def test_filter_sound_and_accurate(tiny, precision, store, image):
     sabs = np.abs(Q) @ np.abs(Z).T
     err = np.abs(g_hat - G)
     kb = kappa_bound(precision, store, 64)
-    assert np.all(err <= kb * sabs + 1e-25), (err / sabs).max()
+    # The bf16 kernel with a bf16 image or store starts its accumulators at
+    # -Q_q (d <= 128): the float32 accumulation then also rounds against
+    # Q_q <= ||q||^2 / 2, and adding Q_q back for the dump rounds once more.
+    folded = precision == "bf16" and (image or store == "bf16")
+    extra = kappa_bound("f32", store, 64) * nq[:, None] / 2 if folded else 0.0
+    assert np.all(err <= kb * sabs + extra + 1e-25), (err / sabs).max()
     # pre-re-check distance relative to ||q||^2 + ||z||^2
     scale = nq[:, None] + nc[None, :]
     rel = 2 * err / scale

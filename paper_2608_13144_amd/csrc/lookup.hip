@@ -10,7 +10,9 @@
 //   pass  <=>  fl(g_hat - Q_q) >= A_i,
 //   Q_q = RD((1 - k) ||q||^2 / 2),  A_i = RD(((1 - k - 4u) ||z_i||^2 - r_i^2) / 2),
 // where k bounds |g_hat - q.z_i| / ((||q||^2 + ||z_i||^2) / 2) (bf16 operand
-// rounding and float32 accumulation, doubled).  Every true hit passes; a pair
+// rounding and float32 accumulation, doubled); for d <= 128 the bf16 filter
+// accumulates onto -Q_q instead (acc >= A_i), which adds one more float32
+// rounding against Q_q, far inside that bound.  Every true hit passes; a pair
 // that passes is re-checked as sum_k (q_k - z_ik)^2 in float64 from the
 // original values, which decides the hit.  Hits are merged per query with a
 // 64-bit atomic minimum of (float bits of d^2) << 32 | i, which orders by
@@ -798,7 +800,8 @@ __device__ __forceinline__ u32x4 lds_operand(const unsigned char* buf, int sub, 
 // the filter.  The cache operands are read from LDS two k-steps ahead of
 // their use (continuing into the next column tile), so LDS latency overlaps
 // the MFMAs.  The filter takes max_j (acc_j - Q_j) over the lane's 16
-// accumulators (maxnum ignores NaN, so a NaN pair never hides another pair)
+// accumulators (max_j acc_j where they started at -Q_j; maxnum ignores NaN,
+// so a NaN pair never hides another pair)
 // and compares once against A_i; the exact per-pair mask is only rebuilt on
 // the rare path.
 // Rare path of one column tile: rebuild the exact per-pair mask and re-check.

@@ -30,7 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # MI355X dense matrix peaks
+PEAK_TFLOPS = {"f16": 2500.0, "f32": 157.3}   # MI355X dense matrix peaks (fp16 = bf16 rate)
 METRIC = "certified lookups/s and query·entry pairs/s at N=1M cache, d=256, C=200"
 
 
@@ -111,6 +111,7 @@ def measured_traffic(workload: str, precision: str):
         return None
     if rec.get("lookup_hip_sha16") != sha:
         return None
+    rec["file"] = os.path.basename(path)
     return rec
 
 
@@ -456,7 +457,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mix-d256-c200")
-    ap.add_argument("--precision", default="bf16", choices=["bf16", "f32"])
+    ap.add_argument("--precision", default="f16", choices=["f16", "f32"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--construct", default="", choices=["", "radius_dedup", "priority", "kcenter"],
@@ -617,7 +618,12 @@ def main() -> int:
         out["roofline"]["traffic"] = tr["traffic_bytes"]
         out["roofline"]["traffic_unit"] = "bytes per launch (FETCH_SIZE x %.4f + WRITE_SIZE x %.4f)" % (
             tr["fetch_scale"], tr["write_scale"])
+        out["roofline"]["traffic_source"] = ("committed counter profile profiles/%s (rocprofv3 --pmc, taken on the "
+                                             "lookup.hip with sha256 prefix %s, which this run also uses); not "
+                                             "measured in this run" % (tr["file"], tr["lookup_hip_sha16"]))
         out["roofline"]["hbm_gbs"] = tr["traffic_bytes"] / (lk * 1e-3) / 1e9
+    else:
+        out["roofline"]["traffic_source"] = "none: no counter profile of the current lookup.hip is committed"
     if args.index_k > 0:
         try:
             out["indexed_lookup"] = indexed_context(cache, zq, res, args)

@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define LIPCACHE_ABI_VERSION 5
+#define LIPCACHE_ABI_VERSION 6
 
 /* Same type as hipStream_t. */
 typedef struct ihipStream_t* lipcache_stream_t;
@@ -52,9 +52,10 @@ typedef enum lipcache_status {
   LIPCACHE_EHIP = 7           /* a HIP runtime call or kernel launch failed            */
 } lipcache_status;
 
-/* Element types: storage of cache features (store_dtype) and the matrix-core
- * precision of the lookup's distance filter (precision). */
-enum { LIPCACHE_F32 = 0, LIPCACHE_BF16 = 1 };
+/* Element types.  Storage of cache features (store_dtype): F32 or BF16.
+ * Matrix-core precision of the lookup's distance filter (precision): F16
+ * (float16 operands, float32 accumulation) or F32. */
+enum { LIPCACHE_F32 = 0, LIPCACHE_BF16 = 1, LIPCACHE_F16 = 2 };
 
 /* Radius modes (policy component rho, Sec. 4.3): the conservative radius of
  * Eq. (21) or the tight per-pair radius of Remark 5.1, Eq. (29). */
@@ -94,11 +95,12 @@ enum {
  */
 typedef struct lipcache_cache {
   void*    z;           /* [capacity][d] features; float (F32) or bf16 bits (BF16)   */
-  void*    zimg;        /* [capacity][d] bf16 image of z for the bf16 distance
-                           filter, or NULL.  Only read for an F32 store; insert
-                           keeps it equal to bf16(z) (round to nearest even). The
-                           bf16 lookup streams it (half the bytes of z); without
-                           it each workgroup converts z on the fly.                   */
+  void*    zimg;        /* [capacity][d] float16 image of the stored features for
+                           the F16 distance filter, or NULL.  Insert keeps it
+                           equal to f16(stored z) (round to nearest even after
+                           clamping to +-65504).  The F16 lookup streams it (half
+                           the bytes of an F32 store); without it each workgroup
+                           converts z on the fly.                                   */
   float*   r;           /* [capacity] certified radius r_i                           */
   int32_t* label;       /* [capacity] payload y~_i                                   */
   float*   norm2;       /* [capacity] ||z_i||^2 of the stored values (derived)       */

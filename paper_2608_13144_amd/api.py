@@ -14,7 +14,7 @@ import torch
 from . import _lib as L
 
 _STORE = {"f32": L.F32, "bf16": L.BF16}
-_PRECISION = {"f32": L.F32, "bf16": L.BF16}
+_PRECISION = {"f32": L.F32, "f16": L.F16}
 _RADIUS = {"conservative": L.RADIUS_CONSERVATIVE, "tight": L.RADIUS_TIGHT}
 _SELECT = {"radius_dedup": L.SELECT_RADIUS_DEDUP, "priority": L.SELECT_PRIORITY, "kcenter": L.SELECT_KCENTER}
 _BOUNDARY = {"scaled": L.BOUNDARY_SCALED, "global": L.BOUNDARY_GLOBAL, "interclass": L.BOUNDARY_INTERCLASS}
@@ -111,16 +111,17 @@ class LipCache:
 
     def __init__(self, d: int, capacity: int, store: str = "f32", device: str | torch.device = "cuda",
                  image: bool = True):
-        """``image``: for an f32 store, also keep the bf16 image that the bf16
-        filter streams (half the bytes of z; costs 2 bytes per element)."""
+        """``image``: also keep the float16 image of the stored features that
+        the f16 filter streams (costs 2 bytes per element; without it the f16
+        lookup converts the rows on the fly)."""
         self.d = int(d)
         self.capacity = int(capacity)
         self.store = store
         self.device = torch.device(device)
         zdt = torch.float32 if store == "f32" else torch.bfloat16
         self.z = torch.empty((self.capacity, self.d), dtype=zdt, device=self.device)
-        self.zimg = (torch.empty((self.capacity, self.d), dtype=torch.bfloat16, device=self.device)
-                     if (image and store == "f32") else None)
+        self.zimg = (torch.empty((self.capacity, self.d), dtype=torch.float16, device=self.device)
+                     if image else None)
         self.r = torch.empty(self.capacity, dtype=torch.float32, device=self.device)
         self.label = torch.empty(self.capacity, dtype=torch.int32, device=self.device)
         self.norm2 = torch.empty(self.capacity, dtype=torch.float32, device=self.device)
@@ -160,7 +161,7 @@ class LipCache:
         self.n = int(cs.n)
         return int(got.value)
 
-    def lookup(self, zq: torch.Tensor, precision: str = "bf16", want_index: bool = True,
+    def lookup(self, zq: torch.Tensor, precision: str = "f16", want_index: bool = True,
                want_dist2: bool = True, want_band: bool = True, out: LookupResult | None = None) -> LookupResult:
         """lipcache_lookup: nearest certified hit per query, or MISS (async)."""
         _need_cuda(zq, "zq", torch.float32, 2)
@@ -185,7 +186,7 @@ class LipCache:
         return out
 
     def serve(self, zq: torch.Tensor, W: torch.Tensor, b: torch.Tensor | None, sigma: float,
-              precision: str = "bf16", out: LookupResult | None = None):
+              precision: str = "f16", out: LookupResult | None = None):
         """One round of certified serving (Alg. 2): look every query up, certify
         every query with the head (the label and radius a miss is cached with;
         for a bfloat16 store the rounded query is certified), and write the
@@ -274,7 +275,7 @@ class LipCache:
         ix._build_ws = ws  # kept alive until the build has run
         return ix
 
-    def lookup_indexed(self, index: "ClusterIndex", zq: torch.Tensor, precision: str = "bf16",
+    def lookup_indexed(self, index: "ClusterIndex", zq: torch.Tensor, precision: str = "f16",
                        out: LookupResult | None = None) -> tuple[LookupResult, int]:
         """lipcache_lookup_indexed: the lookup's outputs through a cluster index
         (sync).  Returns (result, query-entry pairs the filter scanned)."""
@@ -301,7 +302,7 @@ class LipCache:
         L.check("lipcache_lookup_indexed", st)
         return out, int(pairs.value)
 
-    def filter_dump(self, zq: torch.Tensor, precision: str = "bf16"):
+    def filter_dump(self, zq: torch.Tensor, precision: str = "f16"):
         """lipcache_lookup_filter_dump: matrix-core dot products and filter decisions (small sizes)."""
         _need_cuda(zq, "zq", torch.float32, 2)
         lib = L.load()

@@ -687,7 +687,7 @@ struct CWs {
 };
 
 inline size_t sub_ws_bytes(const lipcache_cache* c) {
-  const size_t a = lipcache_lookup_workspace_bytes(kChunk, c->capacity, c->d, LIPCACHE_BF16);
+  const size_t a = lipcache_lookup_workspace_bytes(kChunk, c->capacity, c->d, LIPCACHE_F16);
   const size_t b = lipcache_insert_workspace_bytes(kChunk);
   return a > b ? a : b;
 }
@@ -814,7 +814,7 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
       const int32_t* dup = nullptr;
       if (dedup) {
         if (c->n > 0) {
-          const lipcache_status st = lipcache_lookup(c, w.zc, k, LIPCACHE_BF16, w.dup, nullptr, nullptr, nullptr,
+          const lipcache_status st = lipcache_lookup(c, w.zc, k, LIPCACHE_F16, w.dup, nullptr, nullptr, nullptr,
                                                      nullptr, w.sub_ws, w.sub_bytes, stream);
           if (st != LIPCACHE_OK) return st;
           dup = w.dup;

@@ -178,10 +178,11 @@ __global__ __launch_bounds__(256) void centre_mfma_kernel(const void* __restrict
   }
 }
 
-// Nearest centre of each row for the build, on the bf16 matrix cores: x.mu_c
-// by v_mfma_f32_16x16x32_bf16 from bf16 rows (the image of a float32 store,
-// or a bf16 store itself) and bf16-rounded centres, then ||mu_c||^2 - 2 x.mu_c
-// in float64; ties go to the lower index.  Any assignment keeps the index
+// Nearest centre of each row for the build, on the 16-bit matrix cores:
+// x.mu_c by v_mfma_f32_16x16x32_f16 from the float16 image of the rows and
+// float16-rounded centres (or v_mfma_f32_16x16x32_bf16 from a bf16 store
+// without an image and bf16-rounded centres), then ||mu_c||^2 - 2 x.mu_c in
+// float64; ties go to the lower index.  Any assignment keeps the index
 // exact (R_c is taken from the rows a cluster receives), so the rounding only
 // affects how tight the clusters are.  Rows are j * stride, j < n.
 // Block: 4 waves x 16 rows; a wave keeps its rows' A operands for the whole
@@ -193,15 +194,15 @@ __global__ __launch_bounds__(256) void centre_mfma_kernel(const void* __restrict
 template <int KS>
 struct AssignTraits {
   static constexpr int kChunk = KS <= 8 ? 64 : (KS <= 16 ? 32 : 16);  // centres per LDS chunk
-  static constexpr int kRowBytes = KS * 64 + 16;                       // padded bf16 row
+  static constexpr int kRowBytes = KS * 64 + 16;                       // padded 16-bit row
 };
 
 __device__ __forceinline__ u32x4 load16_or_zero(const uint16_t* base, bool ok) {
   return ok ? *reinterpret_cast<const u32x4*>(base) : u32x4{0u, 0u, 0u, 0u};
 }
 
-template <int KS>
-__global__ __launch_bounds__(256) void assign_bf16_kernel(const uint16_t* __restrict__ rows, int64_t n,
+template <int KS, bool F16>
+__global__ __launch_bounds__(256) void assign16_kernel(const uint16_t* __restrict__ rows, int64_t n,
                                                           int64_t stride, int d,
                                                           const uint16_t* __restrict__ centres16,
                                                           const double* __restrict__ cnorm, int K,
@@ -248,8 +249,13 @@ __global__ __launch_bounds__(256) void assign_bf16_kernel(const uint16_t* __rest
 #pragma unroll
       for (int j = 0; j < kTiles; ++j) {
         const u32x4 b = *reinterpret_cast<const u32x4*>(cs + (16 * j + m16) * T::kRowBytes + (4 * st + g) * 16);
-        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[st]),
-                                                         __builtin_bit_cast(bf16x8, b), acc[j], 0, 0, 0);
+        if constexpr (F16) {
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a[st]),
+                                                          __builtin_bit_cast(f16x8, b), acc[j], 0, 0, 0);
+        } else {
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[st]),
+                                                           __builtin_bit_cast(bf16x8, b), acc[j], 0, 0, 0);
+        }
       }
     }
 #pragma unroll
@@ -284,18 +290,20 @@ __global__ __launch_bounds__(256) void assign_bf16_kernel(const uint16_t* __rest
   }
 }
 
-// bf16 (round to nearest even) copy of the float32 centres.
-__global__ void centre_bf16_kernel(const float* __restrict__ c, int64_t n, uint16_t* __restrict__ out) {
+// 16-bit copy of the float32 centres: float16 (clamped, nearest even) or
+// bf16 (nearest even), the element type of the rows they meet.
+__global__ void centre16_kernel(const float* __restrict__ c, int64_t n, int f16, uint16_t* __restrict__ out) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < n) out[i] = bf16_bits(c[i]);
+  if (i < n) out[i] = f16 ? f16_bits(c[i]) : bf16_bits(c[i]);
 }
 
-// Assignment of rows j * stride (j < n) for the build: the bf16 kernel when
-// bf16 rows exist, else the float32 one.
+// Assignment of rows j * stride (j < n) for the build: the 16-bit kernel on
+// the float16 image, else on a bf16 store, else the float32 one.
 inline void launch_assign(const lipcache_cache* c, int64_t n, int64_t stride, int d, const float* centres,
                           uint16_t* centres16, const double* cnorm, int K, uint32_t* nearest, hipStream_t s) {
-  const uint16_t* rows16 = c->store_dtype == LIPCACHE_BF16 ? static_cast<const uint16_t*>(c->z)
-                                                           : static_cast<const uint16_t*>(c->zimg);
+  const bool f16 = c->zimg != nullptr;
+  const uint16_t* rows16 = f16 ? static_cast<const uint16_t*>(c->zimg)
+                               : (c->store_dtype == LIPCACHE_BF16 ? static_cast<const uint16_t*>(c->z) : nullptr);
   const unsigned grid = static_cast<unsigned>((n + kCr - 1) / kCr);
   if (!rows16) {
     hipLaunchKernelGGL(centre_mfma_kernel, dim3(grid), dim3(256), 0, s, c->z, c->store_dtype, n, stride, d, centres,
@@ -303,21 +311,28 @@ inline void launch_assign(const lipcache_cache* c, int64_t n, int64_t stride, in
     return;
   }
   const int64_t kd = static_cast<int64_t>(K) * d;
-  hipLaunchKernelGGL(centre_bf16_kernel, dim3(static_cast<unsigned>((kd + 255) / 256)), dim3(256), 0, s, centres, kd,
-                     centres16);
+  hipLaunchKernelGGL(centre16_kernel, dim3(static_cast<unsigned>((kd + 255) / 256)), dim3(256), 0, s, centres, kd,
+                     f16 ? 1 : 0, centres16);
   int ks = 1;
   while (ks * 32 < d) ks *= 2;
   auto go = [&](auto kern) {
     hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, rows16, n, stride, d, centres16, cnorm, K, nearest);
   };
-  switch (ks) {
-    case 1: go(assign_bf16_kernel<1>); break;
-    case 2: go(assign_bf16_kernel<2>); break;
-    case 4: go(assign_bf16_kernel<4>); break;
-    case 8: go(assign_bf16_kernel<8>); break;
-    case 16: go(assign_bf16_kernel<16>); break;
-    default: go(assign_bf16_kernel<32>); break;
+#define LC_ASSIGN(KS_)                    \
+  if (f16) {                              \
+    go(assign16_kernel<KS_, true>);       \
+  } else {                                \
+    go(assign16_kernel<KS_, false>);      \
   }
+  switch (ks) {
+    case 1: LC_ASSIGN(1) break;
+    case 2: LC_ASSIGN(2) break;
+    case 4: LC_ASSIGN(4) break;
+    case 8: LC_ASSIGN(8) break;
+    case 16: LC_ASSIGN(16) break;
+    default: LC_ASSIGN(32) break;
+  }
+#undef LC_ASSIGN
 }
 
 __global__ void fill_u32_kernel(uint32_t* __restrict__ p, int64_t n) {
@@ -459,7 +474,7 @@ __global__ __launch_bounds__(256) void count_kernel(const uint32_t* __restrict__
 
 // Sorted rows j0 .. j0+7 (one wave): copy cache rows perm[j] and raise R_c.
 // Lanes 0..7 move the per-row scalars; the feature rows move as 16-byte
-// (f32) or 8-byte (bf16, image) vectors, the eight rows' loads issued
+// (f32) or 8-byte (bf16, float16 image) vectors, the eight rows' loads issued
 // before their stores.  The rows are in cluster order, so the wave keeps a
 // running max of ||z_j - mu_c|| + r_j and flushes one atomic per cluster
 // it covers instead of one per row.
@@ -481,9 +496,9 @@ __device__ __forceinline__ float4 bf16x4_to_f32(uint2 h) {
                      bf16_to_f32(static_cast<uint16_t>(h.y)), bf16_to_f32(static_cast<uint16_t>(h.y >> 16)));
 }
 
-__device__ __forceinline__ uint2 f32x4_to_bf16(float4 v) {
-  return make_uint2(static_cast<uint32_t>(bf16_bits(v.x)) | (static_cast<uint32_t>(bf16_bits(v.y)) << 16),
-                    static_cast<uint32_t>(bf16_bits(v.z)) | (static_cast<uint32_t>(bf16_bits(v.w)) << 16));
+__device__ __forceinline__ uint2 f32x4_to_f16(float4 v) {
+  return make_uint2(static_cast<uint32_t>(f16_bits(v.x)) | (static_cast<uint32_t>(f16_bits(v.y)) << 16),
+                    static_cast<uint32_t>(f16_bits(v.z)) | (static_cast<uint32_t>(f16_bits(v.w)) << 16));
 }
 
 __global__ __launch_bounds__(256) void reorder_kernel(const lipcache_cache c, lipcache_cache out,
@@ -526,25 +541,34 @@ __global__ __launch_bounds__(256) void reorder_kernel(const lipcache_cache c, li
   double part[R];
 #pragma unroll
   for (int t = 0; t < R; ++t) part[t] = 0.0;
+  const uint2* __restrict__ is = static_cast<const uint2*>(c.zimg);
+  uint2* __restrict__ io = static_cast<uint2*>(out.zimg);
   for (int k4 = lane; k4 < d4; k4 += kWave) {
     if (c.store_dtype == LIPCACHE_BF16) {
       const uint2* __restrict__ zs = static_cast<const uint2*>(c.z);
       uint2* __restrict__ zo = static_cast<uint2*>(out.z);
       uint2 v[R];
+      uint2 im[R];
 #pragma unroll
       for (int t = 0; t < R; ++t) v[t] = zs[src[t] * d4 + k4];
+      if (io && is) {
+#pragma unroll
+        for (int t = 0; t < R; ++t) im[t] = is[src[t] * d4 + k4];
+      } else if (io) {
+#pragma unroll
+        for (int t = 0; t < R; ++t) im[t] = f32x4_to_f16(bf16x4_to_f32(v[t]));
+      }
 #pragma unroll
       for (int t = 0; t < R; ++t) {
         if (t < rows) {
           zo[(j0 + t) * d4 + k4] = v[t];
+          if (io) io[(j0 + t) * d4 + k4] = im[t];
           part[t] += diff2_4(bf16x4_to_f32(v[t]), mu4[static_cast<int64_t>(cl[t]) * d4 + k4]);
         }
       }
     } else {
       const float4* __restrict__ zs = static_cast<const float4*>(c.z);
       float4* __restrict__ zo = static_cast<float4*>(out.z);
-      const uint2* __restrict__ is = static_cast<const uint2*>(c.zimg);
-      uint2* __restrict__ io = static_cast<uint2*>(out.zimg);
       float4 v[R];
       uint2 im[R];
 #pragma unroll
@@ -552,9 +576,9 @@ __global__ __launch_bounds__(256) void reorder_kernel(const lipcache_cache c, li
       if (io && is) {
 #pragma unroll
         for (int t = 0; t < R; ++t) im[t] = is[src[t] * d4 + k4];
-      } else {
+      } else if (io) {
 #pragma unroll
-        for (int t = 0; t < R; ++t) im[t] = f32x4_to_bf16(v[t]);
+        for (int t = 0; t < R; ++t) im[t] = f32x4_to_f16(v[t]);
       }
 #pragma unroll
       for (int t = 0; t < R; ++t) {
@@ -613,7 +637,7 @@ struct BuildWs {
   uint32_t* assign;
   uint32_t* cnt;
   int64_t* coff;
-  uint16_t* c16;  // bf16 copy of the centres (bf16 assignment)
+  uint16_t* c16;  // 16-bit copy of the centres (16-bit assignment)
   unsigned long long* rbits;
   double* cnorm;
   uint32_t* keys[2];

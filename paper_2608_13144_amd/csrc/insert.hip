@@ -10,8 +10,9 @@
 //   rank    - each block ranks its selected rows with wave ballots and writes
 //             the source row of every destination row;
 //   copy    - one wave per destination row over the whole chip, 16-byte
-//             loads and stores, casting to the store dtype and recomputing
-//             ||z||^2 of the stored values in float64.
+//             loads and stores, casting to the store dtype, writing the
+//             float16 image of the stored values (when the cache keeps one)
+//             and recomputing ||z||^2 of the stored values in float64.
 #include "lc_common.hpp"
 
 namespace lc {
@@ -107,25 +108,26 @@ __global__ __launch_bounds__(kCopyThreads) void insert_copy_kernel(const InsertP
   const float* zr = p.z_src + src * p.d;
   double s = 0.0;
   for (int k = 4 * lane; k < p.d; k += 4 * kWave) {
-    const f32x4 v = *reinterpret_cast<const f32x4*>(zr + k);
-    uint16_t h[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) h[i] = bf16_bits(v[i]);
-    const uint2 packed = {static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16),
-                          static_cast<uint32_t>(h[2]) | (static_cast<uint32_t>(h[3]) << 16)};
+    f32x4 v = *reinterpret_cast<const f32x4*>(zr + k);
     if (p.store == LIPCACHE_BF16) {
-      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.cz) + dst * p.d + k) = packed;
+      uint16_t h[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const double x = static_cast<double>(bf16_to_f32(h[i]));
-        s = __builtin_fma(x, x, s);
+        h[i] = bf16_bits(v[i]);
+        v[i] = bf16_to_f32(h[i]);  // the stored value
       }
+      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.cz) + dst * p.d + k) =
+          uint2{static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16),
+                static_cast<uint32_t>(h[2]) | (static_cast<uint32_t>(h[3]) << 16)};
     } else {
       *reinterpret_cast<f32x4*>(static_cast<float*>(p.cz) + dst * p.d + k) = v;
-      if (p.cimg) *reinterpret_cast<uint2*>(p.cimg + dst * p.d + k) = packed;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) s = __builtin_fma(static_cast<double>(v[i]), static_cast<double>(v[i]), s);
     }
+    if (p.cimg)
+      *reinterpret_cast<uint2*>(p.cimg + dst * p.d + k) =
+          uint2{static_cast<uint32_t>(f16_bits(v[0])) | (static_cast<uint32_t>(f16_bits(v[1])) << 16),
+                static_cast<uint32_t>(f16_bits(v[2])) | (static_cast<uint32_t>(f16_bits(v[3])) << 16)};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s = __builtin_fma(static_cast<double>(v[i]), static_cast<double>(v[i]), s);
   }
   s = wave_sum(s);
   if (lane == 0) {
@@ -196,7 +198,7 @@ extern "C" lipcache_status lipcache_insert(lipcache_cache* c, const float* z_src
   p.src_of = src_of;
   p.count = host_total;
   p.cz = c->z;
-  p.cimg = c->store_dtype == LIPCACHE_F32 ? static_cast<uint16_t*>(c->zimg) : nullptr;
+  p.cimg = static_cast<uint16_t*>(c->zimg);
   p.cr = c->r;
   p.clabel = c->label;
   p.cnorm2 = c->norm2;

@@ -9,6 +9,7 @@
 namespace lc {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -47,6 +48,29 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float* v) {
   for (int i = 0; i < 4; ++i)
     o[i] = static_cast<uint32_t>(bf16_bits(v[2 * i])) |
            (static_cast<uint32_t>(bf16_bits(v[2 * i + 1])) << 16);
+  return o;
+}
+
+// ------------------------------------------------------------- float16
+// Round to nearest even (v_cvt_f16_f32 in the default rounding mode) after
+// clamping to the finite range, so every image value is finite: a value
+// whose magnitude the clamp changes only occurs in rows with ||x|| >= 2^15,
+// which the distance filter never trusts (see kF16Range2).  NaN becomes a
+// finite value; a NaN row or query has a NaN threshold and never passes.
+__device__ __forceinline__ uint16_t f16_bits(float x) {
+  const _Float16 h = static_cast<_Float16>(__builtin_fminf(__builtin_fmaxf(x, -65504.0f), 65504.0f));
+  return __builtin_bit_cast(uint16_t, h);
+}
+__device__ __forceinline__ float f16_to_f32(uint16_t b) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, b));
+}
+
+// Pack 8 floats into 8 float16 (one 16-byte MFMA operand chunk).
+__device__ __forceinline__ u32x4 pack_f16x8(const float* v) {
+  u32x4 o;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    o[i] = static_cast<uint32_t>(f16_bits(v[2 * i])) | (static_cast<uint32_t>(f16_bits(v[2 * i + 1])) << 16);
   return o;
 }
 
@@ -114,26 +138,64 @@ __device__ __forceinline__ float f32_round_down(double x) {
 }
 
 // --------------------------------------------------------- filter slack
-// Bound on |g_hat - q.c| relative to sum_k |q_k c_k| for the matrix-core dot
-// product of d_pad terms: bf16 rounding of the operands plus float32
-// accumulation in any order (gamma_n = n u / (1 - n u), u = 2^-24).
-inline double filter_kappa(int precision, int store_dtype, int d_pad) {
-  const double u32 = 1.0 / 16777216.0;        // 2^-24
-  const double ub = 1.0 / 256.0;              // 2^-8, bf16 unit roundoff
-  const double n = static_cast<double>(d_pad) + 2.0;
-  const double gam = n * u32 / (1.0 - n * u32);
-  double k;
-  if (precision == LIPCACHE_F32) {
-    k = gam;                                              // products and sums in fp32
-  } else if (store_dtype == LIPCACHE_BF16) {
-    k = ub + gam * (1.0 + ub);                            // only the query is rounded
-  } else {
-    k = 2.0 * ub + ub * ub + gam * (1.0 + ub) * (1.0 + ub); // both operands rounded
-  }
-  return 2.0 * k;  // safety factor: the accumulation order inside MFMA is not specified
-}
-
 // Absolute slack that covers flushed sub-normal products.
 constexpr double kFilterAbsSlack = 1e-25;
+
+// ||x||^2 at or above which the float16 operands cannot be trusted to hold x
+// (some |x_k| may reach the float16 range): such a query or entry passes the
+// filter against everything, so the exact re-check decides all its pairs.
+constexpr double kF16Range2 = 1073741824.0;  // (2^15)^2
+
+// Constants of the matrix-core distance filter.  With u the unit roundoff of
+// the operand type, every component is rounded to x_k (1 + e) + t with
+// |e| <= u and |t| <= eta (eta covers results in the sub-normal range and
+// sub-normal inputs the matrix core may flush); the products (exact in
+// float32 for float16 operands) and the float32 additions add at most
+// gamma = n u32 / (1 - n u32), n = d_pad + 2, of the absolute terms.  Hence
+//   |g_hat - q.z| <= k sum_k |q_k z_k| + eta (1 + u)(1 + gamma)(|q|_1 + |z|_1)
+//                    + (1 + gamma) d_pad eta^2,
+// with k = 2u + u^2 + gamma (1 + u)^2 when both operands are rounded, u +
+// gamma (1 + u) when the cache values are already exact (a bf16 store in a
+// float16 image), gamma for float32 operands.  Using sum |q_k z_k| <=
+// (||q||^2 + ||z||^2) / 2 and |x|_1 <= sqrt(d_pad) ||x||, the filter takes
+// twice each term (the order of the additions inside the matrix core is not
+// specified):
+//   kappa = 2 k                      (relative, on (||q||^2 + ||z||^2) / 2)
+//   eta1  = 2 eta (1 + u)(1 + gamma) sqrt(d_pad)   (per ||q|| and per ||z||)
+//   eta0  = 2 (1 + gamma) d_pad eta^2 + kFilterAbsSlack / 2  (per query)
+struct FilterSlack {
+  double kappa;
+  double eta1;
+  double eta0;
+  double range2;  // kF16Range2 for float16 operands, +inf for float32
+};
+
+inline FilterSlack filter_slack(int precision, int store_dtype, int d_pad) {
+  const double u32 = 1.0 / 16777216.0;  // 2^-24
+  const double n = static_cast<double>(d_pad) + 2.0;
+  const double gam = n * u32 / (1.0 - n * u32);
+  double u, eta, k;
+  FilterSlack f;
+  if (precision == LIPCACHE_F32) {
+    u = 0.0;
+    eta = 1.1754943508222875e-38;  // 2^-126: a flushed float32 sub-normal
+    k = gam;
+    f.range2 = __builtin_inf();
+  } else {
+    u = 1.0 / 2048.0;              // 2^-11, float16 unit roundoff
+    eta = 1.0 / 16384.0;           // 2^-14: float16 sub-normals, or flushed ones
+    k = store_dtype == LIPCACHE_BF16 ? u + gam * (1.0 + u) : 2.0 * u + u * u + gam * (1.0 + u) * (1.0 + u);
+    f.range2 = kF16Range2;
+  }
+  f.kappa = 2.0 * k;
+  f.eta1 = 2.0 * eta * (1.0 + u) * (1.0 + gam) * __builtin_sqrt(static_cast<double>(d_pad));
+  f.eta0 = 2.0 * (1.0 + gam) * d_pad * eta * eta + 0.5 * kFilterAbsSlack;
+  return f;
+}
+
+// Largest finite float: the threshold of a query or entry that passes the
+// filter against everything (-FLT_MAX) while +inf still marks rows that can
+// never be hit.
+constexpr float kPassAll = -3.4028234663852886e38f;
 
 }  // namespace lc

@@ -8,27 +8,30 @@
 // ~1e3 while d^2 is ~1e-2 at the large workloads), so the matrix-core value
 // is only a FILTER:
 //   pass  <=>  fl(g_hat - Q_q) >= A_i,
-//   Q_q = RD((1 - k) ||q||^2 / 2),  A_i = RD(((1 - k - 4u) ||z_i||^2 - r_i^2) / 2),
-// where k bounds |g_hat - q.z_i| / ((||q||^2 + ||z_i||^2) / 2) (bf16 operand
-// rounding and float32 accumulation, doubled); for d <= 128 the bf16 filter
-// accumulates onto -Q_q instead (acc >= A_i), which adds one more float32
-// rounding against Q_q, far inside that bound.  Every true hit passes; a pair
-// that passes is re-checked as sum_k (q_k - z_ik)^2 in float64 from the
-// original values, which decides the hit.  Hits are merged per query with a
-// 64-bit atomic minimum of (float bits of d^2) << 32 | i, which orders by
-// distance and then by index, independent of scheduling.
+//   Q_q = RD((1 - k) ||q||^2 / 2 - eta1 ||q|| - eta0),
+//   A_i = RD(((1 - k - 4u) ||z_i||^2 - r_i^2) / 2 - eta1 ||z_i||),
+// where k bounds |g_hat - q.z_i| / ((||q||^2 + ||z_i||^2) / 2) and eta1, eta0
+// its absolute part (float16 or float32 operand rounding, sub-normals and
+// float32 accumulation, doubled; filter_slack); for d <= 128 the float16
+// filter accumulates onto -Q_q instead (acc >= A_i), which adds one more
+// float32 rounding against Q_q, far inside that bound.  Every true hit
+// passes.  A pair that passes is queued and re-checked after the scan as
+// sum_k (q_k - z_ik)^2 in float64 from the original values, which decides the
+// hit.  Hits are merged per query with a 64-bit atomic minimum of (float bits
+// of d^2) << 32 | i, which orders by distance and then by index, independent
+// of scheduling.
 //
 // Kernel layout (gfx950, wave64):
 //  - workgroup = 8 waves (two per SIMD); wave w holds RT*16 queries as MFMA
-//    A operands in registers for the whole sweep (bf16 or float32, converted
-//    once);
+//    A operands in registers for the whole sweep (float16 or float32,
+//    converted once);
 //  - the workgroup streams its slice of the cache through LDS in tiles of
 //    128 entries (64 KiB, double-buffered), copied global -> LDS without
 //    registers (lookup_dma_kernel), or, when the rows need a conversion,
 //    register-staged tiles of 64 (lookup_kernel);
-//  - per 16-entry column tile: KS k-steps of v_mfma_f32_16x16x32_bf16 (or 4x
+//  - per 16-entry column tile: KS k-steps of v_mfma_f32_16x16x32_f16 (or 4x
 //    v_mfma_f32_16x16x4_f32), then the filter on the accumulators; a wave
-//    ballot skips the re-check path unless a pair passed;
+//    ballot skips the queueing path unless a pair passed;
 //  - grid = query blocks x cache slices; blocks are numbered so that the
 //    blocks a given XCD runs (block id mod 8) share cache slices, so the
 //    resident workgroups of an XCD read each cache tile from its L2 at about
@@ -36,11 +39,12 @@
 //    a work list: up to 512 queries of one cluster's query list (read through
 //    the list, in a separate instantiation) against a chunk of that cluster's
 //    rows.  There a query meets its own cluster's rows, so pairs pass the
-//    filter often: each wave queues them in LDS instead of re-checking at
-//    once (which stalls the whole workgroup at the next tile barrier), hands
-//    the queue to a global queue after its last tile, and a separate kernel
-//    re-checks the queued pairs chip-wide; waves past the list end only
-//    copy.
+//    filter often: each wave queues them in LDS, hands the queue to the
+//    global queue after its last tile in one reservation; waves past the
+//    list end only copy;
+//  - recheck_queue_kernel settles the global queue chip-wide; a pair that
+//    finds the queue full is re-checked by its wave at once (same order of
+//    sums, so the same d^2 either way).
 #include <limits.h>
 
 #include "lc_common.hpp"
@@ -55,16 +59,16 @@ constexpr int kColTile = 16;
 constexpr int kXcds = 8;
 constexpr unsigned long long kNoHit = ~0ull;
 
-enum { kModeBF16 = 0, kModeF32 = 1 };
-// For d <= 128 the bf16 filter starts each accumulator at -Q_q instead of
+enum { kModeF16 = 0, kModeF32 = 1 };
+// For d <= 128 the float16 filter starts each accumulator at -Q_q instead of
 // zero, so the matrix core returns g - Q_q and the filter is one max per
 // accumulator (there the filter's vector work, not the matrix core, is what
-// limits); the extra fp32 rounding is far inside the bf16 slack.  Wider rows
-// keep the subtraction: the extra live registers would spill there.  The
-// fp32 filter, whose slack is tight, always subtracts Q_q after the
+// limits); the extra fp32 rounding is far inside the float16 slack.  Wider
+// rows keep the subtraction: the extra live registers would spill there.
+// The fp32 filter, whose slack is tight, always subtracts Q_q after the
 // contraction.
 template <int MODE, int KS>
-constexpr bool kFoldQ = MODE == kModeBF16 && KS <= 4;
+constexpr bool kFoldQ = MODE == kModeF16 && KS <= 4;
 
 struct LookupParams {
   const float* zq;
@@ -79,8 +83,10 @@ struct LookupParams {
   unsigned int* bflag;
   unsigned long long* stats;
   double kappa_c;        // 1 - k - 4u, applied to ||z_i||^2
+  double eta1;           // absolute slack per unit of ||z_i||
+  double range2;         // ||z_i||^2 from which an entry passes against everything
   const float* athr;     // [n_pad] per-entry filter thresholds A_i (+inf past n)
-  const void* cimg;      // rows streamed by the DMA kernel (bf16 image or z)
+  const void* cimg;      // rows streamed by the DMA kernel (float16 image or z)
   int n_qblocks;
   int64_t slice_len;
   float* g_hat;          // dump mode only
@@ -91,17 +97,19 @@ struct LookupParams {
   // qlist is null).
   const int64_t* items;
   const int32_t* qlist;
-  // bf16 copy of the queries (round to nearest even, as the in-kernel
-  // conversion): the bf16 A operands of the work-list kernel, half the bytes
-  // of the float32 rows every item would otherwise gather.
+  // float16 copy of the queries (the in-kernel conversion): the A operands
+  // of the work-list kernel, half the bytes of the float32 rows every item
+  // would otherwise gather.
   const uint16_t* zq16;
   // Index written into a hit's key: (emap ? emap[e] : e) + eoff.
   const int64_t* emap;
   int64_t eoff;
-  // Work-list mode: after its last tile a wave moves its queued re-checks to
-  // this queue (list position, cache row) when it has room; gq_count counts
-  // reserved slots, and a slot a wave reserved but settled itself holds
-  // position -1.  Null: every wave settles its own queue.
+  // Global re-check queue (query position, cache row): pairs that pass the
+  // filter are appended here and settled chip-wide after the scan (work-list
+  // mode: each wave's LDS queue moves here in one reservation).  gq_count
+  // counts reserved slots; a pair that finds no slot below gq_cap is
+  // re-checked by its wave at once, and a slot a wave reserved but settled
+  // itself holds position -1.  Null (filter dump): nothing is re-checked.
   int64_t* gq_pos;
   int64_t* gq_e;
   unsigned long long* gq_count;
@@ -109,8 +117,38 @@ struct LookupParams {
 };
 
 // ------------------------------------------------------------- prep
+// Filter thresholds.  A pair passes iff fl(g_hat - Q_q) >= A_i with
+//   Q_q = RD((1 - k) ||q||^2 / 2 - eta1 ||q|| - eta0),
+//   A_i = RD(((1 - k - 4u) ||z_i||^2 - r_i^2) / 2 - eta1 ||z_i|| - abs / 2)
+// (k, eta1, eta0 from filter_slack).  A row whose squared norm reaches
+// range2 (the float16 operands may not hold it) gets kPassAll: it passes
+// against every live entry or query and the exact re-check decides.  A NaN
+// norm gives a NaN threshold (never passes: NaN features have no hit), an
+// infinite query norm likewise (its distance to every entry is infinite).
+struct Thresholds {
+  double kq;       // 1 - k
+  double kappa_c;  // 1 - k - 4u
+  double eta1;
+  double eta0;
+  double range2;
+};
+
+__device__ __forceinline__ float query_threshold(double s, const Thresholds& t) {
+  if (s >= t.range2 && s < __builtin_inf()) return kPassAll;
+  return f32_round_down(t.kq * s * 0.5 - t.eta1 * __builtin_sqrt(s) - t.eta0);
+}
+
+// +inf for rows that can never be hit (r_i <= 0 or NaN).
+__device__ __forceinline__ float entry_threshold(float rr, float n2f, double kappa_c, double eta1, double range2) {
+  if (!(rr > 0.0f)) return __builtin_inff();
+  const double n2 = static_cast<double>(n2f);
+  if (n2 >= range2 && n2 < __builtin_inf()) return kPassAll;
+  const double r2 = static_cast<double>(rr) * static_cast<double>(rr);
+  return f32_round_down((kappa_c * n2 - r2) * 0.5 - eta1 * __builtin_sqrt(n2) - 0.5 * kFilterAbsSlack);
+}
+
 // One wave per query: Q_q, reset of the per-query state and of the counters.
-__global__ void lookup_prep_kernel(const float* __restrict__ zq, int64_t B, int d, double kq,
+__global__ void lookup_prep_kernel(const float* __restrict__ zq, int64_t B, int d, const Thresholds t,
                                    float* __restrict__ qthr, unsigned long long* __restrict__ best,
                                    unsigned int* __restrict__ bflag, unsigned long long* __restrict__ stats) {
   const int64_t q = static_cast<int64_t>(blockIdx.x) * kLkWaves + threadIdx.x / kWave;
@@ -121,33 +159,27 @@ __global__ void lookup_prep_kernel(const float* __restrict__ zq, int64_t B, int 
   for (int k = lane_id(); k < d; k += kWave) s = __builtin_fma(static_cast<double>(row[k]), static_cast<double>(row[k]), s);
   s = wave_sum(s);
   if (lane_id() == 0) {
-    qthr[q] = f32_round_down(kq * s * 0.5 - 0.5 * kFilterAbsSlack);
+    qthr[q] = query_threshold(s, t);
     best[q] = kNoHit;
     bflag[q] = 0u;
   }
 }
 
-// Per-entry threshold A_i = RD(((1 - k - 4u) ||z_i||^2 - r_i^2) / 2), +inf for
-// rows that can never be hit (r_i <= 0 or NaN) and for the padding past n.
+// Per-entry thresholds A_i, +inf for the padding past n; thread 0 also
+// empties the global re-check queue of the scan that follows.
 __global__ void lookup_athr_kernel(const float* __restrict__ cr, const float* __restrict__ cnorm2, int64_t n,
-                                   int64_t n_pad, double kappa_c, float* __restrict__ athr) {
+                                   int64_t n_pad, double kappa_c, double eta1, double range2,
+                                   float* __restrict__ athr, unsigned long long* __restrict__ gq_count) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i == 0 && gq_count) *gq_count = 0ull;
   if (i >= n_pad) return;
-  float at = __builtin_inff();
-  if (i < n) {
-    const float rr = cr[i];
-    if (rr > 0.0f) {
-      const double r2 = static_cast<double>(rr) * static_cast<double>(rr);
-      at = f32_round_down((kappa_c * static_cast<double>(cnorm2[i]) - r2) * 0.5 - 0.5 * kFilterAbsSlack);
-    }
-  }
-  athr[i] = at;
+  athr[i] = i < n ? entry_threshold(cr[i], cnorm2[i], kappa_c, eta1, range2) : __builtin_inff();
 }
 
-// bf16 copy of the queries (round to nearest even), for the work-list kernel.
-__global__ void query_bf16_kernel(const float* __restrict__ zq, int64_t n, uint16_t* __restrict__ zq16) {
+// float16 copy of the queries, for the work-list kernel.
+__global__ void query_f16_kernel(const float* __restrict__ zq, int64_t n, uint16_t* __restrict__ zq16) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < n) zq16[i] = bf16_bits(zq[i]);
+  if (i < n) zq16[i] = f16_bits(zq[i]);
 }
 
 // ------------------------------------------------------------- finalize
@@ -207,7 +239,7 @@ __device__ __forceinline__ int64_t query_at(const int32_t* qlist, int64_t j) { r
 template <int MODE>
 struct ModeTraits;
 template <>
-struct ModeTraits<kModeBF16> {
+struct ModeTraits<kModeF16> {
   static constexpr int kElemBytes = 2;
   static constexpr int kPerChunk = 8;                 // elements per 16-byte chunk
   static constexpr int kPerStep = 4 * kPerChunk;      // k per k-step (32)
@@ -222,9 +254,9 @@ struct ModeTraits<kModeF32> {
 // One k-step of the contraction for a 16x16 output tile.
 template <int MODE>
 __device__ __forceinline__ f32x4 mfma_step(u32x4 a, u32x4 b, f32x4 acc) {
-  if constexpr (MODE == kModeBF16) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
-                                                   acc, 0, 0, 0);
+  if constexpr (MODE == kModeF16) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), acc,
+                                                  0, 0, 0);
   } else {
     // Reinterpret the whole 16-byte chunk (a per-element bit cast of a vector
     // subscript is miscompiled to element 0 by this toolchain).
@@ -239,17 +271,28 @@ __device__ __forceinline__ f32x4 mfma_step(u32x4 a, u32x4 b, f32x4 acc) {
 }
 
 // Load PER consecutive elements [k0, k0 + PER) of a row as one 16-byte MFMA
-// operand chunk of the mode's element type; zeros beyond d.
+// operand chunk of the mode's element type; zeros beyond d.  SRC is the
+// element type in memory (LIPCACHE_F32, LIPCACHE_BF16, or LIPCACHE_F16 for
+// rows already converted).
 template <int MODE, int SRC>
 __device__ __forceinline__ u32x4 load_chunk(const void* base, int64_t row, int d, int k0) {
   u32x4 v = {0u, 0u, 0u, 0u};
   if (k0 >= d) return v;
-  if constexpr (MODE == kModeBF16) {
+  if constexpr (MODE == kModeF16) {
     if constexpr (SRC == LIPCACHE_F32) {
       const f32x4* p = reinterpret_cast<const f32x4*>(static_cast<const float*>(base) + row * d + k0);
       const f32x4 x0 = p[0], x1 = p[1];
       const float f[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-      v = pack_bf16x8(f);
+      v = pack_f16x8(f);
+    } else if constexpr (SRC == LIPCACHE_BF16) {
+      const u32x4 h = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(base) + row * d + k0);
+      float f[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f[2 * i] = __builtin_bit_cast(float, h[i] << 16);
+        f[2 * i + 1] = __builtin_bit_cast(float, h[i] & 0xffff0000u);
+      }
+      v = pack_f16x8(f);
     } else {
       v = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(base) + row * d + k0);
     }
@@ -480,9 +523,80 @@ __global__ __launch_bounds__(256) void recheck_queue_kernel(const RecheckArgs p,
     atomicAdd(&p.stats[LIPCACHE_STAT_RECHECKED], static_cast<unsigned long long>(block_done));
 }
 
-// Queues the pairs of `mask` (same bit layout as recheck_pairs: lane (m16, g)
-// holds entry ebase + m16 and query rows 4g + i of each row tile).  Pairs
-// that do not fit are re-checked at once.
+// Reads a wave-uniform 64-bit value from lane 0.
+__device__ __forceinline__ uint64_t lane0_u64(uint64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v)), 0);
+  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v >> 32)), 0);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Slice mode: appends the pairs of `mask` (bit rt*4+i of lane (m16, g) =
+// query row 4g + i of row tile rt against entry ebase + m16) to the global
+// re-check queue, one pair per lane and pass with one reservation per pass.
+// Pairs that find no slot below the capacity are re-checked at once (a cold
+// path: the queue holds several pairs per query).
+template <int SRC>
+__device__ __forceinline__ void enqueue_pairs(const LookupParams& lp, uint32_t mask, int64_t qwave, int64_t ebase,
+                                              int64_t qend, const int32_t* qlist) {
+  const int lane = lane_id();
+  const uint64_t cap = static_cast<uint64_t>(lp.gq_cap);
+  uint32_t rest = 0u;
+  while (true) {
+    const bool has = mask != 0u;
+    const unsigned long long bal = __ballot(has);
+    if (bal == 0ull) break;
+    uint64_t base = 0;
+    if (lane == 0) base = atomicAdd(lp.gq_count, static_cast<unsigned long long>(__popcll(bal)));
+    base = lane0_u64(base);
+    if (has) {
+      const int bit = __builtin_ctz(mask);
+      const uint64_t slot = base + __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(bal >> 32),
+                                                             __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(bal), 0u));
+      if (slot < cap) {
+        lp.gq_pos[slot] = qwave + (bit >> 2) * 16 + 4 * (lane >> 4) + (bit & 3);
+        lp.gq_e[slot] = ebase + (lane & 15);
+      } else {
+        rest |= 1u << bit;
+      }
+      mask &= mask - 1u;
+    }
+  }
+  if (__ballot(rest != 0u) != 0ull) recheck_pairs<SRC>(recheck_args(lp, qend, qlist), rest, qwave, ebase);
+}
+
+// Work-list mode: moves the wave's LDS queue to the global queue when it
+// has room (one 64-bit atomic reserves the slots), else settles it here.
+// The queue was written by other lanes of this wave.
+template <int SRC>
+__device__ __forceinline__ void flush_queue(const LookupParams& lp, const RecheckArgs& p, RecheckQueue& rq,
+                                            int64_t qwave) {
+  if (rq.n == 0) return;
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_wave_barrier();
+  const int lane = lane_id();
+  if (lp.gq_pos) {
+    unsigned long long base = 0;
+    if (lane == 0) base = atomicAdd(lp.gq_count, static_cast<unsigned long long>(rq.n));
+    const uint64_t b0 = lane0_u64(base);
+    const uint64_t cap = static_cast<uint64_t>(lp.gq_cap);
+    if (b0 + static_cast<uint64_t>(rq.n) <= cap) {
+      for (int i = lane; i < rq.n; i += kWave) {
+        lp.gq_pos[b0 + i] = qwave + rq.q[i];
+        lp.gq_e[b0 + i] = rq.e[i];
+      }
+      rq.n = 0;
+      return;
+    }
+    // no room: mark the reserved slots that exist, settle here
+    for (int i = lane; i < rq.n; i += kWave)
+      if (b0 + i < cap) lp.gq_pos[b0 + i] = -1;
+  }
+  settle_queue<SRC>(p, rq.q, rq.e, rq.n, qwave);
+  rq.n = 0;
+}
+
+// Work-list mode: queues the pairs of `mask` (bit layout as enqueue_pairs)
+// in the wave's LDS queue; pairs that do not fit are re-checked at once.
 template <int SRC>
 __device__ __forceinline__ void queue_pairs(const RecheckArgs& p, RecheckQueue& rq, uint32_t mask, int64_t qwave,
                                             int64_t ebase) {
@@ -509,39 +623,6 @@ __device__ __forceinline__ void queue_pairs(const RecheckArgs& p, RecheckQueue& 
   }
 }
 
-// After the wave's last tile: move the queue to the global queue when it has
-// room (one 64-bit atomic reserves the slots), else settle it here.  The
-// queue was written by other lanes of this wave.
-template <int SRC>
-__device__ __forceinline__ void flush_queue(const LookupParams& lp, const RecheckArgs& p, RecheckQueue& rq,
-                                            int64_t qwave) {
-  if (rq.n == 0) return;
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
-  __builtin_amdgcn_wave_barrier();
-  const int lane = lane_id();
-  if (lp.gq_pos) {
-    unsigned long long base = 0;
-    if (lane == 0) base = atomicAdd(lp.gq_count, static_cast<unsigned long long>(rq.n));
-    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(base)), 0);
-    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(base >> 32)), 0);
-    const uint64_t b0 = (static_cast<uint64_t>(hi) << 32) | lo;
-    const uint64_t cap = static_cast<uint64_t>(lp.gq_cap);
-    if (b0 + static_cast<uint64_t>(rq.n) <= cap) {
-      for (int i = lane; i < rq.n; i += kWave) {
-        lp.gq_pos[b0 + i] = qwave + rq.q[i];
-        lp.gq_e[b0 + i] = rq.e[i];
-      }
-      rq.n = 0;
-      return;
-    }
-    // no room: mark the reserved slots that exist, settle here
-    for (int i = lane; i < rq.n; i += kWave)
-      if (b0 + i < cap) lp.gq_pos[b0 + i] = -1;
-  }
-  settle_queue<SRC>(p, rq.q, rq.e, rq.n, qwave);
-  rq.n = 0;
-}
-
 // Queries as MFMA A operands: lane holds row m16 of each row tile and k-chunk
 // g of each k-step (the cache operand uses the same (k-step, chunk) -> k map,
 // so the contraction covers every k exactly once).  Positions past qend load
@@ -559,7 +640,7 @@ __device__ __forceinline__ void load_query_operands(const LookupParams& p, const
     for (int ks = 0; ks < KS; ++ks) {
       const int k0 = ks * T::kPerStep + g * T::kPerChunk;
       if constexpr (Q16) {
-        a[rt][ks] = load_chunk<MODE, LIPCACHE_BF16>(p.zq16, row, p.d, k0);
+        a[rt][ks] = load_chunk<MODE, LIPCACHE_F16>(p.zq16, row, p.d, k0);
       } else {
         a[rt][ks] = load_chunk<MODE, LIPCACHE_F32>(p.zq, row, p.d, k0);
       }
@@ -603,7 +684,7 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_kernel(const LookupParam
 
   u32x4 a[RT][KS];
   float qt[RT][4];
-  load_queries<MODE, KS, RT, LIST && MODE == kModeBF16>(p, qlist, qwave, qend, m16, g, a, qt);
+  load_queries<MODE, KS, RT, LIST && MODE == kModeF16>(p, qlist, qwave, qend, m16, g, a, qt);
 
   for (int64_t t0 = e_begin; t0 < e_end; t0 += kTileN) {
     __syncthreads();
@@ -617,15 +698,8 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_kernel(const LookupParam
     }
     if (threadIdx.x < kTileN) {
       const int64_t e = t0 + threadIdx.x;
-      float at = __builtin_inff();
-      if (e < e_end) {
-        const float rr = p.cr[e];
-        if (rr > 0.0f) {
-          const double r2 = static_cast<double>(rr) * static_cast<double>(rr);
-          at = f32_round_down((p.kappa_c * static_cast<double>(p.cnorm2[e]) - r2) * 0.5 - 0.5 * kFilterAbsSlack);
-        }
-      }
-      athr[threadIdx.x] = at;
+      athr[threadIdx.x] =
+          e < e_end ? entry_threshold(p.cr[e], p.cnorm2[e], p.kappa_c, p.eta1, p.range2) : __builtin_inff();
     }
     __syncthreads();
 
@@ -681,7 +755,7 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_kernel(const LookupParam
 #pragma unroll
             for (int i = 0; i < 4; ++i) mask |= static_cast<uint32_t>((acc[rt][i] - qt[rt][i]) >= an) << (rt * 4 + i);
           }
-          recheck_pairs<SRC>(recheck_args(p, qend, qlist), mask, qwave, ebase);
+          enqueue_pairs<SRC>(p, mask, qwave, ebase, qend, qlist);
         }
       }
     }
@@ -818,7 +892,7 @@ __device__ __forceinline__ void filter_and_recheck(const LookupParams& p, const 
   if constexpr (LIST) {
     queue_pairs<STORE>(recheck_args(p, qend, qlist), rq, mask, qwave, ebase);
   } else {
-    recheck_pairs<STORE>(recheck_args(p, qend, qlist), mask, qwave, ebase);
+    enqueue_pairs<STORE>(p, mask, qwave, ebase, qend, qlist);
   }
 }
 
@@ -983,7 +1057,7 @@ __device__ __forceinline__ void compute_tile(const unsigned char* buf, const flo
         if constexpr (LIST) {
           queue_pairs<STORE>(recheck_args(p, qend, qlist), rq, mask, qwave, ebase);
         } else {
-          recheck_pairs<STORE>(recheck_args(p, qend, qlist), mask, qwave, ebase);
+          enqueue_pairs<STORE>(p, mask, qwave, ebase, qend, qlist);
         }
       }
     }
@@ -1021,7 +1095,7 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
   issue_tile<MODE, KS>(buf0, ath0, p, e_begin, e_end, wave);
 
   u32x4 a[RT][KS];
-  if (active) load_query_operands<MODE, KS, RT, LIST && MODE == kModeBF16>(p, qlist, qwave, qend, m16, g, a);
+  if (active) load_query_operands<MODE, KS, RT, LIST && MODE == kModeF16>(p, qlist, qwave, qend, m16, g, a);
   RecheckQueue rq{rq_q + (LIST ? wave * kRq : 0), rq_e + (LIST ? wave * kRq : 0), 0};
   // Q_q of this lane's accumulator rows 4g .. 4g + 3 of each row tile, kept
   // in registers for the whole slice (reading them from LDS per column tile
@@ -1070,18 +1144,18 @@ struct Plan {
 inline int rt_for(int ks) { return ks <= 8 ? 4 : (ks == 16 ? 2 : 1); }
 
 inline bool make_plan(int precision, const lipcache_cache* c, Plan& pl) {
-  const int per_step = precision == LIPCACHE_BF16 ? 32 : 16;
-  int ks = precision == LIPCACHE_BF16 ? 1 : 2;
+  const int per_step = precision == LIPCACHE_F16 ? 32 : 16;
+  int ks = precision == LIPCACHE_F16 ? 1 : 2;
   while (ks * per_step < c->d) ks *= 2;
   if (ks > 32) return false;
   pl.ks = ks;
   pl.rt = rt_for(ks);
   pl.d_pad = ks * per_step;
   pl.qblock = kLkWaves * pl.rt * 16;
-  // The DMA kernel needs rows already in the MFMA element type and two LDS
-  // tiles of at most 64 KiB.
-  const bool same_type = precision == LIPCACHE_BF16 ? (c->store_dtype == LIPCACHE_BF16 || c->zimg != nullptr)
-                                                    : c->store_dtype == LIPCACHE_F32;
+  // The DMA kernel needs rows already in the MFMA element type (the float16
+  // image, or an fp32 store for the fp32 filter) and two LDS tiles of at
+  // most 64 KiB.
+  const bool same_type = precision == LIPCACHE_F16 ? c->zimg != nullptr : c->store_dtype == LIPCACHE_F32;
   pl.dma = same_type && ks <= 16;
   pl.tile_rows = pl.dma ? (ks <= 8 ? 128 : 64) : kTileN;  // DmaTraits<KS>::kRows
   return true;
@@ -1129,13 +1203,24 @@ hipError_t launch_ks(const Plan& pl, const LookupParams& p, unsigned grid, hipSt
 template <int VAR>
 hipError_t launch_lookup(int precision, int store, const Plan& pl, const LookupParams& p, unsigned grid,
                          hipStream_t s) {
-  if (precision == LIPCACHE_BF16) {
-    return store == LIPCACHE_F32 ? launch_ks<kModeBF16, LIPCACHE_F32, VAR>(pl, p, grid, s)
-                                 : launch_ks<kModeBF16, LIPCACHE_BF16, VAR>(pl, p, grid, s);
+  if (precision == LIPCACHE_F16) {
+    return store == LIPCACHE_F32 ? launch_ks<kModeF16, LIPCACHE_F32, VAR>(pl, p, grid, s)
+                                 : launch_ks<kModeF16, LIPCACHE_BF16, VAR>(pl, p, grid, s);
   }
   return store == LIPCACHE_F32 ? launch_ks<kModeF32, LIPCACHE_F32, VAR>(pl, p, grid, s)
                                : launch_ks<kModeF32, LIPCACHE_BF16, VAR>(pl, p, grid, s);
 }
+
+// The global re-check queue of a scan (workspace memory): 4 B + 65536
+// pairs; a pair that finds it full is re-checked by its wave at once.
+struct GlobalRecheckWs {
+  int64_t* pos;
+  int64_t* e;
+  unsigned long long* count;
+  int64_t cap;
+};
+
+inline int64_t gq_capacity(int64_t B) { return 4 * (B > 0 ? B : 0) + 65536; }
 
 struct Workspace {
   float* qthr;
@@ -1143,6 +1228,7 @@ struct Workspace {
   unsigned int* bflag;
   unsigned long long* stats;
   float* athr;
+  GlobalRecheckWs gq;
 };
 
 // A_i padded with +inf so that any tile that starts below n reads thresholds
@@ -1153,6 +1239,7 @@ inline int64_t athr_len(int64_t n) {
 
 inline size_t ws_layout(int64_t B, int64_t N, Workspace* w, void* base) {
   const size_t nb = static_cast<size_t>(B > 0 ? B : 0);
+  const int64_t cap = gq_capacity(B);
   size_t off = 0;
   const size_t o_best = off;
   off = align_up(off + nb * 8, 256);
@@ -1162,6 +1249,12 @@ inline size_t ws_layout(int64_t B, int64_t N, Workspace* w, void* base) {
   off = align_up(off + nb * 4, 256);
   const size_t o_stats = off;
   off = align_up(off + 4 * 8, 256);
+  const size_t o_gqc = off;
+  off = align_up(off + 8, 256);
+  const size_t o_gqp = off;
+  off = align_up(off + static_cast<size_t>(cap) * 8, 256);
+  const size_t o_gqe = off;
+  off = align_up(off + static_cast<size_t>(cap) * 8, 256);
   const size_t o_athr = off;
   off = align_up(off + static_cast<size_t>(athr_len(N)) * 4, 256);
   if (w && base) {
@@ -1170,6 +1263,8 @@ inline size_t ws_layout(int64_t B, int64_t N, Workspace* w, void* base) {
     w->qthr = reinterpret_cast<float*>(b + o_qthr);
     w->bflag = reinterpret_cast<unsigned int*>(b + o_flag);
     w->stats = reinterpret_cast<unsigned long long*>(b + o_stats);
+    w->gq = GlobalRecheckWs{reinterpret_cast<int64_t*>(b + o_gqp), reinterpret_cast<int64_t*>(b + o_gqe),
+                            reinterpret_cast<unsigned long long*>(b + o_gqc), cap};
     w->athr = reinterpret_cast<float*>(b + o_athr);
   }
   return off;
@@ -1190,16 +1285,19 @@ inline bool cache_ok(const lipcache_cache* c) {
 // Filter constants of one lookup (depend on precision, store and d).
 struct FilterConsts {
   Plan pl;
-  double kappa;
-  double kappa_c;
+  Thresholds t;
 };
 
 lipcache_status lookup_consts(const lipcache_cache* c, int32_t precision, FilterConsts& fc) {
   if (!make_plan(precision, c, fc.pl)) return LIPCACHE_EUNSUPPORTED;
   if (precision == LIPCACHE_F32 && (fc.pl.ks > 32 || c->d > 512)) return LIPCACHE_EUNSUPPORTED;
-  fc.kappa = filter_kappa(precision, c->store_dtype, fc.pl.d_pad);
+  const FilterSlack fs = filter_slack(precision, c->store_dtype, fc.pl.d_pad);
   const double u32 = 1.0 / 16777216.0;
-  fc.kappa_c = 1.0 - fc.kappa - 4.0 * u32;
+  fc.t.kq = 1.0 - fs.kappa;
+  fc.t.kappa_c = 1.0 - fs.kappa - 4.0 * u32;
+  fc.t.eta1 = fs.eta1;
+  fc.t.eta0 = fs.eta0;
+  fc.t.range2 = fs.range2;
   return LIPCACHE_OK;
 }
 
@@ -1208,38 +1306,29 @@ lipcache_status lookup_stage_prep(const float* zq, int64_t B, int d, const Filte
                                   unsigned long long* best, unsigned int* bflag, unsigned long long* stats,
                                   hipStream_t s) {
   const unsigned prep_grid = static_cast<unsigned>(B > 0 ? (B + kLkWaves - 1) / kLkWaves : 1);
-  hipLaunchKernelGGL(lookup_prep_kernel, dim3(prep_grid), dim3(kLkThreads), 0, s, zq, B, d, 1.0 - fc.kappa, qthr,
-                     best, bflag, stats);
+  hipLaunchKernelGGL(lookup_prep_kernel, dim3(prep_grid), dim3(kLkThreads), 0, s, zq, B, d, fc.t, qthr, best, bflag,
+                     stats);
   LC_LAUNCHED();
   return LIPCACHE_OK;
 }
 
-// Stage 2: the filter + re-check kernel of `view` (its n rows) against the
-// B queries, over cache slices or, with `items`, over a work list of
-// n_items (query positions, row range) items whose positions index qlist.
-// Hits are keyed by (emap ? emap[e] : e) + eoff.  athr needs
-// athr_len(view->n) floats.
-// The global re-check queue of a work-list scan (workspace memory).
-struct GlobalRecheckWs {
-  int64_t* pos;
-  int64_t* e;
-  unsigned long long* count;
-  int64_t cap;
-};
-
-__global__ void zero_u64_kernel(unsigned long long* __restrict__ p) { *p = 0ull; }
-
+// Stage 2: the filter kernel of `view` (its n rows) against the B queries,
+// over cache slices or, with `items`, over a work list of n_items (query
+// positions, row range) items whose positions index qlist; then the
+// chip-wide re-check of the pairs it queued in `gq`.  Hits are keyed by
+// (emap ? emap[e] : e) + eoff.  athr needs athr_len(view->n) floats.
 lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision, const FilterConsts& fc,
                                   const float* zq, int64_t B, const float* qthr, unsigned long long* best,
                                   unsigned int* bflag, unsigned long long* stats, float* athr,
                                   const int64_t* items, int64_t n_items, const int32_t* qlist, const uint16_t* zq16,
                                   const int64_t* emap, int64_t eoff, bool dump, float* g_hat, uint8_t* cand,
-                                  hipStream_t s, const GlobalRecheckWs* gq = nullptr) {
+                                  const GlobalRecheckWs& gq, hipStream_t s) {
   if (B <= 0 || view->n <= 0) return LIPCACHE_OK;
   if (items && n_items <= 0) return LIPCACHE_OK;
   const int64_t n_pad = athr_len(view->n);
   hipLaunchKernelGGL(lookup_athr_kernel, dim3(static_cast<unsigned>((n_pad + 255) / 256)), dim3(256), 0, s, view->r,
-                     view->norm2, view->n, n_pad, fc.kappa_c, athr);
+                     view->norm2, view->n, n_pad, fc.t.kappa_c, fc.t.eta1, fc.t.range2, athr,
+                     dump ? nullptr : gq.count);
   LC_LAUNCHED();
   const Plan& pl = fc.pl;
   LookupParams p;
@@ -1254,9 +1343,11 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
   p.best = best;
   p.bflag = bflag;
   p.stats = stats;
-  p.kappa_c = fc.kappa_c;
+  p.kappa_c = fc.t.kappa_c;
+  p.eta1 = fc.t.eta1;
+  p.range2 = fc.t.range2;
   p.athr = athr;
-  p.cimg = (precision == LIPCACHE_BF16 && view->store_dtype == LIPCACHE_F32) ? view->zimg : view->z;
+  p.cimg = precision == LIPCACHE_F16 ? view->zimg : view->z;
   p.n_qblocks = static_cast<int>((B + pl.qblock - 1) / pl.qblock);
   p.g_hat = g_hat;
   p.cand = cand;
@@ -1265,15 +1356,10 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
   p.zq16 = zq16;
   p.emap = emap;
   p.eoff = eoff;
-  const bool queued = items && gq && gq->pos && !dump;
-  p.gq_pos = queued ? gq->pos : nullptr;
-  p.gq_e = queued ? gq->e : nullptr;
-  p.gq_count = queued ? gq->count : nullptr;
-  p.gq_cap = queued ? gq->cap : 0;
-  if (queued) {
-    hipLaunchKernelGGL(zero_u64_kernel, dim3(1), dim3(1), 0, s, gq->count);
-    LC_LAUNCHED();
-  }
+  p.gq_pos = dump ? nullptr : gq.pos;
+  p.gq_e = dump ? nullptr : gq.e;
+  p.gq_count = dump ? nullptr : gq.count;
+  p.gq_cap = dump ? 0 : gq.cap;
   int64_t grid = n_items;
   p.slice_len = 0;
   if (!items) {
@@ -1295,21 +1381,20 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
                        : items ? launch_lookup<kVarList>(precision, view->store_dtype, pl, p, gu, s)
                                : launch_lookup<kVarLookup>(precision, view->store_dtype, pl, p, gu, s);
   if (e != hipSuccess) return LIPCACHE_EHIP;
-  if (queued) {
-    // the pairs the scan's waves handed off, one chip-wide pass
-    const RecheckArgs ra{zq, view->z, view->r, best, bflag, stats, static_cast<int64_t>(LLONG_MAX), view->n, view->d,
-                         emap, eoff, qlist};
-    int64_t blocks = (gq->cap + 15) / 16;
-    if (blocks > 256) blocks = 256;
-    if (view->store_dtype == LIPCACHE_BF16) {
-      hipLaunchKernelGGL(recheck_queue_kernel<LIPCACHE_BF16>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
-                         ra, gq->pos, gq->e, gq->count, gq->cap);
-    } else {
-      hipLaunchKernelGGL(recheck_queue_kernel<LIPCACHE_F32>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
-                         ra, gq->pos, gq->e, gq->count, gq->cap);
-    }
-    LC_LAUNCHED();
+  if (dump) return LIPCACHE_OK;
+  // the pairs the scan's waves queued, one chip-wide pass
+  const RecheckArgs ra{zq, view->z, view->r, best, bflag, stats, static_cast<int64_t>(LLONG_MAX), view->n, view->d,
+                       emap, eoff, qlist};
+  int64_t blocks = (gq.cap + 15) / 16;
+  if (blocks > 512) blocks = 512;
+  if (view->store_dtype == LIPCACHE_BF16) {
+    hipLaunchKernelGGL(recheck_queue_kernel<LIPCACHE_BF16>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, ra,
+                       gq.pos, gq.e, gq.count, gq.cap);
+  } else {
+    hipLaunchKernelGGL(recheck_queue_kernel<LIPCACHE_F32>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, ra,
+                       gq.pos, gq.e, gq.count, gq.cap);
   }
+  LC_LAUNCHED();
   return LIPCACHE_OK;
 }
 
@@ -1326,44 +1411,57 @@ lipcache_status lookup_stage_finalize(int64_t B, const unsigned long long* best,
   return LIPCACHE_OK;
 }
 
-lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, int32_t precision,
-                           int32_t* label_out, int64_t* index_out, float* dist2_out, uint64_t* stats,
-                           uint8_t* band_flag, void* ws, size_t ws_bytes, hipStream_t s, bool dump,
-                           float* g_hat, uint8_t* cand) {
+inline bool precision_ok(int32_t precision) { return precision == LIPCACHE_F16 || precision == LIPCACHE_F32; }
+
+// Host-side validation shared by the lookup entry points (nothing launched).
+lipcache_status lookup_check(const lipcache_cache* c, const float* zq, int64_t B, int32_t precision, bool dump,
+                             const int32_t* label_out, const float* g_hat, const uint8_t* cand) {
   if (!cache_ok(c) || B < 0) return LIPCACHE_EINVAL;
-  if (precision != LIPCACHE_BF16 && precision != LIPCACHE_F32) return LIPCACHE_EINVAL;
+  if (!precision_ok(precision)) return LIPCACHE_EINVAL;
   if (B > 0 && (!zq || (!dump && !label_out))) return LIPCACHE_EINVAL;
   if ((reinterpret_cast<uintptr_t>(zq) & 15u) != 0) return LIPCACHE_EINVAL;
   if (B > static_cast<int64_t>(INT_MAX) / 2) return LIPCACHE_EINVAL;
   if (dump && (!g_hat || !cand || B * c->n > (1ll << 26))) return LIPCACHE_EINVAL;
-  FilterConsts fc;
-  const lipcache_status cs = lookup_consts(c, precision, fc);
-  if (cs != LIPCACHE_OK) return cs;
-  const size_t need = ws_layout(B, c->n, nullptr, nullptr);
-  if (!ws || ws_bytes < need || !aligned256(ws)) return LIPCACHE_EWORKSPACE;
+  return LIPCACHE_OK;
+}
+
+// The whole lookup on a workspace laid out by ws_layout(B, c->n).
+lipcache_status lookup_on(const lipcache_cache* c, const float* zq, int64_t B, int32_t precision,
+                          const FilterConsts& fc, int32_t* label_out, int64_t* index_out, float* dist2_out,
+                          uint64_t* stats, uint8_t* band_flag, void* ws, hipStream_t s, bool dump, float* g_hat,
+                          uint8_t* cand) {
   Workspace w;
   ws_layout(B, c->n, &w, ws);
   unsigned long long* st = stats ? reinterpret_cast<unsigned long long*>(stats) : w.stats;
   lipcache_status r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s);
   if (r != LIPCACHE_OK) return r;
   r = lookup_stage_scan(c, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr, nullptr,
-                        nullptr, 0, dump, g_hat, cand, s);
+                        nullptr, 0, dump, g_hat, cand, w.gq, s);
   if (r != LIPCACHE_OK) return r;
   if (dump) return LIPCACHE_OK;
   return lookup_stage_finalize(B, w.best, w.bflag, c->label, label_out, index_out, dist2_out, band_flag, st, s);
 }
 
+lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, int32_t precision,
+                           int32_t* label_out, int64_t* index_out, float* dist2_out, uint64_t* stats,
+                           uint8_t* band_flag, void* ws, size_t ws_bytes, hipStream_t s, bool dump,
+                           float* g_hat, uint8_t* cand) {
+  const lipcache_status vs = lookup_check(c, zq, B, precision, dump, label_out, g_hat, cand);
+  if (vs != LIPCACHE_OK) return vs;
+  FilterConsts fc;
+  const lipcache_status cs = lookup_consts(c, precision, fc);
+  if (cs != LIPCACHE_OK) return cs;
+  const size_t need = ws_layout(B, c->n, nullptr, nullptr);
+  if (!ws || ws_bytes < need || !aligned256(ws)) return LIPCACHE_EWORKSPACE;
+  return lookup_on(c, zq, B, precision, fc, label_out, index_out, dist2_out, stats, band_flag, ws, s, dump, g_hat,
+                   cand);
+}
+
 // Workspace of an indexed lookup: the dense lookup's buffers (thresholds
-// sized for the larger of the indexed part and the tail) and the plan's.
-// The work-list capacity is sized for the smallest query block of any plan.
-// with_q16: include the bf16 copy of the queries (at the returned offset of
-// the layout without it).
-// Past the lookup and plan workspaces: the bf16 query copy, then the global
-// re-check queue of the work-list scan (count, positions, rows; 2 B + 65536
-// pairs, more go through the scan's own settle path).
+// sized for the larger of the indexed part and the tail), the plan's, then
+// the float16 copy of the queries.
 struct IndexedTail {
-  size_t q16, gq_count, gq_pos, gq_e, total;
-  int64_t gq_cap;
+  size_t q16, total;
 };
 
 inline IndexedTail indexed_ws_layout(int64_t B, int64_t n, int d, int K, int64_t n_indexed, Workspace* w,
@@ -1373,15 +1471,7 @@ inline IndexedTail indexed_ws_layout(int64_t B, int64_t n, int d, int K, int64_t
   char* pb = base ? static_cast<char*>(base) + lk : nullptr;
   IndexedTail t;
   t.q16 = lk + index_plan_layout(B, d, K, n_indexed, kLkWaves * 16, pw, pb);
-  size_t off = t.q16 + align_up(static_cast<size_t>(B) * d * 2, 256);
-  t.gq_cap = 2 * B + 65536;
-  t.gq_count = off;
-  off = align_up(off + 8, 256);
-  t.gq_pos = off;
-  off = align_up(off + static_cast<size_t>(t.gq_cap) * 8, 256);
-  t.gq_e = off;
-  off = align_up(off + static_cast<size_t>(t.gq_cap) * 8, 256);
-  t.total = off;
+  t.total = t.q16 + align_up(static_cast<size_t>(B) * d * 2, 256);
   return t;
 }
 
@@ -1390,7 +1480,7 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
                                    uint64_t* stats, uint8_t* band_flag, int64_t* pairs, void* ws, size_t ws_bytes,
                                    hipStream_t s) {
   if (!cache_ok(c) || !idx || B < 0) return LIPCACHE_EINVAL;
-  if (precision != LIPCACHE_BF16 && precision != LIPCACHE_F32) return LIPCACHE_EINVAL;
+  if (!precision_ok(precision)) return LIPCACHE_EINVAL;
   if (B > 0 && (!zq || !label_out)) return LIPCACHE_EINVAL;
   if ((reinterpret_cast<uintptr_t>(zq) & 15u) != 0) return LIPCACHE_EINVAL;
   if (B > static_cast<int64_t>(INT_MAX) / 2) return LIPCACHE_EINVAL;
@@ -1400,9 +1490,8 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
     return LIPCACHE_EINVAL;
   if (!idx->perm || !idx->offsets || !idx->centers || !idx->bound) return LIPCACHE_EINVAL;
   if ((reinterpret_cast<uintptr_t>(idx->centers) & 15u) != 0) return LIPCACHE_EINVAL;
-  // the bf16 filter streams the bf16 image of float32 rows when the cache has one
-  if (precision == LIPCACHE_BF16 && c->store_dtype == LIPCACHE_F32 && (c->zimg == nullptr) != (so.zimg == nullptr))
-    return LIPCACHE_EINVAL;
+  // the float16 filter streams the images when the cache has one
+  if (precision == LIPCACHE_F16 && (c->zimg == nullptr) != (so.zimg == nullptr)) return LIPCACHE_EINVAL;
   FilterConsts fc;
   const lipcache_status cs = lookup_consts(c, precision, fc);
   if (cs != LIPCACHE_OK) return cs;
@@ -1412,8 +1501,6 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
   IndexPlanWs pw;
   const IndexedTail tl = indexed_ws_layout(B, c->n, c->d, idx->K, idx->n_indexed, &w, &pw, ws);
   char* wsb = static_cast<char*>(ws);
-  const GlobalRecheckWs gq{reinterpret_cast<int64_t*>(wsb + tl.gq_pos), reinterpret_cast<int64_t*>(wsb + tl.gq_e),
-                           reinterpret_cast<unsigned long long*>(wsb + tl.gq_count), tl.gq_cap};
   unsigned long long* st = stats ? reinterpret_cast<unsigned long long*>(stats) : w.stats;
   if (B == 0) {
     lipcache_status r = lookup_stage_prep(zq, 0, c->d, fc, w.qthr, w.best, w.bflag, st, s);
@@ -1426,14 +1513,14 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
   r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s);
   if (r != LIPCACHE_OK) return r;
   uint16_t* zq16 = nullptr;
-  if (precision == LIPCACHE_BF16) {
+  if (precision == LIPCACHE_F16) {
     zq16 = reinterpret_cast<uint16_t*>(wsb + tl.q16);
     const int64_t nq = B * c->d;
-    hipLaunchKernelGGL(query_bf16_kernel, dim3(static_cast<unsigned>((nq + 255) / 256)), dim3(256), 0, s, zq, nq, zq16);
+    hipLaunchKernelGGL(query_f16_kernel, dim3(static_cast<unsigned>((nq + 255) / 256)), dim3(256), 0, s, zq, nq, zq16);
     LC_LAUNCHED();
   }
   r = lookup_stage_scan(&so, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, pw.items, n_items, pw.qlist,
-                        zq16, idx->perm, 0, false, nullptr, nullptr, s, &gq);
+                        zq16, idx->perm, 0, false, nullptr, nullptr, w.gq, s);
   if (r != LIPCACHE_OK) return r;
   const int64_t tail = c->n - idx->n_indexed;
   if (tail > 0) {
@@ -1449,7 +1536,7 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
     view.n = tail;
     view.capacity = tail;
     r = lookup_stage_scan(&view, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr,
-                          nullptr, nullptr, idx->n_indexed, false, nullptr, nullptr, s);
+                          nullptr, nullptr, idx->n_indexed, false, nullptr, nullptr, w.gq, s);
     if (r != LIPCACHE_OK) return r;
   }
   if (pairs) *pairs = idx_pairs + B * tail;

@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported_and_bound():
     for name in names:
         assert hasattr(lib, name), name
         assert name in L.SIGNATURES, f"binding lacks {name}"
-    assert lib.lipcache_abi_version() == 5
+    assert lib.lipcache_abi_version() == 6
 
 
 def test_status_strings():
@@ -45,7 +45,7 @@ def test_workspace_queries():
     assert lib.lipcache_spectral_norm_workspace_bytes(300, 64) >= 64 * 64 * 8
     assert lib.lipcache_certify_workspace_bytes(200, 256, 0) >= 200 * 256 * 8
     assert lib.lipcache_certify_workspace_bytes(200, 256, L.RADIUS_TIGHT) >= 200 * 256 * 8 + 200 * 200 * 8
-    assert lib.lipcache_lookup_workspace_bytes(32768, 1 << 20, 256, L.BF16) >= 32768 * 16
+    assert lib.lipcache_lookup_workspace_bytes(32768, 1 << 20, 256, L.F16) >= 32768 * 16
     assert lib.lipcache_insert_workspace_bytes(65536) >= 2 * 64 * 8
 
 
@@ -102,7 +102,7 @@ def test_certify_validation():
 def test_lookup_validation():
     lib = L.load()
 
-    def call(c, B=8, prec=L.BF16, zq=FAKE, label=FAKE, ws=FAKE, wsb=1 << 20):
+    def call(c, B=8, prec=L.F16, zq=FAKE, label=FAKE, ws=FAKE, wsb=1 << 24):
         return lib.lipcache_lookup(ctypes.byref(c) if c is not None else None, zq, B, prec, label, None, None,
                                    None, None, ws, wsb, None)
     assert call(None) == L.EINVAL
@@ -112,6 +112,7 @@ def test_lookup_validation():
     assert call(_cache(z=None)) == L.EINVAL
     assert call(_cache(), B=-1) == L.EINVAL
     assert call(_cache(), prec=5) == L.EINVAL
+    assert call(_cache(), prec=L.BF16) == L.EINVAL   # a store type, not a filter precision
     assert call(_cache(), zq=None) == L.EINVAL
     assert call(_cache(), label=None) == L.EINVAL
     assert call(_cache(d=1024), prec=L.F32) == L.EUNSUPPORTED
@@ -174,7 +175,7 @@ def test_index_build_validation():
 def test_lookup_indexed_validation():
     lib = L.load()
 
-    def call(c, ix, B=8, prec=L.BF16, ws=FAKE, wsb=1 << 30):
+    def call(c, ix, B=8, prec=L.F16, ws=FAKE, wsb=1 << 30):
         pairs = ctypes.c_int64(-1)
         st = lib.lipcache_lookup_indexed(ctypes.byref(c), ctypes.byref(ix) if ix is not None else None, FAKE, B,
                                          prec, FAKE, None, None, None, None, ctypes.byref(pairs), ws, wsb, None)
@@ -269,7 +270,7 @@ def test_consistency_validation():
 def test_filter_dump_validation():
     lib = L.load()
 
-    def call(c, B=8, prec=L.BF16, g=FAKE, cand=FAKE, ws=FAKE, wsb=1 << 30):
+    def call(c, B=8, prec=L.F16, g=FAKE, cand=FAKE, ws=FAKE, wsb=1 << 30):
         return lib.lipcache_lookup_filter_dump(ctypes.byref(c) if c is not None else None, FAKE, B, prec, g, cand,
                                                ws, wsb, None)
     assert call(None) == L.EINVAL

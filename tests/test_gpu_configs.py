@@ -69,7 +69,7 @@ def test_workload_full_size(name):
         rows = np.sort(np.random.default_rng(7).choice(B, rows, replace=False))
     ref = oracle.lookup_blocked(zq if rows is None else zq[rows], st.z, st.r, st.label)
     say(name, "oracle lookup of", B if rows is None else rows.size, "queries done")
-    for precision in ("bf16", "f32"):
+    for precision in ("f16", "f32"):
         res = cache.lookup(gpu(zq), precision=precision)
         nflag = compare_lookup(res, ref, f"{name}/{precision}", rows=rows)
         nhit = check_hits_valid(res, zq, st, wl.W, wl.b, f"{name}/{precision}")

@@ -86,8 +86,8 @@ def tiny():
     return out
 
 
-CASES = [("f32", "bf16", True), ("f32", "bf16", False), ("bf16", "bf16", True), ("f32", "f32", True),
-         ("bf16", "f32", True)]
+CASES = [("f32", "f16", True), ("f32", "f16", False), ("bf16", "f16", True), ("bf16", "f16", False),
+         ("f32", "f32", True), ("bf16", "f32", True)]
 
 
 @pytest.mark.parametrize("store,prec,image", CASES)
@@ -125,7 +125,7 @@ def test_build_is_deterministic(tiny, K, iters):
     check_index(c, a, f"determinism K={K}")
 
 
-@pytest.mark.parametrize("store,image", [("f32", True), ("bf16", True), ("f32", False)])
+@pytest.mark.parametrize("store,image", [("f32", True), ("bf16", True), ("f32", False), ("bf16", False)])
 def test_build_assigns_nearest_centres(tiny, store, image):
     """The final assignment puts every row in a cluster whose centre is the
     nearest one up to the rounding of the matrix-core distances: bf16 rows and
@@ -156,7 +156,7 @@ def test_every_pair_rechecked_once_when_queues_fill():
     same filter arithmetic, so both re-check the same number of pairs.  With
     256 clusters of about 64 rows and 512 queries, each of the 2,048 waves of
     the scan meets 4,096 passing pairs: its LDS queue fills (the rest are
-    re-checked at once) and the global queue (2 B + 65,536 slots) overflows
+    re-checked at once) and the global queue (4 B + 65,536 slots) overflows
     (the late waves settle their own queues) -- no pair may be lost or
     counted twice on any of these paths."""
     cfg = wlmod.WorkloadConfig("allhit-d64", d=64, C=10, n_cache=16384, batch=512, sigma=0.5)

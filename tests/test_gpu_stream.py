@@ -70,7 +70,7 @@ def test_stream_lockstep():
         idx = wlmod.near_indices(draws, st.n)
         zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
         ref = oracle.lookup_blocked(zq, st.z, st.r, st.label)
-        res = cache.lookup(gpu(zq), precision="bf16")
+        res = cache.lookup(gpu(zq), precision="f16")
         compare_lookup(res, ref, f"stream round {t}")
         lab = host(res.label)
         differs = lab != ref.label
@@ -106,7 +106,7 @@ def test_stream_full_size():
         zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
         n0, n0_o = cache.n, st.n
         before = oracle.CacheState(cfg.d, st.capacity, "bf16", st.z, st.r, st.label, st.norm2)
-        res, cq, got = cache.serve(gpu(zq), W, b, sig, precision="bf16")
+        res, cq, got = cache.serve(gpu(zq), W, b, sig, precision="f16")
         rows = np.sort(rng.choice(cfg.batch, sample, replace=False))
         ref = oracle.lookup_blocked(zq[rows], before.z, before.r, before.label)
         compare_lookup(res, ref, f"stream full round {t}", rows=rows)

@@ -199,6 +199,26 @@ lipcache_status lipcache_lookup(const lipcache_cache* c, const float* zq, int64_
 size_t lipcache_lookup_workspace_bytes(int64_t B, int64_t N, int32_t d, int32_t precision);
 
 /*
+ * lipcache_lookup for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments and results as lipcache_lookup without `ws`/`ws_bytes`.
+ * The workspace is a static device array of LIPCACHE_NOALLOC_SCRATCH_BYTES
+ * (32 MiB) per GPU, held until the process ends; the call allocates nothing.
+ * It serves lookups with lipcache_lookup_workspace_bytes(B, c->n, c->d,
+ * precision) <= LIPCACHE_NOALLOC_SCRATCH_BYTES (e.g. B = 65,536 queries
+ * against 4.5M entries) and returns LIPCACHE_EWORKSPACE, with nothing
+ * written, for larger ones.  Every call on one GPU uses that GPU's array:
+ * calls that overlap on one GPU (other streams or host threads) race, so
+ * serialise them.  (async)
+ */
+#define LIPCACHE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+lipcache_status lipcache_lookup_noalloc(const lipcache_cache* c, const float* zq, int64_t B,
+                                        int32_t precision, int32_t* label_out,
+                                        int64_t* index_out, float* dist2_out,
+                                        uint64_t* stats, uint8_t* band_flag,
+                                        lipcache_stream_t stream);
+
+/*
  * Write-back (Sec. 4.4, Alg. 2; construction, Alg. 1): append, in ascending
  * row order, every row j of z_src with r_src[j] > 0 and (miss_selector ==
  * NULL or miss_selector[j] == LIPCACHE_MISS).  The feature is stored in the

@@ -17,6 +17,7 @@ SELECT_RADIUS_DEDUP, SELECT_PRIORITY, SELECT_KCENTER = 0, 1, 2
 BOUNDARY_SCALED, BOUNDARY_GLOBAL, BOUNDARY_INTERCLASS = 0, 1, 2
 MISS = -1
 STAT_HITS, STAT_RECHECKED, STAT_BAND_PAIRS, STAT_BAND_QUERIES = range(4)
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 # Every function the header declares, with (restype, argtypes).
 _vp, _i32, _i64, _f64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_size_t
@@ -65,6 +66,7 @@ SIGNATURES = {
                                 _vp, _sz, _vp]),
     "lipcache_certify_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "lipcache_lookup": (_i32, [_PCACHE, _vp, _i64, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "lipcache_lookup_noalloc": (_i32, [_PCACHE, _vp, _i64, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
     "lipcache_lookup_workspace_bytes": (_sz, [_i64, _i64, _i32, _i32]),
     "lipcache_insert": (_i32, [_PCACHE, _vp, _vp, _vp, _vp, _i64, ctypes.POINTER(_i64), _vp, _sz, _vp]),
     "lipcache_insert_workspace_bytes": (_sz, [_i64]),

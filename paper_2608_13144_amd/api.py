@@ -185,6 +185,28 @@ class LipCache:
         L.check("lipcache_lookup", st)
         return out
 
+    def lookup_noalloc(self, zq: torch.Tensor, precision: str = "f16",
+                       out: LookupResult | None = None) -> LookupResult:
+        """lipcache_lookup_noalloc: lookup on the library's static per-GPU
+        workspace (no device allocation in the library; async)."""
+        _need_cuda(zq, "zq", torch.float32, 2)
+        if zq.shape[1] != self.d:
+            raise ValueError("lookup_noalloc: query width differs from the cache's d")
+        lib = L.load()
+        B = zq.shape[0]
+        dev = self.device
+        if out is None:
+            out = LookupResult(torch.empty(B, dtype=torch.int32, device=dev),
+                               torch.empty(B, dtype=torch.int64, device=dev),
+                               torch.empty(B, dtype=torch.float32, device=dev),
+                               torch.zeros(4, dtype=torch.int64, device=dev),
+                               torch.empty(B, dtype=torch.uint8, device=dev))
+        cs = self.cstruct()
+        st = lib.lipcache_lookup_noalloc(ctypes.byref(cs), _p(zq), B, _PRECISION[precision], _p(out.label),
+                                         _p(out.index), _p(out.dist2), _p(out.stats), _p(out.band), _stream(dev))
+        L.check("lipcache_lookup_noalloc", st)
+        return out
+
     def serve(self, zq: torch.Tensor, W: torch.Tensor, b: torch.Tensor | None, sigma: float,
               precision: str = "f16", out: LookupResult | None = None):
         """One round of certified serving (Alg. 2): look every query up, certify

@@ -47,6 +47,8 @@
 //    sums, so the same d^2 either way).
 #include <limits.h>
 
+#include <mutex>
+
 #include "lc_common.hpp"
 #include "lc_index.hpp"
 
@@ -1543,6 +1545,31 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
   return lookup_stage_finalize(B, w.best, w.bflag, c->label, label_out, index_out, dist2_out, band_flag, st, s);
 }
 
+// ------------------------------------------------------------- allocation-free entry
+// The workspace of lipcache_lookup_noalloc: one file-scope device array per
+// GPU, held until the process ends.  Host code never uses the array's name
+// as an address: hipGetSymbolAddress gives each device's own copy, looked up
+// once per device (with that device current) and kept in scratch_ptr.
+constexpr size_t kNoAllocBytes = LIPCACHE_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+constexpr int kMaxDevices = 64;
+static std::mutex scratch_mutex;
+static void* scratch_ptr[kMaxDevices];
+
+// This device's copy of `scratch`, or nullptr if it cannot be had.
+void* device_scratch() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(scratch_mutex);
+  if (!scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p || !aligned256(p)) return nullptr;
+    scratch_ptr[dev] = p;
+  }
+  return scratch_ptr[dev];
+}
+
 }  // namespace lc
 
 using namespace lc;
@@ -1581,4 +1608,20 @@ extern "C" lipcache_status lipcache_lookup_filter_dump(const lipcache_cache* c, 
                                                        size_t ws_bytes, lipcache_stream_t stream) {
   return run_lookup(c, zq, B, precision, nullptr, nullptr, nullptr, nullptr, nullptr, ws, ws_bytes,
                     reinterpret_cast<hipStream_t>(stream), true, g_hat, cand);
+}
+
+extern "C" lipcache_status lipcache_lookup_noalloc(const lipcache_cache* c, const float* zq, int64_t B,
+                                                   int32_t precision, int32_t* label_out, int64_t* index_out,
+                                                   float* dist2_out, uint64_t* stats, uint8_t* band_flag,
+                                                   lipcache_stream_t stream) {
+  const lipcache_status vs = lookup_check(c, zq, B, precision, false, label_out, nullptr, nullptr);
+  if (vs != LIPCACHE_OK) return vs;
+  FilterConsts fc;
+  const lipcache_status cs = lookup_consts(c, precision, fc);
+  if (cs != LIPCACHE_OK) return cs;
+  if (ws_layout(B, c->n, nullptr, nullptr) > kNoAllocBytes) return LIPCACHE_EWORKSPACE;
+  void* ws = device_scratch();
+  if (!ws) return LIPCACHE_EHIP;
+  return lookup_on(c, zq, B, precision, fc, label_out, index_out, dist2_out, stats, band_flag, ws,
+                   reinterpret_cast<hipStream_t>(stream), false, nullptr, nullptr);
 }

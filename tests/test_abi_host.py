@@ -120,6 +120,30 @@ def test_lookup_validation():
     assert call(_cache(), wsb=64) == L.EWORKSPACE
 
 
+def test_lookup_noalloc_validation():
+    """The allocation-free lookup validates like lipcache_lookup and refuses,
+    before any device work, a lookup whose workspace exceeds its static array."""
+    lib = L.load()
+
+    def call(c, B=8, prec=L.F16, zq=FAKE, label=FAKE):
+        return lib.lipcache_lookup_noalloc(ctypes.byref(c) if c is not None else None, zq, B, prec, label, None,
+                                           None, None, None, None)
+    assert call(None) == L.EINVAL
+    assert call(_cache(d=48)) == L.EINVAL
+    assert call(_cache(), B=-1) == L.EINVAL
+    assert call(_cache(), prec=L.BF16) == L.EINVAL
+    assert call(_cache(), label=None) == L.EINVAL
+    assert call(_cache(d=1024), prec=L.F32) == L.EUNSUPPORTED
+    # the largest n that fits with B = 65,536, and one row more
+    B = 65536
+    n = 4_500_000
+    assert lib.lipcache_lookup_workspace_bytes(B, n, 64, L.F16) <= L.NOALLOC_SCRATCH_BYTES
+    big = 1 << 23
+    assert lib.lipcache_lookup_workspace_bytes(B, big, 64, L.F16) > L.NOALLOC_SCRATCH_BYTES
+    assert call(_cache(n=big, capacity=big), B=B) == L.EWORKSPACE
+    assert call(_cache(n=16, capacity=16), B=1 << 24) == L.EWORKSPACE
+
+
 def test_insert_validation():
     lib = L.load()
 

@@ -9,4 +9,4 @@ from .lipcache_oracle import (MISS, BAND_REL, DegenerateHead, CapacityError,  # 
                               logits_of, lookup, lookup_rows, lookup_blocked, insert,
                               CacheState, construct, SELECT_STRATEGIES,
                               boundary_radius, consistency, BOUNDARY_MODES,
-                              cluster_pruned_lookup)
+                              cluster_pruned_lookup, lookup_partitioned)

@@ -32,6 +32,10 @@ bfloat16 cache), with float64 as the stand-in for exact arithmetic:
                          pruning clusters by the triangle inequality (the
                          exact sublinear index of Sec. 4.4); pinned equal to
                          ``lookup`` on every partition.
+  * ``lookup_partitioned`` - every field of ``lookup`` (band counts and flags
+                         too) through a partition, for full-size batches;
+                         pinned equal to ``lookup`` on every partition and
+                         at the band's edges.
   * ``boundary_radius``, ``consistency`` - the reuse boundaries compared in
                          Sec. 6 (scaled certified radius, global threshold,
                          inter-class empirical radius) and the
@@ -647,6 +651,81 @@ def cluster_pruned_lookup(zq, cache_z, cache_r, cache_label, assign, centres=Non
     out = LookupResult(cat("label").astype(np.int32), cat("index").astype(np.int64), cat("dist2"),
                        cat("n_hits").astype(np.int64), cat("n_band").astype(np.int64), cat("flagged").astype(bool))
     return out, pairs
+
+
+def lookup_partitioned(zq, cache_z, cache_r, cache_label, assign, centres, band_rel: float = BAND_REL,
+                       widen: float = 1e-6) -> LookupResult:
+    """``lookup`` for full-size batches, through a partition of the rows: the
+    same ``LookupResult`` as ``lookup``, every field (band counts and flags
+    included).
+
+    Row i belongs to cluster ``assign[i]`` with centre ``centres[c]``.  A
+    row of cluster c with ||q - mu_c|| >= R_c = max over its live rows of
+    ||z_i - mu_c|| + (1 + band_rel) r_i lies at D = ||q - z_i|| >= ||q -
+    mu_c|| - ||z_i - mu_c|| >= (1 + band_rel) r_i from the query (triangle
+    inequality): neither a hit (D < r_i, Eq. (13)) nor a band pair (|D - r_i|
+    <= band_rel r_i) unless D sits exactly on the band's outer edge.  So only
+    clusters with ||q - mu_c|| < R_c (1 + widen) + widen are searched; the
+    widening covers that edge and the float64 rounding of these norms.  Every
+    hit and band pair of q lies in its searched clusters, and so do its
+    answer, hit count, band count and flag (all defined by those pairs
+    alone).  A query with one searched cluster gets ``lookup_blocked`` on
+    that cluster's rows; one with several gets ``lookup`` on their union.
+    """
+    Q = np.asarray(zq, dtype=np.float64)
+    Z = np.asarray(cache_z)
+    r = np.asarray(cache_r, dtype=np.float32)
+    lab = np.asarray(cache_label, dtype=np.int32)
+    a = np.asarray(assign, dtype=np.int64)
+    mu = np.asarray(centres, dtype=np.float64)
+    B, K = Q.shape[0], mu.shape[0]
+    out = LookupResult(np.full(B, MISS, dtype=np.int32), np.full(B, -1, dtype=np.int64), np.full(B, np.inf),
+                       np.zeros(B, dtype=np.int64), np.zeros(B, dtype=np.int64), np.zeros(B, dtype=bool))
+    if B == 0 or Z.shape[0] == 0:
+        return out
+    order = np.argsort(a, kind="stable")              # rows of each cluster in ascending order
+    starts = np.searchsorted(a[order], np.arange(K + 1))
+    R = np.full(K, -np.inf)
+    r64 = r.astype(np.float64)
+    for c in range(K):
+        rows = order[starts[c]:starts[c + 1]]
+        live = rows[r[rows] > 0]
+        if live.size:
+            dz = np.sqrt(np.sum((Z[live].astype(np.float64) - mu[c]) ** 2, axis=1))
+            R[c] = np.max(dz + (1.0 + band_rel) * r64[live])
+    reach = R * (1.0 + widen) + widen
+    # ||q - mu_c||^2 from the float64 expansion, less a bound on its rounding
+    # error (4 (d + 4) 2^-53 (||q||^2 + ||mu_c||^2)): a superset of the
+    # clusters with ||q - mu_c|| < reach
+    nq = np.sum(Q * Q, axis=1)
+    nm = np.sum(mu * mu, axis=1)
+    tol = 4.0 * (Q.shape[1] + 4) * 2.0 ** -53
+    searched = np.empty((B, K), dtype=bool)
+    for s0 in range(0, B, 8192):
+        s1 = min(B, s0 + 8192)
+        scale = nq[s0:s1, None] + nm[None, :]
+        d2 = scale - 2.0 * (Q[s0:s1] @ mu.T)
+        searched[s0:s1] = (d2 - tol * scale < (reach * reach)[None, :]) & (R > -np.inf)[None, :]
+    count = searched.sum(axis=1)
+
+    def put(qidx, res, rows):
+        out.label[qidx] = res.label
+        out.index[qidx] = np.where(res.index >= 0, rows[np.maximum(res.index, 0)], -1)
+        out.dist2[qidx] = res.dist2
+        out.n_hits[qidx] = res.n_hits
+        out.n_band[qidx] = res.n_band
+        out.flagged[qidx] = res.flagged
+
+    only = np.where(count == 1, np.argmax(searched, axis=1), -1)
+    for c in range(K):
+        qidx = np.flatnonzero(only == c)
+        rows = order[starts[c]:starts[c + 1]]
+        if qidx.size and rows.size:
+            put(qidx, lookup_blocked(Q[qidx], Z[rows], r[rows], lab[rows], band_rel), rows)
+    for qi in np.flatnonzero(count > 1):
+        rows = np.sort(np.concatenate([order[starts[c]:starts[c + 1]] for c in np.flatnonzero(searched[qi])]))
+        put(np.array([qi]), lookup(Q[qi:qi + 1], Z[rows], r[rows], lab[rows], band_rel), rows)
+    return out
 
 
 def consistency(lookup_label, head_label):

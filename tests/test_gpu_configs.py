@@ -3,10 +3,12 @@
 Per workload: sigma, labels and radii of all N cache candidates against the
 oracle's certify; the cache built on the device from the device's own
 certificates; one batch of queries composed from the oracle's cache state;
-the lookup with both filters, compared with the oracle query by query (all
-queries where the blocked oracle finishes in seconds, a seeded sample of
-2,048 at N = 1M), and every hit of the whole batch checked for validity and
-certified consistency.
+the lookup with both filters compared with the oracle on EVERY query of the
+batch (``oracle.lookup_partitioned`` through the workload's own mixture
+components, itself cross-checked against ``oracle.lookup_blocked`` on a
+seeded sample), and every hit checked for validity and certified
+consistency.  At the headline workload the lookup is also run twice and must
+give the same bytes.
 """
 import numpy as np
 import pytest
@@ -19,7 +21,7 @@ from gpu_helpers import DEV, check_hits_valid, compare_lookup, gpu, host, oracle
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
-SAMPLE = {"tiny-d64-c10": None, "mix-d128-c10": None, "mix-d128-c100": None, "mix-d256-c200": 2048}
+NAMES = ["tiny-d64-c10", "mix-d128-c10", "mix-d128-c100", "mix-d256-c200"]
 
 
 def check_certify(cert_gpu, cert_o, W, what):
@@ -38,7 +40,18 @@ def check_certify(cert_gpu, cert_o, W, what):
     return int(near_tie.sum())
 
 
-@pytest.mark.parametrize("name", list(SAMPLE))
+def full_batch_reference(zq, st, assign, mu, what, sample=512):
+    """The oracle's answer for every query, through the mixture partition;
+    on a seeded sample it must equal the blocked oracle's field by field."""
+    ref = oracle.lookup_partitioned(zq, st.z, st.r, st.label, assign, mu)
+    rows = np.sort(np.random.default_rng(7).choice(zq.shape[0], min(sample, zq.shape[0]), replace=False))
+    chk = oracle.lookup_blocked(zq[rows], st.z, st.r, st.label)
+    for f in ("label", "index", "dist2", "n_hits", "n_band", "flagged"):
+        assert np.array_equal(getattr(chk, f), getattr(ref, f)[rows]), f"{what}: partitioned oracle {f}"
+    return ref
+
+
+@pytest.mark.parametrize("name", NAMES)
 def test_workload_full_size(name):
     cfg = wlmod.CONFIGS[name]
     say("workload", name, "N", cfg.n_cache, "B", cfg.batch, "d", cfg.d, "C", cfg.C)
@@ -48,6 +61,7 @@ def test_workload_full_size(name):
     sig_o = oracle.spectral_norm(wl.W).sigma
     cert_o = oracle.certify(wl.z, wl.W, wl.b, sig_o, store=cfg.store_dtype)
     st = oracle_cache(wl.z, cert_o.label, cert_o.r, d, store=cfg.store_dtype)
+    assign = wl.z_class[cert_o.r > 0]          # insert keeps the certified rows in order
     say(name, "oracle chain done, n", st.n)
 
     W, b, z = gpu(wl.W), gpu(wl.b), gpu(wl.z)
@@ -64,18 +78,20 @@ def test_workload_full_size(name):
     draws = wlmod.draw_queries(wl, 0)
     idx = wlmod.near_indices(draws, st.n)
     zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
-    rows = SAMPLE[name]
-    if rows is not None:
-        rows = np.sort(np.random.default_rng(7).choice(B, rows, replace=False))
-    ref = oracle.lookup_blocked(zq if rows is None else zq[rows], st.z, st.r, st.label)
-    say(name, "oracle lookup of", B if rows is None else rows.size, "queries done")
+    ref = full_batch_reference(zq, st, assign, wl.mu, name)
+    say(name, "oracle lookup of all", B, "queries done; flagged", int(ref.flagged.sum()))
     for precision in ("f16", "f32"):
         res = cache.lookup(gpu(zq), precision=precision)
-        nflag = compare_lookup(res, ref, f"{name}/{precision}", rows=rows)
+        nflag = compare_lookup(res, ref, f"{name}/{precision}")
         nhit = check_hits_valid(res, zq, st, wl.W, wl.b, f"{name}/{precision}")
         stats = host(res.stats)
         assert stats[0] == nhit
         assert 0.2 < nhit / B < 0.32, nhit / B
         say(name, precision, "hits", nhit, "flagged", nflag, "near-tie entries", ties, "stats", stats.tolist())
+        if name == "mix-d256-c200":
+            again = cache.lookup(gpu(zq), precision=precision)
+            for f in ("label", "index", "dist2", "stats", "band"):
+                a, b2 = getattr(res, f), getattr(again, f)
+                assert torch.equal(a.view(torch.uint8), b2.view(torch.uint8)), f"{name}/{precision}: run twice {f}"
     del cache
     torch.cuda.empty_cache()

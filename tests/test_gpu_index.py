@@ -15,7 +15,7 @@ hit and band counters), for both stores and filters, K from 1 to n,
 rows appended after the build, dead rows, duplicated rows (empty
 clusters), queries with more candidate clusters than a list takes, a
 ragged batch, non-finite queries, wide features (d = 512, 1024), and the
-full-size mixture.
+full-size mixture (every query of the batch).
 """
 import numpy as np
 import pytest
@@ -313,7 +313,8 @@ def test_full_size_mixture():
     res_i, pairs = c.lookup_indexed(ix, q)
     res_d = c.lookup(q)
     same_as_dense(res_i, res_d, "full")
-    rows = np.sort(np.random.default_rng(7).choice(zq.shape[0], 2048, replace=False))
-    compare_lookup(res_i, oracle.lookup_blocked(zq[rows], st.z, st.r, st.label), "full sample", rows=rows)
+    keep = cert_o.r > 0
+    ref = oracle.lookup_partitioned(zq, st.z, st.r, st.label, wl.z_class[keep], wl.mu)
+    compare_lookup(res_i, ref, "full batch")
     say("index full size pairs", pairs, "fraction", pairs / (zq.shape[0] * st.n))
     assert pairs < 0.5 * zq.shape[0] * st.n

@@ -9,12 +9,14 @@ miss is stored as) and appends the misses.
   only on queries the oracle flags (a pair within relative 1e-5 of a ball
   boundary), both append the oracle's miss set, so the states stay in
   lockstep; any other difference fails.
-* ``test_stream_full_size`` runs the full workload (2,097,152 initial entries,
-  16 rounds of 65,536 queries) on the device as bench.py does.  The oracle
-  cannot afford 16 full rounds, so per round it checks a seeded sample of
-  queries exactly, every hit for validity and certified consistency, and the
-  appended rows (bf16 values, labels, radii) against its own certify of the
-  queries; its state then appends the rows the device's miss set selects.
+* ``test_stream_full_size_round`` runs the full workload (2,097,152 initial
+  entries, 16 rounds of 65,536 queries, one test per round) with the same
+  protocol: every query of every round is compared with the oracle
+  (``oracle.lookup_partitioned`` through the mixture components; appended
+  rows join the cluster of their nearest class mean), every hit is checked
+  for validity and certified consistency, both sides append the oracle's
+  miss set, and the appended rows (bf16 values, labels, radii) must equal
+  the oracle's certify of the queries.
 """
 import numpy as np
 import pytest
@@ -43,7 +45,7 @@ def _initial(cfg, n_cache, capacity):
     cert = api.certify(gpu(wl.z), W, b, sig.sigma, store="bf16")
     cache.insert(gpu(wl.z), cert.label, cert.r)
     assert cache.n == st.n
-    return wl, sig_o, st, W, b, sig.sigma, cache
+    return wl, sig_o, st, W, b, sig.sigma, cache, cert_o.r > 0
 
 
 def _check_appended(cache, n0, st, n0_o, what):
@@ -62,7 +64,7 @@ def test_stream_lockstep():
     cfg = wlmod.CONFIGS[NAME]
     n_cache, B, rounds = 8192, 1024, 4
     cap = n_cache + rounds * B
-    wl, sig_o, st, W, b, sig, cache = _initial(cfg, n_cache, cap)
+    wl, sig_o, st, W, b, sig, cache, _ = _initial(cfg, n_cache, cap)
     adopted = 0
     for t in range(rounds):
         say("stream lockstep round", t, "n", st.n)
@@ -93,29 +95,59 @@ def test_stream_lockstep():
     assert st.n > n_cache + rounds * B // 2
 
 
-@pytest.mark.slow
-def test_stream_full_size():
+def _nearest_mean(x, mu):
+    """Cluster of appended rows for the oracle's partition: the nearest class
+    mean (any assignment keeps lookup_partitioned exact)."""
+    X = np.asarray(x, dtype=np.float64)
+    d2 = (X * X).sum(1)[:, None] + (mu * mu).sum(1)[None, :] - 2.0 * X @ mu.T
+    return np.argmin(d2, axis=1)
+
+
+@pytest.fixture(scope="module")
+def full_stream():
     cfg = wlmod.CONFIGS[NAME]
-    sample = 256
-    wl, sig_o, st, W, b, sig, cache = _initial(cfg, cfg.n_cache, cfg.capacity)
+    wl, sig_o, st, W, b, sig, cache, keep = _initial(cfg, cfg.n_cache, cfg.capacity)
+    state = dict(cfg=cfg, wl=wl, sig_o=sig_o, st=st, W=W, b=b, sig=sig, cache=cache,
+                 assign=wl.z_class[keep].astype(np.int64), round=0, adopted=0)
     say("stream full size: initial n", st.n)
-    rng = np.random.default_rng(11)
-    for t in range(cfg.rounds):
-        draws = wlmod.draw_queries(wl, t)
-        idx = wlmod.near_indices(draws, st.n)
-        zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
-        n0, n0_o = cache.n, st.n
-        before = oracle.CacheState(cfg.d, st.capacity, "bf16", st.z, st.r, st.label, st.norm2)
-        res, cq, got = cache.serve(gpu(zq), W, b, sig, precision="f16")
-        rows = np.sort(rng.choice(cfg.batch, sample, replace=False))
-        ref = oracle.lookup_blocked(zq[rows], before.z, before.r, before.label)
-        compare_lookup(res, ref, f"stream full round {t}", rows=rows)
-        nhit = check_hits_valid(res, zq, before, wl.W, wl.b, f"stream full round {t}")
-        cq_o = oracle.certify(zq, wl.W, wl.b, sig_o, store="bf16")
-        oracle.insert(st, zq, cq_o.label, cq_o.r, host(res.label))
-        assert got == st.n - n0_o and cache.n == st.n
-        _check_appended(cache, n0, st, n0_o, f"full round {t}")
-        say("stream full round", t, "n", n0, "->", cache.n, "hits", nhit, "stats", host(res.stats).tolist())
-    assert cache.n > cfg.n_cache + cfg.rounds * cfg.batch // 2
-    del cache
+    yield state
+    del state["cache"]
     torch.cuda.empty_cache()
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("t", range(16))
+def test_stream_full_size_round(full_stream, t):
+    """Round t of the full streaming workload (65,536 queries against 2.1M ->
+    2.9M bf16 entries): every query compared with the oracle (through the
+    mixture partition), every hit valid and certified-consistent, both sides
+    append the oracle's miss set, and the appended rows (bf16 bits, labels,
+    radii) equal the oracle's certify."""
+    S = full_stream
+    assert S["round"] == t, "rounds run in order"
+    cfg, wl, st, cache = S["cfg"], S["wl"], S["st"], S["cache"]
+    draws = wlmod.draw_queries(wl, t)
+    idx = wlmod.near_indices(draws, st.n)
+    zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
+    n0, n0_o = cache.n, st.n
+    before = oracle.CacheState(cfg.d, st.capacity, "bf16", st.z, st.r, st.label, st.norm2)
+    res = cache.lookup(gpu(zq), precision="f16")
+    ref = oracle.lookup_partitioned(zq, st.z, st.r, st.label, S["assign"], wl.mu)
+    compare_lookup(res, ref, f"stream full round {t}")
+    nhit = check_hits_valid(res, zq, before, wl.W, wl.b, f"stream full round {t}")
+    lab = host(res.label)
+    differs = lab != ref.label          # only flagged queries can get here
+    S["adopted"] += int(differs.sum())
+    sel = gpu(ref.label) if differs.any() else res.label
+    cq_o = oracle.certify(zq, wl.W, wl.b, S["sig_o"], store="bf16")
+    oracle.insert(st, zq, cq_o.label, cq_o.r, ref.label)
+    cq = api.certify(gpu(zq), S["W"], S["b"], S["sig"], store="bf16")
+    got = cache.insert(gpu(zq), cq.label, cq.r, sel)
+    assert got == st.n - n0_o and cache.n == st.n
+    _check_appended(cache, n0, st, n0_o, f"full round {t}")
+    S["assign"] = np.concatenate([S["assign"], _nearest_mean(st.z[n0_o:], wl.mu)])
+    S["round"] = t + 1
+    say("stream full round", t, "n", n0, "->", cache.n, "hits", nhit, "flagged", int(ref.flagged.sum()),
+        "adopted so far", S["adopted"], "stats", host(res.stats).tolist())
+    if t == cfg.rounds - 1:
+        assert cache.n > cfg.n_cache + cfg.rounds * cfg.batch // 2

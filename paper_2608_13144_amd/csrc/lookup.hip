@@ -149,12 +149,39 @@ __device__ __forceinline__ float entry_threshold(float rr, float n2f, double kap
   return f32_round_down((kappa_c * n2 - r2) * 0.5 - eta1 * __builtin_sqrt(n2) - 0.5 * kFilterAbsSlack);
 }
 
-// One wave per query: Q_q, reset of the per-query state and of the counters.
+// Per-entry threshold of row i < n_pad (+inf for the padding past n).
+__device__ __forceinline__ void write_athr(int64_t i, const float* __restrict__ cr, const float* __restrict__ cnorm2,
+                                           int64_t n, int64_t n_pad, double kappa_c, double eta1, double range2,
+                                           float* __restrict__ athr) {
+  if (i >= n_pad) return;
+  athr[i] = i < n ? entry_threshold(cr[i], cnorm2[i], kappa_c, eta1, range2) : __builtin_inff();
+}
+
+// The entries a prep launch also covers (athr == nullptr: none).
+struct PrepEntries {
+  const float* cr;
+  const float* cnorm2;
+  int64_t n;
+  int64_t n_pad;
+  float* athr;
+  unsigned long long* gq_count;  // emptied for the scan that follows (nullable)
+};
+
+// Blocks [0, qblocks): one wave per query, Q_q, reset of the per-query state
+// and (block 0) of the counters.  Blocks past qblocks: the per-entry
+// thresholds A_i, 512 rows per block.  One launch for both.
 __global__ void lookup_prep_kernel(const float* __restrict__ zq, int64_t B, int d, const Thresholds t,
                                    float* __restrict__ qthr, unsigned long long* __restrict__ best,
-                                   unsigned int* __restrict__ bflag, unsigned long long* __restrict__ stats) {
+                                   unsigned int* __restrict__ bflag, unsigned long long* __restrict__ stats,
+                                   unsigned qblocks, const PrepEntries pe) {
+  if (blockIdx.x >= qblocks) {
+    write_athr(static_cast<int64_t>(blockIdx.x - qblocks) * kLkThreads + threadIdx.x, pe.cr, pe.cnorm2, pe.n,
+               pe.n_pad, t.kappa_c, t.eta1, t.range2, pe.athr);
+    return;
+  }
   const int64_t q = static_cast<int64_t>(blockIdx.x) * kLkWaves + threadIdx.x / kWave;
   if (blockIdx.x == 0 && threadIdx.x < 4) stats[threadIdx.x] = 0;
+  if (blockIdx.x == 0 && threadIdx.x == 4 && pe.gq_count) *pe.gq_count = 0ull;
   if (q >= B) return;
   const float* row = zq + q * d;
   double s = 0.0;
@@ -174,8 +201,7 @@ __global__ void lookup_athr_kernel(const float* __restrict__ cr, const float* __
                                    float* __restrict__ athr, unsigned long long* __restrict__ gq_count) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i == 0 && gq_count) *gq_count = 0ull;
-  if (i >= n_pad) return;
-  athr[i] = i < n ? entry_threshold(cr[i], cnorm2[i], kappa_c, eta1, range2) : __builtin_inff();
+  write_athr(i, cr, cnorm2, n, n_pad, kappa_c, eta1, range2, athr);
 }
 
 // float16 copy of the queries, for the work-list kernel.
@@ -812,23 +838,33 @@ __device__ __forceinline__ void lds_copy(const void* sbase, uint32_t voff, const
   }
 }
 
-// Cache rows per LDS tile of the DMA kernel: 64 KiB per buffer (rows of
-// 64 * KS bytes in either element type), at most 128 rows.
-template <int KS>
+// Waves per workgroup of the slice-mode DMA kernel (the work-list kernel
+// keeps 8).
+#ifndef LC_DMA_WAVES
+#define LC_DMA_WAVES 8
+#endif
+constexpr int kDmaWaves = LC_DMA_WAVES;
+
+// Cache rows per LDS tile of the DMA kernel with NW waves: 64 KiB per buffer
+// for 8 waves, 32 KiB for 4 (rows of 64 * KS bytes in either element type),
+// at most 128 rows.
+template <int KS, int NW>
 struct DmaTraits {
-  static constexpr int kRows = KS <= 8 ? 128 : 64;
+  static constexpr int kRows = NW == 8 ? (KS <= 8 ? 128 : 64) : (KS <= 8 ? 64 : 32);
+  static constexpr int kAthr = kRows < kWave ? kWave : kRows;  // thresholds staged per tile
 };
 constexpr int kDmaMaxRows = 128;
 
-template <int MODE, int KS>
+template <int MODE, int KS, int NW>
 __device__ __forceinline__ void issue_tile(unsigned char* buf, float* athr_buf, const LookupParams& p, int64_t t0,
                                            int64_t e_end, int wave) {
   using T = ModeTraits<MODE>;
+  constexpr int kThreads = NW * kWave;
   constexpr int kCPR = 4 * KS;  // 16-byte chunks per LDS row
-  constexpr int kRows = DmaTraits<KS>::kRows;
-  constexpr int kIters = kRows * kCPR / kLkThreads;
-  static_assert(kIters >= 1 && kIters * kLkThreads == kRows * kCPR, "whole copies per thread");
-  constexpr int kRowsPerIter = kLkThreads / kCPR;
+  constexpr int kRows = DmaTraits<KS, NW>::kRows;
+  constexpr int kIters = kRows * kCPR / kThreads;
+  static_assert(kIters >= 1 && kIters * kThreads == kRows * kCPR, "whole copies per thread");
+  constexpr int kRowsPerIter = kThreads / kCPR;
   const int d_chunks = p.d * T::kElemBytes / 16;
   const int row_bytes = p.d * T::kElemBytes;
   const int tid = static_cast<int>(threadIdx.x);
@@ -846,10 +882,12 @@ __device__ __forceinline__ void issue_tile(unsigned char* buf, float* athr_buf, 
     // there, so they add nothing.
     if (c >= d_chunks) c -= d_chunks;
     const int rr = row < last ? row : last;
-    lds_copy<16>(base, static_cast<uint32_t>(rr * row_bytes + c * 16), buf + (j * kLkThreads + wave * kWave) * 16);
+    lds_copy<16>(base, static_cast<uint32_t>(rr * row_bytes + c * 16), buf + (j * kThreads + wave * kWave) * 16);
   }
-  // thresholds of the tile's rows (+inf padding past n): one wave per 64
-  if (wave < kRows / kWave)
+  // thresholds of the tile's rows (+inf padding past n): one wave per 64,
+  // at least 64 (a tile of fewer rows stages the next ones too; the array
+  // holds them: it is padded by kDmaMaxRows past the last tile start)
+  if (wave < DmaTraits<KS, NW>::kAthr / kWave)
     lds_copy<4>(p.athr + t0 + wave * kWave, static_cast<uint32_t>(lane_id() * 4),
                 static_cast<unsigned char*>(static_cast<void*>(athr_buf)) + wave * kWave * 4);
 }
@@ -902,13 +940,13 @@ __device__ __forceinline__ void filter_and_recheck(const LookupParams& p, const 
 // the same wave evaluates the filter of column tile s - 1 (its accumulators
 // are kept one step longer), so the filter's VALU work fills the matrix
 // pipe's shadow instead of following it.
-template <int MODE, int STORE, int KS, int RT, bool LIST>
+template <int MODE, int STORE, int KS, int RT, int NW, bool LIST>
 __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, const float* athr_buf,
                                                   const LookupParams& p, int64_t t0, int64_t qwave, int64_t qend,
                                                   const int32_t* qlist, int m16, int g,
                                                   const u32x4 (&a)[RT][KS], const f32x4 (&qv)[RT],
                                                   RecheckQueue& rq) {
-  constexpr int kSubs = DmaTraits<KS>::kRows / kColTile;
+  constexpr int kSubs = DmaTraits<KS, NW>::kRows / kColTile;
   constexpr int kE = RT * 4;                      // accumulators per lane
   constexpr int kPer = (kE + KS - 1) / KS;        // filter terms folded into each k-step
   u32x4 b0 = lds_operand<KS>(buf, 0, 0, m16, g);
@@ -974,16 +1012,16 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
   }
 }
 
-template <int MODE, int STORE, int KS, int RT, bool DUMP, bool LIST>
+template <int MODE, int STORE, int KS, int RT, int NW, bool DUMP, bool LIST>
 __device__ __forceinline__ void compute_tile(const unsigned char* buf, const float* athr_buf, const LookupParams& p,
                                              int64_t t0, int64_t e_end, int64_t qwave, int64_t qend,
                                              const int32_t* qlist, int m16, int g, const u32x4 (&a)[RT][KS],
                                              const f32x4 (&qv)[RT], RecheckQueue& rq) {
-  constexpr int kRows = DmaTraits<KS>::kRows;
+  constexpr int kRows = DmaTraits<KS, NW>::kRows;
   const int64_t left = e_end - t0;
   if constexpr (!DUMP) {
     if (left >= kRows) {
-      compute_full_tile<MODE, STORE, KS, RT, LIST>(buf, athr_buf, p, t0, qwave, qend, qlist, m16, g, a, qv, rq);
+      compute_full_tile<MODE, STORE, KS, RT, NW, LIST>(buf, athr_buf, p, t0, qwave, qend, qlist, m16, g, a, qv, rq);
       return;
     }
   }
@@ -1066,21 +1104,23 @@ __device__ __forceinline__ void compute_tile(const unsigned char* buf, const flo
   }
 }
 
-template <int MODE, int STORE, int KS, int RT, bool DUMP, bool LIST>
-__global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupParams p) {
+// NW waves per workgroup (8, or 4 with two workgroups per CU), two waves
+// per SIMD either way.
+template <int MODE, int STORE, int KS, int RT, int NW, bool DUMP, bool LIST>
+__global__ __launch_bounds__(NW * kWave, 2) void lookup_dma_kernel(const LookupParams p) {
   using T = ModeTraits<MODE>;
   constexpr int kCPR = 4 * KS;
-  constexpr int kRows = DmaTraits<KS>::kRows;
+  constexpr int kRows = DmaTraits<KS, NW>::kRows;
   constexpr int kTileBytes = kRows * kCPR * 16;
   __shared__ __attribute__((aligned(16))) unsigned char buf0[kTileBytes];
   __shared__ __attribute__((aligned(16))) unsigned char buf1[kTileBytes];
-  __shared__ __attribute__((aligned(16))) float ath0[kRows];
-  __shared__ __attribute__((aligned(16))) float ath1[kRows];
-  __shared__ int64_t rq_e[LIST ? kLkWaves * kRq : 1];
-  __shared__ int32_t rq_q[LIST ? kLkWaves * kRq : 1];
+  __shared__ __attribute__((aligned(16))) float ath0[DmaTraits<KS, NW>::kAthr];
+  __shared__ __attribute__((aligned(16))) float ath1[DmaTraits<KS, NW>::kAthr];
+  __shared__ int64_t rq_e[LIST ? NW * kRq : 1];
+  __shared__ int32_t rq_q[LIST ? NW * kRq : 1];
 
   int64_t q0, qend, e_begin, e_end;
-  block_work(p, kLkWaves * RT * 16, q0, qend, e_begin, e_end);
+  block_work(p, NW * RT * 16, q0, qend, e_begin, e_end);
   const int32_t* qlist = LIST ? p.qlist : nullptr;
   if constexpr (!LIST) qend = p.B;
 
@@ -1094,7 +1134,7 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
   // Work-list mode: a wave whose queries all lie past the list's end only
   // moves its share of each tile (the copies and barriers are the block's).
   const bool active = !LIST || qwave < qend;
-  issue_tile<MODE, KS>(buf0, ath0, p, e_begin, e_end, wave);
+  issue_tile<MODE, KS, NW>(buf0, ath0, p, e_begin, e_end, wave);
 
   u32x4 a[RT][KS];
   if (active) load_query_operands<MODE, KS, RT, LIST && MODE == kModeF16>(p, qlist, qwave, qend, m16, g, a);
@@ -1118,14 +1158,16 @@ __global__ __launch_bounds__(kLkThreads, 2) void lookup_dma_kernel(const LookupP
     wait_copies();
     __syncthreads();
     const bool more1 = t0 + kRows < e_end;
-    if (more1) issue_tile<MODE, KS>(buf1, ath1, p, t0 + kRows, e_end, wave);
-    if (active) compute_tile<MODE, STORE, KS, RT, DUMP, LIST>(buf0, ath0, p, t0, e_end, qwave, qend, qlist, m16, g, a, qv, rq);
+    if (more1) issue_tile<MODE, KS, NW>(buf1, ath1, p, t0 + kRows, e_end, wave);
+    if (active)
+      compute_tile<MODE, STORE, KS, RT, NW, DUMP, LIST>(buf0, ath0, p, t0, e_end, qwave, qend, qlist, m16, g, a, qv, rq);
     if (!more1) break;
     wait_copies();
     __syncthreads();
     const bool more2 = t0 + 2 * kRows < e_end;
-    if (more2) issue_tile<MODE, KS>(buf0, ath0, p, t0 + 2 * kRows, e_end, wave);
-    if (active) compute_tile<MODE, STORE, KS, RT, DUMP, LIST>(buf1, ath1, p, t0 + kRows, e_end, qwave, qend, qlist, m16, g, a, qv, rq);
+    if (more2) issue_tile<MODE, KS, NW>(buf0, ath0, p, t0 + 2 * kRows, e_end, wave);
+    if (active)
+      compute_tile<MODE, STORE, KS, RT, NW, DUMP, LIST>(buf1, ath1, p, t0 + kRows, e_end, qwave, qend, qlist, m16, g, a, qv, rq);
     if (!more2) break;
   }
   if constexpr (LIST) {
@@ -1140,12 +1182,13 @@ struct Plan {
   int d_pad = 0;
   int qblock = 0;
   bool dma = false;
+  int waves = 0;      // waves per workgroup
   int tile_rows = 0;  // cache rows per LDS tile of the chosen kernel
 };
 
 inline int rt_for(int ks) { return ks <= 8 ? 4 : (ks == 16 ? 2 : 1); }
 
-inline bool make_plan(int precision, const lipcache_cache* c, Plan& pl) {
+inline bool make_plan(int precision, const lipcache_cache* c, bool list, Plan& pl) {
   const int per_step = precision == LIPCACHE_F16 ? 32 : 16;
   int ks = precision == LIPCACHE_F16 ? 1 : 2;
   while (ks * per_step < c->d) ks *= 2;
@@ -1153,13 +1196,18 @@ inline bool make_plan(int precision, const lipcache_cache* c, Plan& pl) {
   pl.ks = ks;
   pl.rt = rt_for(ks);
   pl.d_pad = ks * per_step;
-  pl.qblock = kLkWaves * pl.rt * 16;
   // The DMA kernel needs rows already in the MFMA element type (the float16
   // image, or an fp32 store for the fp32 filter) and two LDS tiles of at
   // most 64 KiB.
   const bool same_type = precision == LIPCACHE_F16 ? c->zimg != nullptr : c->store_dtype == LIPCACHE_F32;
   pl.dma = same_type && ks <= 16;
-  pl.tile_rows = pl.dma ? (ks <= 8 ? 128 : 64) : kTileN;  // DmaTraits<KS>::kRows
+  pl.waves = pl.dma && !list ? kDmaWaves : kLkWaves;
+  pl.qblock = pl.waves * pl.rt * 16;
+  if (pl.dma) {
+    pl.tile_rows = pl.waves == 8 ? (ks <= 8 ? 128 : 64) : (ks <= 8 ? 64 : 32);  // DmaTraits<KS, NW>::kRows
+  } else {
+    pl.tile_rows = kTileN;
+  }
   return true;
 }
 
@@ -1178,8 +1226,9 @@ hipError_t launch_v1(const LookupParams& p, unsigned grid, hipStream_t s) {
 template <int MODE, int STORE, int KS, int VAR>
 hipError_t launch_dma(const LookupParams& p, unsigned grid, hipStream_t s) {
   if constexpr (KS <= 16) {
-    hipLaunchKernelGGL((lookup_dma_kernel<MODE, STORE, KS, (KS <= 8 ? 4 : 2), VAR == kVarDump, VAR == kVarList>),
-                       dim3(grid), dim3(kLkThreads), 0, s, p);
+    constexpr int kNW = VAR == kVarList ? kLkWaves : kDmaWaves;
+    hipLaunchKernelGGL((lookup_dma_kernel<MODE, STORE, KS, (KS <= 8 ? 4 : 2), kNW, VAR == kVarDump, VAR == kVarList>),
+                       dim3(grid), dim3(kNW * kWave), 0, s, p);
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;
@@ -1212,6 +1261,12 @@ hipError_t launch_lookup(int precision, int store, const Plan& pl, const LookupP
   return store == LIPCACHE_F32 ? launch_ks<kModeF32, LIPCACHE_F32, VAR>(pl, p, grid, s)
                                : launch_ks<kModeF32, LIPCACHE_BF16, VAR>(pl, p, grid, s);
 }
+
+// Workgroups a slice scan aims for (at least a few per CU, for balance).
+#ifndef LC_GRID_TARGET
+#define LC_GRID_TARGET 256
+#endif
+constexpr int64_t kGridTarget = LC_GRID_TARGET;
 
 // The global re-check queue of a scan (workspace memory): 4 B + 65536
 // pairs; a pair that finds it full is re-checked by its wave at once.
@@ -1284,14 +1339,17 @@ inline bool cache_ok(const lipcache_cache* c) {
   return true;
 }
 
-// Filter constants of one lookup (depend on precision, store and d).
+// Filter constants of one lookup (depend on precision, store and d) and
+// the kernel plans of a slice scan and of a work-list scan.
 struct FilterConsts {
   Plan pl;
+  Plan pl_list;
   Thresholds t;
 };
 
 lipcache_status lookup_consts(const lipcache_cache* c, int32_t precision, FilterConsts& fc) {
-  if (!make_plan(precision, c, fc.pl)) return LIPCACHE_EUNSUPPORTED;
+  if (!make_plan(precision, c, false, fc.pl) || !make_plan(precision, c, true, fc.pl_list))
+    return LIPCACHE_EUNSUPPORTED;
   if (precision == LIPCACHE_F32 && (fc.pl.ks > 32 || c->d > 512)) return LIPCACHE_EUNSUPPORTED;
   const FilterSlack fs = filter_slack(precision, c->store_dtype, fc.pl.d_pad);
   const double u32 = 1.0 / 16777216.0;
@@ -1303,13 +1361,23 @@ lipcache_status lookup_consts(const lipcache_cache* c, int32_t precision, Filter
   return LIPCACHE_OK;
 }
 
-// Stage 1: Q_q, and the reset of best / band flags / counters.
+// Stage 1: Q_q, and the reset of best / band flags / counters; with `view`
+// also the thresholds A_i of its rows and the emptying of the re-check queue
+// of the scan that follows (in the same launch).
 lipcache_status lookup_stage_prep(const float* zq, int64_t B, int d, const FilterConsts& fc, float* qthr,
                                   unsigned long long* best, unsigned int* bflag, unsigned long long* stats,
-                                  hipStream_t s) {
-  const unsigned prep_grid = static_cast<unsigned>(B > 0 ? (B + kLkWaves - 1) / kLkWaves : 1);
-  hipLaunchKernelGGL(lookup_prep_kernel, dim3(prep_grid), dim3(kLkThreads), 0, s, zq, B, d, fc.t, qthr, best, bflag,
-                     stats);
+                                  hipStream_t s, const lipcache_cache* view = nullptr, float* athr = nullptr,
+                                  unsigned long long* gq_count = nullptr) {
+  const int64_t qblocks = B > 0 ? (B + kLkWaves - 1) / kLkWaves : 1;
+  PrepEntries pe{nullptr, nullptr, 0, 0, nullptr, nullptr};
+  int64_t eblocks = 0;
+  if (view && view->n > 0) {
+    pe = PrepEntries{view->r, view->norm2, view->n, athr_len(view->n), athr, gq_count};
+    eblocks = (pe.n_pad + kLkThreads - 1) / kLkThreads;
+  }
+  if (qblocks + eblocks > INT_MAX) return LIPCACHE_EUNSUPPORTED;
+  hipLaunchKernelGGL(lookup_prep_kernel, dim3(static_cast<unsigned>(qblocks + eblocks)), dim3(kLkThreads), 0, s, zq,
+                     B, d, fc.t, qthr, best, bflag, stats, static_cast<unsigned>(qblocks), pe);
   LC_LAUNCHED();
   return LIPCACHE_OK;
 }
@@ -1324,15 +1392,17 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
                                   unsigned int* bflag, unsigned long long* stats, float* athr,
                                   const int64_t* items, int64_t n_items, const int32_t* qlist, const uint16_t* zq16,
                                   const int64_t* emap, int64_t eoff, bool dump, float* g_hat, uint8_t* cand,
-                                  const GlobalRecheckWs& gq, hipStream_t s) {
+                                  const GlobalRecheckWs& gq, hipStream_t s, bool athr_ready = false) {
   if (B <= 0 || view->n <= 0) return LIPCACHE_OK;
   if (items && n_items <= 0) return LIPCACHE_OK;
-  const int64_t n_pad = athr_len(view->n);
-  hipLaunchKernelGGL(lookup_athr_kernel, dim3(static_cast<unsigned>((n_pad + 255) / 256)), dim3(256), 0, s, view->r,
-                     view->norm2, view->n, n_pad, fc.t.kappa_c, fc.t.eta1, fc.t.range2, athr,
-                     dump ? nullptr : gq.count);
-  LC_LAUNCHED();
-  const Plan& pl = fc.pl;
+  if (!athr_ready) {
+    const int64_t n_pad = athr_len(view->n);
+    hipLaunchKernelGGL(lookup_athr_kernel, dim3(static_cast<unsigned>((n_pad + 255) / 256)), dim3(256), 0, s,
+                       view->r, view->norm2, view->n, n_pad, fc.t.kappa_c, fc.t.eta1, fc.t.range2, athr,
+                       dump ? nullptr : gq.count);
+    LC_LAUNCHED();
+  }
+  const Plan& pl = items ? fc.pl_list : fc.pl;
   LookupParams p;
   p.zq = zq;
   p.B = B;
@@ -1366,9 +1436,9 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
   p.slice_len = 0;
   if (!items) {
     // Cache slices: a multiple of 8 (one set per XCD), enough blocks to fill
-    // the chip (~1024), but at least 4 tiles per slice.
+    // the chip (~kGridTarget), but at least 4 tiles per slice.
     const int64_t tiles = (view->n + pl.tile_rows - 1) / pl.tile_rows;
-    int64_t s8 = (1024 + kXcds * p.n_qblocks - 1) / (kXcds * static_cast<int64_t>(p.n_qblocks));
+    int64_t s8 = (kGridTarget + kXcds * p.n_qblocks - 1) / (kXcds * static_cast<int64_t>(p.n_qblocks));
     int64_t s8_max = tiles / (kXcds * 4);
     if (s8_max < 1) s8_max = 1;
     if (s8 > s8_max) s8 = s8_max;
@@ -1435,10 +1505,11 @@ lipcache_status lookup_on(const lipcache_cache* c, const float* zq, int64_t B, i
   Workspace w;
   ws_layout(B, c->n, &w, ws);
   unsigned long long* st = stats ? reinterpret_cast<unsigned long long*>(stats) : w.stats;
-  lipcache_status r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s);
+  lipcache_status r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s, c, w.athr,
+                                       dump ? nullptr : w.gq.count);
   if (r != LIPCACHE_OK) return r;
   r = lookup_stage_scan(c, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr, nullptr,
-                        nullptr, 0, dump, g_hat, cand, w.gq, s);
+                        nullptr, 0, dump, g_hat, cand, w.gq, s, true);
   if (r != LIPCACHE_OK) return r;
   if (dump) return LIPCACHE_OK;
   return lookup_stage_finalize(B, w.best, w.bflag, c->label, label_out, index_out, dist2_out, band_flag, st, s);
@@ -1510,9 +1581,9 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
     return r;
   }
   int64_t n_items = 0, idx_pairs = 0;
-  lipcache_status r = index_query_plan(idx, zq, B, c->d, fc.pl.qblock, pw, n_items, idx_pairs, s);
+  lipcache_status r = index_query_plan(idx, zq, B, c->d, fc.pl_list.qblock, pw, n_items, idx_pairs, s);
   if (r != LIPCACHE_OK) return r;
-  r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s);
+  r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s, &so, w.athr, w.gq.count);
   if (r != LIPCACHE_OK) return r;
   uint16_t* zq16 = nullptr;
   if (precision == LIPCACHE_F16) {
@@ -1522,7 +1593,7 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
     LC_LAUNCHED();
   }
   r = lookup_stage_scan(&so, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, pw.items, n_items, pw.qlist,
-                        zq16, idx->perm, 0, false, nullptr, nullptr, w.gq, s);
+                        zq16, idx->perm, 0, false, nullptr, nullptr, w.gq, s, true);
   if (r != LIPCACHE_OK) return r;
   const int64_t tail = c->n - idx->n_indexed;
   if (tail > 0) {

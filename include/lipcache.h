@@ -142,11 +142,12 @@ size_t lipcache_spectral_norm_workspace_bytes(int32_t C, int32_t d);
  *   logits s = W z_i + b accumulated in float64 (Eq. (5)),
  *   label y_i = argmax_c s_c, lowest index on ties (Eq. (6)),
  *   margin m_i = s_y - max_{j != y} s_j (Eq. (20)),
- *   radius r_i = m_i / (sigma sqrt 2) (Eq. (21)), rounded to nearest float,
+ *   radius r_i = m_i / (sigma sqrt 2) (Eq. (21)) in float64,
  *   or with LIPCACHE_RADIUS_TIGHT the per-pair radius of Remark 5.1,
- *   r*_i = min_{j != y} (s_y - s_j) / ||W_y - W_j||_2 (float64, then rounded),
+ *   r*_i = min_{j != y} (s_y - s_j) / ||W_y - W_j||_2 (float64),
  *   where a class with W_j = W_y sets no finite constraint (r*_i = +inf when
- *   no class does).  r*_i >= r_i.
+ *   no class does).  r*_i >= r_i.  The radius is stored rounded toward
+ *   zero, so the float32 ball never reaches past the certified one.
  * A radius <= 0 (a tie) marks a candidate that must be discarded (Alg. 1).
  *
  *  z [N][d] float; W [C][d] float, C >= 2; b [C] float or NULL (= 0)

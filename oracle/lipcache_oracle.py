@@ -85,6 +85,16 @@ def bf16_round(x) -> np.ndarray:
     return out.reshape(a.shape)
 
 
+def to_f32_toward_zero(x) -> np.ndarray:
+    """float64 -> float32 rounded toward zero, so a stored radius never exceeds
+    the certificate it comes from (Lemma 5.1 holds for any r' <= r)."""
+    x = np.asarray(x, dtype=np.float64)
+    f = x.astype(np.float32)
+    over = np.abs(f.astype(np.float64)) > np.abs(x)
+    f[over] = np.nextafter(f[over], np.float32(0.0))
+    return f
+
+
 def stored_values(z, store: str) -> np.ndarray:
     """The values a cache of dtype ``store`` ("f32" or "bf16") holds for z."""
     z32 = np.asarray(z, dtype=np.float32)
@@ -146,7 +156,7 @@ def spectral_norm(W, max_iters: int = 20000, rel_tol: float = 1e-13,
 @dataclass
 class Certified:
     label: np.ndarray      # int32, argmax of the logits (lowest index on ties)
-    r: np.ndarray          # float32 radius, round-to-nearest of the float64 value
+    r: np.ndarray          # float32 radius, the float64 value rounded toward zero
     r64: np.ndarray        # float64 radius before rounding
     margin: np.ndarray     # float64 top-1 minus top-2 logit
     norm2: np.ndarray      # float64 squared norm of the stored feature
@@ -210,7 +220,7 @@ def certify(z, W, b, sigma: float, store: str = "f32",
             r64[i] = best
     else:
         raise ValueError(f"unknown radius mode {radius_mode!r}")
-    r = r64.astype(np.float32)
+    r = to_f32_toward_zero(r64)
     norm2 = np.sum(zs.astype(np.float64) ** 2, axis=1)
     return Certified(label.astype(np.int32), r, r64, margin, norm2, zs, s)
 

@@ -226,7 +226,7 @@ __global__ __launch_bounds__(kCertThreads) void certify_kernel(
   if (wave != 0 || !valid) return;
   const int64_t i = base + lane;
   label_out[i] = I1;
-  r_out[i] = static_cast<float>(r);
+  r_out[i] = f32_round_down(r);  // toward zero (r >= 0): never above the certificate
   if (margin_out) margin_out[i] = static_cast<float>(m);
   if (norm2_out) norm2_out[i] = static_cast<float>(nrm);
 }
@@ -426,7 +426,7 @@ __global__ __launch_bounds__(kCmThreads) void certify_mfma_kernel(
         }
       }
       label_out[i] = lab;
-      r_out[i] = static_cast<float>(rv);
+      r_out[i] = f32_round_down(rv);  // toward zero (r >= 0): never above the certificate
       if (margin_out) margin_out[i] = static_cast<float>(mv);
       if (norm2_out) norm2_out[i] = static_cast<float>(n_out);
     }

@@ -121,7 +121,7 @@ def test_certify_ties_and_empty():
     assert host(out.label).tolist() == [0, 0, 1, 0]
     r = host(out.r)
     assert r[1] == 0.0 and r[3] == 0.0
-    assert r[0] == np.float32(1 / math.sqrt(2)) and r[2] == np.float32(1.5 / math.sqrt(2))
+    assert r[0] == oracle.to_f32_toward_zero(1 / math.sqrt(2)) and r[2] == oracle.to_f32_toward_zero(1.5 / math.sqrt(2))
     e = api.certify(gpu(np.zeros((0, 32), np.float32)), gpu(W), None, 1.0)
     assert e.label.numel() == 0
 
@@ -144,8 +144,8 @@ def test_certify_tight_hand_cases():
     t = api.certify(gpu(z), gpu(W), None, 2.0, radius_mode="tight")
     c = api.certify(gpu(z), gpu(W), None, 2.0)
     assert host(t.label)[0] == 0
-    assert host(t.r)[0] == np.float32(1 / math.sqrt(5))
-    assert host(c.r)[0] == np.float32(1 / (2 * math.sqrt(2)))
+    assert host(t.r)[0] == oracle.to_f32_toward_zero(1 / math.sqrt(5))
+    assert host(c.r)[0] == oracle.to_f32_toward_zero(1 / (2 * math.sqrt(2)))
     # a duplicated row sets no constraint: s = (2, 2.5, 0) at z = (2, 0)
     z2 = np.zeros((1, d), np.float32)
     z2[0, 0] = 2
@@ -153,7 +153,7 @@ def test_certify_tight_hand_cases():
     b = np.array([0, 0.5, 0], np.float32)
     t = api.certify(gpu(z2), gpu(W), gpu(b), math.sqrt(2), radius_mode="tight")
     assert host(t.label)[0] == 1
-    assert host(t.r)[0] == np.float32(2.5 / math.sqrt(2))
+    assert host(t.r)[0] == oracle.to_f32_toward_zero(2.5 / math.sqrt(2))
     # every competitor duplicated: no finite constraint at all
     W = head([[1, 0], [1, 0]])
     b = np.array([0, 1], np.float32)

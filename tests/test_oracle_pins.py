@@ -47,3 +47,27 @@ def test_golden_fixtures():
             assert res.index.tolist() == fx["want_index"], name
         else:
             raise AssertionError(f"unknown fixture kind {kind}")
+
+
+def test_stored_radius_never_exceeds_the_certificate():
+    """The float32 radius is the float64 certificate rounded toward zero:
+    r32 <= r64 < next float32 above r32 (both radius modes), so a query the
+    float32 ball admits lies inside the certified ball (Lemma 5.1 holds for
+    every radius up to r)."""
+    import oracle
+    from paper_2608_13144_amd import workload as wlmod
+    wl = wlmod.make_workload("tiny-d64-c10", seed=0, n_cache=2000)
+    sig = oracle.spectral_norm(wl.W).sigma
+    for mode in ("conservative", "tight"):
+        c = oracle.certify(wl.z, wl.W, wl.b, sig, radius_mode=mode)
+        r32 = c.r.astype(np.float64)
+        assert np.all(r32 <= c.r64)
+        up = np.nextafter(c.r, np.float32(np.inf)).astype(np.float64)
+        assert np.all(c.r64 < up)
+        # about half the values round differently from round-to-nearest
+        assert np.mean(c.r != c.r64.astype(np.float32)) > 0.2
+    # exact values stay exact; 0 (a tie) stays 0; +inf (no constraint) stays +inf
+    x = np.array([0.0, 0.5, 1.0 / 3.0, np.inf])
+    f = oracle.to_f32_toward_zero(x)
+    assert f[0] == 0.0 and f[1] == 0.5 and f[3] == np.inf
+    assert f[2] < np.float32(1.0 / 3.0) or np.float64(np.float32(1.0 / 3.0)) < 1.0 / 3.0

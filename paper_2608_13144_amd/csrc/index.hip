@@ -16,7 +16,7 @@
 // tight.
 //
 // Query plan: for every query the clusters with ||q - mu_c|| < R_c (tested
-// on the matrix cores with a rigorous float32 slack, so no such cluster is
+// on the float16 matrix cores with a rigorous slack, so no such cluster is
 // missed); for every cluster the list of queries that need it; and work
 // items pairing a block of a cluster's list with a chunk of its rows, which
 // the fused lookup kernel scans through the list.
@@ -201,12 +201,29 @@ __device__ __forceinline__ u32x4 load16_or_zero(const uint16_t* base, bool ok) {
   return ok ? *reinterpret_cast<const u32x4*>(base) : u32x4{0u, 0u, 0u, 0u};
 }
 
-template <int KS, bool F16>
+// The same kernel with CAND sets bit c of row r's candidate mask instead
+// (the query plan): the float16 dot product g_hat of a query and a centre,
+// both rounded (u = 2^-11, sub-normal error eta = 2^-14, float32
+// accumulation gamma over d_pad + 2 terms), is within
+//   E = k (||q||^2 + ||mu||^2) / 2 + e1 (||q|| + ||mu||) + e0,
+//   k = 2u + u^2 + gamma (1 + u)^2, e1 = eta (1 + u)(1 + gamma) sqrt(d_pad),
+//   e0 = (1 + gamma) d_pad eta^2,
+// of q . mu, so ||q - mu_c|| < R_c implies ||q||^2 + ||mu||^2 - 2 g_hat <
+// R_c^2 + 2E; the test takes 4E.  A query or centre of norm >= 2^15 (the
+// float16 copy may not hold it) is a candidate of everything.
+struct CandTest {
+  const double* qnorm;  // ||q||^2 of every row
+  const float* bound;   // R_c (no candidate unless > 0)
+  uint32_t* mask;
+  double k, e1, e0;
+};
+
+template <int KS, bool F16, bool CAND>
 __global__ __launch_bounds__(256) void assign16_kernel(const uint16_t* __restrict__ rows, int64_t n,
                                                           int64_t stride, int d,
                                                           const uint16_t* __restrict__ centres16,
                                                           const double* __restrict__ cnorm, int K,
-                                                          uint32_t* __restrict__ nearest) {
+                                                          uint32_t* __restrict__ nearest, const CandTest ct) {
   using T = AssignTraits<KS>;
   constexpr int kTiles = T::kChunk / 16;
   __shared__ __attribute__((aligned(16))) unsigned char cs[T::kChunk * T::kRowBytes];
@@ -263,16 +280,35 @@ __global__ __launch_bounds__(256) void assign16_kernel(const uint16_t* __restric
       const int c = c0 + 16 * j + m16;
       if (c >= K) continue;
       const double cn = cnorm[c];
+      if constexpr (CAND) {
+        const float R = ct.bound[c];
+        if (!(R > 0.0f)) continue;
+        const double R2 = static_cast<double>(R) * static_cast<double>(R) * (1.0 + 0x1p-50);
+        const bool cbig = cn >= kF16Range2;
+        const double cl = __builtin_sqrt(cn);
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const double score = cn - 2.0 * static_cast<double>(acc[j][v]);
-        if (score < bs[v] || (score == bs[v] && c < bi[v])) {
-          bs[v] = score;
-          bi[v] = c;
+        for (int v = 0; v < 4; ++v) {
+          const int64_t row = r0 + w * 16 + 4 * g + v;
+          if (row >= n) continue;
+          const double qn = ct.qnorm[row];
+          const bool big = cbig || (qn >= kF16Range2 && qn < __builtin_inf());
+          const double slack = 2.0 * ct.k * (qn + cn) + 4.0 * ct.e1 * (__builtin_sqrt(qn) + cl) + 4.0 * ct.e0;
+          if (big || qn + cn - 2.0 * static_cast<double>(acc[j][v]) < R2 + slack)
+            atomicOr(&ct.mask[row * ((K + 31) / 32) + c / 32], 1u << (c % 32));
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const double score = cn - 2.0 * static_cast<double>(acc[j][v]);
+          if (score < bs[v] || (score == bs[v] && c < bi[v])) {
+            bs[v] = score;
+            bi[v] = c;
+          }
         }
       }
     }
   }
+  if constexpr (CAND) return;
   // least score over the 16 lanes that share g (same rows)
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
@@ -316,13 +352,14 @@ inline void launch_assign(const lipcache_cache* c, int64_t n, int64_t stride, in
   int ks = 1;
   while (ks * 32 < d) ks *= 2;
   auto go = [&](auto kern) {
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, rows16, n, stride, d, centres16, cnorm, K, nearest);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, rows16, n, stride, d, centres16, cnorm, K, nearest,
+                       CandTest{});
   };
-#define LC_ASSIGN(KS_)                    \
-  if (f16) {                              \
-    go(assign16_kernel<KS_, true>);       \
-  } else {                                \
-    go(assign16_kernel<KS_, false>);      \
+#define LC_ASSIGN(KS_)                          \
+  if (f16) {                                    \
+    go(assign16_kernel<KS_, true, false>);      \
+  } else {                                      \
+    go(assign16_kernel<KS_, false, false>);     \
   }
   switch (ks) {
     case 1: LC_ASSIGN(1) break;
@@ -866,42 +903,80 @@ size_t index_plan_layout(int64_t B, int d, int K, int64_t n_indexed, int qblock,
   t.counters = reinterpret_cast<unsigned long long*>(take(64));
   t.qnorm = reinterpret_cast<double*>(take(static_cast<size_t>(B) * 8));
   t.cnorm = reinterpret_cast<double*>(take(static_cast<size_t>(K) * 8));
+  t.c16 = reinterpret_cast<uint16_t*>(take(static_cast<size_t>(K) * d * 2));
   if (w) *w = t;
   return off;
 }
 
-lipcache_status index_query_plan(const lipcache_index* idx, const float* zq, int64_t B, int d, int qblock,
+// Plan set-up in one launch: blocks [0, zblocks) zero the candidate masks,
+// the list counts and cursors and the counters; the others take four
+// centres each (one wave per centre): ||mu_c||^2 in float64 and the float16
+// copy of the centre.
+__global__ __launch_bounds__(256) void plan_init_kernel(uint32_t* __restrict__ mask, int64_t mwords,
+                                                        uint32_t* __restrict__ ccount, uint32_t* __restrict__ cfill,
+                                                        int K, unsigned long long* __restrict__ counters,
+                                                        unsigned zblocks, const float* __restrict__ centres, int d,
+                                                        double* __restrict__ cnorm, uint16_t* __restrict__ c16) {
+  if (blockIdx.x < zblocks) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < mwords) mask[i] = 0u;
+    if (i <= K) {
+      ccount[i] = 0u;
+      cfill[i] = 0u;
+    }
+    if (i < 8) counters[i] = 0ull;
+    return;
+  }
+  const int64_t c = static_cast<int64_t>(blockIdx.x - zblocks) * (blockDim.x / kWave) + threadIdx.x / kWave;
+  if (c >= K) return;
+  double s = 0.0;
+  for (int k = lane_id(); k < d; k += kWave) {
+    const float x = centres[c * d + k];
+    s = __builtin_fma(static_cast<double>(x), static_cast<double>(x), s);
+    c16[c * d + k] = f16_bits(x);
+  }
+  s = wave_sum(s);
+  if (lane_id() == 0) cnorm[c] = s;
+}
+
+lipcache_status index_query_plan(const lipcache_index* idx, const uint16_t* zq16, int64_t B, int d, int qblock,
                                  const IndexPlanWs& w, int64_t& n_items, int64_t& pairs, hipStream_t s) {
   const int K = idx->K;
   const int words = (K + 31) / 32;
   const int64_t mwords = B * words;
-  hipLaunchKernelGGL(fill_u64x_kernel, dim3(1), dim3(64), 0, s, w.counters, 8, 0ull);
+  int64_t zn = mwords > K + 1 ? mwords : K + 1;
+  if (zn < 8) zn = 8;
+  const int64_t zblocks = (zn + 255) / 256;
+  const int64_t cblocks = (K + 3) / 4;
+  hipLaunchKernelGGL(plan_init_kernel, dim3(static_cast<unsigned>(zblocks + cblocks)), dim3(256), 0, s, w.mask, mwords,
+                     w.ccount, w.cfill, K, w.counters, static_cast<unsigned>(zblocks), idx->centers, d, w.cnorm, w.c16);
   LC_LAUNCHED();
-  hipLaunchKernelGGL(fill_u32_kernel, dim3(static_cast<unsigned>((mwords + 255) / 256)), dim3(256), 0, s, w.mask,
-                     mwords);
-  LC_LAUNCHED();
-  hipLaunchKernelGGL(fill_u32_kernel, dim3(static_cast<unsigned>((K + 1 + 255) / 256)), dim3(256), 0, s, w.ccount,
-                     static_cast<int64_t>(K + 1));
-  LC_LAUNCHED();
-  hipLaunchKernelGGL(fill_u32_kernel, dim3(static_cast<unsigned>((K + 1 + 255) / 256)), dim3(256), 0, s, w.cfill,
-                     static_cast<int64_t>(K + 1));
-  LC_LAUNCHED();
-  hipLaunchKernelGGL(row_norm_kernel, dim3(static_cast<unsigned>((B + 3) / 4)), dim3(256), 0, s, zq, LIPCACHE_F32, B,
-                     d, w.qnorm);
-  LC_LAUNCHED();
-  hipLaunchKernelGGL(row_norm_kernel, dim3(static_cast<unsigned>((K + 3) / 4)), dim3(256), 0, s, idx->centers,
-                     LIPCACHE_F32, static_cast<int64_t>(K), d, w.cnorm);
-  LC_LAUNCHED();
-  const double slack = 2.0 * (d + 2) / 16777216.0;
-  // query blocks x centre groups, about 2048 workgroups in all
-  const int64_t gx = (B + kCr - 1) / kCr;
-  int64_t gy = (2048 + gx - 1) / gx;
-  const int64_t chunks = (K + kCc - 1) / kCc;
-  if (gy > chunks) gy = chunks;
-  if (gy < 1) gy = 1;
-  hipLaunchKernelGGL(centre_mfma_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy)), dim3(256), 0, s,
-                     zq, LIPCACHE_F32, B, static_cast<int64_t>(1), d, idx->centers, w.cnorm, K, w.qnorm, idx->bound,
-                     slack, w.mask, nullptr);
+  // candidate clusters on the float16 matrix cores (the slack of CandTest)
+  int ks = 1;
+  while (ks * 32 < d) ks *= 2;
+  const double u = 1.0 / 2048.0, eta = 1.0 / 16384.0;
+  const double nn = 32.0 * ks + 2.0;
+  const double gam = nn / 16777216.0 / (1.0 - nn / 16777216.0);
+  CandTest ct;
+  ct.qnorm = w.qnorm;
+  ct.bound = idx->bound;
+  ct.mask = w.mask;
+  ct.k = 2.0 * u + u * u + gam * (1.0 + u) * (1.0 + u);
+  ct.e1 = eta * (1.0 + u) * (1.0 + gam) * __builtin_sqrt(32.0 * ks);
+  ct.e0 = (1.0 + gam) * 32.0 * ks * eta * eta;
+  const unsigned grid = static_cast<unsigned>((B + kCr - 1) / kCr);
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, zq16, B, static_cast<int64_t>(1), d, w.c16, w.cnorm, K,
+                       nullptr, ct);
+  };
+  switch (ks) {
+    case 1: go(assign16_kernel<1, true, true>); break;
+    case 2: go(assign16_kernel<2, true, true>); break;
+    case 4: go(assign16_kernel<4, true, true>); break;
+    case 8: go(assign16_kernel<8, true, true>); break;
+    case 16: go(assign16_kernel<16, true, true>); break;
+    default: go(assign16_kernel<32, true, true>); break;
+  }
   LC_LAUNCHED();
   const unsigned gq = static_cast<unsigned>((B + 255) / 256);
   const unsigned gl = static_cast<unsigned>((K + 1 + 255) / 256);

@@ -21,19 +21,21 @@ struct IndexPlanWs {
   uint32_t* icount;                // [K + 1] work items per list
   int64_t* ioff;                   // [K + 2] first item of each list
   unsigned long long* counters;    // [0] items, [1] pairs, [2] overflow
-  double* qnorm;                   // [B] ||q||^2
+  double* qnorm;                   // [B] ||q||^2 (written by the lookup's query pass)
   double* cnorm;                   // [K] ||mu_c||^2
+  uint16_t* c16;                   // [K][d] float16 copy of the centres
 };
 
 size_t index_plan_layout(int64_t B, int d, int K, int64_t n_indexed, int qblock, IndexPlanWs* w, char* base);
 
-// Candidate clusters of every query (||q - mu_c|| < R_c, tested with a
-// rigorous float32 slack), the list of queries of every cluster, and the
-// work list: for every cluster, its queries in blocks of `qblock` against
-// its rows in items of <= kItemRows rows.  A query with more than kMaxCand
-// candidates joins list K, which is scanned against all indexed rows.
-// Reads back the item and pair counts (sync).
-lipcache_status index_query_plan(const lipcache_index* idx, const float* zq, int64_t B, int d, int qblock,
+// Candidate clusters of every query (||q - mu_c|| < R_c, tested on the
+// float16 matrix cores with a rigorous slack), the list of queries of every
+// cluster, and the work list: for every cluster, its queries in blocks of
+// `qblock` against its rows in items of <= kItemRows rows.  A query with more
+// than kMaxCand candidates joins list K, which is scanned against all indexed
+// rows.  Needs w.qnorm (||q||^2 in float64) and zq16 (the float16 copy of
+// the queries) filled.  Reads back the item and pair counts (sync).
+lipcache_status index_query_plan(const lipcache_index* idx, const uint16_t* zq16, int64_t B, int d, int qblock,
                                  const IndexPlanWs& w, int64_t& n_items, int64_t& pairs, hipStream_t s);
 
 }  // namespace lc

@@ -165,6 +165,8 @@ struct PrepEntries {
   int64_t n_pad;
   float* athr;
   unsigned long long* gq_count;  // emptied for the scan that follows (nullable)
+  double* qnorm;                 // ||q||^2 in float64 of every query (nullable)
+  uint16_t* zq16;                // float16 copy of the queries (nullable)
 };
 
 // Blocks [0, qblocks): one wave per query, Q_q, reset of the per-query state
@@ -185,12 +187,17 @@ __global__ void lookup_prep_kernel(const float* __restrict__ zq, int64_t B, int 
   if (q >= B) return;
   const float* row = zq + q * d;
   double s = 0.0;
-  for (int k = lane_id(); k < d; k += kWave) s = __builtin_fma(static_cast<double>(row[k]), static_cast<double>(row[k]), s);
+  for (int k = lane_id(); k < d; k += kWave) {
+    const float x = row[k];
+    s = __builtin_fma(static_cast<double>(x), static_cast<double>(x), s);
+    if (pe.zq16) pe.zq16[q * d + k] = f16_bits(x);
+  }
   s = wave_sum(s);
   if (lane_id() == 0) {
     qthr[q] = query_threshold(s, t);
     best[q] = kNoHit;
     bflag[q] = 0u;
+    if (pe.qnorm) pe.qnorm[q] = s;
   }
 }
 
@@ -202,12 +209,6 @@ __global__ void lookup_athr_kernel(const float* __restrict__ cr, const float* __
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i == 0 && gq_count) *gq_count = 0ull;
   write_athr(i, cr, cnorm2, n, n_pad, kappa_c, eta1, range2, athr);
-}
-
-// float16 copy of the queries, for the work-list kernel.
-__global__ void query_f16_kernel(const float* __restrict__ zq, int64_t n, uint16_t* __restrict__ zq16) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < n) zq16[i] = f16_bits(zq[i]);
 }
 
 // ------------------------------------------------------------- finalize
@@ -1363,16 +1364,18 @@ lipcache_status lookup_consts(const lipcache_cache* c, int32_t precision, Filter
 
 // Stage 1: Q_q, and the reset of best / band flags / counters; with `view`
 // also the thresholds A_i of its rows and the emptying of the re-check queue
-// of the scan that follows (in the same launch).
+// of the scan that follows (in the same launch); with qnorm / zq16 also
+// ||q||^2 and the float16 copy of the queries (the indexed lookup's plan).
 lipcache_status lookup_stage_prep(const float* zq, int64_t B, int d, const FilterConsts& fc, float* qthr,
                                   unsigned long long* best, unsigned int* bflag, unsigned long long* stats,
                                   hipStream_t s, const lipcache_cache* view = nullptr, float* athr = nullptr,
-                                  unsigned long long* gq_count = nullptr) {
+                                  unsigned long long* gq_count = nullptr, double* qnorm = nullptr,
+                                  uint16_t* zq16 = nullptr) {
   const int64_t qblocks = B > 0 ? (B + kLkWaves - 1) / kLkWaves : 1;
-  PrepEntries pe{nullptr, nullptr, 0, 0, nullptr, nullptr};
+  PrepEntries pe{nullptr, nullptr, 0, 0, nullptr, nullptr, qnorm, zq16};
   int64_t eblocks = 0;
   if (view && view->n > 0) {
-    pe = PrepEntries{view->r, view->norm2, view->n, athr_len(view->n), athr, gq_count};
+    pe = PrepEntries{view->r, view->norm2, view->n, athr_len(view->n), athr, gq_count, qnorm, zq16};
     eblocks = (pe.n_pad + kLkThreads - 1) / kLkThreads;
   }
   if (qblocks + eblocks > INT_MAX) return LIPCACHE_EUNSUPPORTED;
@@ -1580,20 +1583,18 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
     if (r == LIPCACHE_OK && pairs) *pairs = 0;
     return r;
   }
+  // one pass over the queries: Q_q and the per-query state, ||q||^2 and the
+  // float16 copy for the plan (and the float16 scan), and A_i of the sorted rows
+  uint16_t* zq16 = reinterpret_cast<uint16_t*>(wsb + tl.q16);
+  lipcache_status r =
+      lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s, &so, w.athr, w.gq.count, pw.qnorm, zq16);
+  if (r != LIPCACHE_OK) return r;
   int64_t n_items = 0, idx_pairs = 0;
-  lipcache_status r = index_query_plan(idx, zq, B, c->d, fc.pl_list.qblock, pw, n_items, idx_pairs, s);
+  r = index_query_plan(idx, zq16, B, c->d, fc.pl_list.qblock, pw, n_items, idx_pairs, s);
   if (r != LIPCACHE_OK) return r;
-  r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s, &so, w.athr, w.gq.count);
-  if (r != LIPCACHE_OK) return r;
-  uint16_t* zq16 = nullptr;
-  if (precision == LIPCACHE_F16) {
-    zq16 = reinterpret_cast<uint16_t*>(wsb + tl.q16);
-    const int64_t nq = B * c->d;
-    hipLaunchKernelGGL(query_f16_kernel, dim3(static_cast<unsigned>((nq + 255) / 256)), dim3(256), 0, s, zq, nq, zq16);
-    LC_LAUNCHED();
-  }
   r = lookup_stage_scan(&so, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, pw.items, n_items, pw.qlist,
-                        zq16, idx->perm, 0, false, nullptr, nullptr, w.gq, s, true);
+                        precision == LIPCACHE_F16 ? zq16 : nullptr, idx->perm, 0, false, nullptr, nullptr, w.gq, s,
+                        true);
   if (r != LIPCACHE_OK) return r;
   const int64_t tail = c->n - idx->n_indexed;
   if (tail > 0) {

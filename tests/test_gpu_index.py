@@ -71,6 +71,43 @@ def same_as_dense(res_i, res_d, what):
     assert si[1] <= sd[1], f"{what}: re-checked {si[1]} > dense {sd[1]}"
 
 
+def plan_pairs_bounds(ix, zq):
+    """Pairs the plan must and may scan, from the host in float64.  Must:
+    every cluster with ||q - mu_c|| < R_c is a candidate of q (soundness).
+    May: the float16 cross term 2<q, mu> is within 2E of the exact one, E =
+    k (||q||^2 + ||mu||^2) / 2 + e1 (||q|| + ||mu||) + e0 (k = 2u + u^2 +
+    gamma (1 + u)^2, e1 = eta (1 + u) (1 + gamma) sqrt(d_pad), e0 = (1 +
+    gamma) d_pad eta^2, u = 2^-11, eta = 2^-14), and the plan admits a
+    cluster when the computed ||q - mu||^2 is below R^2 + 4E, so no cluster
+    with an exact ||q - mu||^2 >= R^2 + 6E is ever a candidate.  A query with
+    more than 256 candidates scans every indexed row."""
+    mu = host(ix.centers).astype(np.float64)
+    R = host(ix.bound).astype(np.float64)
+    off = host(ix.offsets)
+    size = np.diff(off)
+    n = int(off[-1])
+    Q = zq.astype(np.float64)
+    D2 = ((Q[:, None, :] - mu[None, :, :]) ** 2).sum(-1)
+    live = (R > 0)[None, :]
+    d_pad = 32
+    while d_pad < Q.shape[1]:
+        d_pad *= 2
+    u, eta = 2.0 ** -11, 2.0 ** -14
+    gam = (d_pad + 2) * 2.0 ** -24 / (1 - (d_pad + 2) * 2.0 ** -24)
+    k = 2 * u + u * u + gam * (1 + u) ** 2
+    e1 = eta * (1 + u) * (1 + gam) * np.sqrt(d_pad)
+    e0 = (1 + gam) * d_pad * eta * eta
+    qn, cn = (Q * Q).sum(1)[:, None], (mu * mu).sum(1)[None, :]
+    E = k * (qn + cn) / 2 + e1 * (np.sqrt(qn) + np.sqrt(cn)) + e0
+
+    def pairs_of(cand):
+        kk = cand.sum(1)
+        per = np.where(kk > 256, n, (cand * size[None, :]).sum(1))
+        return int(per.sum())
+    return (pairs_of((D2 < (R * R)[None, :]) & live),
+            pairs_of((D2 < (R * R)[None, :] * (1 + 1e-12) + 6.01 * E) & live))
+
+
 @pytest.fixture(scope="module")
 def tiny():
     wl = wlmod.make_workload("tiny-d64-c10", seed=0)
@@ -105,7 +142,9 @@ def test_indexed_matches_oracle_and_dense(tiny, store, prec, image, K, iters):
     res_d = c.lookup(q, precision=prec)
     same_as_dense(res_i, res_d, what)
     assert 0 < pairs <= zq.shape[0] * st.n
-    say("index", what, "pairs", pairs, "of", zq.shape[0] * st.n)
+    lo, hi = plan_pairs_bounds(ix, zq)
+    assert lo <= pairs <= hi, (what, lo, pairs, hi)
+    say("index", what, "pairs", pairs, "of", zq.shape[0] * st.n, "exact plan", lo)
 
 
 @pytest.mark.parametrize("K,iters", [(4, 3), (64, 2)])

@@ -201,29 +201,12 @@ __device__ __forceinline__ u32x4 load16_or_zero(const uint16_t* base, bool ok) {
   return ok ? *reinterpret_cast<const u32x4*>(base) : u32x4{0u, 0u, 0u, 0u};
 }
 
-// The same kernel with CAND sets bit c of row r's candidate mask instead
-// (the query plan): the float16 dot product g_hat of a query and a centre,
-// both rounded (u = 2^-11, sub-normal error eta = 2^-14, float32
-// accumulation gamma over d_pad + 2 terms), is within
-//   E = k (||q||^2 + ||mu||^2) / 2 + e1 (||q|| + ||mu||) + e0,
-//   k = 2u + u^2 + gamma (1 + u)^2, e1 = eta (1 + u)(1 + gamma) sqrt(d_pad),
-//   e0 = (1 + gamma) d_pad eta^2,
-// of q . mu, so ||q - mu_c|| < R_c implies ||q||^2 + ||mu||^2 - 2 g_hat <
-// R_c^2 + 2E; the test takes 4E.  A query or centre of norm >= 2^15 (the
-// float16 copy may not hold it) is a candidate of everything.
-struct CandTest {
-  const double* qnorm;  // ||q||^2 of every row
-  const float* bound;   // R_c (no candidate unless > 0)
-  uint32_t* mask;
-  double k, e1, e0;
-};
-
-template <int KS, bool F16, bool CAND>
+template <int KS, bool F16>
 __global__ __launch_bounds__(256) void assign16_kernel(const uint16_t* __restrict__ rows, int64_t n,
                                                           int64_t stride, int d,
                                                           const uint16_t* __restrict__ centres16,
                                                           const double* __restrict__ cnorm, int K,
-                                                          uint32_t* __restrict__ nearest, const CandTest ct) {
+                                                          uint32_t* __restrict__ nearest) {
   using T = AssignTraits<KS>;
   constexpr int kTiles = T::kChunk / 16;
   __shared__ __attribute__((aligned(16))) unsigned char cs[T::kChunk * T::kRowBytes];
@@ -280,35 +263,16 @@ __global__ __launch_bounds__(256) void assign16_kernel(const uint16_t* __restric
       const int c = c0 + 16 * j + m16;
       if (c >= K) continue;
       const double cn = cnorm[c];
-      if constexpr (CAND) {
-        const float R = ct.bound[c];
-        if (!(R > 0.0f)) continue;
-        const double R2 = static_cast<double>(R) * static_cast<double>(R) * (1.0 + 0x1p-50);
-        const bool cbig = cn >= kF16Range2;
-        const double cl = __builtin_sqrt(cn);
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int64_t row = r0 + w * 16 + 4 * g + v;
-          if (row >= n) continue;
-          const double qn = ct.qnorm[row];
-          const bool big = cbig || (qn >= kF16Range2 && qn < __builtin_inf());
-          const double slack = 2.0 * ct.k * (qn + cn) + 4.0 * ct.e1 * (__builtin_sqrt(qn) + cl) + 4.0 * ct.e0;
-          if (big || qn + cn - 2.0 * static_cast<double>(acc[j][v]) < R2 + slack)
-            atomicOr(&ct.mask[row * ((K + 31) / 32) + c / 32], 1u << (c % 32));
-        }
-      } else {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const double score = cn - 2.0 * static_cast<double>(acc[j][v]);
-          if (score < bs[v] || (score == bs[v] && c < bi[v])) {
-            bs[v] = score;
-            bi[v] = c;
-          }
+      for (int v = 0; v < 4; ++v) {
+        const double score = cn - 2.0 * static_cast<double>(acc[j][v]);
+        if (score < bs[v] || (score == bs[v] && c < bi[v])) {
+          bs[v] = score;
+          bi[v] = c;
         }
       }
     }
   }
-  if constexpr (CAND) return;
   // least score over the 16 lanes that share g (same rows)
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
@@ -352,14 +316,13 @@ inline void launch_assign(const lipcache_cache* c, int64_t n, int64_t stride, in
   int ks = 1;
   while (ks * 32 < d) ks *= 2;
   auto go = [&](auto kern) {
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, rows16, n, stride, d, centres16, cnorm, K, nearest,
-                       CandTest{});
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, rows16, n, stride, d, centres16, cnorm, K, nearest);
   };
 #define LC_ASSIGN(KS_)                          \
   if (f16) {                                    \
-    go(assign16_kernel<KS_, true, false>);      \
+    go(assign16_kernel<KS_, true>);             \
   } else {                                      \
-    go(assign16_kernel<KS_, false, false>);     \
+    go(assign16_kernel<KS_, false>);            \
   }
   switch (ks) {
     case 1: LC_ASSIGN(1) break;
@@ -902,24 +865,57 @@ size_t index_plan_layout(int64_t B, int d, int K, int64_t n_indexed, int qblock,
   t.ioff = reinterpret_cast<int64_t*>(take(static_cast<size_t>(K + 2) * 8));
   t.counters = reinterpret_cast<unsigned long long*>(take(64));
   t.qnorm = reinterpret_cast<double*>(take(static_cast<size_t>(B) * 8));
-  t.cnorm = reinterpret_cast<double*>(take(static_cast<size_t>(K) * 8));
+  t.cterm = reinterpret_cast<double*>(take(static_cast<size_t>(K) * 8));
   t.c16 = reinterpret_cast<uint16_t*>(take(static_cast<size_t>(K) * d * 2));
   if (w) *w = t;
   return off;
 }
 
-// Plan set-up in one launch: blocks [0, zblocks) zero the candidate masks,
-// the list counts and cursors and the counters; the others take four
-// centres each (one wave per centre): ||mu_c||^2 in float64 and the float16
-// copy of the centre.
-__global__ __launch_bounds__(256) void plan_init_kernel(uint32_t* __restrict__ mask, int64_t mwords,
-                                                        uint32_t* __restrict__ ccount, uint32_t* __restrict__ cfill,
+// Candidate test of the query plan.  The float16 dot product g_hat of a
+// query and a centre, both rounded (u = 2^-11, sub-normal error eta =
+// 2^-14, float32 accumulation gamma over d_pad + 2 terms), is within
+//   E = k (||q||^2 + ||mu||^2) / 2 + e1 (||q|| + ||mu||) + e0,
+//   k = 2u + u^2 + gamma (1 + u)^2, e1 = eta (1 + u)(1 + gamma) sqrt(d_pad),
+//   e0 = (1 + gamma) d_pad eta^2,
+// of q . mu, so ||q - mu_c|| < R_c implies ||q||^2 + ||mu||^2 - 2 g_hat <
+// R_c^2 + 2E.  The test allows 4E, split into a query term and a centre term
+//   X_q = (1 - 2k) ||q||^2 - 4 e1 ||q|| - 2 e0,
+//   Y_c = (1 - 2k) ||mu||^2 - 4 e1 ||mu|| - 2 e0 - R_c^2 (1 + 2^-50),
+// and c is a candidate of q iff X_q + Y_c < 2 g_hat (splitting the sum moves
+// its float64 rounding by a few units in the last place of ||q||^2 +
+// ||mu||^2, far inside the second 2E).  A query or centre of squared norm
+// >= 2^30 (its float16 copy may not hold it) is a candidate of every live
+// cluster (Y_c = -inf marks such a centre); a cluster with R_c <= 0 is
+// nobody's (Y_c = NaN).
+struct CandSlack {
+  double k2;    // 2k
+  double e1x4;  // 4 e1
+  double e0x2;  // 2 e0
+};
+
+inline CandSlack cand_slack(int d) {
+  int ks = 1;
+  while (ks * 32 < d) ks *= 2;
+  const double u = 1.0 / 2048.0, eta = 1.0 / 16384.0;
+  const double dp = 32.0 * ks;
+  const double nn = dp + 2.0;
+  const double gam = nn / 16777216.0 / (1.0 - nn / 16777216.0);
+  const double k = 2.0 * u + u * u + gam * (1.0 + u) * (1.0 + u);
+  const double e1 = eta * (1.0 + u) * (1.0 + gam) * __builtin_sqrt(dp);
+  const double e0 = (1.0 + gam) * dp * eta * eta;
+  return CandSlack{2.0 * k, 4.0 * e1, 2.0 * e0};
+}
+
+// Plan set-up in one launch: blocks [0, zblocks) zero the list counts and
+// cursors and the counters; the others take four centres each (one wave per
+// centre): the float16 copy of the centre and its term Y_c.
+__global__ __launch_bounds__(256) void plan_init_kernel(uint32_t* __restrict__ ccount, uint32_t* __restrict__ cfill,
                                                         int K, unsigned long long* __restrict__ counters,
-                                                        unsigned zblocks, const float* __restrict__ centres, int d,
-                                                        double* __restrict__ cnorm, uint16_t* __restrict__ c16) {
+                                                        unsigned zblocks, const float* __restrict__ centres,
+                                                        const float* __restrict__ bound, int d, CandSlack sl,
+                                                        double* __restrict__ cterm, uint16_t* __restrict__ c16) {
   if (blockIdx.x < zblocks) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i < mwords) mask[i] = 0u;
     if (i <= K) {
       ccount[i] = 0u;
       cfill[i] = 0u;
@@ -936,46 +932,125 @@ __global__ __launch_bounds__(256) void plan_init_kernel(uint32_t* __restrict__ m
     c16[c * d + k] = f16_bits(x);
   }
   s = wave_sum(s);
-  if (lane_id() == 0) cnorm[c] = s;
+  if (lane_id() == 0) {
+    const float R = bound[c];
+    double y = __builtin_nan("");
+    if (R > 0.0f) {
+      const double R2 = static_cast<double>(R) * static_cast<double>(R) * (1.0 + 0x1p-50);
+      y = s >= kF16Range2 ? -__builtin_inf() : s - sl.k2 * s - sl.e1x4 * __builtin_sqrt(s) - sl.e0x2 - R2;
+    }
+    cterm[c] = y;
+  }
+}
+
+// Candidate masks of the queries: bit c of word c / 32 of row r is set iff
+// cluster c passes the test above for query r.  Same tiling as
+// assign16_kernel (4 waves x 16 queries, centres through LDS); every word of
+// every row is written once (no clearing, no atomics): for each 16-centre
+// tile and each of its four rows a lane's pass bits are gathered by a wave
+// ballot, and lane (v, g) keeps the half-words of row 4 g + v until its
+// word is complete.
+template <int KS>
+__global__ __launch_bounds__(256) void cand16_kernel(const uint16_t* __restrict__ zq16, const double* __restrict__ qnorm,
+                                                     int64_t B, int d, const uint16_t* __restrict__ centres16,
+                                                     const double* __restrict__ cterm, int K, int words, CandSlack sl,
+                                                     uint32_t* __restrict__ mask) {
+  using T = AssignTraits<KS>;
+  constexpr int kTiles = T::kChunk / 16;
+  __shared__ __attribute__((aligned(16))) unsigned char cs[T::kChunk * T::kRowBytes];
+  const int t = static_cast<int>(threadIdx.x);
+  const int lane = lane_id(), w = t / kWave;
+  const int m16 = lane & 15, g = lane >> 4;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kCr;
+  int64_t ra = r0 + w * 16 + m16;
+  ra = ra < B ? ra : B - 1;
+  u32x4 a[KS];
+#pragma unroll
+  for (int st = 0; st < KS; ++st) {
+    const int k0 = 32 * st + 8 * g;
+    a[st] = load16_or_zero(zq16 + ra * d + k0, k0 < d);
+  }
+  // query terms of this lane's accumulator rows 4 g + v
+  double X[4];
+  bool big[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int64_t row = r0 + w * 16 + 4 * g + v;
+    const double qn = row < B ? qnorm[row] : __builtin_nan("");
+    X[v] = qn - sl.k2 * qn - sl.e1x4 * __builtin_sqrt(qn) - sl.e0x2;
+    big[v] = qn >= kF16Range2 && qn < __builtin_inf();
+  }
+  const int64_t myrow = r0 + w * 16 + 4 * g + (m16 & 3);
+  uint32_t word = 0u;
+  constexpr int kChunksPerRow = 4 * KS;
+  for (int c0 = 0; c0 < K; c0 += T::kChunk) {
+    __syncthreads();
+    for (int e = t; e < T::kChunk * kChunksPerRow; e += 256) {
+      const int cr = e / kChunksPerRow, q = e % kChunksPerRow;
+      const int c = c0 + cr, k0 = 8 * q;
+      const u32x4 v = load16_or_zero(centres16 + static_cast<int64_t>(c < K ? c : 0) * d + k0, c < K && k0 < d);
+      *reinterpret_cast<u32x4*>(cs + cr * T::kRowBytes + q * 16) = v;
+    }
+    __syncthreads();
+    f32x4 acc[kTiles];
+#pragma unroll
+    for (int j = 0; j < kTiles; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < KS; ++st) {
+#pragma unroll
+      for (int j = 0; j < kTiles; ++j) {
+        const u32x4 b = *reinterpret_cast<const u32x4*>(cs + (16 * j + m16) * T::kRowBytes + (4 * st + g) * 16);
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a[st]), __builtin_bit_cast(f16x8, b),
+                                                        acc[j], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kTiles; ++j) {
+      const int cbase = c0 + 16 * j;  // wave-uniform
+      if (cbase >= K) break;
+      const int c = cbase + m16;
+      const double Y = c < K ? cterm[c] : __builtin_nan("");
+      const bool live = Y == Y;  // not NaN: a live cluster
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const bool pass = live && (big[v] || Y == -__builtin_inf() || X[v] + Y < 2.0 * static_cast<double>(acc[j][v]));
+        const unsigned long long bal = __ballot(pass);
+        const uint32_t half = static_cast<uint32_t>(bal >> (16 * g)) & 0xFFFFu;
+        if ((m16 & 3) == v) word |= half << (16 * ((cbase >> 4) & 1));
+      }
+      if (((cbase >> 4) & 1) || cbase + 16 >= K) {
+        if (m16 < 4 && myrow < B) mask[myrow * words + (cbase >> 5)] = word;
+        word = 0u;
+      }
+    }
+  }
 }
 
 lipcache_status index_query_plan(const lipcache_index* idx, const uint16_t* zq16, int64_t B, int d, int qblock,
                                  const IndexPlanWs& w, int64_t& n_items, int64_t& pairs, hipStream_t s) {
   const int K = idx->K;
   const int words = (K + 31) / 32;
-  const int64_t mwords = B * words;
-  int64_t zn = mwords > K + 1 ? mwords : K + 1;
-  if (zn < 8) zn = 8;
+  const CandSlack sl = cand_slack(d);
+  const int64_t zn = K + 1 > 8 ? K + 1 : 8;
   const int64_t zblocks = (zn + 255) / 256;
   const int64_t cblocks = (K + 3) / 4;
-  hipLaunchKernelGGL(plan_init_kernel, dim3(static_cast<unsigned>(zblocks + cblocks)), dim3(256), 0, s, w.mask, mwords,
-                     w.ccount, w.cfill, K, w.counters, static_cast<unsigned>(zblocks), idx->centers, d, w.cnorm, w.c16);
+  hipLaunchKernelGGL(plan_init_kernel, dim3(static_cast<unsigned>(zblocks + cblocks)), dim3(256), 0, s, w.ccount,
+                     w.cfill, K, w.counters, static_cast<unsigned>(zblocks), idx->centers, idx->bound, d, sl, w.cterm,
+                     w.c16);
   LC_LAUNCHED();
-  // candidate clusters on the float16 matrix cores (the slack of CandTest)
   int ks = 1;
   while (ks * 32 < d) ks *= 2;
-  const double u = 1.0 / 2048.0, eta = 1.0 / 16384.0;
-  const double nn = 32.0 * ks + 2.0;
-  const double gam = nn / 16777216.0 / (1.0 - nn / 16777216.0);
-  CandTest ct;
-  ct.qnorm = w.qnorm;
-  ct.bound = idx->bound;
-  ct.mask = w.mask;
-  ct.k = 2.0 * u + u * u + gam * (1.0 + u) * (1.0 + u);
-  ct.e1 = eta * (1.0 + u) * (1.0 + gam) * __builtin_sqrt(32.0 * ks);
-  ct.e0 = (1.0 + gam) * 32.0 * ks * eta * eta;
   const unsigned grid = static_cast<unsigned>((B + kCr - 1) / kCr);
   auto go = [&](auto kern) {
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, zq16, B, static_cast<int64_t>(1), d, w.c16, w.cnorm, K,
-                       nullptr, ct);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, zq16, w.qnorm, B, d, w.c16, w.cterm, K, words, sl, w.mask);
   };
   switch (ks) {
-    case 1: go(assign16_kernel<1, true, true>); break;
-    case 2: go(assign16_kernel<2, true, true>); break;
-    case 4: go(assign16_kernel<4, true, true>); break;
-    case 8: go(assign16_kernel<8, true, true>); break;
-    case 16: go(assign16_kernel<16, true, true>); break;
-    default: go(assign16_kernel<32, true, true>); break;
+    case 1: go(cand16_kernel<1>); break;
+    case 2: go(cand16_kernel<2>); break;
+    case 4: go(cand16_kernel<4>); break;
+    case 8: go(cand16_kernel<8>); break;
+    case 16: go(cand16_kernel<16>); break;
+    default: go(cand16_kernel<32>); break;
   }
   LC_LAUNCHED();
   const unsigned gq = static_cast<unsigned>((B + 255) / 256);

@@ -22,14 +22,14 @@ struct IndexPlanWs {
   int64_t* ioff;                   // [K + 2] first item of each list
   unsigned long long* counters;    // [0] items, [1] pairs, [2] overflow
   double* qnorm;                   // [B] ||q||^2 (written by the lookup's query pass)
-  double* cnorm;                   // [K] ||mu_c||^2
+  double* cterm;                   // [K] centre term of the candidate test (Y_c)
   uint16_t* c16;                   // [K][d] float16 copy of the centres
 };
 
 size_t index_plan_layout(int64_t B, int d, int K, int64_t n_indexed, int qblock, IndexPlanWs* w, char* base);
 
-// Candidate clusters of every query (||q - mu_c|| < R_c, tested on the
-// float16 matrix cores with a rigorous slack), the list of queries of every
+// Candidate clusters of every query (every c with ||q - mu_c|| < R_c, tested
+// on the float16 matrix cores with a rigorous slack), the list of queries of every
 // cluster, and the work list: for every cluster, its queries in blocks of
 // `qblock` against its rows in items of <= kItemRows rows.  A query with more
 // than kMaxCand candidates joins list K, which is scanned against all indexed

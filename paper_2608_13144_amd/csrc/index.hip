@@ -680,47 +680,66 @@ inline int sort_passes(int K) {
 }
 
 // ---------------------------------------------------------------- query plan
-// The per-cluster query lists.  A workgroup takes 256 queries (a thread
-// each); a query with more than kMaxCand candidate clusters joins list K,
-// otherwise every candidate cluster's list.  Counts are gathered in LDS and
-// flushed with one global atomic per list and workgroup (lists above
-// kPlanLds fall back to global atomics).
+// The per-cluster query lists.  A workgroup takes kPlanRows consecutive
+// queries, whose mask words are contiguous: its threads read them coalesced
+// (thread i takes words i, i + 256, ...), first summing each query's
+// candidate count in LDS.  A query with more than kMaxCand candidate
+// clusters joins list K, otherwise every candidate cluster's list.  Counts
+// are gathered in LDS and flushed with one global atomic per list and
+// workgroup (lists above kPlanLds fall back to global atomics).
 constexpr int kPlanLds = 4096;
+constexpr int kPlanRows = 128;
 
-__device__ __forceinline__ int query_candidates(const uint32_t* row, int words) {
-  int cand = 0;
-  for (int wd = 0; wd < words; ++wd) cand += __builtin_popcount(row[wd]);
-  return cand;
+// Candidate counts of the workgroup's rows q0 .. q0 + rows - 1 into rc.
+__device__ __forceinline__ void plan_row_counts(const uint32_t* __restrict__ mask, int words, int64_t q0, int rows,
+                                                uint32_t* rc) {
+  for (int i = threadIdx.x; i < rows; i += blockDim.x) rc[i] = 0u;
+  __syncthreads();
+  const uint32_t* base = mask + q0 * words;
+  const int nw = rows * words;
+  for (int i = threadIdx.x; i < nw; i += blockDim.x) {
+    const uint32_t v = base[i];
+    if (v) atomicAdd(&rc[i / words], static_cast<uint32_t>(__builtin_popcount(v)));
+  }
+  __syncthreads();
+}
+
+// Calls f(list, row) for every list entry of the workgroup's rows (any order).
+template <typename F>
+__device__ __forceinline__ void plan_entries(const uint32_t* __restrict__ mask, int words, int64_t q0, int rows,
+                                             int K, const uint32_t* rc, F&& f) {
+  const uint32_t* base = mask + q0 * words;
+  const int nw = rows * words;
+  for (int i = threadIdx.x; i < nw; i += blockDim.x) {
+    const int row = i / words, wd = i - row * words;
+    if (rc[row] > static_cast<uint32_t>(kMaxCand)) {
+      if (wd == 0) f(K, row);
+      continue;
+    }
+    uint32_t v = base[i];
+    while (v) {
+      f(32 * wd + __builtin_ctz(v), row);
+      v &= v - 1u;
+    }
+  }
 }
 
 __global__ __launch_bounds__(256) void plan_count_kernel(const uint32_t* __restrict__ mask, int words, int64_t B,
                                                          int K, uint32_t* __restrict__ ccount) {
   __shared__ uint32_t h[kPlanLds];
+  __shared__ uint32_t rc[kPlanRows];
   const int lists = K + 1;
   for (int c = threadIdx.x; c < lists && c < kPlanLds; c += 256) h[c] = 0u;
-  __syncthreads();
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (q < B) {
-    const uint32_t* row = mask + q * words;
-    auto count = [&](int c) {
-      if (c < kPlanLds) {
-        atomicAdd(&h[c], 1u);
-      } else {
-        atomicAdd(&ccount[c], 1u);
-      }
-    };
-    if (query_candidates(row, words) > kMaxCand) {
-      count(K);
+  const int64_t q0 = static_cast<int64_t>(blockIdx.x) * kPlanRows;
+  const int rows = static_cast<int>(B - q0 < kPlanRows ? B - q0 : kPlanRows);
+  plan_row_counts(mask, words, q0, rows, rc);  // (its barrier also publishes h)
+  plan_entries(mask, words, q0, rows, K, rc, [&](int c, int) {
+    if (c < kPlanLds) {
+      atomicAdd(&h[c], 1u);
     } else {
-      for (int wd = 0; wd < words; ++wd) {
-        uint32_t v = row[wd];
-        while (v) {
-          count(32 * wd + __builtin_ctz(v));
-          v &= v - 1u;
-        }
-      }
+      atomicAdd(&ccount[c], 1u);
     }
-  }
+  });
   __syncthreads();
   for (int c = threadIdx.x; c < lists && c < kPlanLds; c += 256)
     if (h[c]) atomicAdd(&ccount[c], h[c]);
@@ -733,48 +752,25 @@ __global__ __launch_bounds__(256) void plan_fill_kernel(const uint32_t* __restri
                                                         uint32_t* __restrict__ cfill, int32_t* __restrict__ qlist) {
   __shared__ uint32_t h[kPlanLds];
   __shared__ uint32_t base[kPlanLds];
+  __shared__ uint32_t rc[kPlanRows];
   const int lists = K + 1;
   for (int c = threadIdx.x; c < lists && c < kPlanLds; c += 256) h[c] = 0u;
-  __syncthreads();
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  const uint32_t* row = mask + (q < B ? q : 0) * words;
-  const bool dense = q < B && query_candidates(row, words) > kMaxCand;
-  if (q < B) {
-    if (dense) {
-      if (K < kPlanLds) atomicAdd(&h[K], 1u);
-    } else {
-      for (int wd = 0; wd < words; ++wd) {
-        uint32_t v = row[wd];
-        while (v) {
-          const int c = 32 * wd + __builtin_ctz(v);
-          v &= v - 1u;
-          if (c < kPlanLds) atomicAdd(&h[c], 1u);
-        }
-      }
-    }
-  }
+  const int64_t q0 = static_cast<int64_t>(blockIdx.x) * kPlanRows;
+  const int rows = static_cast<int>(B - q0 < kPlanRows ? B - q0 : kPlanRows);
+  plan_row_counts(mask, words, q0, rows, rc);
+  plan_entries(mask, words, q0, rows, K, rc, [&](int c, int) {
+    if (c < kPlanLds) atomicAdd(&h[c], 1u);
+  });
   __syncthreads();
   for (int c = threadIdx.x; c < lists && c < kPlanLds; c += 256) {
     base[c] = h[c] ? atomicAdd(&cfill[c], h[c]) : 0u;
     h[c] = 0u;  // becomes the workgroup's cursor
   }
   __syncthreads();
-  if (q >= B) return;
-  auto place = [&](int c) {
+  plan_entries(mask, words, q0, rows, K, rc, [&](int c, int row) {
     const uint32_t slot = c < kPlanLds ? base[c] + atomicAdd(&h[c], 1u) : atomicAdd(&cfill[c], 1u);
-    qlist[coff[c] + slot] = static_cast<int32_t>(q);
-  };
-  if (dense) {
-    place(K);
-    return;
-  }
-  for (int wd = 0; wd < words; ++wd) {
-    uint32_t v = row[wd];
-    while (v) {
-      place(32 * wd + __builtin_ctz(v));
-      v &= v - 1u;
-    }
-  }
+    qlist[coff[c] + slot] = static_cast<int32_t>(q0 + row);
+  });
 }
 
 // Rows of list c: cluster c, or every indexed row for list K; cut into
@@ -837,6 +833,7 @@ using namespace lc;
 namespace lc {
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
 
 size_t index_plan_layout(int64_t B, int d, int K, int64_t n_indexed, int qblock, IndexPlanWs* w, char* base) {
   (void)d;
@@ -944,85 +941,132 @@ __global__ __launch_bounds__(256) void plan_init_kernel(uint32_t* __restrict__ c
 }
 
 // Candidate masks of the queries: bit c of word c / 32 of row r is set iff
-// cluster c passes the test above for query r.  Same tiling as
-// assign16_kernel (4 waves x 16 queries, centres through LDS); every word of
+// cluster c passes the test above for query r.  Block: 4 waves x kRT row
+// tiles of 16 queries, their A operands in registers for the whole feature
+// range; blockIdx.y takes a range of `cspan` centres (a multiple of 64, so
+// no mask word is shared by two blocks), staged through LDS in chunks
+// (padded rows, as in assign16_kernel), double-buffered: the next chunk's
+// loads are in flight while the current one is multiplied.  Every word of
 // every row is written once (no clearing, no atomics): for each 16-centre
 // tile and each of its four rows a lane's pass bits are gathered by a wave
 // ballot, and lane (v, g) keeps the half-words of row 4 g + v until its
 // word is complete.
 template <int KS>
+struct CandTraits {
+  static constexpr int kRT = KS <= 8 ? 2 : 1;                              // row tiles per wave
+  static constexpr int kRows = 4 * kRT * 16;                               // queries per block
+  static constexpr int kChunk = AssignTraits<KS>::kChunk;                  // centres per LDS chunk
+  static constexpr int kRowBytes = AssignTraits<KS>::kRowBytes;
+  static constexpr int kCPR = 4 * KS;                                      // 16-byte chunks per row
+  static constexpr int kStage = kChunk * kCPR / 256;                       // loads per thread per chunk
+};
+
+template <int KS>
 __global__ __launch_bounds__(256) void cand16_kernel(const uint16_t* __restrict__ zq16, const double* __restrict__ qnorm,
                                                      int64_t B, int d, const uint16_t* __restrict__ centres16,
-                                                     const double* __restrict__ cterm, int K, int words, CandSlack sl,
-                                                     uint32_t* __restrict__ mask) {
-  using T = AssignTraits<KS>;
+                                                     const double* __restrict__ cterm, int K, int cspan, int words,
+                                                     CandSlack sl, uint32_t* __restrict__ mask) {
+  using T = CandTraits<KS>;
+  constexpr int RT = T::kRT;
   constexpr int kTiles = T::kChunk / 16;
-  __shared__ __attribute__((aligned(16))) unsigned char cs[T::kChunk * T::kRowBytes];
+  static_assert(T::kStage >= 1 && T::kStage * 256 == T::kChunk * T::kCPR, "whole loads per thread");
+  __shared__ __attribute__((aligned(16))) unsigned char cs[2][T::kChunk * T::kRowBytes];
   const int t = static_cast<int>(threadIdx.x);
   const int lane = lane_id(), w = t / kWave;
   const int m16 = lane & 15, g = lane >> 4;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kCr;
-  int64_t ra = r0 + w * 16 + m16;
-  ra = ra < B ? ra : B - 1;
-  u32x4 a[KS];
+  const int c_begin = static_cast<int>(blockIdx.y) * cspan;
+  const int c_end = c_begin + cspan < K ? c_begin + cspan : K;
+  if (c_begin >= c_end) return;  // whole block
+  const int64_t rw = static_cast<int64_t>(blockIdx.x) * T::kRows + w * (RT * 16);  // the wave's first row
+  u32x4 a[RT][KS];
+  double X[RT][4];
+  bool big[RT][4];
+  uint32_t word[RT];
 #pragma unroll
-  for (int st = 0; st < KS; ++st) {
-    const int k0 = 32 * st + 8 * g;
-    a[st] = load16_or_zero(zq16 + ra * d + k0, k0 < d);
-  }
-  // query terms of this lane's accumulator rows 4 g + v
-  double X[4];
-  bool big[4];
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int64_t row = r0 + w * 16 + 4 * g + v;
-    const double qn = row < B ? qnorm[row] : __builtin_nan("");
-    X[v] = qn - sl.k2 * qn - sl.e1x4 * __builtin_sqrt(qn) - sl.e0x2;
-    big[v] = qn >= kF16Range2 && qn < __builtin_inf();
-  }
-  const int64_t myrow = r0 + w * 16 + 4 * g + (m16 & 3);
-  uint32_t word = 0u;
-  constexpr int kChunksPerRow = 4 * KS;
-  for (int c0 = 0; c0 < K; c0 += T::kChunk) {
-    __syncthreads();
-    for (int e = t; e < T::kChunk * kChunksPerRow; e += 256) {
-      const int cr = e / kChunksPerRow, q = e % kChunksPerRow;
-      const int c = c0 + cr, k0 = 8 * q;
-      const u32x4 v = load16_or_zero(centres16 + static_cast<int64_t>(c < K ? c : 0) * d + k0, c < K && k0 < d);
-      *reinterpret_cast<u32x4*>(cs + cr * T::kRowBytes + q * 16) = v;
-    }
-    __syncthreads();
-    f32x4 acc[kTiles];
-#pragma unroll
-    for (int j = 0; j < kTiles; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int rt = 0; rt < RT; ++rt) {
+    int64_t ra = rw + rt * 16 + m16;
+    ra = ra < B ? ra : B - 1;
 #pragma unroll
     for (int st = 0; st < KS; ++st) {
-#pragma unroll
-      for (int j = 0; j < kTiles; ++j) {
-        const u32x4 b = *reinterpret_cast<const u32x4*>(cs + (16 * j + m16) * T::kRowBytes + (4 * st + g) * 16);
-        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a[st]), __builtin_bit_cast(f16x8, b),
-                                                        acc[j], 0, 0, 0);
-      }
+      const int k0 = 32 * st + 8 * g;
+      a[rt][st] = load16_or_zero(zq16 + ra * d + k0, k0 < d);
     }
+    // query terms of this lane's accumulator rows 4 g + v
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t row = rw + rt * 16 + 4 * g + v;
+      const double qn = row < B ? qnorm[row] : __builtin_nan("");
+      X[rt][v] = qn - sl.k2 * qn - sl.e1x4 * __builtin_sqrt(qn) - sl.e0x2;
+      big[rt][v] = qn >= kF16Range2 && qn < __builtin_inf();
+    }
+    word[rt] = 0u;
+  }
+  u32x4 stage[T::kStage];
+  auto load_chunk16 = [&](int c0) {
+#pragma unroll
+    for (int i = 0; i < T::kStage; ++i) {
+      const int e = t + 256 * i;
+      const int c = c0 + e / T::kCPR, k0 = 8 * (e % T::kCPR);
+      stage[i] = load16_or_zero(centres16 + static_cast<int64_t>(c < c_end ? c : 0) * d + k0, c < c_end && k0 < d);
+    }
+  };
+  auto store_chunk16 = [&](unsigned char* buf) {
+#pragma unroll
+    for (int i = 0; i < T::kStage; ++i) {
+      const int e = t + 256 * i;
+      *reinterpret_cast<u32x4*>(buf + (e / T::kCPR) * T::kRowBytes + (e % T::kCPR) * 16) = stage[i];
+    }
+  };
+  load_chunk16(c_begin);
+  store_chunk16(cs[0]);
+  __syncthreads();
+  int cur = 0;
+  for (int c0 = c_begin; c0 < c_end; c0 += T::kChunk) {
+    const bool more = c0 + T::kChunk < c_end;
+    if (more) load_chunk16(c0 + T::kChunk);  // in flight while this chunk is multiplied
+    const unsigned char* buf = cs[cur];
 #pragma unroll
     for (int j = 0; j < kTiles; ++j) {
-      const int cbase = c0 + 16 * j;  // wave-uniform
-      if (cbase >= K) break;
-      const int c = cbase + m16;
-      const double Y = c < K ? cterm[c] : __builtin_nan("");
-      const bool live = Y == Y;  // not NaN: a live cluster
+      const int cbase = c0 + 16 * j;  // block-uniform
+      if (cbase >= c_end) break;
+      f32x4 acc[RT];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const bool pass = live && (big[v] || Y == -__builtin_inf() || X[v] + Y < 2.0 * static_cast<double>(acc[j][v]));
-        const unsigned long long bal = __ballot(pass);
-        const uint32_t half = static_cast<uint32_t>(bal >> (16 * g)) & 0xFFFFu;
-        if ((m16 & 3) == v) word |= half << (16 * ((cbase >> 4) & 1));
+      for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < KS; ++st) {
+        const u32x4 b = *reinterpret_cast<const u32x4*>(buf + (16 * j + m16) * T::kRowBytes + (4 * st + g) * 16);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+          acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a[rt][st]),
+                                                           __builtin_bit_cast(f16x8, b), acc[rt], 0, 0, 0);
       }
-      if (((cbase >> 4) & 1) || cbase + 16 >= K) {
-        if (m16 < 4 && myrow < B) mask[myrow * words + (cbase >> 5)] = word;
-        word = 0u;
+      const int c = cbase + m16;
+      const double Y = c < c_end ? cterm[c] : __builtin_nan("");
+      const bool live = Y == Y;  // not NaN: a live cluster
+      const bool ybig = Y == -__builtin_inf();
+      const int sh = 16 * ((cbase >> 4) & 1);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const bool pass = live && (big[rt][v] || ybig || X[rt][v] + Y < 2.0 * static_cast<double>(acc[rt][v]));
+          const unsigned long long bal = __ballot(pass);
+          const uint32_t half = static_cast<uint32_t>(bal >> (16 * g)) & 0xFFFFu;
+          if ((m16 & 3) == v) word[rt] |= half << sh;
+        }
+      }
+      if (sh || cbase + 16 >= c_end) {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+          const int64_t row = rw + rt * 16 + 4 * g + (m16 & 3);
+          if (m16 < 4 && row < B) mask[row * words + (cbase >> 5)] = word[rt];
+          word[rt] = 0u;
+        }
       }
     }
+    if (more) store_chunk16(cs[cur ^ 1]);  // that buffer was last read before the previous barrier
+    __syncthreads();
+    cur ^= 1;
   }
 }
 
@@ -1040,20 +1084,30 @@ lipcache_status index_query_plan(const lipcache_index* idx, const uint16_t* zq16
   LC_LAUNCHED();
   int ks = 1;
   while (ks * 32 < d) ks *= 2;
-  const unsigned grid = static_cast<unsigned>((B + kCr - 1) / kCr);
-  auto go = [&](auto kern) {
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, zq16, w.qnorm, B, d, w.c16, w.cterm, K, words, sl, w.mask);
+  auto go = [&](auto kern, int rows) {
+    // about two blocks per CU: split the centres when the queries alone
+    // give fewer
+    const int64_t gx = (B + rows - 1) / rows;
+    const int64_t chunks64 = (K + 63) / 64;
+    int64_t gy = (512 + gx - 1) / gx;
+    gy = gy < 1 ? 1 : (gy > chunks64 ? chunks64 : gy);
+    const int cspan = static_cast<int>(((K + gy - 1) / gy + 63) / 64 * 64);
+    gy = (K + cspan - 1) / cspan;
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy)), dim3(256), 0, s, zq16,
+                       w.qnorm, B, d, w.c16, w.cterm, K, cspan, words, sl, w.mask);
   };
+#define LC_CAND(KS_) go(cand16_kernel<KS_>, CandTraits<KS_>::kRows)
   switch (ks) {
-    case 1: go(cand16_kernel<1>); break;
-    case 2: go(cand16_kernel<2>); break;
-    case 4: go(cand16_kernel<4>); break;
-    case 8: go(cand16_kernel<8>); break;
-    case 16: go(cand16_kernel<16>); break;
-    default: go(cand16_kernel<32>); break;
+    case 1: LC_CAND(1); break;
+    case 2: LC_CAND(2); break;
+    case 4: LC_CAND(4); break;
+    case 8: LC_CAND(8); break;
+    case 16: LC_CAND(16); break;
+    default: LC_CAND(32); break;
   }
+#undef LC_CAND
   LC_LAUNCHED();
-  const unsigned gq = static_cast<unsigned>((B + 255) / 256);
+  const unsigned gq = static_cast<unsigned>((B + kPlanRows - 1) / kPlanRows);
   const unsigned gl = static_cast<unsigned>((K + 1 + 255) / 256);
   hipLaunchKernelGGL(plan_count_kernel, dim3(gq), dim3(256), 0, s, w.mask, words, B, K, w.ccount);
   LC_LAUNCHED();

@@ -6,7 +6,7 @@
 
 namespace lc {
 
-constexpr int64_t kItemRows = 2048;  // cluster rows per work item at most
+constexpr int64_t kItemRows = 1024;  // cluster rows per work item at most
 constexpr int kMaxCand = 256;        // a query with more candidate clusters scans every indexed row
 
 struct IndexPlanWs {

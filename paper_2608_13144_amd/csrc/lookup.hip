@@ -35,10 +35,10 @@
 //  - grid = query blocks x cache slices; blocks are numbered so that the
 //    blocks a given XCD runs (block id mod 8) share cache slices, so the
 //    resident workgroups of an XCD read each cache tile from its L2 at about
-//    the same time.  The indexed lookup instead gives each block one item of
-//    a work list: up to 512 queries of one cluster's query list (read through
-//    the list, in a separate instantiation) against a chunk of that cluster's
-//    rows.  There a query meets its own cluster's rows, so pairs pass the
+//    the same time.  The indexed lookup instead gives each block (4 waves,
+//    64-row tiles, two blocks per CU) one item of a work list: up to 256
+//    queries of one cluster's query list (read through the list, in a
+//    separate instantiation) against a chunk of that cluster's rows.  There a query meets its own cluster's rows, so pairs pass the
 //    filter often: each wave queues them in LDS, hands the queue to the
 //    global queue after its last tile in one reservation; waves past the
 //    list end only copy;
@@ -839,12 +839,16 @@ __device__ __forceinline__ void lds_copy(const void* sbase, uint32_t voff, const
   }
 }
 
-// Waves per workgroup of the slice-mode DMA kernel (the work-list kernel
-// keeps 8).
+// Waves per workgroup of the slice-mode DMA kernel.
 #ifndef LC_DMA_WAVES
 #define LC_DMA_WAVES 8
 #endif
 constexpr int kDmaWaves = LC_DMA_WAVES;
+// Waves per workgroup of the work-list DMA kernel: a cluster's query list
+// is short (a few hundred queries), so an item of 4 waves (256 queries) and
+// 64-row tiles lets two items share a CU where one 8-wave item would leave
+// most of its waves idle.
+constexpr int kListWaves = 4;
 
 // Cache rows per LDS tile of the DMA kernel with NW waves: 64 KiB per buffer
 // for 8 waves, 32 KiB for 4 (rows of 64 * KS bytes in either element type),
@@ -1202,7 +1206,7 @@ inline bool make_plan(int precision, const lipcache_cache* c, bool list, Plan& p
   // most 64 KiB.
   const bool same_type = precision == LIPCACHE_F16 ? c->zimg != nullptr : c->store_dtype == LIPCACHE_F32;
   pl.dma = same_type && ks <= 16;
-  pl.waves = pl.dma && !list ? kDmaWaves : kLkWaves;
+  pl.waves = pl.dma ? (list ? kListWaves : kDmaWaves) : kLkWaves;
   pl.qblock = pl.waves * pl.rt * 16;
   if (pl.dma) {
     pl.tile_rows = pl.waves == 8 ? (ks <= 8 ? 128 : 64) : (ks <= 8 ? 64 : 32);  // DmaTraits<KS, NW>::kRows
@@ -1227,7 +1231,7 @@ hipError_t launch_v1(const LookupParams& p, unsigned grid, hipStream_t s) {
 template <int MODE, int STORE, int KS, int VAR>
 hipError_t launch_dma(const LookupParams& p, unsigned grid, hipStream_t s) {
   if constexpr (KS <= 16) {
-    constexpr int kNW = VAR == kVarList ? kLkWaves : kDmaWaves;
+    constexpr int kNW = VAR == kVarList ? kListWaves : kDmaWaves;
     hipLaunchKernelGGL((lookup_dma_kernel<MODE, STORE, KS, (KS <= 8 ? 4 : 2), kNW, VAR == kVarDump, VAR == kVarList>),
                        dim3(grid), dim3(kNW * kWave), 0, s, p);
     return hipGetLastError();

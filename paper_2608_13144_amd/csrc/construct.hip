@@ -81,6 +81,68 @@ __global__ void construct_keys_kernel(const float* __restrict__ r, const float* 
   if (lane_id() == 0 && bal != 0ull) atomicAdd(n_elig, static_cast<unsigned long long>(__builtin_popcountll(bal)));
 }
 
+// The next chunk of the greedy visit: the first kChunk candidates, from
+// position cursor[0] of the visit order on, whose class still has room
+// (every candidate without a per-class budget).  A candidate of a full class
+// would be skipped by the one-by-one visit without touching the accepted set,
+// the class counts or the total, so leaving it out changes no decision.  One
+// workgroup scans windows of 1024 positions (a ballot and a workgroup prefix
+// per window); cursor[0] becomes the position after the last candidate taken
+// (or the end), cursor[1] the chunk's size, cand[] its candidates in order.
+__global__ __launch_bounds__(1024) void construct_compact_kernel(const uint32_t* __restrict__ order, int64_t n_elig,
+                                                                 const int32_t* __restrict__ label,
+                                                                 const int32_t* __restrict__ class_count,
+                                                                 int per_class, unsigned long long* __restrict__ cursor,
+                                                                 uint32_t* __restrict__ cand) {
+  __shared__ int wsum[1024 / kWave];
+  __shared__ int64_t s_cur;
+  __shared__ int s_k;
+  const int t = static_cast<int>(threadIdx.x);
+  const int lane = lane_id(), wave = t / kWave;
+  constexpr int kWaves = 1024 / kWave;
+  if (t == 0) {
+    s_cur = static_cast<int64_t>(cursor[0]);
+    s_k = 0;
+  }
+  __syncthreads();
+  while (true) {
+    const int64_t cur = s_cur;
+    const int k = s_k;
+    if (k >= kChunk || cur >= n_elig) break;  // uniform
+    const int64_t pos = cur + t;
+    const bool in = pos < n_elig;
+    const uint32_t ci = in ? order[pos] : 0u;
+    bool f = in;
+    if (f && per_class > 0) f = class_count[label[ci]] < per_class;
+    const unsigned long long bal = __ballot(f);
+    const int rank = __builtin_popcountll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) wsum[wave] = __builtin_popcountll(bal);
+    __syncthreads();
+    int before = 0, total = 0;
+    for (int w = 0; w < kWaves; ++w) {
+      before += w < wave ? wsum[w] : 0;
+      total += wsum[w];
+    }
+    const int r = k + before + rank;
+    if (f && r < kChunk) cand[r] = ci;
+    __syncthreads();  // s_cur, s_k and wsum are read; update them
+    if (k + total <= kChunk) {
+      if (t == 0) {
+        s_k = k + total;
+        s_cur = cur + 1024 < n_elig ? cur + 1024 : n_elig;
+      }
+    } else if (f && r == kChunk - 1) {
+      s_k = kChunk;
+      s_cur = pos + 1;
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    cursor[0] = static_cast<unsigned long long>(s_cur);
+    cursor[1] = static_cast<unsigned long long>(s_k);
+  }
+}
+
 // Chunk rows in visit order: the stored values (bf16-rounded for a bf16
 // cache) as float32, with their payload and radius.  One wave per row.
 __global__ void construct_gather_kernel(const float* __restrict__ z, const int32_t* __restrict__ label,
@@ -666,6 +728,7 @@ struct CWs {
   int32_t* lc;
   float* rc;
   int64_t* src_c;
+  uint32_t* cand;       // [kChunk] candidates of the current chunk, in visit order
   int32_t* dup;
   int32_t* sel;
   uint32_t* rel;
@@ -713,6 +776,7 @@ inline CWs cws_layout(int64_t n, int d, int n_classes, int64_t budget, size_t su
   w.lc = reinterpret_cast<int32_t*>(take(kChunk * 4));
   w.rc = reinterpret_cast<float*>(take(kChunk * 4));
   w.src_c = reinterpret_cast<int64_t*>(take(kChunk * 8));
+  w.cand = reinterpret_cast<uint32_t*>(take(kChunk * 4));
   w.dup = reinterpret_cast<int32_t*>(take(kChunk * 4));
   w.sel = reinterpret_cast<int32_t*>(take(kChunk * 4));
   w.rel = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(kChunk) * kChunkWords * 4));
@@ -806,10 +870,21 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
   int64_t added = 0;
   if (strategy != LIPCACHE_SELECT_KCENTER) {
     const int dedup = strategy == LIPCACHE_SELECT_RADIUS_DEDUP ? 1 : 0;
-    for (int64_t s0 = 0; s0 < n_elig && added < bud; s0 += kChunk) {
-      const int k = static_cast<int>(n_elig - s0 < kChunk ? n_elig - s0 : kChunk);
+    // counters[2], [3]: visit cursor and size of the next chunk
+    unsigned long long* cursor = w.counters + 2;
+    auto next_chunk = [&]() {
+      hipLaunchKernelGGL(construct_compact_kernel, dim3(1), dim3(1024), 0, s, order, n_elig, label, w.class_count,
+                         per_class, cursor, w.cand);
+      return hipGetLastError();
+    };
+    LC_HIP(next_chunk());
+    unsigned long long cur_k[2] = {0ull, 0ull};
+    LC_HIP(hipMemcpyAsync(cur_k, cursor, 16, hipMemcpyDeviceToHost, s));
+    LC_HIP(hipStreamSynchronize(s));
+    while (cur_k[1] > 0 && added < bud) {
+      const int k = static_cast<int>(cur_k[1]);
       hipLaunchKernelGGL(construct_gather_kernel, dim3(static_cast<unsigned>((k + 3) / 4)), dim3(256), 0, s, z, label,
-                         r, order + s0, k, d, bf16, w.zc, w.lc, w.rc, w.src_c);
+                         r, w.cand, k, d, bf16, w.zc, w.lc, w.rc, w.src_c);
       LC_LAUNCHED();
       const int32_t* dup = nullptr;
       if (dedup) {
@@ -839,10 +914,15 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
       ap.selected_out = selected_out;
       hipLaunchKernelGGL(construct_accept_kernel, dim3(1), dim3(1024), 0, s, ap);
       LC_LAUNCHED();
+      // the next chunk, from the class counts this one leaves (its
+      // candidates were copied to zc by the gather above)
+      LC_HIP(next_chunk());
       int64_t got = 0;
       const lipcache_status st = lipcache_insert(c, w.zc, w.lc, w.rc, w.sel, k, &got, w.sub_ws, w.sub_bytes, stream);
       if (st != LIPCACHE_OK) return st;
       added += got;
+      LC_HIP(hipMemcpyAsync(cur_k, cursor, 16, hipMemcpyDeviceToHost, s));
+      LC_HIP(hipStreamSynchronize(s));
     }
   } else {
     if (per_class > 0) {

@@ -171,3 +171,32 @@ def test_construct_larger_dedup():
     cert = oracle.certify(wl.z, wl.W, wl.b, sig, radius_mode="tight")
     _, st, sel = run_both(wl.z, cert.label, cert.r, 128, per_class=200, n_classes=10)
     assert 1000 < sel.size <= 2000 and np.bincount(st.label).max() <= 200
+
+
+@pytest.mark.parametrize("strategy", ["radius_dedup", "priority"])
+def test_construct_skips_full_classes(strategy):
+    """Chunks are formed from candidates whose class still has room: three
+    large classes fill within the first chunk, the candidates of a small
+    class come last in the visit (smallest radii or priorities), thousands
+    of candidates of full classes lie between, and duplicates (points inside
+    an earlier ball) fall on both sides of a class filling.  The selection
+    must equal the one-by-one visit of the oracle."""
+    say("construct skips full classes", strategy)
+    rng = np.random.default_rng(21)
+    d, C, n_big, n_small = 32, 4, 2500, 300
+    lab = np.concatenate([np.repeat(np.arange(3), n_big), np.full(n_small, 3)]).astype(np.int32)
+    n = lab.size
+    # 60 sub-clusters per class, points 0.3 apart on average: many fall in
+    # each other's balls (radius 0.2 - 0.6), so about 130 - 220 candidates
+    # are visited before each large class holds its 40
+    centres = 4.0 * rng.standard_normal((C, 60, d))
+    z = (centres[lab, rng.integers(0, 60, n)] + (0.3 / math.sqrt(2 * d)) * rng.standard_normal((n, d))).astype(np.float32)
+    r = np.where(lab < 3, rng.uniform(0.2, 0.6, n), rng.uniform(0.01, 0.05, n)).astype(np.float32)
+    pri = np.where(lab < 3, rng.uniform(1.0, 2.0, n), rng.uniform(0.0, 0.5, n)).astype(np.float32)
+    perm = rng.permutation(n)
+    z, lab, r, pri = z[perm], lab[perm], r[perm], pri[perm]
+    _, st, sel = run_both(z, lab, r, d, strategy=strategy, per_class=40, n_classes=C,
+                          priority=pri if strategy == "priority" else None)
+    counts = np.bincount(st.label, minlength=C)
+    assert counts[:3].tolist() == [40, 40, 40] and counts[3] > 0
+    say("construct skips full classes", strategy, "counts", counts.tolist())

@@ -86,20 +86,25 @@ __global__ void construct_keys_kernel(const float* __restrict__ r, const float* 
 // (every candidate without a per-class budget).  A candidate of a full class
 // would be skipped by the one-by-one visit without touching the accepted set,
 // the class counts or the total, so leaving it out changes no decision.  One
-// workgroup scans windows of 1024 positions (a ballot and a workgroup prefix
-// per window); cursor[0] becomes the position after the last candidate taken
-// (or the end), cursor[1] the chunk's size, cand[] its candidates in order.
+// workgroup scans windows of kCompactPer x 1024 positions (thread t takes
+// kCompactPer consecutive ones; a workgroup prefix sum of the per-thread
+// counts places them); cursor[0] becomes the position after the last
+// candidate taken (or the end), cursor[1] the chunk's size, cand[] its
+// candidates in order.
+constexpr int kCompactPer = 8;
+
 __global__ __launch_bounds__(1024) void construct_compact_kernel(const uint32_t* __restrict__ order, int64_t n_elig,
                                                                  const int32_t* __restrict__ label,
                                                                  const int32_t* __restrict__ class_count,
                                                                  int per_class, unsigned long long* __restrict__ cursor,
                                                                  uint32_t* __restrict__ cand) {
-  __shared__ int wsum[1024 / kWave];
+  constexpr int kWaves = 1024 / kWave;
+  constexpr int kWindow = 1024 * kCompactPer;
+  __shared__ int wsum[kWaves];
   __shared__ int64_t s_cur;
   __shared__ int s_k;
   const int t = static_cast<int>(threadIdx.x);
   const int lane = lane_id(), wave = t / kWave;
-  constexpr int kWaves = 1024 / kWave;
   if (t == 0) {
     s_cur = static_cast<int64_t>(cursor[0]);
     s_k = 0;
@@ -109,31 +114,57 @@ __global__ __launch_bounds__(1024) void construct_compact_kernel(const uint32_t*
     const int64_t cur = s_cur;
     const int k = s_k;
     if (k >= kChunk || cur >= n_elig) break;  // uniform
-    const int64_t pos = cur + t;
-    const bool in = pos < n_elig;
-    const uint32_t ci = in ? order[pos] : 0u;
-    bool f = in;
-    if (f && per_class > 0) f = class_count[label[ci]] < per_class;
-    const unsigned long long bal = __ballot(f);
-    const int rank = __builtin_popcountll(bal & ((1ull << lane) - 1ull));
-    if (lane == 0) wsum[wave] = __builtin_popcountll(bal);
+    const int64_t p0 = cur + static_cast<int64_t>(t) * kCompactPer;
+    uint32_t ci[kCompactPer];
+    bool f[kCompactPer];
+#pragma unroll
+    for (int j = 0; j < kCompactPer; ++j) {
+      f[j] = p0 + j < n_elig;
+      ci[j] = f[j] ? order[p0 + j] : 0u;
+    }
+    if (per_class > 0) {
+      int cl[kCompactPer];
+#pragma unroll
+      for (int j = 0; j < kCompactPer; ++j) cl[j] = f[j] ? label[ci[j]] : 0;
+#pragma unroll
+      for (int j = 0; j < kCompactPer; ++j) f[j] = f[j] && class_count[cl[j]] < per_class;
+    }
+    int mine = 0;
+#pragma unroll
+    for (int j = 0; j < kCompactPer; ++j) mine += f[j] ? 1 : 0;
+    // inclusive prefix of the per-thread counts within the wave
+    int incl = mine;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int o = __shfl_up(incl, off, kWave);
+      if (lane >= off) incl += o;
+    }
+    if (lane == kWave - 1) wsum[wave] = incl;
     __syncthreads();
     int before = 0, total = 0;
     for (int w = 0; w < kWaves; ++w) {
       before += w < wave ? wsum[w] : 0;
       total += wsum[w];
     }
-    const int r = k + before + rank;
-    if (f && r < kChunk) cand[r] = ci;
+    int r = k + before + incl - mine;  // chunk slot of this thread's first flagged candidate
+    int64_t last_pos = -1;            // position of the candidate that fills the chunk, if this thread holds it
+#pragma unroll
+    for (int j = 0; j < kCompactPer; ++j) {
+      if (f[j]) {
+        if (r < kChunk) cand[r] = ci[j];
+        if (r == kChunk - 1) last_pos = p0 + j;
+        ++r;
+      }
+    }
     __syncthreads();  // s_cur, s_k and wsum are read; update them
     if (k + total <= kChunk) {
       if (t == 0) {
         s_k = k + total;
-        s_cur = cur + 1024 < n_elig ? cur + 1024 : n_elig;
+        s_cur = cur + kWindow < n_elig ? cur + kWindow : n_elig;
       }
-    } else if (f && r == kChunk - 1) {
+    } else if (last_pos >= 0) {
       s_k = kChunk;
-      s_cur = pos + 1;
+      s_cur = last_pos + 1;
     }
     __syncthreads();
   }

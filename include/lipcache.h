@@ -154,8 +154,9 @@ size_t lipcache_spectral_norm_workspace_bytes(int32_t C, int32_t d);
  *  sigma       > 0, normally lipcache_spectral_norm's result (used by the
  *              conservative radius only, but validated in both modes)
  *  radius_mode LIPCACHE_RADIUS_CONSERVATIVE or LIPCACHE_RADIUS_TIGHT; the
- *              tight mode evaluates the logits twice and needs a C x C
- *              float64 table in the workspace
+ *              tight mode needs a C x C float64 table of row distances in
+ *              the workspace, and evaluates the logits a second time only
+ *              for the rows whose minimum its first pass cannot prove
  *  label_out [N] int32, r_out [N] float (required)
  *  margin_out [N] float, norm2_out [N] float (nullable): m_i and ||z_i||^2
  *  ws          lipcache_certify_workspace_bytes(C, d, radius_mode) bytes

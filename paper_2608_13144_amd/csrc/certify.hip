@@ -65,6 +65,19 @@ __global__ void row_distance_kernel(const double* __restrict__ W64, int C, int d
   dist[t] = __builtin_sqrt(acc);
 }
 
+// dmax[y] = max over j with dist[y * C + j] > 0 of that distance (0 when
+// every other row equals W_y): bounds every denominator of row y.
+__global__ void row_dmax_kernel(const double* __restrict__ dist, int C, double* __restrict__ dmax) {
+  const int y = static_cast<int>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (y >= C) return;
+  double m = 0.0;
+  for (int j = 0; j < C; ++j) {
+    const double v = dist[static_cast<int64_t>(y) * C + j];
+    m = v > m ? v : m;
+  }
+  dmax[y] = m;
+}
+
 // W z (no bias) for the classes c0 .. c0 + 7 below C, from the lane's feature
 // row zr in LDS and the float64 head (rows read through scalar loads).
 __device__ __forceinline__ void chunk_logits(const float* zr, const double* __restrict__ W64, int c0, int C, int d,
@@ -243,7 +256,13 @@ __global__ __launch_bounds__(kCertThreads) void certify_kernel(
 // a running (top-1, class, top-2) per feature over its classes in increasing
 // order, and a butterfly over the 16 lanes of its row group merges them (the
 // larger top-1 wins, the lower class on equal values, the rest competes for
-// top-2): the same result as one pass over the classes in order.
+// top-2): the same result as one pass over the classes in order.  For the
+// tight radius each lane also keeps the classes of its own two largest
+// logits and its third largest value; the minimum of (s_y - s_j) /
+// ||W_y - W_j|| over the listed classes is the tight radius whenever a bound
+// through the third values and the largest row distance of y shows that no
+// unlisted class goes below it, and a workgroup with any row it cannot
+// settle evaluates all logits a second time.
 constexpr int kCmThreads = 256;
 constexpr int kCmRows = 64;        // features per workgroup
 constexpr int kCmClasses = 32;     // head rows per LDS stage
@@ -299,8 +318,8 @@ __device__ __forceinline__ void stage_head(const float* __restrict__ W, int C, i
 template <bool BF16_STORE, bool TIGHT, int KQ>
 __global__ __launch_bounds__(kCmThreads) void certify_mfma_kernel(
     const float* __restrict__ z, int64_t N, int d, const float* __restrict__ W, const float* __restrict__ b, int C,
-    double sigma, const double* __restrict__ row_dist, int32_t* __restrict__ label_out, float* __restrict__ r_out,
-    float* __restrict__ margin_out, float* __restrict__ norm2_out) {
+    double sigma, const double* __restrict__ row_dist, const double* __restrict__ dmax, int32_t* __restrict__ label_out,
+    float* __restrict__ r_out, float* __restrict__ margin_out, float* __restrict__ norm2_out) {
   extern __shared__ float wl[];  // kCmClasses rows of stride 16 KQ + 4 floats
   constexpr int kWidth = 16 * KQ;
   constexpr int stride = kWidth + 4;
@@ -334,11 +353,17 @@ __global__ __launch_bounds__(kCmThreads) void certify_mfma_kernel(
 
   double v1[4], v2[4];
   int i1[4];
+  // tight radius: the lane's own two largest logits with their classes and
+  // its third largest value, per feature
+  double a1[4], a2[4], a3[4];
+  int c1[4], c2[4];
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     v1[v] = -__builtin_inf();
     v2[v] = -__builtin_inf();
     i1[v] = INT_MAX;
+    a1[v] = a2[v] = a3[v] = -__builtin_inf();
+    c1[v] = c2[v] = -1;
   }
   for (int c0 = 0; c0 < C; c0 += kCmClasses) {
     __syncthreads();
@@ -352,8 +377,35 @@ __global__ __launch_bounds__(kCmThreads) void certify_mfma_kernel(
       if (c < C) {
         const double bc = b ? static_cast<double>(b[c]) : 0.0;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) top2_push(acc[t][v] + bc, c, v1[v], i1[v], v2[v]);
+        for (int v = 0; v < 4; ++v) {
+          const double sv = acc[t][v] + bc;
+          if constexpr (TIGHT) {
+            if (sv > a1[v]) {
+              a3[v] = a2[v];
+              a2[v] = a1[v];
+              c2[v] = c1[v];
+              a1[v] = sv;
+              c1[v] = c;
+            } else if (sv > a2[v]) {
+              a3[v] = a2[v];
+              a2[v] = sv;
+              c2[v] = c;
+            } else if (sv > a3[v]) {
+              a3[v] = sv;
+            }
+          } else {
+            top2_push(sv, c, v1[v], i1[v], v2[v]);
+          }
+        }
       }
+    }
+  }
+  if constexpr (TIGHT) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      v1[v] = a1[v];
+      i1[v] = c1[v] < 0 ? INT_MAX : c1[v];
+      v2[v] = a2[v];
     }
   }
 #pragma unroll
@@ -371,7 +423,50 @@ __global__ __launch_bounds__(kCmThreads) void certify_mfma_kernel(
 #pragma unroll
   for (int v = 0; v < 4; ++v) r[v] = (v1[v] - v2[v]) / (sigma * kSqrt2);
   if constexpr (TIGHT) {
+    // r* = min over j != y of (s_y - s_j) / ||W_y - W_j||.  First from the
+    // lanes' lists: rl = the least ratio over every listed class.  A class a
+    // lane did not list has s_j <= a3 of that lane and a denominator <=
+    // dmax[y], so (rounding being monotone) its computed ratio is at least
+    // fl(fl(s_y - a3) / dmax[y]); when that is >= rl on all 16 lanes, rl is
+    // the minimum over all classes.  Otherwise the workgroup recomputes
+    // every logit (same arithmetic, so the same values) and takes the
+    // minimum over all of them; the result is the same number either way.
     double best[4];
+    bool ok = true;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int y = i1[v];
+      double rl = __builtin_inf();
+      bool lane_ok = true;
+      if (y >= 0 && y < C) {
+        if (c1[v] >= 0 && c1[v] != y) {
+          const double den = row_dist[static_cast<int64_t>(y) * C + c1[v]];
+          if (den > 0.0) {
+            const double q = (v1[v] - a1[v]) / den;
+            rl = q < rl ? q : rl;
+          }
+        }
+        if (c2[v] >= 0 && c2[v] != y) {
+          const double den = row_dist[static_cast<int64_t>(y) * C + c2[v]];
+          if (den > 0.0) {
+            const double q = (v1[v] - a2[v]) / den;
+            rl = q < rl ? q : rl;
+          }
+        }
+      }
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) {
+        const double o = __shfl_xor(rl, off, kWave);
+        rl = o < rl ? o : rl;
+      }
+      if (y >= 0 && y < C && a3[v] > -__builtin_inf()) {
+        const double dm = dmax[y];
+        if (dm > 0.0) lane_ok = (v1[v] - a3[v]) / dm >= rl;
+      }
+      ok = ok && lane_ok;
+      best[v] = rl;
+    }
+    if (__syncthreads_or(ok ? 0 : 1)) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) best[v] = __builtin_inf();
     for (int c0 = 0; c0 < C; c0 += kCmClasses) {
@@ -406,6 +501,10 @@ __global__ __launch_bounds__(kCmThreads) void certify_mfma_kernel(
         const double o = __shfl_xor(best[v], off, kWave);
         best[v] = o < best[v] ? o : best[v];
       }
+    }
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
       // no label when the feature is not finite
       r[v] = (i1[v] >= 0 && i1[v] < C) ? best[v] : __builtin_nan("");
     }
@@ -455,7 +554,7 @@ hipError_t launch_certify(unsigned grid, size_t lds, hipStream_t s, const float*
 
 template <bool BF16_STORE, bool TIGHT, int KQ>
 hipError_t launch_mfma_kq(unsigned grid, size_t lds, hipStream_t s, const float* z, int64_t N, int d, const float* W,
-                          const float* b, int C, double sigma, const double* row_dist, int32_t* label_out,
+                          const float* b, int C, double sigma, const double* row_dist, const double* dmax, int32_t* label_out,
                           float* r_out, float* margin_out, float* norm2_out) {
   if (lds > 65536) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(certify_mfma_kernel<BF16_STORE, TIGHT, KQ>),
@@ -463,46 +562,46 @@ hipError_t launch_mfma_kq(unsigned grid, size_t lds, hipStream_t s, const float*
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL((certify_mfma_kernel<BF16_STORE, TIGHT, KQ>), dim3(grid), dim3(kCmThreads), lds, s, z, N, d, W,
-                     b, C, sigma, row_dist, label_out, r_out, margin_out, norm2_out);
+                     b, C, sigma, row_dist, dmax, label_out, r_out, margin_out, norm2_out);
   return hipGetLastError();
 }
 
 template <bool BF16_STORE, bool TIGHT>
 hipError_t launch_mfma_d(int d, unsigned grid, size_t lds, hipStream_t s, const float* z, int64_t N, const float* W,
-                         const float* b, int C, double sigma, const double* row_dist, int32_t* label_out,
+                         const float* b, int C, double sigma, const double* row_dist, const double* dmax, int32_t* label_out,
                          float* r_out, float* margin_out, float* norm2_out) {
   // registers for d / 16 k-groups, rounded up to a power of two
   const int nk = d / 16;
   if (nk <= 2)
-    return launch_mfma_kq<BF16_STORE, TIGHT, 2>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, label_out, r_out,
+    return launch_mfma_kq<BF16_STORE, TIGHT, 2>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, dmax, label_out, r_out,
                                                 margin_out, norm2_out);
   if (nk <= 4)
-    return launch_mfma_kq<BF16_STORE, TIGHT, 4>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, label_out, r_out,
+    return launch_mfma_kq<BF16_STORE, TIGHT, 4>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, dmax, label_out, r_out,
                                                 margin_out, norm2_out);
   if (nk <= 8)
-    return launch_mfma_kq<BF16_STORE, TIGHT, 8>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, label_out, r_out,
+    return launch_mfma_kq<BF16_STORE, TIGHT, 8>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, dmax, label_out, r_out,
                                                 margin_out, norm2_out);
   if (nk <= 16)
-    return launch_mfma_kq<BF16_STORE, TIGHT, 16>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, label_out, r_out,
+    return launch_mfma_kq<BF16_STORE, TIGHT, 16>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, dmax, label_out, r_out,
                                                  margin_out, norm2_out);
-  return launch_mfma_kq<BF16_STORE, TIGHT, 32>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, label_out, r_out,
+  return launch_mfma_kq<BF16_STORE, TIGHT, 32>(grid, lds, s, z, N, d, W, b, C, sigma, row_dist, dmax, label_out, r_out,
                                                margin_out, norm2_out);
 }
 
 hipError_t launch_certify_mfma(bool bf16, bool tight, int d, unsigned grid, size_t lds, hipStream_t s, const float* z,
                                int64_t N, const float* W, const float* b, int C, double sigma,
-                               const double* row_dist, int32_t* label_out, float* r_out, float* margin_out,
+                               const double* row_dist, const double* dmax, int32_t* label_out, float* r_out, float* margin_out,
                                float* norm2_out) {
   if (bf16 && tight)
-    return launch_mfma_d<true, true>(d, grid, lds, s, z, N, W, b, C, sigma, row_dist, label_out, r_out, margin_out,
+    return launch_mfma_d<true, true>(d, grid, lds, s, z, N, W, b, C, sigma, row_dist, dmax, label_out, r_out, margin_out,
                                      norm2_out);
   if (bf16)
-    return launch_mfma_d<true, false>(d, grid, lds, s, z, N, W, b, C, sigma, row_dist, label_out, r_out, margin_out,
+    return launch_mfma_d<true, false>(d, grid, lds, s, z, N, W, b, C, sigma, row_dist, dmax, label_out, r_out, margin_out,
                                       norm2_out);
   if (tight)
-    return launch_mfma_d<false, true>(d, grid, lds, s, z, N, W, b, C, sigma, row_dist, label_out, r_out, margin_out,
+    return launch_mfma_d<false, true>(d, grid, lds, s, z, N, W, b, C, sigma, row_dist, dmax, label_out, r_out, margin_out,
                                       norm2_out);
-  return launch_mfma_d<false, false>(d, grid, lds, s, z, N, W, b, C, sigma, row_dist, label_out, r_out, margin_out,
+  return launch_mfma_d<false, false>(d, grid, lds, s, z, N, W, b, C, sigma, row_dist, dmax, label_out, r_out, margin_out,
                                      norm2_out);
 }
 
@@ -511,7 +610,8 @@ hipError_t launch_certify_mfma(bool bf16, bool tight, int d, unsigned grid, size
 extern "C" size_t lipcache_certify_workspace_bytes(int32_t C, int32_t d, int32_t radius_mode) {
   if (C < 1 || d < 1) return 0;
   size_t n = head_bytes(C, d);
-  if (radius_mode == LIPCACHE_RADIUS_TIGHT) n += align_up(static_cast<size_t>(C) * C * sizeof(double), 256);
+  if (radius_mode == LIPCACHE_RADIUS_TIGHT)
+    n += align_up(static_cast<size_t>(C) * C * sizeof(double), 256) + align_up(static_cast<size_t>(C) * sizeof(double), 256);
   return n;
 }
 
@@ -542,11 +642,17 @@ extern "C" lipcache_status lipcache_certify(const float* z, int64_t N, int32_t d
     LC_LAUNCHED();
   }
   double* row_dist = nullptr;
+  double* dmax = nullptr;
   if (tight) {
     row_dist = reinterpret_cast<double*>(static_cast<unsigned char*>(ws) + head_bytes(C, d));
+    dmax = reinterpret_cast<double*>(reinterpret_cast<unsigned char*>(row_dist) +
+                                     align_up(static_cast<size_t>(C) * C * sizeof(double), 256));
     const int64_t cc = static_cast<int64_t>(C) * C;
     hipLaunchKernelGGL(row_distance_kernel, dim3(static_cast<unsigned>((cc + 255) / 256)), dim3(256), 0, s, W64, C, d,
                        row_dist);
+    LC_LAUNCHED();
+    hipLaunchKernelGGL(row_dmax_kernel, dim3(static_cast<unsigned>((C + 255) / 256)), dim3(256), 0, s, row_dist, C,
+                       dmax);
     LC_LAUNCHED();
   }
 
@@ -556,7 +662,7 @@ extern "C" lipcache_status lipcache_certify(const float* z, int64_t N, int32_t d
     const size_t lds_m = static_cast<size_t>(kCmClasses) * (16 * kq + 4) * sizeof(float);
     const unsigned grid_m = static_cast<unsigned>((N + kCmRows - 1) / kCmRows);
     const hipError_t em = launch_certify_mfma(store_dtype == LIPCACHE_BF16, radius_mode == LIPCACHE_RADIUS_TIGHT, d,
-                                              grid_m, lds_m, s, z, N, W, b, C, sigma, row_dist, label_out, r_out,
+                                              grid_m, lds_m, s, z, N, W, b, C, sigma, row_dist, dmax, label_out, r_out,
                                               margin_out, norm2_out);
     return em == hipSuccess ? LIPCACHE_OK : LIPCACHE_EHIP;
   }

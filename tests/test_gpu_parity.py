@@ -163,6 +163,77 @@ def test_certify_tight_hand_cases():
     assert np.isposinf(ref.r[0])
 
 
+def _tight_second_pass_blocks(logits, W, rows_per_block=64):
+    """Which 64-feature workgroups cannot settle the tight radius from the
+    two largest logits each lane saw (lane = class mod 16) and must evaluate
+    the logits again: host model of the device's proof, on float64 logits,
+    to show that a case exercises both paths."""
+    C = W.shape[0]
+    Wd = W.astype(np.float64)
+    D = np.sqrt(((Wd[:, None, :] - Wd[None, :, :]) ** 2).sum(-1))
+    dmax = D.max(axis=1)
+    need = np.zeros(logits.shape[0], bool)
+    for i, s in enumerate(logits):
+        y = int(np.argmax(s))
+        listed, a3 = [], np.full(16, -np.inf)
+        for lane in range(16):
+            cl = np.arange(lane, C, 16)
+            o = cl[np.argsort(-s[cl], kind="stable")]
+            listed += list(o[:2])
+            if o.size > 2:
+                a3[lane] = s[o[2]]
+        q = [(s[y] - s[j]) / D[y, j] for j in listed if j != y and D[y, j] > 0]
+        rl = min(q) if q else np.inf
+        need[i] = dmax[y] > 0 and np.any((s[y] - a3[np.isfinite(a3)]) / dmax[y] < rl)
+    pad = (-need.size) % rows_per_block
+    return np.concatenate([need, np.zeros(pad, bool)]).reshape(-1, rows_per_block).any(axis=1)
+
+
+@pytest.mark.parametrize("far", [False, True])
+def test_certify_tight_crowded_heads(far):
+    """Remark 5.1 where the lists of the first pass cannot settle the
+    minimum.  Classes 16, 32 and 48 are near-copies of class 0 (all four
+    fall to the same lane, class mod 16).  The first 512 features (8
+    workgroups) lie far along W_0, so four near-equal logits lead and one
+    lane holds three of them: those workgroups must evaluate the logits
+    again.  The others lie between two other classes (two equal leading
+    logits, the rest far below): settled from the lists.  With `far`, one
+    more row lies far from all others, which loosens the bound of every row,
+    so every workgroup recomputes.  Labels and radii against the oracle; the
+    host model of the proof checks which workgroups take which path."""
+    say("certify tight crowded", far)
+    rng = np.random.default_rng(5)
+    C, d, N = 64, 64, 2048
+    W = (rng.standard_normal((C, d)) / math.sqrt(d)).astype(np.float32)
+    for j in (16, 32, 48):
+        W[j] = W[0] + (0.01 * rng.standard_normal(d) / math.sqrt(d)).astype(np.float32)
+    if far:
+        W[C - 1] = (6.0 * rng.standard_normal(d) / math.sqrt(d)).astype(np.float32)
+    Wd = W.astype(np.float64)
+    others = np.setdiff1d(np.arange(C - 1), [0, 16, 32, 48])
+    a = rng.choice(others, N - 512)
+    b = rng.choice(others, N - 512)
+    b = np.where(a == b, others[(np.searchsorted(others, b) + 1) % others.size], b)
+    z = np.concatenate([4.0 * math.sqrt(d) * np.repeat(Wd[:1], 512, 0), 2.0 * math.sqrt(d) * (Wd[a] + Wd[b])])
+    z = (z + 0.05 * rng.standard_normal((N, d))).astype(np.float32)
+    sig = oracle.spectral_norm(W).sigma
+    ref = oracle.certify(z, W, None, sig, radius_mode="tight")
+    blocks = _tight_second_pass_blocks(ref.logits, W)
+    say("certify tight crowded: workgroups recomputing", int(blocks.sum()), "of", blocks.size)
+    if far:
+        assert blocks.all()
+    else:
+        assert blocks[:8].all() and not blocks[8:].any()
+    out = api.certify(gpu(z), gpu(W), None, sig, radius_mode="tight")
+    lab, r = host(out.label), host(out.r)
+    scale = np.abs(ref.logits).max(axis=1) + 1.0
+    ok = ref.margin > 1e-9 * scale
+    assert ok.mean() > 0.99
+    assert np.array_equal(lab[ok], ref.label[ok])
+    rel = np.abs(r[ok].astype(np.float64) - ref.r64[ok]) / np.abs(ref.r64[ok])
+    assert rel.max() <= 1e-5, rel.max()
+
+
 # --------------------------------------------------------------- insert
 @pytest.mark.parametrize("store", ["f32", "bf16"])
 def test_insert_matches_oracle(store):

@@ -774,55 +774,81 @@ __global__ __launch_bounds__(256) void plan_fill_kernel(const uint32_t* __restri
 }
 
 // Rows of list c: cluster c, or every indexed row for list K; cut into
-// nearly equal chunks of at most kItemRows.
-__device__ __forceinline__ void list_rows(const int64_t* offsets, int K, int64_t n_indexed, int c, int64_t& e0,
-                                          int64_t& e1, int64_t& chunks, int64_t& step) {
+// nearly equal chunks of at most item_rows (<= kItemRowsMax).
+__device__ __forceinline__ void list_rows(const int64_t* offsets, int K, int64_t n_indexed, int c, int64_t item_rows,
+                                          int64_t& e0, int64_t& e1, int64_t& chunks, int64_t& step) {
   e0 = c < K ? offsets[c] : 0;
   e1 = c < K ? offsets[c + 1] : n_indexed;
-  chunks = e1 > e0 ? (e1 - e0 + kItemRows - 1) / kItemRows : 0;
+  chunks = e1 > e0 ? (e1 - e0 + item_rows - 1) / item_rows : 0;
   step = chunks ? (e1 - e0 + chunks - 1) / chunks : 1;
 }
 
-// Items per list: (query blocks of qblock) x (row chunks); one thread per list.
+// Work-item shape: lists of 512 queries or more on average (over the K + 1
+// lists) take the long shape (query blocks of qb_long, row chunks of at
+// most kItemRowsMax), others the short one (qb_short, kItemRows).  Every
+// kernel that cuts items takes the same decision from coff.
+__device__ __forceinline__ bool plan_long(const int64_t* __restrict__ coff, int K) {
+  return coff[K + 1] >= 512 * static_cast<int64_t>(K + 1);
+}
+
+// Items per list: (query blocks) x (row chunks); one thread per list.
 __global__ void plan_item_count_kernel(const int64_t* __restrict__ coff, const int64_t* __restrict__ offsets, int K,
-                                       int64_t n_indexed, int qblock, uint32_t* __restrict__ icount,
+                                       int64_t n_indexed, int qb_short, int qb_long, uint32_t* __restrict__ icount,
                                        unsigned long long* __restrict__ counters) {
   const int c = static_cast<int>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (c > K) return;
+  const bool lng = plan_long(coff, K);
+  const int qblock = lng ? qb_long : qb_short;
   const int64_t nq = coff[c + 1] - coff[c];
   int64_t e0, e1, chunks, step;
-  list_rows(offsets, K, n_indexed, c, e0, e1, chunks, step);
+  list_rows(offsets, K, n_indexed, c, lng ? kItemRowsMax : kItemRows, e0, e1, chunks, step);
   const int64_t qb = (nq + qblock - 1) / qblock;
   icount[c] = static_cast<uint32_t>(qb * chunks);
   if (nq > 0 && e1 > e0) atomicAdd(&counters[1], static_cast<unsigned long long>(nq * (e1 - e0)));
 }
 
-// The items of list c at ioff[c] (in list order); counters[0] = the total.
-__global__ void plan_items_kernel(const int64_t* __restrict__ coff, const int64_t* __restrict__ offsets, int K,
-                                  int64_t n_indexed, int qblock, const int64_t* __restrict__ ioff,
-                                  int64_t* __restrict__ items, int64_t capacity,
-                                  unsigned long long* __restrict__ counters) {
-  const int c = static_cast<int>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (c > K) return;
-  if (c == 0) {
-    counters[0] = static_cast<unsigned long long>(ioff[K + 1]);
-    if (ioff[K + 1] > capacity) counters[2] = 1ull;
+// Item i of the work list (list order; within a list, query blocks outer
+// and row chunks inner), one thread per item over a grid-stride loop: its
+// list is the last c with ioff[c] <= i.  counters[0] = the number of items,
+// counters[3] = 1 for the long shape.
+__global__ __launch_bounds__(256) void plan_items_kernel(const int64_t* __restrict__ coff,
+                                                         const int64_t* __restrict__ offsets, int K, int64_t n_indexed,
+                                                         int qb_short, int qb_long, const int64_t* __restrict__ ioff,
+                                                         int64_t* __restrict__ items, int64_t capacity,
+                                                         unsigned long long* __restrict__ counters) {
+  const int64_t total = ioff[K + 1];
+  const bool lng = plan_long(coff, K);
+  const int qblock = lng ? qb_long : qb_short;
+  const int64_t item_rows = lng ? kItemRowsMax : kItemRows;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    counters[0] = static_cast<unsigned long long>(total);
+    counters[3] = lng ? 1ull : 0ull;
+    if (total > capacity) counters[2] = 1ull;
   }
-  if (ioff[K + 1] > capacity) return;
-  const int64_t q0 = coff[c], q1 = coff[c + 1];
-  int64_t e0, e1, chunks, step;
-  list_rows(offsets, K, n_indexed, c, e0, e1, chunks, step);
-  if (q0 >= q1 || e0 >= e1) return;
-  int64_t slot = ioff[c];
-  for (int64_t qa = q0; qa < q1; qa += qblock) {
-    const int64_t qb = qa + qblock < q1 ? qa + qblock : q1;
-    for (int64_t ea = e0; ea < e1; ea += step) {
-      int64_t* it = items + 4 * slot++;
-      it[0] = qa;
-      it[1] = qb;
-      it[2] = ea;
-      it[3] = ea + step < e1 ? ea + step : e1;
+  if (total > capacity) return;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < total; i += stride) {
+    int lo = 0, hi = K;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (ioff[mid] <= i) {
+        lo = mid;
+      } else {
+        hi = mid - 1;
+      }
     }
+    const int c = lo;
+    int64_t e0, e1, chunks, step;
+    list_rows(offsets, K, n_indexed, c, item_rows, e0, e1, chunks, step);
+    const int64_t local = i - ioff[c];
+    const int64_t qa = coff[c] + (local / chunks) * qblock;
+    const int64_t qend = coff[c + 1];
+    const int64_t ea = e0 + (local % chunks) * step;
+    int64_t* it = items + 4 * i;
+    it[0] = qa;
+    it[1] = qa + qblock < qend ? qa + qblock : qend;
+    it[2] = ea;
+    it[3] = ea + step < e1 ? ea + step : e1;
   }
 }
 
@@ -1070,8 +1096,9 @@ __global__ __launch_bounds__(256) void cand16_kernel(const uint16_t* __restrict_
   }
 }
 
-lipcache_status index_query_plan(const lipcache_index* idx, const uint16_t* zq16, int64_t B, int d, int qblock,
-                                 const IndexPlanWs& w, int64_t& n_items, int64_t& pairs, hipStream_t s) {
+lipcache_status index_query_plan(const lipcache_index* idx, const uint16_t* zq16, int64_t B, int d, int qb_short,
+                                 int qb_long, const IndexPlanWs& w, int64_t& n_items, int64_t& pairs, bool& long_items,
+                                 hipStream_t s) {
   const int K = idx->K;
   const int words = (K + 31) / 32;
   const CandSlack sl = cand_slack(d);
@@ -1116,19 +1143,20 @@ lipcache_status index_query_plan(const lipcache_index* idx, const uint16_t* zq16
   hipLaunchKernelGGL(plan_fill_kernel, dim3(gq), dim3(256), 0, s, w.mask, words, B, K, w.coff, w.cfill, w.qlist);
   LC_LAUNCHED();
   hipLaunchKernelGGL(plan_item_count_kernel, dim3(gl), dim3(256), 0, s, w.coff, idx->offsets, K, idx->n_indexed,
-                     qblock, w.icount, w.counters);
+                     qb_short, qb_long, w.icount, w.counters);
   LC_LAUNCHED();
   hipLaunchKernelGGL(exclusive_scan_kernel, dim3(1), dim3(1024), 0, s, w.icount, K + 1, w.ioff);
   LC_LAUNCHED();
-  hipLaunchKernelGGL(plan_items_kernel, dim3(gl), dim3(256), 0, s, w.coff, idx->offsets, K, idx->n_indexed, qblock,
-                     w.ioff, w.items, w.capacity, w.counters);
+  hipLaunchKernelGGL(plan_items_kernel, dim3(256), dim3(256), 0, s, w.coff, idx->offsets, K, idx->n_indexed, qb_short,
+                     qb_long, w.ioff, w.items, w.capacity, w.counters);
   LC_LAUNCHED();
-  unsigned long long host[3] = {0ull, 0ull, 0ull};
+  unsigned long long host[4] = {0ull, 0ull, 0ull, 0ull};
   LC_HIP(hipMemcpyAsync(host, w.counters, sizeof(host), hipMemcpyDeviceToHost, s));
   LC_HIP(hipStreamSynchronize(s));
   if (host[2] != 0ull) return LIPCACHE_EHIP;  // the capacity bound was wrong: never expected
   n_items = static_cast<int64_t>(host[0]);
   pairs = static_cast<int64_t>(host[1]);
+  long_items = host[3] != 0ull;
   return LIPCACHE_OK;
 }
 

@@ -1193,7 +1193,7 @@ struct Plan {
 
 inline int rt_for(int ks) { return ks <= 8 ? 4 : (ks == 16 ? 2 : 1); }
 
-inline bool make_plan(int precision, const lipcache_cache* c, bool list, Plan& pl) {
+inline bool make_plan(int precision, const lipcache_cache* c, bool list, Plan& pl, int list_waves = kListWaves) {
   const int per_step = precision == LIPCACHE_F16 ? 32 : 16;
   int ks = precision == LIPCACHE_F16 ? 1 : 2;
   while (ks * per_step < c->d) ks *= 2;
@@ -1206,7 +1206,7 @@ inline bool make_plan(int precision, const lipcache_cache* c, bool list, Plan& p
   // most 64 KiB.
   const bool same_type = precision == LIPCACHE_F16 ? c->zimg != nullptr : c->store_dtype == LIPCACHE_F32;
   pl.dma = same_type && ks <= 16;
-  pl.waves = pl.dma ? (list ? kListWaves : kDmaWaves) : kLkWaves;
+  pl.waves = pl.dma ? (list ? list_waves : kDmaWaves) : kLkWaves;
   pl.qblock = pl.waves * pl.rt * 16;
   if (pl.dma) {
     pl.tile_rows = pl.waves == 8 ? (ks <= 8 ? 128 : 64) : (ks <= 8 ? 64 : 32);  // DmaTraits<KS, NW>::kRows
@@ -1218,12 +1218,12 @@ inline bool make_plan(int precision, const lipcache_cache* c, bool list, Plan& p
 
 // Kernel variants: the lookup, the filter dump, and the work-list lookup of
 // the cluster index.
-enum { kVarLookup = 0, kVarDump = 1, kVarList = 2 };
+enum { kVarLookup = 0, kVarDump = 1, kVarList = 2, kVarList8 = 3 };
 
 template <int MODE, int SRC, int KS, int VAR>
 hipError_t launch_v1(const LookupParams& p, unsigned grid, hipStream_t s) {
   hipLaunchKernelGGL((lookup_kernel<MODE, SRC, KS, (KS <= 8 ? 4 : (KS == 16 ? 2 : 1)), VAR == kVarDump,
-                                    VAR == kVarList>),
+                                    VAR == kVarList || VAR == kVarList8>),
                      dim3(grid), dim3(kLkThreads), 0, s, p);
   return hipGetLastError();
 }
@@ -1232,7 +1232,8 @@ template <int MODE, int STORE, int KS, int VAR>
 hipError_t launch_dma(const LookupParams& p, unsigned grid, hipStream_t s) {
   if constexpr (KS <= 16) {
     constexpr int kNW = VAR == kVarList ? kListWaves : kDmaWaves;
-    hipLaunchKernelGGL((lookup_dma_kernel<MODE, STORE, KS, (KS <= 8 ? 4 : 2), kNW, VAR == kVarDump, VAR == kVarList>),
+    hipLaunchKernelGGL((lookup_dma_kernel<MODE, STORE, KS, (KS <= 8 ? 4 : 2), kNW, VAR == kVarDump,
+                                          VAR == kVarList || VAR == kVarList8>),
                        dim3(grid), dim3(kNW * kWave), 0, s, p);
     return hipGetLastError();
   } else {
@@ -1348,12 +1349,14 @@ inline bool cache_ok(const lipcache_cache* c) {
 // the kernel plans of a slice scan and of a work-list scan.
 struct FilterConsts {
   Plan pl;
-  Plan pl_list;
+  Plan pl_list;    // work-list scan: 4-wave blocks (short cluster lists)
+  Plan pl_list8;   // work-list scan: 8-wave blocks (long cluster lists)
   Thresholds t;
 };
 
 lipcache_status lookup_consts(const lipcache_cache* c, int32_t precision, FilterConsts& fc) {
-  if (!make_plan(precision, c, false, fc.pl) || !make_plan(precision, c, true, fc.pl_list))
+  if (!make_plan(precision, c, false, fc.pl) || !make_plan(precision, c, true, fc.pl_list) ||
+      !make_plan(precision, c, true, fc.pl_list8, kDmaWaves))
     return LIPCACHE_EUNSUPPORTED;
   if (precision == LIPCACHE_F32 && (fc.pl.ks > 32 || c->d > 512)) return LIPCACHE_EUNSUPPORTED;
   const FilterSlack fs = filter_slack(precision, c->store_dtype, fc.pl.d_pad);
@@ -1457,7 +1460,8 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
   if (grid > INT_MAX) return LIPCACHE_EUNSUPPORTED;
   const unsigned gu = static_cast<unsigned>(grid);
   const hipError_t e = dump    ? launch_lookup<kVarDump>(precision, view->store_dtype, pl, p, gu, s)
-                       : items ? launch_lookup<kVarList>(precision, view->store_dtype, pl, p, gu, s)
+                       : items ? (pl.waves == kListWaves ? launch_lookup<kVarList>(precision, view->store_dtype, pl, p, gu, s)
+                                                         : launch_lookup<kVarList8>(precision, view->store_dtype, pl, p, gu, s))
                                : launch_lookup<kVarLookup>(precision, view->store_dtype, pl, p, gu, s);
   if (e != hipSuccess) return LIPCACHE_EHIP;
   if (dump) return LIPCACHE_OK;
@@ -1594,9 +1598,16 @@ lipcache_status run_lookup_indexed(const lipcache_cache* c, const lipcache_index
       lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s, &so, w.athr, w.gq.count, pw.qnorm, zq16);
   if (r != LIPCACHE_OK) return r;
   int64_t n_items = 0, idx_pairs = 0;
-  r = index_query_plan(idx, zq16, B, c->d, fc.pl_list.qblock, pw, n_items, idx_pairs, s);
+  bool long_items = false;
+  r = index_query_plan(idx, zq16, B, c->d, fc.pl_list.qblock, fc.pl_list8.qblock, pw, n_items, idx_pairs, long_items,
+                       s);
   if (r != LIPCACHE_OK) return r;
-  r = lookup_stage_scan(&so, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, pw.items, n_items, pw.qlist,
+  // Long lists (most items full) run 8-wave blocks sharing 128-row tiles
+  // (the slice scan's shape, half the tile bytes per pair), short lists
+  // 4-wave blocks, two per CU.
+  FilterConsts fl = fc;
+  if (long_items) fl.pl_list = fc.pl_list8;
+  r = lookup_stage_scan(&so, precision, fl, zq, B, w.qthr, w.best, w.bflag, st, w.athr, pw.items, n_items, pw.qlist,
                         precision == LIPCACHE_F16 ? zq16 : nullptr, idx->perm, 0, false, nullptr, nullptr, w.gq, s,
                         true);
   if (r != LIPCACHE_OK) return r;

@@ -13,9 +13,10 @@ The indexed lookup returns the oracle's answers query by query and the
 dense device lookup's outputs bit for bit (label, index, d^2, band flags,
 hit and band counters), for both stores and filters, K from 1 to n,
 rows appended after the build, dead rows, duplicated rows (empty
-clusters), queries with more candidate clusters than a list takes, a
-ragged batch, non-finite queries, wide features (d = 512, 1024), and the
-full-size mixture (every query of the batch).
+clusters), queries with more candidate clusters than a list takes, long
+lists (items cut for 8-wave blocks), a ragged batch, non-finite queries,
+wide features (d = 512, 1024), and the full-size mixture (every query of
+the batch).
 """
 import numpy as np
 import pytest
@@ -145,6 +146,31 @@ def test_indexed_matches_oracle_and_dense(tiny, store, prec, image, K, iters):
     lo, hi = plan_pairs_bounds(ix, zq)
     assert lo <= pairs <= hi, (what, lo, pairs, hi)
     say("index", what, "pairs", pairs, "of", zq.shape[0] * st.n, "exact plan", lo)
+
+
+@pytest.mark.parametrize("store,prec", [("f32", "f16"), ("bf16", "f16"), ("f32", "f32")])
+@pytest.mark.parametrize("K", [1, 4])
+def test_long_lists(tiny, store, prec, K):
+    """8,192 queries against 1 or 4 clusters: the lists average 512 queries
+    or more, so the items are cut again for 8-wave blocks of 512 queries and
+    longer row chunks.  Same answers as the oracle and the dense lookup, and
+    the plan's pair bounds."""
+    wl, st, _, _ = tiny[store]
+    what = f"long lists {store}/{prec}/K={K}"
+    say("index", what)
+    draws = wlmod.draw_queries(wl, 1, batch=8192)
+    idx = wlmod.near_indices(draws, st.n)
+    zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
+    ref = oracle.lookup_blocked(zq, st.z, st.r, st.label)
+    c = build_cache(st)
+    ix = c.build_index(K, 2)
+    q = gpu(zq)
+    res_i, pairs = c.lookup_indexed(ix, q, precision=prec)
+    compare_lookup(res_i, ref, what)
+    same_as_dense(res_i, c.lookup(q, precision=prec), what)
+    lo, hi = plan_pairs_bounds(ix, zq)
+    assert lo <= pairs <= hi, (what, lo, pairs, hi)
+    say("index", what, "pairs", pairs, "of", zq.shape[0] * st.n)
 
 
 @pytest.mark.parametrize("K,iters", [(4, 3), (64, 2)])

@@ -566,24 +566,36 @@ __global__ __launch_bounds__(256) void class_keys_kernel(const int32_t* __restri
 }
 
 constexpr int kKcThreads = 1024;
+constexpr int kKcPickLds = 2048;  // picks whose distances to the newest pick are kept (pruning)
 
 // Farthest-first traversal of class blockIdx.x over its list
 // list[coff[c] .. coff[c + 1]): up to min(per_class, budget, size) picks into
 // cpicks[coff[c] ..], their number into ccount[c].  mind[coff[c] + j] holds
-// candidate j's squared distance to the chosen set (-1 once chosen).  Each
-// wave measures four candidates at a time (16 lanes each, float64 sums of the
-// stored values against the newest pick, kept in LDS); the block arg-max
-// takes the larger distance, then the lower candidate index.  U = row chunks
-// of 64 features per lane (d <= 64 U); wide rows run 512 threads, so each
-// lane may keep two rows of chunks in registers.
+// candidate j's squared distance to the chosen set (-1 once chosen) and
+// own[coff[c] + j] the pick that set it.  Each wave measures four candidates
+// at a time (16 lanes each, float64 sums of the stored values against the
+// newest pick, kept in LDS); the block arg-max takes the larger distance,
+// then the lower candidate index.  U = row chunks of 64 features per lane
+// (d <= 64 U); wide rows run 512 threads, so each lane may keep two rows of
+// chunks in registers.
+//
+// Pruning (exact).  With a = own[j] and D the computed distance between pick
+// a and the newest pick p, the triangle inequality gives ||z_j - p|| >= D -
+// ||z_j - a||.  When D >= 2 sqrt(mind_j) (1 + 1e-9), that bound exceeds
+// sqrt(mind_j) (1 + 1e-9 - 3 gamma), gamma <= 1024 * 2^-53 the relative
+// error of a float64 sum of squares, so the computed squared distance would
+// be above mind_j and the minimum would not change: the row is not read.
+// The picks, the distances and the arg-max are those of the full update.
 template <int U, int THREADS>
 __global__ __launch_bounds__(THREADS) void kcenter_class_kernel(const float* __restrict__ z, int d, int bf16,
                                                                    const uint32_t* __restrict__ list,
                                                                    const int64_t* __restrict__ coff, int per_class,
                                                                    int64_t budget, double* __restrict__ mind,
+                                                                   int32_t* __restrict__ own,
                                                                    int64_t* __restrict__ cpicks,
                                                                    uint32_t* __restrict__ ccount) {
   __shared__ __attribute__((aligned(16))) float prow[1024];
+  __shared__ double dpp[kKcPickLds];  // distance of pick t to the newest pick
   constexpr int kWaves = THREADS / kWave;
   __shared__ double sv[kWaves];
   __shared__ int64_t si[kWaves];
@@ -610,22 +622,49 @@ __global__ __launch_bounds__(THREADS) void kcenter_class_kernel(const float* __r
       prow[k] = bf16 ? bf16_round_f32(v) : v;
     }
     __syncthreads();
+    // distances of the earlier picks to the newest one (index cnt - 1), one
+    // wave per pick
+    const int np = static_cast<int>(cnt - 1 < kKcPickLds ? cnt - 1 : kKcPickLds);
+    for (int q = wave; q < np; q += kWaves) {
+      const int64_t row = cpicks[j0 + q];
+      double acc = 0.0;
+      for (int k = lane; k < d; k += kWave) {
+        const float v = z[row * d + k];
+        const double diff = static_cast<double>(bf16 ? bf16_round_f32(v) : v) - static_cast<double>(prow[k]);
+        acc = __builtin_fma(diff, diff, acc);
+      }
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) acc += __shfl_xor(acc, off, kWave);
+      if (lane == 0) dpp[q] = __builtin_sqrt(acc);
+    }
+    __syncthreads();
+    const int32_t cur = static_cast<int32_t>(cnt - 1);
+    // whether candidate (m, a) needs its distance to the newest pick
+    auto needed = [&](double m, int32_t a) {
+      if (pass == 0 || !(m >= 0.0) || a < 0 || a >= np) return true;
+      return !(dpp[a] >= 2.0 * __builtin_sqrt(m) * (1.0 + 1e-9));
+    };
     double bv = -1.0;
     int64_t bi = -1;
     // Software pipeline: while the distances of batch b are summed, the rows
-    // of batch b + 1 and the candidate and distance of batch b + 2 are in
-    // flight.  Every load is unconditional (indices clamped into range,
-    // validity applied where the value is used), so no wait comes early.
+    // of batch b + 1 and the candidate, distance and owner of batch b + 2 are
+    // in flight.  Index loads are unconditional (clamped into range, validity
+    // applied where the value is used); a row is loaded only if needed.
     const int64_t step = 4 * kWaves;
     auto clamp = [&](int64_t j) { return j < nc ? j : nc - 1; };
     int64_t j = 4 * static_cast<int64_t>(wave) + grp;
     uint32_t cand_raw = list[j0 + clamp(j)];
     double m_raw = mind[j0 + clamp(j)];
+    int32_t o_raw = own[j0 + clamp(j)];
     uint32_t cand_raw2 = list[j0 + clamp(j + step)];
     double m_raw2 = mind[j0 + clamp(j + step)];
+    int32_t o_raw2 = own[j0 + clamp(j + step)];
+    bool need = j < nc && needed(m_raw, o_raw);
     f32x4 v[U];
-    {
-      const int64_t row = j < nc ? static_cast<int64_t>(cand_raw) : pick;
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (need) {
+      const int64_t row = static_cast<int64_t>(cand_raw);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int k = 4 * lr + 64 * u;
@@ -636,41 +675,64 @@ __global__ __launch_bounds__(THREADS) void kcenter_class_kernel(const float* __r
       const bool in = j < nc;
       const int64_t cand = in ? static_cast<int64_t>(cand_raw) : -1;
       double m = in ? (pass == 0 ? __builtin_inf() : m_raw) : -1.0;
-      // next batch: its rows now, the one after: its candidate and distance
+      const bool need_cur = need;
+      // next batch: its rows now (if needed), the one after: its candidate,
+      // distance and owner
       const int64_t j1 = j + step;
-      const int64_t row1 = j1 < nc ? static_cast<int64_t>(cand_raw2) : pick;
+      need = j1 < nc && needed(m_raw2, o_raw2);
       f32x4 vn[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int k = 4 * lr + 64 * u;
-        vn[u] = *reinterpret_cast<const f32x4*>(z + row1 * d + (k < d ? k : 0));
+      for (int u = 0; u < U; ++u) vn[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (need) {
+        const int64_t row1 = static_cast<int64_t>(cand_raw2);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int k = 4 * lr + 64 * u;
+          vn[u] = *reinterpret_cast<const f32x4*>(z + row1 * d + (k < d ? k : 0));
+        }
       }
       cand_raw = cand_raw2;
       m_raw = m_raw2;
+      o_raw = o_raw2;
       cand_raw2 = list[j0 + clamp(j1 + step)];
       m_raw2 = mind[j0 + clamp(j1 + step)];
+      o_raw2 = own[j0 + clamp(j1 + step)];
       double part = 0.0;
+      if (need_cur) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int k = 4 * lr + 64 * u;
-        if (k < d) {
-          const f32x4 p = *reinterpret_cast<const f32x4*>(prow + k);
+        for (int u = 0; u < U; ++u) {
+          const int k = 4 * lr + 64 * u;
+          if (k < d) {
+            const f32x4 p = *reinterpret_cast<const f32x4*>(prow + k);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float sv_ = bf16 ? bf16_round_f32(v[u][e]) : v[u][e];
-            const double diff = static_cast<double>(sv_) - static_cast<double>(p[e]);
-            part = __builtin_fma(diff, diff, part);
+            for (int e = 0; e < 4; ++e) {
+              const float sv_ = bf16 ? bf16_round_f32(v[u][e]) : v[u][e];
+              const double diff = static_cast<double>(sv_) - static_cast<double>(p[e]);
+              part = __builtin_fma(diff, diff, part);
+            }
           }
         }
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) v[u] = vn[u];
-      // sum over the 16 lanes of the group (fixed butterfly)
+      // sum over the 16 lanes of the group (fixed butterfly; the group
+      // shares need_cur)
 #pragma unroll
       for (int off = 1; off < 16; off <<= 1) part += __shfl_xor(part, off, kWave);
       if (m >= 0.0) {
-        m = cand == pick ? -1.0 : (part < m ? part : m);
-        if (lr == 0) mind[j0 + j] = m;
+        if (cand == pick) {
+          m = -1.0;
+          if (lr == 0) mind[j0 + j] = m;
+        } else if (need_cur && part < m) {
+          m = part;
+          if (lr == 0) {
+            mind[j0 + j] = m;
+            own[j0 + j] = cur;
+          }
+        } else if (pass == 0 && lr == 0) {
+          mind[j0 + j] = m;  // the first pass writes every distance (inf stays for NaN rows)
+          own[j0 + j] = cur;
+        }
       }
       double gv = m >= 0.0 ? m : -1.0;
       int64_t gi = m >= 0.0 ? cand : -1;
@@ -772,6 +834,7 @@ struct CWs {
   int64_t* part_i;
   int64_t* picks;
   int64_t* cpicks;      // [n] per-class picks (per-class K-center)
+  int32_t* own;         // [n] the pick that set mind (per-class K-center)
   uint32_t* ccount;     // [n_classes] candidates, then picks, per class
   int64_t* coff;        // [n_classes + 1] class list offsets
   int64_t* cdst;        // [2 n_classes] output offset and count per class
@@ -822,6 +885,7 @@ inline CWs cws_layout(int64_t n, int d, int n_classes, int64_t budget, size_t su
   w.picks = reinterpret_cast<int64_t*>(take(static_cast<size_t>(budget > 0 ? budget : 1) * 8));
   const size_t nc = static_cast<size_t>(n_classes > 0 ? n_classes : 1);
   w.cpicks = reinterpret_cast<int64_t*>(take(static_cast<size_t>(n > 0 ? n : 1) * 8));
+  w.own = reinterpret_cast<int32_t*>(take(static_cast<size_t>(n > 0 ? n : 1) * 4));
   w.ccount = reinterpret_cast<uint32_t*>(take(nc * 4));
   w.coff = reinterpret_cast<int64_t*>(take((nc + 1) * 8));
   w.cdst = reinterpret_cast<int64_t*>(take(2 * nc * 8));
@@ -973,19 +1037,19 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
       const uint32_t* clist = w.vals[ccur];
       if (d <= 64)
         hipLaunchKernelGGL((kcenter_class_kernel<1, kKcThreads>), kgrid, dim3(kKcThreads), 0, s, z, d, bf16, clist, w.coff,
-                           per_class, bud, w.mind, w.cpicks, w.ccount);
+                           per_class, bud, w.mind, w.own, w.cpicks, w.ccount);
       else if (d <= 128)
         hipLaunchKernelGGL((kcenter_class_kernel<2, kKcThreads>), kgrid, dim3(kKcThreads), 0, s, z, d, bf16, clist, w.coff,
-                           per_class, bud, w.mind, w.cpicks, w.ccount);
+                           per_class, bud, w.mind, w.own, w.cpicks, w.ccount);
       else if (d <= 256)
         hipLaunchKernelGGL((kcenter_class_kernel<4, kKcThreads>), kgrid, dim3(kKcThreads), 0, s, z, d, bf16, clist, w.coff,
-                           per_class, bud, w.mind, w.cpicks, w.ccount);
+                           per_class, bud, w.mind, w.own, w.cpicks, w.ccount);
       else if (d <= 512)
         hipLaunchKernelGGL((kcenter_class_kernel<8, 512>), kgrid, dim3(512), 0, s, z, d, bf16, clist, w.coff,
-                           per_class, bud, w.mind, w.cpicks, w.ccount);
+                           per_class, bud, w.mind, w.own, w.cpicks, w.ccount);
       else
         hipLaunchKernelGGL((kcenter_class_kernel<16, 512>), kgrid, dim3(512), 0, s, z, d, bf16, clist, w.coff,
-                           per_class, bud, w.mind, w.cpicks, w.ccount);
+                           per_class, bud, w.mind, w.own, w.cpicks, w.ccount);
       LC_LAUNCHED();
       hipLaunchKernelGGL(kcenter_budget_kernel, dim3(1), dim3(1024), 0, s, w.ccount, w.coff, ncls, bud, w.cpicks,
                          w.picks, w.cdst, total_dev);

@@ -136,6 +136,26 @@ def test_kcenter_per_class(per_class, budget, store, d):
     say("kcenter per class selected", sel.size, "counts", counts.tolist())
 
 
+@pytest.mark.parametrize("store,d", [("f32", 128), ("bf16", 64)])
+def test_kcenter_deep_traversal(store, d):
+    """A class of ~3,700 candidates traversed for 600 picks (the pruned
+    updates skip most rows late in the traversal) with exact duplicates of
+    some candidates (distance 0 to a pick); the selection order must equal
+    the oracle's."""
+    say("kcenter deep", store, d)
+    C = 2
+    W, z, rng = mixture(4000, d, C, seed=31 + d)
+    z[3000:3200] = z[100:300]                      # exact duplicates
+    sig = oracle.spectral_norm(W).sigma
+    cert = oracle.certify(z, W, None, sig, store=store)
+    lab = np.zeros(z.shape[0], np.int32)
+    lab[::12] = 1
+    _, st, sel = run_both(z, lab, cert.r, d, strategy="kcenter", per_class=600, n_classes=C, store=store)
+    counts = np.bincount(st.label, minlength=C)
+    assert counts[0] == 600
+    say("kcenter deep selected", sel.size, "counts", counts.tolist())
+
+
 def test_construct_chain_then_lookup():
     """Alg. 1 end to end on the device (tight radius, de-dup, 40 per class), then Alg. 2's lookup."""
     say("construct chain")

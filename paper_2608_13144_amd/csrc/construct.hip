@@ -567,17 +567,58 @@ __global__ __launch_bounds__(256) void class_keys_kernel(const int32_t* __restri
 
 constexpr int kKcThreads = 1024;
 constexpr int kKcPickLds = 2048;  // picks whose distances to the newest pick are kept (pruning)
+constexpr int kKcWin = 4096;      // candidates per window of a pass
+
+// Squared distances (float64 of the stored values) of R rows to the staged
+// row prow, one 16-lane group per row set: lane lr of the group sums
+// features 4 lr + 64 u + e of each row, then a fixed butterfly over the
+// group.  All R x U loads are issued before the first sum.
+template <int U, int R>
+__device__ __forceinline__ void group_dist2(const float* __restrict__ z, int d, int bf16, const int64_t (&row)[R],
+                                            const bool (&ok)[R], const float* prow, int lr, double (&out)[R]) {
+  f32x4 v[R][U];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = 4 * lr + 64 * u;
+      v[r][u] = (ok[r] && k < d) ? *reinterpret_cast<const f32x4*>(z + row[r] * d + k) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    double part = 0.0;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = 4 * lr + 64 * u;
+      if (k < d) {
+        const f32x4 pv = *reinterpret_cast<const f32x4*>(prow + k);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float sv_ = bf16 ? bf16_round_f32(v[r][u][e]) : v[r][u][e];
+          const double diff = static_cast<double>(sv_) - static_cast<double>(pv[e]);
+          part = __builtin_fma(diff, diff, part);
+        }
+      }
+    }
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) part += __shfl_xor(part, off, kWave);
+    out[r] = part;
+  }
+}
 
 // Farthest-first traversal of class blockIdx.x over its list
 // list[coff[c] .. coff[c + 1]): up to min(per_class, budget, size) picks into
 // cpicks[coff[c] ..], their number into ccount[c].  mind[coff[c] + j] holds
 // candidate j's squared distance to the chosen set (-1 once chosen) and
-// own[coff[c] + j] the pick that set it.  Each wave measures four candidates
-// at a time (16 lanes each, float64 sums of the stored values against the
-// newest pick, kept in LDS); the block arg-max takes the larger distance,
+// own[coff[c] + j] the pick that set it.  A pass (one pick) takes the
+// candidates in windows of kKcWin: every thread reads the distance and owner
+// of its candidates of the window and lists in LDS those whose distance to
+// the newest pick (staged in LDS) is needed; then each 16-lane group sums
+// those distances in float64 over the stored values, R rows at a time with
+// all their loads in flight.  The block arg-max takes the larger distance,
 // then the lower candidate index.  U = row chunks of 64 features per lane
-// (d <= 64 U); wide rows run 512 threads, so each lane may keep two rows of
-// chunks in registers.
+// (d <= 64 U); wide rows run 512 threads.
 //
 // Pruning (exact).  With a = own[j] and D the computed distance between pick
 // a and the newest pick p, the triangle inequality gives ||z_j - p|| >= D -
@@ -594,9 +635,15 @@ __global__ __launch_bounds__(THREADS) void kcenter_class_kernel(const float* __r
                                                                    int32_t* __restrict__ own,
                                                                    int64_t* __restrict__ cpicks,
                                                                    uint32_t* __restrict__ ccount) {
-  __shared__ __attribute__((aligned(16))) float prow[1024];
-  __shared__ double dpp[kKcPickLds];  // distance of pick t to the newest pick
+  constexpr int R = U >= 8 ? 16 / U : 4;  // rows per group per step (R x U <= 16 chunks in flight)
   constexpr int kWaves = THREADS / kWave;
+  constexpr int kGroups = 4 * kWaves;      // 16-lane groups of the block
+  __shared__ __attribute__((aligned(16))) float prow[1024];
+  __shared__ double dpp[kKcPickLds];       // distance of pick q to the newest pick
+  __shared__ int32_t lj[kKcWin];           // the window's listed candidates: position,
+  __shared__ uint32_t lc[kKcWin];          // candidate index
+  __shared__ double lm[kKcWin];            // and current distance
+  __shared__ int s_n;
   __shared__ double sv[kWaves];
   __shared__ int64_t si[kWaves];
   __shared__ int64_t s_pick;
@@ -604,6 +651,7 @@ __global__ __launch_bounds__(THREADS) void kcenter_class_kernel(const float* __r
   const int t = static_cast<int>(threadIdx.x);
   const int lane = lane_id(), wave = t / kWave;
   const int grp = lane >> 4, lr = lane & 15;
+  const int gid = 4 * wave + grp;
   const int64_t j0 = coff[c];
   const int64_t nc = coff[c + 1] - j0;
   int64_t lim = per_class < nc ? per_class : nc;
@@ -622,125 +670,103 @@ __global__ __launch_bounds__(THREADS) void kcenter_class_kernel(const float* __r
       prow[k] = bf16 ? bf16_round_f32(v) : v;
     }
     __syncthreads();
-    // distances of the earlier picks to the newest one (index cnt - 1), one
-    // wave per pick
+    // distances of the earlier picks to the newest one (index cnt - 1)
     const int np = static_cast<int>(cnt - 1 < kKcPickLds ? cnt - 1 : kKcPickLds);
-    for (int q = wave; q < np; q += kWaves) {
-      const int64_t row = cpicks[j0 + q];
-      double acc = 0.0;
-      for (int k = lane; k < d; k += kWave) {
-        const float v = z[row * d + k];
-        const double diff = static_cast<double>(bf16 ? bf16_round_f32(v) : v) - static_cast<double>(prow[k]);
-        acc = __builtin_fma(diff, diff, acc);
-      }
+    for (int q0 = gid; q0 < np; q0 += kGroups * R) {
+      int64_t row[R];
+      bool ok[R];
+      double dd[R];
 #pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) acc += __shfl_xor(acc, off, kWave);
-      if (lane == 0) dpp[q] = __builtin_sqrt(acc);
+      for (int r = 0; r < R; ++r) {
+        const int q = q0 + r * kGroups;
+        ok[r] = q < np;
+        row[r] = ok[r] ? cpicks[j0 + q] : 0;
+      }
+      group_dist2<U, R>(z, d, bf16, row, ok, prow, lr, dd);
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const int q = q0 + r * kGroups;
+        if (ok[r] && lr == 0) dpp[q] = __builtin_sqrt(dd[r]);
+      }
     }
     __syncthreads();
     const int32_t cur = static_cast<int32_t>(cnt - 1);
-    // whether candidate (m, a) needs its distance to the newest pick
-    auto needed = [&](double m, int32_t a) {
-      if (pass == 0 || !(m >= 0.0) || a < 0 || a >= np) return true;
-      return !(dpp[a] >= 2.0 * __builtin_sqrt(m) * (1.0 + 1e-9));
-    };
     double bv = -1.0;
     int64_t bi = -1;
-    // Software pipeline: while the distances of batch b are summed, the rows
-    // of batch b + 1 and the candidate, distance and owner of batch b + 2 are
-    // in flight.  Index loads are unconditional (clamped into range, validity
-    // applied where the value is used); a row is loaded only if needed.
-    const int64_t step = 4 * kWaves;
-    auto clamp = [&](int64_t j) { return j < nc ? j : nc - 1; };
-    int64_t j = 4 * static_cast<int64_t>(wave) + grp;
-    uint32_t cand_raw = list[j0 + clamp(j)];
-    double m_raw = mind[j0 + clamp(j)];
-    int32_t o_raw = own[j0 + clamp(j)];
-    uint32_t cand_raw2 = list[j0 + clamp(j + step)];
-    double m_raw2 = mind[j0 + clamp(j + step)];
-    int32_t o_raw2 = own[j0 + clamp(j + step)];
-    bool need = j < nc && needed(m_raw, o_raw);
-    f32x4 v[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) v[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (need) {
-      const int64_t row = static_cast<int64_t>(cand_raw);
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int k = 4 * lr + 64 * u;
-        v[u] = *reinterpret_cast<const f32x4*>(z + row * d + (k < d ? k : 0));
-      }
-    }
-    for (int64_t jb = 4 * static_cast<int64_t>(wave); jb < nc; jb += step, j += step) {
-      const bool in = j < nc;
-      const int64_t cand = in ? static_cast<int64_t>(cand_raw) : -1;
-      double m = in ? (pass == 0 ? __builtin_inf() : m_raw) : -1.0;
-      const bool need_cur = need;
-      // next batch: its rows now (if needed), the one after: its candidate,
-      // distance and owner
-      const int64_t j1 = j + step;
-      need = j1 < nc && needed(m_raw2, o_raw2);
-      f32x4 vn[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) vn[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (need) {
-        const int64_t row1 = static_cast<int64_t>(cand_raw2);
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int k = 4 * lr + 64 * u;
-          vn[u] = *reinterpret_cast<const f32x4*>(z + row1 * d + (k < d ? k : 0));
-        }
-      }
-      cand_raw = cand_raw2;
-      m_raw = m_raw2;
-      o_raw = o_raw2;
-      cand_raw2 = list[j0 + clamp(j1 + step)];
-      m_raw2 = mind[j0 + clamp(j1 + step)];
-      o_raw2 = own[j0 + clamp(j1 + step)];
-      double part = 0.0;
-      if (need_cur) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int k = 4 * lr + 64 * u;
-          if (k < d) {
-            const f32x4 p = *reinterpret_cast<const f32x4*>(prow + k);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const float sv_ = bf16 ? bf16_round_f32(v[u][e]) : v[u][e];
-              const double diff = static_cast<double>(sv_) - static_cast<double>(p[e]);
-              part = __builtin_fma(diff, diff, part);
-            }
+    for (int64_t w0 = 0; w0 < nc; w0 += kKcWin) {
+      const int wn = static_cast<int>(nc - w0 < kKcWin ? nc - w0 : kKcWin);
+      if (t == 0) s_n = 0;
+      __syncthreads();
+      // phase 1: distances and owners of the window; list what must be
+      // measured, take the rest into the arg-max as they are
+      for (int i0 = 0; i0 < wn; i0 += THREADS) {
+        const int i = i0 + t;
+        const bool in = i < wn;
+        const int64_t j = w0 + (in ? i : 0);
+        const uint32_t cand = list[j0 + j];
+        double m = pass == 0 ? __builtin_inf() : mind[j0 + j];
+        const int32_t a = pass == 0 ? -1 : own[j0 + j];
+        bool need = false;
+        if (in && m >= 0.0) {
+          if (static_cast<int64_t>(cand) == pick) {
+            m = -1.0;
+            mind[j0 + j] = m;
+          } else {
+            need = pass == 0 || a < 0 || a >= np || !(dpp[a] >= 2.0 * __builtin_sqrt(m) * (1.0 + 1e-9));
           }
         }
+        const unsigned long long bal = __ballot(need);
+        int base = 0;
+        if (lane == 0 && bal) base = atomicAdd(&s_n, __builtin_popcountll(bal));
+        base = __shfl(base, 0, kWave);
+        if (need) {
+          const int slot = base + __builtin_popcountll(bal & ((1ull << lane) - 1ull));
+          lj[slot] = static_cast<int32_t>(i);
+          lc[slot] = cand;
+          lm[slot] = m;
+        } else if (in) {
+          better(bv, bi, m >= 0.0 ? m : -1.0, m >= 0.0 ? static_cast<int64_t>(cand) : -1);
+        }
       }
+      __syncthreads();
+      const int nl = s_n;
+      // phase 2: the listed candidates, R per group per step
+      for (int s0 = gid; s0 < nl; s0 += kGroups * R) {
+        int64_t row[R];
+        bool ok[R];
+        double dd[R];
 #pragma unroll
-      for (int u = 0; u < U; ++u) v[u] = vn[u];
-      // sum over the 16 lanes of the group (fixed butterfly; the group
-      // shares need_cur)
+        for (int r = 0; r < R; ++r) {
+          const int sl = s0 + r * kGroups;
+          ok[r] = sl < nl;
+          row[r] = ok[r] ? static_cast<int64_t>(lc[sl]) : 0;
+        }
+        group_dist2<U, R>(z, d, bf16, row, ok, prow, lr, dd);
 #pragma unroll
-      for (int off = 1; off < 16; off <<= 1) part += __shfl_xor(part, off, kWave);
-      if (m >= 0.0) {
-        if (cand == pick) {
-          m = -1.0;
-          if (lr == 0) mind[j0 + j] = m;
-        } else if (need_cur && part < m) {
-          m = part;
-          if (lr == 0) {
-            mind[j0 + j] = m;
+        for (int r = 0; r < R; ++r) {
+          const int sl = s0 + r * kGroups;
+          if (!ok[r]) continue;
+          double m = lm[sl];
+          const int64_t j = w0 + lj[sl];
+          if (dd[r] < m) {
+            m = dd[r];
+            if (lr == 0) {
+              mind[j0 + j] = m;
+              own[j0 + j] = cur;
+            }
+          } else if (pass == 0 && lr == 0) {
+            mind[j0 + j] = m;  // the first pass writes every distance (inf stays for NaN rows)
             own[j0 + j] = cur;
           }
-        } else if (pass == 0 && lr == 0) {
-          mind[j0 + j] = m;  // the first pass writes every distance (inf stays for NaN rows)
-          own[j0 + j] = cur;
+          better(bv, bi, m, row[r]);
         }
       }
-      double gv = m >= 0.0 ? m : -1.0;
-      int64_t gi = m >= 0.0 ? cand : -1;
-      better(bv, bi, gv, gi);
+      __syncthreads();  // the list is read; the next window may overwrite it
     }
-    // wave: merge the four groups; block: merge the waves
+    // wave: merge all lanes (phase 1 leaves each lane its own candidates);
+    // block: merge the waves
 #pragma unroll
-    for (int off = 16; off < 64; off <<= 1) {
+    for (int off = 1; off < 64; off <<= 1) {
       const double ov = __shfl_xor(bv, off, kWave);
       const int64_t oi = __shfl_xor(bi, off, kWave);
       better(bv, bi, ov, oi);

@@ -860,6 +860,13 @@ struct DmaTraits {
 };
 constexpr int kDmaMaxRows = 128;
 
+// k-steps of a full tile the cache operands are read from LDS ahead of
+// their use.
+#ifndef LC_PREFETCH
+#define LC_PREFETCH 3
+#endif
+constexpr int kPrefetch = LC_PREFETCH;
+
 template <int MODE, int KS, int NW>
 __device__ __forceinline__ void issue_tile(unsigned char* buf, float* athr_buf, const LookupParams& p, int64_t t0,
                                            int64_t e_end, int wave) {
@@ -877,17 +884,32 @@ __device__ __forceinline__ void issue_tile(unsigned char* buf, float* athr_buf, 
   const int cs = tid % kCPR;
   // Wave-uniform tile base; per-thread 32-bit offsets inside the tile.
   const unsigned char* base = static_cast<const unsigned char*>(p.cimg) + t0 * static_cast<int64_t>(row_bytes);
-  // Rows past the slice end repeat its last row (their thresholds are +inf).
-  const int last = e_end - t0 < kRows ? static_cast<int>(e_end - t0) - 1 : kRows - 1;
-#pragma unroll
-  for (int j = 0; j < kIters; ++j) {
-    const int row = j * kRowsPerIter + r0;
-    int c = cs ^ lds_swizzle<kCPR>(row);
-    // Chunks past d hold a copy of a real chunk: the query operand is zero
-    // there, so they add nothing.
+  // The swizzle repeats every 16 rows.  When a thread's rows are 16k apart
+  // its chunk column is the same in every copy of a full tile, so one offset
+  // serves them all and the row step goes into the scalar base (one live
+  // VGPR instead of one per copy).
+  constexpr bool kSameColumn = kRowsPerIter % 16 == 0;
+  if (kSameColumn && e_end - t0 >= kRows) {
+    int c = cs ^ lds_swizzle<kCPR>(r0);
     if (c >= d_chunks) c -= d_chunks;
-    const int rr = row < last ? row : last;
-    lds_copy<16>(base, static_cast<uint32_t>(rr * row_bytes + c * 16), buf + (j * kThreads + wave * kWave) * 16);
+    const uint32_t voff = static_cast<uint32_t>(r0 * row_bytes + c * 16);
+#pragma unroll
+    for (int j = 0; j < kIters; ++j)
+      lds_copy<16>(base + static_cast<int64_t>(j * kRowsPerIter) * row_bytes, voff,
+                   buf + (j * kThreads + wave * kWave) * 16);
+  } else {
+    // Rows past the slice end repeat its last row (their thresholds are +inf).
+    const int last = e_end - t0 < kRows ? static_cast<int>(e_end - t0) - 1 : kRows - 1;
+#pragma unroll
+    for (int j = 0; j < kIters; ++j) {
+      const int row = j * kRowsPerIter + r0;
+      int c = cs ^ lds_swizzle<kCPR>(row);
+      // Chunks past d hold a copy of a real chunk: the query operand is zero
+      // there, so they add nothing.
+      if (c >= d_chunks) c -= d_chunks;
+      const int rr = row < last ? row : last;
+      lds_copy<16>(base, static_cast<uint32_t>(rr * row_bytes + c * 16), buf + (j * kThreads + wave * kWave) * 16);
+    }
   }
   // thresholds of the tile's rows (+inf padding past n): one wave per 64,
   // at least 64 (a tile of fewer rows stages the next ones too; the array
@@ -954,8 +976,13 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
   constexpr int kSubs = DmaTraits<KS, NW>::kRows / kColTile;
   constexpr int kE = RT * 4;                      // accumulators per lane
   constexpr int kPer = (kE + KS - 1) / KS;        // filter terms folded into each k-step
-  u32x4 b0 = lds_operand<KS>(buf, 0, 0, m16, g);
-  u32x4 b1 = KS > 1 ? lds_operand<KS>(buf, 0, 1, m16, g) : b0;
+  constexpr int kSteps = kSubs * KS;              // k-steps of the whole tile
+  constexpr int kPre = kPrefetch < kSteps ? kPrefetch : kSteps;
+  // Ring of the cache operands read ahead: step j of the tile (column tile
+  // j / KS, k-step j % KS) uses slot j % kPre, filled kPre steps earlier.
+  u32x4 bq[kPre];
+#pragma unroll
+  for (int j = 0; j < kPre; ++j) bq[j] = lds_operand<KS>(buf, j / KS, j % KS, m16, g);
   f32x4 accp[RT];
   float anp = 0.0f;
 #pragma unroll
@@ -978,35 +1005,26 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       if (cur) {
-        const u32x4 op = (ks & 1) ? b1 : b0;
-        int nks = ks + 2, nsb = sub;
-        if (nks >= KS) {
-          nks -= KS;
-          nsb += 1;
-        }
-        u32x4 pre = op;
-        if (KS > 1 && nsb < kSubs) pre = lds_operand<KS>(buf, nsb, nks, m16, g);
+        const int step = sub * KS + ks;
+        const u32x4 op = bq[step % kPre];
+        if (step + kPre < kSteps) bq[step % kPre] = lds_operand<KS>(buf, (step + kPre) / KS, (step + kPre) % KS, m16, g);
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) acc[rt] = mfma_step<MODE>(a[rt][ks], op, acc[rt]);
-        if (ks & 1) {
-          b1 = pre;
-        } else {
-          b0 = pre;
-        }
       }
       if (prev) {
 #pragma unroll
         for (int e = ks * kPer; e < (ks + 1) * kPer && e < kE; ++e)
           mx = __builtin_fmaxf(mx, kFoldQ<MODE, KS> ? accp[e / 4][e % 4] : accp[e / 4][e % 4] - qt[e / 4][e % 4]);
       }
-      // Keep the operand read for k-step ks + 2 in this step: left to
-      // itself the scheduler sinks it next to its use and the wave stalls
-      // on the LDS latency every few MFMAs.
+      // Keep the operand read for step + kPre in this step: left to itself
+      // the scheduler sinks it next to its use and the wave stalls on the
+      // LDS latency every few MFMAs.
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (cur && KS == 1 && sub + 1 < kSubs) b0 = lds_operand<KS>(buf, sub + 1, 0, m16, g);
     if (prev) {
-      if (__ballot(mx >= anp) != 0ull)
+      // rare: the rare path is laid out of line, so the column tiles run as
+      // one straight sequence and the common case takes no branch
+      if (__builtin_expect(__ballot(mx >= anp) != 0ull, 0))
         filter_and_recheck<STORE, RT, LIST>(p, accp, qt, anp, qwave, qend, qlist, t0 + (sub - 1) * kColTile, rq);
     }
     if (cur) {

@@ -177,7 +177,7 @@ def stream_bench(args, cfg) -> int:
         torch.cuda.synchronize()
         ts = time.perf_counter()
         e0.record()
-        res = cache.lookup(zq, precision=args.precision)
+        res = cache.lookup(zq, precision=args.precision, prune=args.prune)
         e1.record()
         cq = api.certify(zq, W, b, sig.sigma, store=cfg.store_dtype)
         ins = cache.insert(zq, cq.label, cq.r, res.label)
@@ -468,6 +468,10 @@ def main() -> int:
     ap.add_argument("--index-iters", type=int, default=4, help="Lloyd iterations of the index build")
     ap.add_argument("--index-k", type=int, default=256, metavar="K",
                     help="also run the batch through a K-cluster index after the timed steps (0: skip)")
+    ap.add_argument("--prune", action="store_true",
+                    help="time the step with the pruned lookup (LIPCACHE_LOOKUP_PRUNE; same answers)")
+    ap.add_argument("--no-prune-context", action="store_true",
+                    help="skip timing the pruned lookup of the batch after the timed steps")
     ap.add_argument("--boundaries", action="store_true",
                     help="compare reuse boundaries (hit rate, certified-consistency rate) on the workload")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -548,7 +552,7 @@ def main() -> int:
     def step(i: int | None):
         if i is not None:
             ev[i][0].record()
-        cache.lookup(zq, precision=args.precision, out=res)
+        cache.lookup(zq, precision=args.precision, out=res, prune=args.prune)
         if i is not None:
             ev[i][1].record()
         s = api.spectral_norm(W).sigma
@@ -583,6 +587,10 @@ def main() -> int:
         f"hits {hits}/{B}; rechecked {stats[1]}; band pairs {stats[2]}; inserted/step {inserted[-1]}")
 
     flops = 2.0 * B * n0 * d
+    if args.prune:
+        # the matrix work every pair gets: the first 32 features (blocks the
+        # prefix filter keeps also run the rest of the contraction)
+        flops = 2.0 * B * n0 * min(d, 32)
     achieved = flops / (lk * 1e-3) / 1e12
     peak = PEAK_TFLOPS[args.precision]
     out = {
@@ -610,7 +618,8 @@ def main() -> int:
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": None,
                      "kernel": "lookup_dma_kernel (fused contraction + filter + re-check)",
-                     "algorithmic": f"2*B*N*d = {flops:.4e} flop per launch"},
+                     "algorithmic": (f"2*B*N*d = {flops:.4e} flop per launch" if not args.prune else
+                                     f"prefix contraction 2*B*N*32 = {flops:.4e} flop per launch (pruned lookup)")},
         "cpu_baseline": None,
     }
     tr = measured_traffic(cfg.name, args.precision)
@@ -624,6 +633,14 @@ def main() -> int:
         out["roofline"]["hbm_gbs"] = tr["traffic_bytes"] / (lk * 1e-3) / 1e9
     else:
         out["roofline"]["traffic_source"] = "none: no counter profile of the current lookup.hip is committed"
+    if args.prune:
+        out["config"]["lookup"] = "pruned (LIPCACHE_LOOKUP_PRUNE)"
+    elif not args.no_prune_context:
+        try:
+            out["pruned_lookup"] = pruned_context(cache, zq, res, lk, args)
+        except Exception as e:  # context only: report it, keep the headline line
+            log(f"pruned lookup context failed: {e}")
+            out["pruned_lookup"] = {"error": str(e)}
     if args.index_k > 0:
         try:
             out["indexed_lookup"] = indexed_context(cache, zq, res, args)
@@ -634,6 +651,37 @@ def main() -> int:
         out["cpu_baseline"] = cpu_baseline(wl, zq_host, args.cpu_seconds)
     print(json.dumps(out), flush=True)
     return 0
+
+
+def pruned_context(cache, zq, res, full_ms, args) -> dict:
+    """The same batch through the pruned lookup (LIPCACHE_LOOKUP_PRUNE; outside
+    the timed steps): HIP-event time of the call and whether every answer
+    equals the full lookup's.  Context for the headline, which stays the full
+    contraction of every pair."""
+    import numpy as np
+    import torch
+
+    out_p = cache.lookup(zq, precision=args.precision, prune=True)
+    torch.cuda.synchronize()
+    same = all(torch.equal(getattr(res, f).view(torch.uint8), getattr(out_p, f).view(torch.uint8))
+               for f in ("label", "index", "dist2", "band"))
+    sf, sp = res.stats.cpu().tolist(), out_p.stats.cpu().tolist()
+    same = same and sf[0] == sp[0] and sf[2] == sp[2] and sf[3] == sp[3]
+    ts = []
+    for _ in range(10):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        cache.lookup(zq, precision=args.precision, out=out_p, prune=True)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ms = float(np.median(ts))
+    B = zq.shape[0]
+    log(f"pruned lookup: {ms:.3f} ms ({full_ms / ms:.2f}x the full lookup), same answers: {same}, "
+        f"re-checked pairs {sp[1]} (full {sf[1]})")
+    return {"lookup_ms": ms, "lookups_per_s": B / (ms * 1e-3), "pairs_per_s": B * cache.n / (ms * 1e-3),
+            "speedup_vs_full_lookup": full_ms / ms, "same_answers_as_full": bool(same),
+            "rechecked_pairs": int(sp[1]), "rechecked_pairs_full": int(sf[1])}
 
 
 def indexed_context(cache, zq, res, args) -> dict:

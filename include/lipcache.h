@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define LIPCACHE_ABI_VERSION 6
+#define LIPCACHE_ABI_VERSION 7
 
 /* Same type as hipStream_t. */
 typedef struct ihipStream_t* lipcache_stream_t;
@@ -56,6 +56,20 @@ typedef enum lipcache_status {
  * Matrix-core precision of the lookup's distance filter (precision): F16
  * (float16 operands, float32 accumulation) or F32. */
 enum { LIPCACHE_F32 = 0, LIPCACHE_BF16 = 1, LIPCACHE_F16 = 2 };
+
+/* Lookup option, ORed into `precision` (LIPCACHE_F16 | LIPCACHE_LOOKUP_PRUNE):
+ * prefix pruning.  The squared distance over the first 32 features is a
+ * lower bound of the full one (Eq. (13) sums non-negative terms), so a block
+ * of query-entry pairs whose prefix filter (the same rigorous slack, with
+ * the ball widened to r_i (1 + 3e-5) so that every pair of the boundary
+ * band survives) rejects every pair cannot hold a hit or a band pair, and
+ * the rest of its contraction is skipped.  Every output equals the lookup
+ * without the option except stats[LIPCACHE_STAT_RECHECKED], which counts
+ * fewer pairs the filter let through that were not hits.  Applies to the
+ * float16 filter with 64 <= d <= 512 (other cases run the full
+ * contraction, with the same answers); the workspace grows by
+ * 4 B + 4 n bytes. */
+#define LIPCACHE_LOOKUP_PRUNE 0x100
 
 /* Radius modes (policy component rho, Sec. 4.3): the conservative radius of
  * Eq. (21) or the tight per-pair radius of Remark 5.1, Eq. (29). */
@@ -177,13 +191,15 @@ size_t lipcache_certify_workspace_bytes(int32_t C, int32_t d, int32_t radius_mod
  * the answer is the nearest hit i* (least distance, lowest index among equal
  * float32-rounded distances) with its payload, or a miss.
  *
- * Distances are filtered on the matrix cores (bf16 or fp32 MFMA) with a
- * rigorous error slack, so no true hit is ever dropped; every surviving pair
- * is re-checked as sum_k (q_k - z_ik)^2 in float64, which decides the hit.
+ * Distances are filtered on the matrix cores (float16 or float32 MFMA) with
+ * a rigorous error slack, so no true hit is ever dropped; every surviving
+ * pair is re-checked as sum_k (q_k - z_ik)^2 in float64, which decides the
+ * hit.
  *
  *  c          cache (host struct; its arrays on the device), n >= 0
  *  zq         [B][c->d] float queries, B >= 0
- *  precision  LIPCACHE_BF16 or LIPCACHE_F32 (F32 requires d <= 512)
+ *  precision  LIPCACHE_F16 or LIPCACHE_F32 (F32 requires d <= 512), either
+ *             optionally | LIPCACHE_LOOKUP_PRUNE
  *  label_out  [B] int32: y~_{i*}, or LIPCACHE_MISS (required)
  *  index_out  [B] int64: i*, or -1 (nullable)
  *  dist2_out  [B] float: ||q - z_{i*}||^2 rounded to nearest, +inf on a miss (nullable)

@@ -12,6 +12,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblipcache
 
 OK, EINVAL, EDEGENERATE, ENOCONV, ECAPACITY, EUNSUPPORTED, EWORKSPACE, EHIP = range(8)
 F32, BF16, F16 = 0, 1, 2
+LOOKUP_PRUNE = 0x100
 RADIUS_CONSERVATIVE, RADIUS_TIGHT = 0, 1
 SELECT_RADIUS_DEDUP, SELECT_PRIORITY, SELECT_KCENTER = 0, 1, 2
 BOUNDARY_SCALED, BOUNDARY_GLOBAL, BOUNDARY_INTERCLASS = 0, 1, 2

@@ -162,8 +162,10 @@ class LipCache:
         return int(got.value)
 
     def lookup(self, zq: torch.Tensor, precision: str = "f16", want_index: bool = True,
-               want_dist2: bool = True, want_band: bool = True, out: LookupResult | None = None) -> LookupResult:
-        """lipcache_lookup: nearest certified hit per query, or MISS (async)."""
+               want_dist2: bool = True, want_band: bool = True, out: LookupResult | None = None,
+               prune: bool = False) -> LookupResult:
+        """lipcache_lookup: nearest certified hit per query, or MISS (async).
+        ``prune``: LIPCACHE_LOOKUP_PRUNE (prefix pruning; same answers)."""
         _need_cuda(zq, "zq", torch.float32, 2)
         if zq.shape[1] != self.d:
             raise ValueError("lookup: query width differs from the cache's d")
@@ -177,7 +179,7 @@ class LipCache:
                 torch.empty(B, dtype=torch.float32, device=dev) if want_dist2 else None,
                 torch.zeros(4, dtype=torch.int64, device=dev),
                 torch.empty(B, dtype=torch.uint8, device=dev) if want_band else None)
-        prec = _PRECISION[precision]
+        prec = _PRECISION[precision] | (L.LOOKUP_PRUNE if prune else 0)
         ws = self._workspace(lib.lipcache_lookup_workspace_bytes(B, self.n, self.d, prec))
         cs = self.cstruct()
         st = lib.lipcache_lookup(ctypes.byref(cs), _p(zq), B, prec, _p(out.label), _p(out.index), _p(out.dist2),
@@ -186,7 +188,7 @@ class LipCache:
         return out
 
     def lookup_noalloc(self, zq: torch.Tensor, precision: str = "f16",
-                       out: LookupResult | None = None) -> LookupResult:
+                       out: LookupResult | None = None, prune: bool = False) -> LookupResult:
         """lipcache_lookup_noalloc: lookup on the library's static per-GPU
         workspace (no device allocation in the library; async)."""
         _need_cuda(zq, "zq", torch.float32, 2)
@@ -202,7 +204,8 @@ class LipCache:
                                torch.zeros(4, dtype=torch.int64, device=dev),
                                torch.empty(B, dtype=torch.uint8, device=dev))
         cs = self.cstruct()
-        st = lib.lipcache_lookup_noalloc(ctypes.byref(cs), _p(zq), B, _PRECISION[precision], _p(out.label),
+        prec = _PRECISION[precision] | (L.LOOKUP_PRUNE if prune else 0)
+        st = lib.lipcache_lookup_noalloc(ctypes.byref(cs), _p(zq), B, prec, _p(out.label),
                                          _p(out.index), _p(out.dist2), _p(out.stats), _p(out.band), _stream(dev))
         L.check("lipcache_lookup_noalloc", st)
         return out

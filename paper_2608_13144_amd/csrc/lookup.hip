@@ -88,6 +88,10 @@ struct LookupParams {
   double eta1;           // absolute slack per unit of ||z_i||
   double range2;         // ||z_i||^2 from which an entry passes against everything
   const float* athr;     // [n_pad] per-entry filter thresholds A_i (+inf past n)
+  // Prefix pruning: thresholds of the filter over features 0..31 (Q'_q per
+  // query, A'_i per entry, +inf past n); null without the option.
+  const float* qthr_p;
+  const float* athr_p;
   const void* cimg;      // rows streamed by the DMA kernel (float16 image or z)
   int n_qblocks;
   int64_t slice_len;
@@ -149,6 +153,62 @@ __device__ __forceinline__ float entry_threshold(float rr, float n2f, double kap
   return f32_round_down((kappa_c * n2 - r2) * 0.5 - eta1 * __builtin_sqrt(n2) - 0.5 * kFilterAbsSlack);
 }
 
+// Prefix filter (features 0..kPrefixDims-1, the first float16 k-step).  The
+// prefix of a squared distance is a lower bound of the whole, so a pair with
+// ||q - z_i|| < r_i (a hit) or within the boundary band has a prefix below
+// r_i^2 (1 + 1e-5)^2 < r_i^2 (1 + 3e-5); the thresholds are those of the
+// full filter with d_pad = kPrefixDims, the prefix norms, and that widened
+// ball, so such a pair always passes.  A row whose full squared norm
+// reaches range2 passes (as in the full filter); a NaN or infinite query
+// norm never does (it has no hit).
+constexpr int kPrefixDims = 32;
+constexpr double kPrefixBand = 3e-5;
+
+__device__ __forceinline__ float prefix_query_threshold(double s, double sp, const Thresholds& t) {
+  if (!(s < __builtin_inf())) return __builtin_nanf("");
+  if (s >= t.range2) return kPassAll;
+  return f32_round_down(t.kq * sp * 0.5 - t.eta1 * __builtin_sqrt(sp) - t.eta0);
+}
+
+__device__ __forceinline__ float prefix_entry_threshold(float rr, float n2f, double n2p, const Thresholds& t) {
+  if (!(rr > 0.0f)) return __builtin_inff();
+  const double n2 = static_cast<double>(n2f);
+  if (n2 >= t.range2 && n2 < __builtin_inf()) return kPassAll;
+  const double r2 = static_cast<double>(rr) * static_cast<double>(rr) * (1.0 + kPrefixBand);
+  return f32_round_down((t.kappa_c * n2p - r2) * 0.5 - t.eta1 * __builtin_sqrt(n2p) - 0.5 * kFilterAbsSlack);
+}
+
+// Squared norm of the first kPrefixDims stored features of row i, in float64.
+__device__ __forceinline__ double prefix_norm2(const void* cz, int store, int d, int64_t i) {
+  double s = 0.0;
+  if (store == LIPCACHE_BF16) {
+    const uint4* row = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(cz) + i * d);
+#pragma unroll
+    for (int c = 0; c < kPrefixDims / 8; ++c) {
+      const uint4 v = row[c];
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const double lo = static_cast<double>(__builtin_bit_cast(float, w[j] << 16));
+        const double hi = static_cast<double>(__builtin_bit_cast(float, w[j] & 0xffff0000u));
+        s = __builtin_fma(lo, lo, s);
+        s = __builtin_fma(hi, hi, s);
+      }
+    }
+  } else {
+    const float4* row = reinterpret_cast<const float4*>(static_cast<const float*>(cz) + i * d);
+#pragma unroll
+    for (int c = 0; c < kPrefixDims / 4; ++c) {
+      const float4 v = row[c];
+      s = __builtin_fma(static_cast<double>(v.x), static_cast<double>(v.x), s);
+      s = __builtin_fma(static_cast<double>(v.y), static_cast<double>(v.y), s);
+      s = __builtin_fma(static_cast<double>(v.z), static_cast<double>(v.z), s);
+      s = __builtin_fma(static_cast<double>(v.w), static_cast<double>(v.w), s);
+    }
+  }
+  return s;
+}
+
 // Per-entry threshold of row i < n_pad (+inf for the padding past n).
 __device__ __forceinline__ void write_athr(int64_t i, const float* __restrict__ cr, const float* __restrict__ cnorm2,
                                            int64_t n, int64_t n_pad, double kappa_c, double eta1, double range2,
@@ -167,6 +227,12 @@ struct PrepEntries {
   unsigned long long* gq_count;  // emptied for the scan that follows (nullable)
   double* qnorm;                 // ||q||^2 in float64 of every query (nullable)
   uint16_t* zq16;                // float16 copy of the queries (nullable)
+  // prefix pruning (qthr_p == nullptr: off): Q'_q, A'_i and their constants
+  float* qthr_p;
+  float* athr_p;
+  const void* cz;
+  int store;
+  Thresholds tp;
 };
 
 // Blocks [0, qblocks): one wave per query, Q_q, reset of the per-query state
@@ -177,8 +243,11 @@ __global__ void lookup_prep_kernel(const float* __restrict__ zq, int64_t B, int 
                                    unsigned int* __restrict__ bflag, unsigned long long* __restrict__ stats,
                                    unsigned qblocks, const PrepEntries pe) {
   if (blockIdx.x >= qblocks) {
-    write_athr(static_cast<int64_t>(blockIdx.x - qblocks) * kLkThreads + threadIdx.x, pe.cr, pe.cnorm2, pe.n,
-               pe.n_pad, t.kappa_c, t.eta1, t.range2, pe.athr);
+    const int64_t i = static_cast<int64_t>(blockIdx.x - qblocks) * kLkThreads + threadIdx.x;
+    write_athr(i, pe.cr, pe.cnorm2, pe.n, pe.n_pad, t.kappa_c, t.eta1, t.range2, pe.athr);
+    if (pe.athr_p && i < pe.n_pad)
+      pe.athr_p[i] = i < pe.n ? prefix_entry_threshold(pe.cr[i], pe.cnorm2[i], prefix_norm2(pe.cz, pe.store, d, i), pe.tp)
+                              : __builtin_inff();
     return;
   }
   const int64_t q = static_cast<int64_t>(blockIdx.x) * kLkWaves + threadIdx.x / kWave;
@@ -186,18 +255,21 @@ __global__ void lookup_prep_kernel(const float* __restrict__ zq, int64_t B, int 
   if (blockIdx.x == 0 && threadIdx.x == 4 && pe.gq_count) *pe.gq_count = 0ull;
   if (q >= B) return;
   const float* row = zq + q * d;
-  double s = 0.0;
+  double s = 0.0, sp = 0.0;
   for (int k = lane_id(); k < d; k += kWave) {
     const float x = row[k];
     s = __builtin_fma(static_cast<double>(x), static_cast<double>(x), s);
+    if (k < kPrefixDims) sp = s;
     if (pe.zq16) pe.zq16[q * d + k] = f16_bits(x);
   }
   s = wave_sum(s);
+  if (pe.qthr_p) sp = wave_sum(sp);
   if (lane_id() == 0) {
     qthr[q] = query_threshold(s, t);
     best[q] = kNoHit;
     bflag[q] = 0u;
     if (pe.qnorm) pe.qnorm[q] = s;
+    if (pe.qthr_p) pe.qthr_p[q] = prefix_query_threshold(s, sp, pe.tp);
   }
 }
 
@@ -869,7 +941,7 @@ constexpr int kPrefetch = LC_PREFETCH;
 
 template <int MODE, int KS, int NW>
 __device__ __forceinline__ void issue_tile(unsigned char* buf, float* athr_buf, const LookupParams& p, int64_t t0,
-                                           int64_t e_end, int wave) {
+                                           int64_t e_end, int wave, float* athp_buf = nullptr) {
   using T = ModeTraits<MODE>;
   constexpr int kThreads = NW * kWave;
   constexpr int kCPR = 4 * KS;  // 16-byte chunks per LDS row
@@ -914,9 +986,16 @@ __device__ __forceinline__ void issue_tile(unsigned char* buf, float* athr_buf, 
   // thresholds of the tile's rows (+inf padding past n): one wave per 64,
   // at least 64 (a tile of fewer rows stages the next ones too; the array
   // holds them: it is padded by kDmaMaxRows past the last tile start)
-  if (wave < DmaTraits<KS, NW>::kAthr / kWave)
+  constexpr int kAthrWaves = DmaTraits<KS, NW>::kAthr / kWave;
+  if (wave < kAthrWaves)
     lds_copy<4>(p.athr + t0 + wave * kWave, static_cast<uint32_t>(lane_id() * 4),
                 static_cast<unsigned char*>(static_cast<void*>(athr_buf)) + wave * kWave * 4);
+  // prefix thresholds (pruned lookup), by the next waves
+  if (athp_buf && wave >= kAthrWaves && wave < 2 * kAthrWaves) {
+    const int w = wave - kAthrWaves;
+    lds_copy<4>(p.athr_p + t0 + w * kWave, static_cast<uint32_t>(lane_id() * 4),
+                static_cast<unsigned char*>(static_cast<void*>(athp_buf)) + w * kWave * 4);
+  }
 }
 
 // The cache operand of (column tile `sub`, k-step ks) for this lane: chunk
@@ -1035,14 +1114,123 @@ __device__ __forceinline__ void compute_full_tile(const unsigned char* buf, cons
   }
 }
 
-template <int MODE, int STORE, int KS, int RT, int NW, bool DUMP, bool LIST>
+// Thresholds of the lane's accumulator rows 4g .. 4g + 3 of each row tile
+// (+inf past qend), negated where the accumulators start at -Q_q.
+template <int RT>
+__device__ __forceinline__ void load_thresholds(const float* thr, int64_t qwave, int64_t qend, const int32_t* qlist,
+                                                int g, bool negate, f32x4 (&qv)[RT]) {
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t q = qwave + rt * 16 + 4 * g + i;
+      const float qq = q < qend ? thr[query_at(qlist, q)] : __builtin_inff();
+      qv[rt][i] = negate ? -qq : qq;
+    }
+  }
+}
+
+// Pruned lookup, rare path of a full tile: column tile `sub` passed the
+// prefix filter.  Its accumulators are formed again exactly as the full
+// kernel forms them (same start value, same MFMAs in the same order), so the
+// full filter takes the same decisions and picks the pairs to re-check.
+template <int STORE, int KS, int RT, int NW>
+__device__ __forceinline__ void continue_column_tile(const unsigned char* buf, const float* athr_buf,
+                                                     const LookupParams& p, int64_t t0, int sub, int64_t qwave,
+                                                     int64_t qend, int m16, int g, const u32x4 (&a)[RT][KS],
+                                                     RecheckQueue& rq) {
+  constexpr bool kFold = kFoldQ<kModeF16, KS>;
+  f32x4 qf[RT];
+  load_thresholds<RT>(p.qthr, qwave, qend, nullptr, g, kFold, qf);
+  f32x4 acc[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) acc[rt] = kFold ? qf[rt] : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const u32x4 op = lds_operand<KS>(buf, sub, ks, m16, g);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) acc[rt] = mfma_step<kModeF16>(a[rt][ks], op, acc[rt]);
+  }
+  f32x4 qt[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) qt[rt] = kFold ? f32x4{0.f, 0.f, 0.f, 0.f} : qf[rt];
+  const float an = athr_buf[sub * kColTile + m16];
+  float mx = -__builtin_inff();
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mx = __builtin_fmaxf(mx, acc[rt][i] - qt[rt][i]);
+  }
+  if (__ballot(mx >= an) != 0ull)
+    filter_and_recheck<STORE, RT, false>(p, acc, qt, an, qwave, qend, nullptr, t0 + sub * kColTile, rq);
+}
+
+// Pruned lookup, a full LDS tile: k-step 0 of every column tile (features
+// 0..31 against the lane's 16 queries, accumulators started at -Q'_q, so
+// the prefix filter is max_16(acc) >= A'_i) and the prefix filter,
+// software-pipelined one column tile behind.  A column tile with no passing
+// pair holds no hit and no boundary-band pair and is done after 1 of its KS
+// k-steps; the others are only marked in a wave-uniform bit mask and
+// finished after the loop (the tile stays in LDS until the next barrier),
+// where only the query operands are live.
+template <int STORE, int KS, int RT, int NW>
+__device__ __forceinline__ void compute_full_tile_pruned(const unsigned char* buf, const float* athr_buf,
+                                                         const float* athp_buf, const LookupParams& p, int64_t t0,
+                                                         int64_t qwave, int64_t qend, int m16, int g,
+                                                         const u32x4 (&a)[RT][KS], const f32x4 (&nqp)[RT],
+                                                         RecheckQueue& rq) {
+  constexpr int kSubs = DmaTraits<KS, NW>::kRows / kColTile;
+  static_assert(kSubs >= 2, "two column tiles per LDS tile");
+  u32x4 bq[2];  // k-step 0 operands of the next two column tiles
+  bq[0] = lds_operand<KS>(buf, 0, 0, m16, g);
+  bq[1] = lds_operand<KS>(buf, 1, 0, m16, g);
+  f32x4 pacc[RT];
+  float anp = 0.0f;
+  uint32_t pass = 0u;  // bit s: column tile s passed the prefix filter somewhere
+#pragma unroll
+  for (int sub = 0; sub <= kSubs; ++sub) {
+    const bool cur = sub < kSubs;  // compile-time after unrolling
+    const bool prev = sub > 0;
+    f32x4 acc[RT];
+    float an = 0.0f;
+    if (cur) {
+      const u32x4 op = bq[sub & 1];
+      if (sub + 2 < kSubs) bq[sub & 1] = lds_operand<KS>(buf, sub + 2, 0, m16, g);
+      an = athp_buf[sub * kColTile + m16];
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) acc[rt] = mfma_step<kModeF16>(a[rt][0], op, nqp[rt]);
+    }
+    if (prev) {
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mx = __builtin_fmaxf(mx, pacc[rt][i]);
+      }
+      pass |= __ballot(mx >= anp) != 0ull ? 1u << (sub - 1) : 0u;
+    }
+    if (cur) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) pacc[rt] = acc[rt];
+      anp = an;
+    }
+  }
+  if (__builtin_expect(pass != 0u, 0)) {
+#pragma unroll 1
+    for (int sub = 0; sub < kSubs; ++sub)
+      if ((pass >> sub) & 1u) continue_column_tile<STORE, KS, RT, NW>(buf, athr_buf, p, t0, sub, qwave, qend, m16, g, a, rq);
+  }
+}
+
+// FULL: the tile may be full (else only the partial-tile path is compiled).
+template <int MODE, int STORE, int KS, int RT, int NW, bool DUMP, bool LIST, bool FULL = true>
 __device__ __forceinline__ void compute_tile(const unsigned char* buf, const float* athr_buf, const LookupParams& p,
                                              int64_t t0, int64_t e_end, int64_t qwave, int64_t qend,
                                              const int32_t* qlist, int m16, int g, const u32x4 (&a)[RT][KS],
                                              const f32x4 (&qv)[RT], RecheckQueue& rq) {
   constexpr int kRows = DmaTraits<KS, NW>::kRows;
   const int64_t left = e_end - t0;
-  if constexpr (!DUMP) {
+  if constexpr (!DUMP && FULL) {
     if (left >= kRows) {
       compute_full_tile<MODE, STORE, KS, RT, NW, LIST>(buf, athr_buf, p, t0, qwave, qend, qlist, m16, g, a, qv, rq);
       return;
@@ -1127,10 +1315,34 @@ __device__ __forceinline__ void compute_tile(const unsigned char* buf, const flo
   }
 }
 
+// One LDS tile of the scan; with PRUNE full tiles take the pruned path (qv:
+// prefix thresholds) and a partial tile the full one (its thresholds loaded
+// here).
+template <int MODE, int STORE, int KS, int RT, int NW, bool DUMP, bool LIST, bool PRUNE>
+__device__ __forceinline__ void run_tile(const unsigned char* buf, const float* athr_buf, const float* athp_buf,
+                                         const LookupParams& p, int64_t t0, int64_t e_end, int64_t qwave,
+                                         int64_t qend, const int32_t* qlist, int m16, int g, const u32x4 (&a)[RT][KS],
+                                         const f32x4 (&qv)[RT], RecheckQueue& rq) {
+  if constexpr (PRUNE) {
+    if (e_end - t0 >= DmaTraits<KS, NW>::kRows) {
+      compute_full_tile_pruned<STORE, KS, RT, NW>(buf, athr_buf, athp_buf, p, t0, qwave, qend, m16, g, a, qv, rq);
+    } else {
+      f32x4 qf[RT];
+      load_thresholds<RT>(p.qthr, qwave, qend, qlist, g, kFoldQ<MODE, KS>, qf);
+      compute_tile<MODE, STORE, KS, RT, NW, DUMP, LIST, false>(buf, athr_buf, p, t0, e_end, qwave, qend, qlist, m16,
+                                                               g, a, qf, rq);
+    }
+  } else {
+    compute_tile<MODE, STORE, KS, RT, NW, DUMP, LIST>(buf, athr_buf, p, t0, e_end, qwave, qend, qlist, m16, g, a, qv,
+                                                      rq);
+  }
+}
+
 // NW waves per workgroup (8, or 4 with two workgroups per CU), two waves
-// per SIMD either way.
-template <int MODE, int STORE, int KS, int RT, int NW, bool DUMP, bool LIST>
+// per SIMD either way.  PRUNE: the pruned lookup (slice mode, float16).
+template <int MODE, int STORE, int KS, int RT, int NW, bool DUMP, bool LIST, bool PRUNE = false>
 __global__ __launch_bounds__(NW * kWave, 2) void lookup_dma_kernel(const LookupParams p) {
+  static_assert(!PRUNE || (MODE == kModeF16 && !DUMP && !LIST && KS >= 2), "pruned lookup: float16 slice scan");
   using T = ModeTraits<MODE>;
   constexpr int kCPR = 4 * KS;
   constexpr int kRows = DmaTraits<KS, NW>::kRows;
@@ -1141,6 +1353,10 @@ __global__ __launch_bounds__(NW * kWave, 2) void lookup_dma_kernel(const LookupP
   __shared__ __attribute__((aligned(16))) float ath1[DmaTraits<KS, NW>::kAthr];
   __shared__ int64_t rq_e[LIST ? NW * kRq : 1];
   __shared__ int32_t rq_q[LIST ? NW * kRq : 1];
+  __shared__ __attribute__((aligned(16))) float athp0[PRUNE ? DmaTraits<KS, NW>::kAthr : 1];
+  __shared__ __attribute__((aligned(16))) float athp1[PRUNE ? DmaTraits<KS, NW>::kAthr : 1];
+  float* const athp0p = PRUNE ? athp0 : nullptr;
+  float* const athp1p = PRUNE ? athp1 : nullptr;
 
   int64_t q0, qend, e_begin, e_end;
   block_work(p, NW * RT * 16, q0, qend, e_begin, e_end);
@@ -1157,7 +1373,7 @@ __global__ __launch_bounds__(NW * kWave, 2) void lookup_dma_kernel(const LookupP
   // Work-list mode: a wave whose queries all lie past the list's end only
   // moves its share of each tile (the copies and barriers are the block's).
   const bool active = !LIST || qwave < qend;
-  issue_tile<MODE, KS, NW>(buf0, ath0, p, e_begin, e_end, wave);
+  issue_tile<MODE, KS, NW>(buf0, ath0, p, e_begin, e_end, wave, athp0p);
 
   u32x4 a[RT][KS];
   if (active) load_query_operands<MODE, KS, RT, LIST && MODE == kModeF16>(p, qlist, qwave, qend, m16, g, a);
@@ -1165,32 +1381,27 @@ __global__ __launch_bounds__(NW * kWave, 2) void lookup_dma_kernel(const LookupP
   // Q_q of this lane's accumulator rows 4g .. 4g + 3 of each row tile, kept
   // in registers for the whole slice (reading them from LDS per column tile
   // costs a third of the operand traffic); +inf past B.  Negated where the
-  // accumulators start at -Q_q.
+  // accumulators start at -Q_q.  The pruned lookup keeps the prefix
+  // thresholds here instead, negated (its accumulators start at -Q'_q).
   f32x4 qv[RT];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t q = qwave + rt * 16 + 4 * g + i;
-      const float qq = q < qend ? p.qthr[query_at(qlist, q)] : __builtin_inff();
-      qv[rt][i] = kFoldQ<MODE, KS> ? -qq : qq;
-    }
-  }
+  load_thresholds<RT>(PRUNE ? p.qthr_p : p.qthr, qwave, qend, qlist, g, PRUNE || kFoldQ<MODE, KS>, qv);
 
   for (int64_t t0 = e_begin;; t0 += 2 * kRows) {
     wait_copies();
     __syncthreads();
     const bool more1 = t0 + kRows < e_end;
-    if (more1) issue_tile<MODE, KS, NW>(buf1, ath1, p, t0 + kRows, e_end, wave);
+    if (more1) issue_tile<MODE, KS, NW>(buf1, ath1, p, t0 + kRows, e_end, wave, athp1p);
     if (active)
-      compute_tile<MODE, STORE, KS, RT, NW, DUMP, LIST>(buf0, ath0, p, t0, e_end, qwave, qend, qlist, m16, g, a, qv, rq);
+      run_tile<MODE, STORE, KS, RT, NW, DUMP, LIST, PRUNE>(buf0, ath0, athp0p, p, t0, e_end, qwave, qend, qlist, m16,
+                                                            g, a, qv, rq);
     if (!more1) break;
     wait_copies();
     __syncthreads();
     const bool more2 = t0 + 2 * kRows < e_end;
-    if (more2) issue_tile<MODE, KS, NW>(buf0, ath0, p, t0 + 2 * kRows, e_end, wave);
+    if (more2) issue_tile<MODE, KS, NW>(buf0, ath0, p, t0 + 2 * kRows, e_end, wave, athp0p);
     if (active)
-      compute_tile<MODE, STORE, KS, RT, NW, DUMP, LIST>(buf1, ath1, p, t0 + kRows, e_end, qwave, qend, qlist, m16, g, a, qv, rq);
+      run_tile<MODE, STORE, KS, RT, NW, DUMP, LIST, PRUNE>(buf1, ath1, athp1p, p, t0 + kRows, e_end, qwave, qend,
+                                                            qlist, m16, g, a, qv, rq);
     if (!more2) break;
   }
   if constexpr (LIST) {
@@ -1236,7 +1447,7 @@ inline bool make_plan(int precision, const lipcache_cache* c, bool list, Plan& p
 
 // Kernel variants: the lookup, the filter dump, and the work-list lookup of
 // the cluster index.
-enum { kVarLookup = 0, kVarDump = 1, kVarList = 2, kVarList8 = 3 };
+enum { kVarLookup = 0, kVarDump = 1, kVarList = 2, kVarList8 = 3, kVarPrune = 4 };
 
 template <int MODE, int SRC, int KS, int VAR>
 hipError_t launch_v1(const LookupParams& p, unsigned grid, hipStream_t s) {
@@ -1248,7 +1459,15 @@ hipError_t launch_v1(const LookupParams& p, unsigned grid, hipStream_t s) {
 
 template <int MODE, int STORE, int KS, int VAR>
 hipError_t launch_dma(const LookupParams& p, unsigned grid, hipStream_t s) {
-  if constexpr (KS <= 16) {
+  if constexpr (VAR == kVarPrune) {
+    if constexpr (MODE == kModeF16 && KS >= 2 && KS <= 16) {
+      hipLaunchKernelGGL((lookup_dma_kernel<MODE, STORE, KS, (KS <= 8 ? 4 : 2), kDmaWaves, false, false, true>),
+                         dim3(grid), dim3(kDmaWaves * kWave), 0, s, p);
+      return hipGetLastError();
+    } else {
+      return hipErrorInvalidValue;
+    }
+  } else if constexpr (KS <= 16) {
     constexpr int kNW = VAR == kVarList ? kListWaves : kDmaWaves;
     hipLaunchKernelGGL((lookup_dma_kernel<MODE, STORE, KS, (KS <= 8 ? 4 : 2), kNW, VAR == kVarDump,
                                           VAR == kVarList || VAR == kVarList8>),
@@ -1310,6 +1529,8 @@ struct Workspace {
   unsigned long long* stats;
   float* athr;
   GlobalRecheckWs gq;
+  float* qthr_p;  // pruned lookup only: Q'_q [B], A'_i [athr_len(N)]
+  float* athr_p;
 };
 
 // A_i padded with +inf so that any tile that starts below n reads thresholds
@@ -1318,7 +1539,7 @@ inline int64_t athr_len(int64_t n) {
   return ((n > 0 ? n : 0) + kDmaMaxRows - 1) / kDmaMaxRows * kDmaMaxRows + kDmaMaxRows;
 }
 
-inline size_t ws_layout(int64_t B, int64_t N, Workspace* w, void* base) {
+inline size_t ws_layout(int64_t B, int64_t N, Workspace* w, void* base, bool prune = false) {
   const size_t nb = static_cast<size_t>(B > 0 ? B : 0);
   const int64_t cap = gq_capacity(B);
   size_t off = 0;
@@ -1338,6 +1559,10 @@ inline size_t ws_layout(int64_t B, int64_t N, Workspace* w, void* base) {
   off = align_up(off + static_cast<size_t>(cap) * 8, 256);
   const size_t o_athr = off;
   off = align_up(off + static_cast<size_t>(athr_len(N)) * 4, 256);
+  const size_t o_qp = off;
+  if (prune) off = align_up(off + nb * 4, 256);
+  const size_t o_ap = off;
+  if (prune) off = align_up(off + static_cast<size_t>(athr_len(N)) * 4, 256);
   if (w && base) {
     char* b = static_cast<char*>(base);
     w->best = reinterpret_cast<unsigned long long*>(b + o_best);
@@ -1347,6 +1572,8 @@ inline size_t ws_layout(int64_t B, int64_t N, Workspace* w, void* base) {
     w->gq = GlobalRecheckWs{reinterpret_cast<int64_t*>(b + o_gqp), reinterpret_cast<int64_t*>(b + o_gqe),
                             reinterpret_cast<unsigned long long*>(b + o_gqc), cap};
     w->athr = reinterpret_cast<float*>(b + o_athr);
+    w->qthr_p = prune ? reinterpret_cast<float*>(b + o_qp) : nullptr;
+    w->athr_p = prune ? reinterpret_cast<float*>(b + o_ap) : nullptr;
   }
   return off;
 }
@@ -1370,7 +1597,13 @@ struct FilterConsts {
   Plan pl_list;    // work-list scan: 4-wave blocks (short cluster lists)
   Plan pl_list8;   // work-list scan: 8-wave blocks (long cluster lists)
   Thresholds t;
+  bool prune = false;  // pruned slice scan (prefix thresholds tp)
+  Thresholds tp;
 };
+
+// Precision argument: the filter precision, optionally | LIPCACHE_LOOKUP_PRUNE.
+inline int32_t filter_precision(int32_t precision) { return precision & ~LIPCACHE_LOOKUP_PRUNE; }
+inline bool wants_prune(int32_t precision) { return (precision & LIPCACHE_LOOKUP_PRUNE) != 0; }
 
 lipcache_status lookup_consts(const lipcache_cache* c, int32_t precision, FilterConsts& fc) {
   if (!make_plan(precision, c, false, fc.pl) || !make_plan(precision, c, true, fc.pl_list) ||
@@ -1387,6 +1620,26 @@ lipcache_status lookup_consts(const lipcache_cache* c, int32_t precision, Filter
   return LIPCACHE_OK;
 }
 
+// The pruned scan runs where the slice kernel is the float16 DMA kernel with
+// at least two k-steps; elsewhere the option changes nothing.
+void prune_consts(const lipcache_cache* c, int32_t precision, FilterConsts& fc) {
+  fc.prune = precision == LIPCACHE_F16 && fc.pl.dma && fc.pl.ks >= 2 && fc.pl.ks <= 16;
+  if (!fc.prune) return;
+  const FilterSlack fs = filter_slack(precision, c->store_dtype, kPrefixDims);
+  const double u32 = 1.0 / 16777216.0;
+  // The prefix accumulation starts at -Q'_q, which adds gam |Q'_q| to its
+  // rounding error (gam for the kPrefixDims products and the start value):
+  // Q'_q = RD((1 - kappa - gam) s / 2 - (1 + 2 gam)(eta1 sqrt(s) + eta0))
+  // keeps every pair the unfolded test would pass, for either sign of Q'_q.
+  const double n = static_cast<double>(kPrefixDims) + 2.0;
+  const double gam = n * u32 / (1.0 - n * u32);
+  fc.tp.kq = 1.0 - fs.kappa - gam;
+  fc.tp.kappa_c = 1.0 - fs.kappa - 4.0 * u32;
+  fc.tp.eta1 = fs.eta1 * (1.0 + 2.0 * gam);
+  fc.tp.eta0 = fs.eta0 * (1.0 + 2.0 * gam);
+  fc.tp.range2 = fs.range2;
+}
+
 // Stage 1: Q_q, and the reset of best / band flags / counters; with `view`
 // also the thresholds A_i of its rows and the emptying of the re-check queue
 // of the scan that follows (in the same launch); with qnorm / zq16 also
@@ -1395,12 +1648,14 @@ lipcache_status lookup_stage_prep(const float* zq, int64_t B, int d, const Filte
                                   unsigned long long* best, unsigned int* bflag, unsigned long long* stats,
                                   hipStream_t s, const lipcache_cache* view = nullptr, float* athr = nullptr,
                                   unsigned long long* gq_count = nullptr, double* qnorm = nullptr,
-                                  uint16_t* zq16 = nullptr) {
+                                  uint16_t* zq16 = nullptr, float* qthr_p = nullptr, float* athr_p = nullptr) {
   const int64_t qblocks = B > 0 ? (B + kLkWaves - 1) / kLkWaves : 1;
-  PrepEntries pe{nullptr, nullptr, 0, 0, nullptr, nullptr, qnorm, zq16};
+  PrepEntries pe{nullptr, nullptr, 0, 0, nullptr, nullptr, qnorm, zq16, nullptr, nullptr, nullptr, 0, fc.tp};
   int64_t eblocks = 0;
   if (view && view->n > 0) {
-    pe = PrepEntries{view->r, view->norm2, view->n, athr_len(view->n), athr, gq_count, qnorm, zq16};
+    const bool pr = qthr_p && athr_p;
+    pe = PrepEntries{view->r,     view->norm2,        view->n, athr_len(view->n), athr, gq_count, qnorm, zq16,
+                     pr ? qthr_p : nullptr, pr ? athr_p : nullptr, view->z, view->store_dtype, fc.tp};
     eblocks = (pe.n_pad + kLkThreads - 1) / kLkThreads;
   }
   if (qblocks + eblocks > INT_MAX) return LIPCACHE_EUNSUPPORTED;
@@ -1420,7 +1675,8 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
                                   unsigned int* bflag, unsigned long long* stats, float* athr,
                                   const int64_t* items, int64_t n_items, const int32_t* qlist, const uint16_t* zq16,
                                   const int64_t* emap, int64_t eoff, bool dump, float* g_hat, uint8_t* cand,
-                                  const GlobalRecheckWs& gq, hipStream_t s, bool athr_ready = false) {
+                                  const GlobalRecheckWs& gq, hipStream_t s, bool athr_ready = false,
+                                  const float* qthr_p = nullptr, const float* athr_p = nullptr) {
   if (B <= 0 || view->n <= 0) return LIPCACHE_OK;
   if (items && n_items <= 0) return LIPCACHE_OK;
   if (!athr_ready) {
@@ -1447,6 +1703,8 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
   p.eta1 = fc.t.eta1;
   p.range2 = fc.t.range2;
   p.athr = athr;
+  p.qthr_p = qthr_p;
+  p.athr_p = athr_p;
   p.cimg = precision == LIPCACHE_F16 ? view->zimg : view->z;
   p.n_qblocks = static_cast<int>((B + pl.qblock - 1) / pl.qblock);
   p.g_hat = g_hat;
@@ -1480,7 +1738,9 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
   const hipError_t e = dump    ? launch_lookup<kVarDump>(precision, view->store_dtype, pl, p, gu, s)
                        : items ? (pl.waves == kListWaves ? launch_lookup<kVarList>(precision, view->store_dtype, pl, p, gu, s)
                                                          : launch_lookup<kVarList8>(precision, view->store_dtype, pl, p, gu, s))
-                               : launch_lookup<kVarLookup>(precision, view->store_dtype, pl, p, gu, s);
+                       : (qthr_p && athr_p && !items)
+                           ? launch_lookup<kVarPrune>(precision, view->store_dtype, pl, p, gu, s)
+                           : launch_lookup<kVarLookup>(precision, view->store_dtype, pl, p, gu, s);
   if (e != hipSuccess) return LIPCACHE_EHIP;
   if (dump) return LIPCACHE_OK;
   // the pairs the scan's waves queued, one chip-wide pass
@@ -1532,28 +1792,31 @@ lipcache_status lookup_on(const lipcache_cache* c, const float* zq, int64_t B, i
                           uint64_t* stats, uint8_t* band_flag, void* ws, hipStream_t s, bool dump, float* g_hat,
                           uint8_t* cand) {
   Workspace w;
-  ws_layout(B, c->n, &w, ws);
+  ws_layout(B, c->n, &w, ws, fc.prune);
   unsigned long long* st = stats ? reinterpret_cast<unsigned long long*>(stats) : w.stats;
   lipcache_status r = lookup_stage_prep(zq, B, c->d, fc, w.qthr, w.best, w.bflag, st, s, c, w.athr,
-                                       dump ? nullptr : w.gq.count);
+                                       dump ? nullptr : w.gq.count, nullptr, nullptr, w.qthr_p, w.athr_p);
   if (r != LIPCACHE_OK) return r;
   r = lookup_stage_scan(c, precision, fc, zq, B, w.qthr, w.best, w.bflag, st, w.athr, nullptr, 0, nullptr, nullptr,
-                        nullptr, 0, dump, g_hat, cand, w.gq, s, true);
+                        nullptr, 0, dump, g_hat, cand, w.gq, s, true, w.qthr_p, w.athr_p);
   if (r != LIPCACHE_OK) return r;
   if (dump) return LIPCACHE_OK;
   return lookup_stage_finalize(B, w.best, w.bflag, c->label, label_out, index_out, dist2_out, band_flag, st, s);
 }
 
-lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, int32_t precision,
+lipcache_status run_lookup(const lipcache_cache* c, const float* zq, int64_t B, int32_t precision_arg,
                            int32_t* label_out, int64_t* index_out, float* dist2_out, uint64_t* stats,
                            uint8_t* band_flag, void* ws, size_t ws_bytes, hipStream_t s, bool dump,
                            float* g_hat, uint8_t* cand) {
+  const int32_t precision = filter_precision(precision_arg);
+  if (dump && wants_prune(precision_arg)) return LIPCACHE_EINVAL;
   const lipcache_status vs = lookup_check(c, zq, B, precision, dump, label_out, g_hat, cand);
   if (vs != LIPCACHE_OK) return vs;
   FilterConsts fc;
   const lipcache_status cs = lookup_consts(c, precision, fc);
   if (cs != LIPCACHE_OK) return cs;
-  const size_t need = ws_layout(B, c->n, nullptr, nullptr);
+  if (wants_prune(precision_arg)) prune_consts(c, precision, fc);
+  const size_t need = ws_layout(B, c->n, nullptr, nullptr, wants_prune(precision_arg));
   if (!ws || ws_bytes < need || !aligned256(ws)) return LIPCACHE_EWORKSPACE;
   return lookup_on(c, zq, B, precision, fc, label_out, index_out, dist2_out, stats, band_flag, ws, s, dump, g_hat,
                    cand);
@@ -1696,8 +1959,7 @@ extern "C" lipcache_status lipcache_lookup_indexed(const lipcache_cache* c, cons
 
 extern "C" size_t lipcache_lookup_workspace_bytes(int64_t B, int64_t N, int32_t d, int32_t precision) {
   (void)d;
-  (void)precision;
-  return ws_layout(B, N, nullptr, nullptr);
+  return ws_layout(B, N, nullptr, nullptr, wants_prune(precision));
 }
 
 extern "C" lipcache_status lipcache_lookup(const lipcache_cache* c, const float* zq, int64_t B, int32_t precision,
@@ -1716,15 +1978,17 @@ extern "C" lipcache_status lipcache_lookup_filter_dump(const lipcache_cache* c, 
 }
 
 extern "C" lipcache_status lipcache_lookup_noalloc(const lipcache_cache* c, const float* zq, int64_t B,
-                                                   int32_t precision, int32_t* label_out, int64_t* index_out,
+                                                   int32_t precision_arg, int32_t* label_out, int64_t* index_out,
                                                    float* dist2_out, uint64_t* stats, uint8_t* band_flag,
                                                    lipcache_stream_t stream) {
+  const int32_t precision = filter_precision(precision_arg);
   const lipcache_status vs = lookup_check(c, zq, B, precision, false, label_out, nullptr, nullptr);
   if (vs != LIPCACHE_OK) return vs;
   FilterConsts fc;
   const lipcache_status cs = lookup_consts(c, precision, fc);
   if (cs != LIPCACHE_OK) return cs;
-  if (ws_layout(B, c->n, nullptr, nullptr) > kNoAllocBytes) return LIPCACHE_EWORKSPACE;
+  if (wants_prune(precision_arg)) prune_consts(c, precision, fc);
+  if (ws_layout(B, c->n, nullptr, nullptr, wants_prune(precision_arg)) > kNoAllocBytes) return LIPCACHE_EWORKSPACE;
   void* ws = device_scratch();
   if (!ws) return LIPCACHE_EHIP;
   return lookup_on(c, zq, B, precision, fc, label_out, index_out, dist2_out, stats, band_flag, ws,

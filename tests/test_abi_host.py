@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported_and_bound():
     for name in names:
         assert hasattr(lib, name), name
         assert name in L.SIGNATURES, f"binding lacks {name}"
-    assert lib.lipcache_abi_version() == 6
+    assert lib.lipcache_abi_version() == 7
 
 
 def test_status_strings():

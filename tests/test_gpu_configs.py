@@ -3,12 +3,13 @@
 Per workload: sigma, labels and radii of all N cache candidates against the
 oracle's certify; the cache built on the device from the device's own
 certificates; one batch of queries composed from the oracle's cache state;
-the lookup with both filters compared with the oracle on EVERY query of the
-batch (``oracle.lookup_partitioned`` through the workload's own mixture
-components, itself cross-checked against ``oracle.lookup_blocked`` on a
-seeded sample), and every hit checked for validity and certified
-consistency.  At the headline workload the lookup is also run twice and must
-give the same bytes.
+the lookup with both filters, and the pruned float16 lookup, compared with
+the oracle on EVERY query of the batch (``oracle.lookup_partitioned``
+through the workload's own mixture components, itself cross-checked against
+``oracle.lookup_blocked`` on a seeded sample), and every hit checked for
+validity and certified consistency.  The pruned lookup must also equal the
+full float16 lookup bit for bit.  At the headline workload each lookup is
+run twice and must give the same bytes.
 """
 import numpy as np
 import pytest
@@ -80,18 +81,32 @@ def test_workload_full_size(name):
     zq = wlmod.compose_queries(draws, st.z[idx], st.r[idx])
     ref = full_batch_reference(zq, st, assign, wl.mu, name)
     say(name, "oracle lookup of all", B, "queries done; flagged", int(ref.flagged.sum()))
-    for precision in ("f16", "f32"):
-        res = cache.lookup(gpu(zq), precision=precision)
-        nflag = compare_lookup(res, ref, f"{name}/{precision}")
-        nhit = check_hits_valid(res, zq, st, wl.W, wl.b, f"{name}/{precision}")
+    full = {}
+    for precision, prune in (("f16", False), ("f32", False), ("f16", True)):
+        what = f"{name}/{precision}{'/pruned' if prune else ''}"
+        res = cache.lookup(gpu(zq), precision=precision, prune=prune)
+        nflag = compare_lookup(res, ref, what)
+        nhit = check_hits_valid(res, zq, st, wl.W, wl.b, what)
         stats = host(res.stats)
         assert stats[0] == nhit
         assert 0.2 < nhit / B < 0.32, nhit / B
-        say(name, precision, "hits", nhit, "flagged", nflag, "near-tie entries", ties, "stats", stats.tolist())
+        say(what, "hits", nhit, "flagged", nflag, "near-tie entries", ties, "stats", stats.tolist())
         if name == "mix-d256-c200":
-            again = cache.lookup(gpu(zq), precision=precision)
+            again = cache.lookup(gpu(zq), precision=precision, prune=prune)
             for f in ("label", "index", "dist2", "stats", "band"):
                 a, b2 = getattr(res, f), getattr(again, f)
-                assert torch.equal(a.view(torch.uint8), b2.view(torch.uint8)), f"{name}/{precision}: run twice {f}"
+                assert torch.equal(a.view(torch.uint8), b2.view(torch.uint8)), f"{what}: run twice {f}"
+        if prune:
+            # the pruned lookup gives the full float16 lookup's answers, bit for bit
+            f16 = full["f16"]
+            for f in ("label", "index", "dist2", "band"):
+                a, b2 = getattr(f16, f), getattr(res, f)
+                assert torch.equal(a.view(torch.uint8), b2.view(torch.uint8)), f"{what}: {f} differs from full"
+            s16 = host(f16.stats)
+            assert stats[0] == s16[0] and stats[2] == s16[2] and stats[3] == s16[3], (stats, s16)
+            assert stats[1] <= s16[1], (stats, s16)
+        else:
+            full[precision] = res
+
     del cache
     torch.cuda.empty_cache()

@@ -4,7 +4,8 @@ Called through the C ABI (ctypes), twice in a row on the same GPU array, the
 second time with a smaller batch and a smaller cache, so state the first
 call left in the array must not leak into the second: every output (label,
 index, d^2 bits, band flags, counters) must equal lipcache_lookup's on the
-same inputs bit for bit.
+same inputs bit for bit.  The pruned lookup (LIPCACHE_LOOKUP_PRUNE) is
+checked the same way; its prefix thresholds live in the same array.
 """
 import ctypes
 
@@ -56,7 +57,7 @@ def _case(name, n_cache, B):
     return st, wlmod.compose_queries(draws, st.z[idx], st.r[idx])
 
 
-@pytest.mark.parametrize("precision", [L.F16, L.F32])
+@pytest.mark.parametrize("precision", [L.F16, L.F32, L.F16 | L.LOOKUP_PRUNE])
 def test_noalloc_matches_lookup_twice(precision):
     lib = L.load()
     big_st, big_q = _case("mix-d128-c10", 65536, 8192)

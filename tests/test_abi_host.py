@@ -118,6 +118,23 @@ def test_lookup_validation():
     assert call(_cache(d=1024), prec=L.F32) == L.EUNSUPPORTED
     assert call(_cache(), ws=None) == L.EWORKSPACE
     assert call(_cache(), wsb=64) == L.EWORKSPACE
+    # lookup options: only LIPCACHE_LOOKUP_PRUNE, on a filter precision
+    assert call(_cache(), prec=L.F16 | 0x200) == L.EINVAL
+    assert call(_cache(), prec=L.BF16 | L.LOOKUP_PRUNE) == L.EINVAL
+    assert call(_cache(d=1024), prec=L.F32 | L.LOOKUP_PRUNE) == L.EUNSUPPORTED
+    assert call(_cache(), prec=L.F16 | L.LOOKUP_PRUNE, ws=None) == L.EWORKSPACE
+
+
+def test_pruned_lookup_workspace():
+    """The pruned lookup's workspace adds its prefix thresholds: 4 bytes per
+    query and per entry (plus padding), and the plain size is unchanged."""
+    lib = L.load()
+    B, n = 32768, 1 << 20
+    plain = lib.lipcache_lookup_workspace_bytes(B, n, 256, L.F16)
+    pruned = lib.lipcache_lookup_workspace_bytes(B, n, 256, L.F16 | L.LOOKUP_PRUNE)
+    assert pruned >= plain + 4 * B + 4 * n
+    assert pruned <= plain + 4 * B + 4 * (n + 256) + 512
+    assert lib.lipcache_lookup_workspace_bytes(B, n, 256, L.F32) == plain
 
 
 def test_lookup_noalloc_validation():

@@ -66,9 +66,10 @@ enum { LIPCACHE_F32 = 0, LIPCACHE_BF16 = 1, LIPCACHE_F16 = 2 };
  * the rest of its contraction is skipped.  Every output equals the lookup
  * without the option except stats[LIPCACHE_STAT_RECHECKED], which counts
  * fewer pairs the filter let through that were not hits.  Applies to the
- * float16 filter with 64 <= d <= 512 (other cases run the full
- * contraction, with the same answers); the workspace grows by
- * 4 B + 4 n bytes. */
+ * float16 filter with 64 <= d <= 512 on caches of n >= 32768 rows with a
+ * float16 image (other cases run the full contraction, with the same
+ * answers); the workspace grows by about
+ * 4 B + 4 n bytes (the entry thresholds padded to a multiple of 1024 rows). */
 #define LIPCACHE_LOOKUP_PRUNE 0x100
 
 /* Radius modes (policy component rho, Sec. 4.3): the conservative radius of

@@ -227,9 +227,11 @@ struct PrepEntries {
   unsigned long long* gq_count;  // emptied for the scan that follows (nullable)
   double* qnorm;                 // ||q||^2 in float64 of every query (nullable)
   uint16_t* zq16;                // float16 copy of the queries (nullable)
-  // prefix pruning (qthr_p == nullptr: off): Q'_q, A'_i and their constants
+  // prefix pruning (qthr_p == nullptr: off): Q'_q, A'_i [np_pad] and their
+  // constants
   float* qthr_p;
   float* athr_p;
+  int64_t np_pad;
   const void* cz;
   int store;
   Thresholds tp;
@@ -245,7 +247,7 @@ __global__ void lookup_prep_kernel(const float* __restrict__ zq, int64_t B, int 
   if (blockIdx.x >= qblocks) {
     const int64_t i = static_cast<int64_t>(blockIdx.x - qblocks) * kLkThreads + threadIdx.x;
     write_athr(i, pe.cr, pe.cnorm2, pe.n, pe.n_pad, t.kappa_c, t.eta1, t.range2, pe.athr);
-    if (pe.athr_p && i < pe.n_pad)
+    if (pe.athr_p && i < pe.np_pad)
       pe.athr_p[i] = i < pe.n ? prefix_entry_threshold(pe.cr[i], pe.cnorm2[i], prefix_norm2(pe.cz, pe.store, d, i), pe.tp)
                               : __builtin_inff();
     return;
@@ -941,7 +943,7 @@ constexpr int kPrefetch = LC_PREFETCH;
 
 template <int MODE, int KS, int NW>
 __device__ __forceinline__ void issue_tile(unsigned char* buf, float* athr_buf, const LookupParams& p, int64_t t0,
-                                           int64_t e_end, int wave, float* athp_buf = nullptr) {
+                                           int64_t e_end, int wave) {
   using T = ModeTraits<MODE>;
   constexpr int kThreads = NW * kWave;
   constexpr int kCPR = 4 * KS;  // 16-byte chunks per LDS row
@@ -986,16 +988,9 @@ __device__ __forceinline__ void issue_tile(unsigned char* buf, float* athr_buf, 
   // thresholds of the tile's rows (+inf padding past n): one wave per 64,
   // at least 64 (a tile of fewer rows stages the next ones too; the array
   // holds them: it is padded by kDmaMaxRows past the last tile start)
-  constexpr int kAthrWaves = DmaTraits<KS, NW>::kAthr / kWave;
-  if (wave < kAthrWaves)
+  if (wave < DmaTraits<KS, NW>::kAthr / kWave)
     lds_copy<4>(p.athr + t0 + wave * kWave, static_cast<uint32_t>(lane_id() * 4),
                 static_cast<unsigned char*>(static_cast<void*>(athr_buf)) + wave * kWave * 4);
-  // prefix thresholds (pruned lookup), by the next waves
-  if (athp_buf && wave >= kAthrWaves && wave < 2 * kAthrWaves) {
-    const int w = wave - kAthrWaves;
-    lds_copy<4>(p.athr_p + t0 + w * kWave, static_cast<uint32_t>(lane_id() * 4),
-                static_cast<unsigned char*>(static_cast<void*>(athp_buf)) + w * kWave * 4);
-  }
 }
 
 // The cache operand of (column tile `sub`, k-step ks) for this lane: chunk
@@ -1130,107 +1125,14 @@ __device__ __forceinline__ void load_thresholds(const float* thr, int64_t qwave,
   }
 }
 
-// Pruned lookup, rare path of a full tile: column tile `sub` passed the
-// prefix filter.  Its accumulators are formed again exactly as the full
-// kernel forms them (same start value, same MFMAs in the same order), so the
-// full filter takes the same decisions and picks the pairs to re-check.
-template <int STORE, int KS, int RT, int NW>
-__device__ __forceinline__ void continue_column_tile(const unsigned char* buf, const float* athr_buf,
-                                                     const LookupParams& p, int64_t t0, int sub, int64_t qwave,
-                                                     int64_t qend, int m16, int g, const u32x4 (&a)[RT][KS],
-                                                     RecheckQueue& rq) {
-  constexpr bool kFold = kFoldQ<kModeF16, KS>;
-  f32x4 qf[RT];
-  load_thresholds<RT>(p.qthr, qwave, qend, nullptr, g, kFold, qf);
-  f32x4 acc[RT];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) acc[rt] = kFold ? qf[rt] : f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    const u32x4 op = lds_operand<KS>(buf, sub, ks, m16, g);
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) acc[rt] = mfma_step<kModeF16>(a[rt][ks], op, acc[rt]);
-  }
-  f32x4 qt[RT];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) qt[rt] = kFold ? f32x4{0.f, 0.f, 0.f, 0.f} : qf[rt];
-  const float an = athr_buf[sub * kColTile + m16];
-  float mx = -__builtin_inff();
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) mx = __builtin_fmaxf(mx, acc[rt][i] - qt[rt][i]);
-  }
-  if (__ballot(mx >= an) != 0ull)
-    filter_and_recheck<STORE, RT, false>(p, acc, qt, an, qwave, qend, nullptr, t0 + sub * kColTile, rq);
-}
-
-// Pruned lookup, a full LDS tile: k-step 0 of every column tile (features
-// 0..31 against the lane's 16 queries, accumulators started at -Q'_q, so
-// the prefix filter is max_16(acc) >= A'_i) and the prefix filter,
-// software-pipelined one column tile behind.  A column tile with no passing
-// pair holds no hit and no boundary-band pair and is done after 1 of its KS
-// k-steps; the others are only marked in a wave-uniform bit mask and
-// finished after the loop (the tile stays in LDS until the next barrier),
-// where only the query operands are live.
-template <int STORE, int KS, int RT, int NW>
-__device__ __forceinline__ void compute_full_tile_pruned(const unsigned char* buf, const float* athr_buf,
-                                                         const float* athp_buf, const LookupParams& p, int64_t t0,
-                                                         int64_t qwave, int64_t qend, int m16, int g,
-                                                         const u32x4 (&a)[RT][KS], const f32x4 (&nqp)[RT],
-                                                         RecheckQueue& rq) {
-  constexpr int kSubs = DmaTraits<KS, NW>::kRows / kColTile;
-  static_assert(kSubs >= 2, "two column tiles per LDS tile");
-  u32x4 bq[2];  // k-step 0 operands of the next two column tiles
-  bq[0] = lds_operand<KS>(buf, 0, 0, m16, g);
-  bq[1] = lds_operand<KS>(buf, 1, 0, m16, g);
-  f32x4 pacc[RT];
-  float anp = 0.0f;
-  uint32_t pass = 0u;  // bit s: column tile s passed the prefix filter somewhere
-#pragma unroll
-  for (int sub = 0; sub <= kSubs; ++sub) {
-    const bool cur = sub < kSubs;  // compile-time after unrolling
-    const bool prev = sub > 0;
-    f32x4 acc[RT];
-    float an = 0.0f;
-    if (cur) {
-      const u32x4 op = bq[sub & 1];
-      if (sub + 2 < kSubs) bq[sub & 1] = lds_operand<KS>(buf, sub + 2, 0, m16, g);
-      an = athp_buf[sub * kColTile + m16];
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) acc[rt] = mfma_step<kModeF16>(a[rt][0], op, nqp[rt]);
-    }
-    if (prev) {
-      float mx = -__builtin_inff();
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) mx = __builtin_fmaxf(mx, pacc[rt][i]);
-      }
-      pass |= __ballot(mx >= anp) != 0ull ? 1u << (sub - 1) : 0u;
-    }
-    if (cur) {
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) pacc[rt] = acc[rt];
-      anp = an;
-    }
-  }
-  if (__builtin_expect(pass != 0u, 0)) {
-#pragma unroll 1
-    for (int sub = 0; sub < kSubs; ++sub)
-      if ((pass >> sub) & 1u) continue_column_tile<STORE, KS, RT, NW>(buf, athr_buf, p, t0, sub, qwave, qend, m16, g, a, rq);
-  }
-}
-
-// FULL: the tile may be full (else only the partial-tile path is compiled).
-template <int MODE, int STORE, int KS, int RT, int NW, bool DUMP, bool LIST, bool FULL = true>
+template <int MODE, int STORE, int KS, int RT, int NW, bool DUMP, bool LIST>
 __device__ __forceinline__ void compute_tile(const unsigned char* buf, const float* athr_buf, const LookupParams& p,
                                              int64_t t0, int64_t e_end, int64_t qwave, int64_t qend,
                                              const int32_t* qlist, int m16, int g, const u32x4 (&a)[RT][KS],
                                              const f32x4 (&qv)[RT], RecheckQueue& rq) {
   constexpr int kRows = DmaTraits<KS, NW>::kRows;
   const int64_t left = e_end - t0;
-  if constexpr (!DUMP && FULL) {
+  if constexpr (!DUMP) {
     if (left >= kRows) {
       compute_full_tile<MODE, STORE, KS, RT, NW, LIST>(buf, athr_buf, p, t0, qwave, qend, qlist, m16, g, a, qv, rq);
       return;
@@ -1315,34 +1217,10 @@ __device__ __forceinline__ void compute_tile(const unsigned char* buf, const flo
   }
 }
 
-// One LDS tile of the scan; with PRUNE full tiles take the pruned path (qv:
-// prefix thresholds) and a partial tile the full one (its thresholds loaded
-// here).
-template <int MODE, int STORE, int KS, int RT, int NW, bool DUMP, bool LIST, bool PRUNE>
-__device__ __forceinline__ void run_tile(const unsigned char* buf, const float* athr_buf, const float* athp_buf,
-                                         const LookupParams& p, int64_t t0, int64_t e_end, int64_t qwave,
-                                         int64_t qend, const int32_t* qlist, int m16, int g, const u32x4 (&a)[RT][KS],
-                                         const f32x4 (&qv)[RT], RecheckQueue& rq) {
-  if constexpr (PRUNE) {
-    if (e_end - t0 >= DmaTraits<KS, NW>::kRows) {
-      compute_full_tile_pruned<STORE, KS, RT, NW>(buf, athr_buf, athp_buf, p, t0, qwave, qend, m16, g, a, qv, rq);
-    } else {
-      f32x4 qf[RT];
-      load_thresholds<RT>(p.qthr, qwave, qend, qlist, g, kFoldQ<MODE, KS>, qf);
-      compute_tile<MODE, STORE, KS, RT, NW, DUMP, LIST, false>(buf, athr_buf, p, t0, e_end, qwave, qend, qlist, m16,
-                                                               g, a, qf, rq);
-    }
-  } else {
-    compute_tile<MODE, STORE, KS, RT, NW, DUMP, LIST>(buf, athr_buf, p, t0, e_end, qwave, qend, qlist, m16, g, a, qv,
-                                                      rq);
-  }
-}
-
 // NW waves per workgroup (8, or 4 with two workgroups per CU), two waves
-// per SIMD either way.  PRUNE: the pruned lookup (slice mode, float16).
-template <int MODE, int STORE, int KS, int RT, int NW, bool DUMP, bool LIST, bool PRUNE = false>
+// per SIMD either way.
+template <int MODE, int STORE, int KS, int RT, int NW, bool DUMP, bool LIST>
 __global__ __launch_bounds__(NW * kWave, 2) void lookup_dma_kernel(const LookupParams p) {
-  static_assert(!PRUNE || (MODE == kModeF16 && !DUMP && !LIST && KS >= 2), "pruned lookup: float16 slice scan");
   using T = ModeTraits<MODE>;
   constexpr int kCPR = 4 * KS;
   constexpr int kRows = DmaTraits<KS, NW>::kRows;
@@ -1353,10 +1231,6 @@ __global__ __launch_bounds__(NW * kWave, 2) void lookup_dma_kernel(const LookupP
   __shared__ __attribute__((aligned(16))) float ath1[DmaTraits<KS, NW>::kAthr];
   __shared__ int64_t rq_e[LIST ? NW * kRq : 1];
   __shared__ int32_t rq_q[LIST ? NW * kRq : 1];
-  __shared__ __attribute__((aligned(16))) float athp0[PRUNE ? DmaTraits<KS, NW>::kAthr : 1];
-  __shared__ __attribute__((aligned(16))) float athp1[PRUNE ? DmaTraits<KS, NW>::kAthr : 1];
-  float* const athp0p = PRUNE ? athp0 : nullptr;
-  float* const athp1p = PRUNE ? athp1 : nullptr;
 
   int64_t q0, qend, e_begin, e_end;
   block_work(p, NW * RT * 16, q0, qend, e_begin, e_end);
@@ -1373,7 +1247,7 @@ __global__ __launch_bounds__(NW * kWave, 2) void lookup_dma_kernel(const LookupP
   // Work-list mode: a wave whose queries all lie past the list's end only
   // moves its share of each tile (the copies and barriers are the block's).
   const bool active = !LIST || qwave < qend;
-  issue_tile<MODE, KS, NW>(buf0, ath0, p, e_begin, e_end, wave, athp0p);
+  issue_tile<MODE, KS, NW>(buf0, ath0, p, e_begin, e_end, wave);
 
   u32x4 a[RT][KS];
   if (active) load_query_operands<MODE, KS, RT, LIST && MODE == kModeF16>(p, qlist, qwave, qend, m16, g, a);
@@ -1381,31 +1255,232 @@ __global__ __launch_bounds__(NW * kWave, 2) void lookup_dma_kernel(const LookupP
   // Q_q of this lane's accumulator rows 4g .. 4g + 3 of each row tile, kept
   // in registers for the whole slice (reading them from LDS per column tile
   // costs a third of the operand traffic); +inf past B.  Negated where the
-  // accumulators start at -Q_q.  The pruned lookup keeps the prefix
-  // thresholds here instead, negated (its accumulators start at -Q'_q).
+  // accumulators start at -Q_q.
   f32x4 qv[RT];
-  load_thresholds<RT>(PRUNE ? p.qthr_p : p.qthr, qwave, qend, qlist, g, PRUNE || kFoldQ<MODE, KS>, qv);
+  load_thresholds<RT>(p.qthr, qwave, qend, qlist, g, kFoldQ<MODE, KS>, qv);
 
   for (int64_t t0 = e_begin;; t0 += 2 * kRows) {
     wait_copies();
     __syncthreads();
     const bool more1 = t0 + kRows < e_end;
-    if (more1) issue_tile<MODE, KS, NW>(buf1, ath1, p, t0 + kRows, e_end, wave, athp1p);
+    if (more1) issue_tile<MODE, KS, NW>(buf1, ath1, p, t0 + kRows, e_end, wave);
     if (active)
-      run_tile<MODE, STORE, KS, RT, NW, DUMP, LIST, PRUNE>(buf0, ath0, athp0p, p, t0, e_end, qwave, qend, qlist, m16,
-                                                            g, a, qv, rq);
+      compute_tile<MODE, STORE, KS, RT, NW, DUMP, LIST>(buf0, ath0, p, t0, e_end, qwave, qend, qlist, m16, g, a, qv, rq);
     if (!more1) break;
     wait_copies();
     __syncthreads();
     const bool more2 = t0 + 2 * kRows < e_end;
-    if (more2) issue_tile<MODE, KS, NW>(buf0, ath0, p, t0 + 2 * kRows, e_end, wave, athp0p);
+    if (more2) issue_tile<MODE, KS, NW>(buf0, ath0, p, t0 + 2 * kRows, e_end, wave);
     if (active)
-      run_tile<MODE, STORE, KS, RT, NW, DUMP, LIST, PRUNE>(buf1, ath1, athp1p, p, t0 + kRows, e_end, qwave, qend,
-                                                            qlist, m16, g, a, qv, rq);
+      compute_tile<MODE, STORE, KS, RT, NW, DUMP, LIST>(buf1, ath1, p, t0 + kRows, e_end, qwave, qend, qlist, m16, g, a, qv, rq);
     if (!more2) break;
   }
   if constexpr (LIST) {
     if (active) flush_queue<STORE>(p, recheck_args(p, qend, qlist), rq, qwave);
+  }
+}
+
+// ------------------------------------------------------------- pruned scan
+// The pruned lookup (LIPCACHE_LOOKUP_PRUNE) streams only the prefix of every
+// row: 64 bytes (features 0..31 of the float16 image) per row, 1024 rows per
+// 64 KiB LDS tile, double-buffered, with the prefix thresholds A'_i of the
+// tile's rows.  Each 16-entry column tile gets k-step 0 only; the rare column
+// tiles where a pair passes the prefix filter are formed again from the
+// image in global memory, exactly as the full kernel forms them, and go
+// through the full filter and the re-check.
+constexpr int kPrRows = 1024;                 // rows per prefix tile
+constexpr int kPrSubs = kPrRows / kColTile;   // column tiles per prefix tile
+
+// Copies rows [t0, t0 + kPrRows) of the prefix into an LDS tile (rows past
+// e_end repeat its last row) and their thresholds A'_i.  Thread tid copies
+// chunk tid % 4 of rows tid / 4 + 128 j; in the tile, chunk c of row r sits
+// in slot c ^ swz(r) (the layout lds_operand<1> reads), and swz(r) =
+// (r / 4) % 4 is the same for all of a thread's rows.
+__device__ __forceinline__ void issue_prefix_tile(unsigned char* buf, float* athp_buf, const LookupParams& p,
+                                                  int64_t t0, int64_t e_end, int wave) {
+  constexpr int kThreads = kDmaWaves * kWave;
+  constexpr int kRowsPerIter = kThreads / 4;
+  constexpr int kIters = kPrRows / kRowsPerIter;
+  const int row_bytes = p.d * 2;
+  const int tid = static_cast<int>(threadIdx.x);
+  const int r0 = tid / 4;
+  const int c = (tid % 4) ^ lds_swizzle<4>(r0);
+  const unsigned char* base = static_cast<const unsigned char*>(p.cimg) + t0 * static_cast<int64_t>(row_bytes);
+  if (e_end - t0 >= kPrRows) {
+    const uint32_t voff = static_cast<uint32_t>(r0 * row_bytes + c * 16);
+#pragma unroll
+    for (int j = 0; j < kIters; ++j)
+      lds_copy<16>(base + static_cast<int64_t>(j * kRowsPerIter) * row_bytes, voff,
+                   buf + (j * kThreads + wave * kWave) * 16);
+  } else {
+    const int last = static_cast<int>(e_end - t0) - 1;
+#pragma unroll
+    for (int j = 0; j < kIters; ++j) {
+      const int row = j * kRowsPerIter + r0;
+      const int rr = row < last ? row : last;
+      lds_copy<16>(base, static_cast<uint32_t>(rr * row_bytes + c * 16), buf + (j * kThreads + wave * kWave) * 16);
+    }
+  }
+  // thresholds: 1024 floats, two 64-float copies per wave (the array is
+  // padded with +inf past n by more than a tile)
+#pragma unroll
+  for (int i = 0; i < kPrRows / (kDmaWaves * kWave); ++i) {
+    const int w = wave * (kPrRows / (kDmaWaves * kWave)) + i;
+    lds_copy<4>(p.athr_p + t0 + w * kWave, static_cast<uint32_t>(lane_id() * 4),
+                static_cast<unsigned char*>(static_cast<void*>(athp_buf)) + w * kWave * 4);
+  }
+}
+
+// Rare path of the pruned scan: column tile `sub` of the prefix tile at t0
+// (rows e = t0 + 16 sub + m16, those at or past e_end never pass) formed as
+// the full kernel forms it, from the image in global memory, then the full
+// filter and the re-check.
+template <int STORE, int KS, int RT>
+__device__ __forceinline__ void prune_survivor(const LookupParams& p, int64_t t0, int sub, int64_t e_end,
+                                               int64_t qwave, int64_t qend, int m16, int g,
+                                               const u32x4 (&a)[RT][KS], RecheckQueue& rq) {
+  constexpr bool kFold = kFoldQ<kModeF16, KS>;
+  const int64_t ebase = t0 + static_cast<int64_t>(sub) * kColTile;
+  const int64_t e = ebase + m16;
+  const bool live = e < e_end;
+  const int64_t er = live ? e : e_end - 1;
+  f32x4 qf[RT];
+  load_thresholds<RT>(p.qthr, qwave, qend, nullptr, g, kFold, qf);
+  f32x4 acc[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) acc[rt] = kFold ? qf[rt] : f32x4{0.f, 0.f, 0.f, 0.f};
+  u32x4 b[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) b[ks] = load_chunk<kModeF16, LIPCACHE_F16>(p.cimg, er, p.d, ks * 32 + g * 8);
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) acc[rt] = mfma_step<kModeF16>(a[rt][ks], b[ks], acc[rt]);
+  }
+  f32x4 qt[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) qt[rt] = kFold ? f32x4{0.f, 0.f, 0.f, 0.f} : qf[rt];
+  const float an = live ? p.athr[e] : __builtin_inff();
+  float mx = -__builtin_inff();
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mx = __builtin_fmaxf(mx, acc[rt][i] - qt[rt][i]);
+  }
+  if (__ballot(mx >= an) != 0ull) filter_and_recheck<STORE, RT, false>(p, acc, qt, an, qwave, qend, nullptr, ebase, rq);
+}
+
+// One prefix tile: k-step 0 of every column tile against the lane's 16
+// queries (accumulators started at -Q'_q: the test is max_16(acc) >= A'_i),
+// software-pipelined one column tile behind, with the operands read two
+// column tiles ahead; passing column tiles are marked in a wave-uniform
+// mask and formed again after the tile.  A partial tile (the end of a
+// slice) takes a plain loop that also masks rows past e_end.
+template <int STORE, int KS, int RT>
+__device__ __forceinline__ void prune_tile(const unsigned char* buf, const float* athp_buf, const LookupParams& p,
+                                           int64_t t0, int64_t e_end, int64_t qwave, int64_t qend, int m16, int g,
+                                           const u32x4 (&a)[RT][KS], const f32x4 (&nqp)[RT], RecheckQueue& rq) {
+  uint64_t pass = 0ull;
+  if (e_end - t0 >= kPrRows) {
+    u32x4 bq[2];
+    bq[0] = lds_operand<1>(buf, 0, 0, m16, g);
+    bq[1] = lds_operand<1>(buf, 1, 0, m16, g);
+    f32x4 pacc[RT];
+    float anp = 0.0f;
+#pragma unroll
+    for (int sub = 0; sub <= kPrSubs; ++sub) {
+      const bool cur = sub < kPrSubs;  // compile-time after unrolling
+      const bool prev = sub > 0;
+      f32x4 acc[RT];
+      float an = 0.0f;
+      if (cur) {
+        const u32x4 op = bq[sub & 1];
+        if (sub + 2 < kPrSubs) bq[sub & 1] = lds_operand<1>(buf, sub + 2, 0, m16, g);
+        an = athp_buf[sub * kColTile + m16];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) acc[rt] = mfma_step<kModeF16>(a[rt][0], op, nqp[rt]);
+      }
+      if (prev) {
+        float mx = -__builtin_inff();
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) mx = __builtin_fmaxf(mx, pacc[rt][i]);
+        }
+        pass |= __ballot(mx >= anp) != 0ull ? 1ull << (sub - 1) : 0ull;
+      }
+      if (cur) {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) pacc[rt] = acc[rt];
+        anp = an;
+      }
+    }
+  } else {
+    const int64_t left = e_end - t0;
+    const int nsub = static_cast<int>((left + kColTile - 1) / kColTile);
+#pragma unroll 1
+    for (int sub = 0; sub < nsub; ++sub) {
+      const u32x4 op = lds_operand<1>(buf, sub, 0, m16, g);
+      const float an = sub * kColTile + m16 < left ? athp_buf[sub * kColTile + m16] : __builtin_inff();
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const f32x4 acc = mfma_step<kModeF16>(a[rt][0], op, nqp[rt]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mx = __builtin_fmaxf(mx, acc[i]);
+      }
+      pass |= __ballot(mx >= an) != 0ull ? 1ull << sub : 0ull;
+    }
+  }
+  if (__builtin_expect(pass != 0ull, 0)) {
+#pragma unroll 1
+    for (int sub = 0; sub < kPrSubs; ++sub)
+      if ((pass >> sub) & 1ull) prune_survivor<STORE, KS, RT>(p, t0, sub, e_end, qwave, qend, m16, g, a, rq);
+  }
+}
+
+// The pruned scan (slice mode): one 512-thread workgroup per (query block,
+// cache slice), 8 waves of RT row tiles of queries, the query operands of
+// all KS k-steps in registers (the survivors need them), the negated prefix
+// thresholds of the lane's 16 queries as the start value of k-step 0.
+template <int STORE, int KS, int RT>
+__global__ __launch_bounds__(kDmaWaves * kWave, 2) void lookup_prune_kernel(const LookupParams p) {
+  static_assert(KS >= 2, "a prefix shorter than the row");
+  __shared__ __attribute__((aligned(16))) unsigned char buf0[kPrRows * 64];
+  __shared__ __attribute__((aligned(16))) unsigned char buf1[kPrRows * 64];
+  __shared__ __attribute__((aligned(16))) float athp0[kPrRows];
+  __shared__ __attribute__((aligned(16))) float athp1[kPrRows];
+
+  int64_t q0, qend, e_begin, e_end;
+  block_work(p, kDmaWaves * RT * 16, q0, qend, e_begin, e_end);
+  qend = p.B;
+  const int lane = lane_id();
+  const int wave = uniform(static_cast<int>(threadIdx.x) / kWave);
+  const int m16 = lane & 15;
+  const int g = lane >> 4;
+  const int64_t qwave = q0 + wave * (RT * 16);
+  if (e_begin >= e_end) return;  // whole workgroup: an empty slice
+  issue_prefix_tile(buf0, athp0, p, e_begin, e_end, wave);
+
+  u32x4 a[RT][KS];
+  load_query_operands<kModeF16, KS, RT, false>(p, nullptr, qwave, qend, m16, g, a);
+  f32x4 nqp[RT];
+  load_thresholds<RT>(p.qthr_p, qwave, qend, nullptr, g, true, nqp);
+  RecheckQueue rq{nullptr, nullptr, 0};
+
+  for (int64_t t0 = e_begin;; t0 += 2 * kPrRows) {
+    wait_copies();
+    __syncthreads();
+    const bool more1 = t0 + kPrRows < e_end;
+    if (more1) issue_prefix_tile(buf1, athp1, p, t0 + kPrRows, e_end, wave);
+    prune_tile<STORE, KS, RT>(buf0, athp0, p, t0, e_end, qwave, qend, m16, g, a, nqp, rq);
+    if (!more1) break;
+    wait_copies();
+    __syncthreads();
+    const bool more2 = t0 + 2 * kPrRows < e_end;
+    if (more2) issue_prefix_tile(buf0, athp0, p, t0 + 2 * kPrRows, e_end, wave);
+    prune_tile<STORE, KS, RT>(buf1, athp1, p, t0 + kPrRows, e_end, qwave, qend, m16, g, a, nqp, rq);
+    if (!more2) break;
   }
 }
 
@@ -1447,7 +1522,7 @@ inline bool make_plan(int precision, const lipcache_cache* c, bool list, Plan& p
 
 // Kernel variants: the lookup, the filter dump, and the work-list lookup of
 // the cluster index.
-enum { kVarLookup = 0, kVarDump = 1, kVarList = 2, kVarList8 = 3, kVarPrune = 4 };
+enum { kVarLookup = 0, kVarDump = 1, kVarList = 2, kVarList8 = 3 };
 
 template <int MODE, int SRC, int KS, int VAR>
 hipError_t launch_v1(const LookupParams& p, unsigned grid, hipStream_t s) {
@@ -1459,15 +1534,7 @@ hipError_t launch_v1(const LookupParams& p, unsigned grid, hipStream_t s) {
 
 template <int MODE, int STORE, int KS, int VAR>
 hipError_t launch_dma(const LookupParams& p, unsigned grid, hipStream_t s) {
-  if constexpr (VAR == kVarPrune) {
-    if constexpr (MODE == kModeF16 && KS >= 2 && KS <= 16) {
-      hipLaunchKernelGGL((lookup_dma_kernel<MODE, STORE, KS, (KS <= 8 ? 4 : 2), kDmaWaves, false, false, true>),
-                         dim3(grid), dim3(kDmaWaves * kWave), 0, s, p);
-      return hipGetLastError();
-    } else {
-      return hipErrorInvalidValue;
-    }
-  } else if constexpr (KS <= 16) {
+  if constexpr (KS <= 16) {
     constexpr int kNW = VAR == kVarList ? kListWaves : kDmaWaves;
     hipLaunchKernelGGL((lookup_dma_kernel<MODE, STORE, KS, (KS <= 8 ? 4 : 2), kNW, VAR == kVarDump,
                                           VAR == kVarList || VAR == kVarList8>),
@@ -1505,6 +1572,29 @@ hipError_t launch_lookup(int precision, int store, const Plan& pl, const LookupP
                                : launch_ks<kModeF32, LIPCACHE_BF16, VAR>(pl, p, grid, s);
 }
 
+// The pruned scan (float16 image, 2 <= KS <= 16; see prune_consts).
+template <int STORE>
+hipError_t launch_prune_store(const Plan& pl, const LookupParams& p, unsigned grid, hipStream_t s) {
+  switch (pl.ks) {
+#define LC_PCASE(K)                                                                                            \
+  case K:                                                                                                      \
+    hipLaunchKernelGGL((lookup_prune_kernel<STORE, K, (K <= 8 ? 4 : 2)>), dim3(grid), dim3(kDmaWaves * kWave), 0, \
+                       s, p);                                                                                  \
+    return hipGetLastError();
+    LC_PCASE(2)
+    LC_PCASE(4)
+    LC_PCASE(8)
+    LC_PCASE(16)
+#undef LC_PCASE
+    default: return hipErrorInvalidValue;
+  }
+}
+
+inline hipError_t launch_prune(int store, const Plan& pl, const LookupParams& p, unsigned grid, hipStream_t s) {
+  return store == LIPCACHE_F32 ? launch_prune_store<LIPCACHE_F32>(pl, p, grid, s)
+                               : launch_prune_store<LIPCACHE_BF16>(pl, p, grid, s);
+}
+
 // Workgroups a slice scan aims for (at least a few per CU, for balance).
 #ifndef LC_GRID_TARGET
 #define LC_GRID_TARGET 256
@@ -1529,7 +1619,7 @@ struct Workspace {
   unsigned long long* stats;
   float* athr;
   GlobalRecheckWs gq;
-  float* qthr_p;  // pruned lookup only: Q'_q [B], A'_i [athr_len(N)]
+  float* qthr_p;  // pruned lookup only: Q'_q [B], A'_i [athp_len(N)]
   float* athr_p;
 };
 
@@ -1538,6 +1628,10 @@ struct Workspace {
 inline int64_t athr_len(int64_t n) {
   return ((n > 0 ? n : 0) + kDmaMaxRows - 1) / kDmaMaxRows * kDmaMaxRows + kDmaMaxRows;
 }
+
+// A'_i of the pruned scan, padded with +inf so that a prefix tile starting
+// below n reads only this array.
+inline int64_t athp_len(int64_t n) { return ((n > 0 ? n : 0) + kPrRows - 1) / kPrRows * kPrRows + kPrRows; }
 
 inline size_t ws_layout(int64_t B, int64_t N, Workspace* w, void* base, bool prune = false) {
   const size_t nb = static_cast<size_t>(B > 0 ? B : 0);
@@ -1562,7 +1656,7 @@ inline size_t ws_layout(int64_t B, int64_t N, Workspace* w, void* base, bool pru
   const size_t o_qp = off;
   if (prune) off = align_up(off + nb * 4, 256);
   const size_t o_ap = off;
-  if (prune) off = align_up(off + static_cast<size_t>(athr_len(N)) * 4, 256);
+  if (prune) off = align_up(off + static_cast<size_t>(athp_len(N)) * 4, 256);
   if (w && base) {
     char* b = static_cast<char*>(base);
     w->best = reinterpret_cast<unsigned long long*>(b + o_best);
@@ -1621,9 +1715,13 @@ lipcache_status lookup_consts(const lipcache_cache* c, int32_t precision, Filter
 }
 
 // The pruned scan runs where the slice kernel is the float16 DMA kernel with
-// at least two k-steps; elsewhere the option changes nothing.
+// at least two k-steps, on caches of at least kPruneMinRows rows (fewer fill
+// too few 1024-row prefix tiles to pay for the prefix thresholds); elsewhere
+// the option changes nothing.
+constexpr int64_t kPruneMinRows = 32 * kPrRows;
+
 void prune_consts(const lipcache_cache* c, int32_t precision, FilterConsts& fc) {
-  fc.prune = precision == LIPCACHE_F16 && fc.pl.dma && fc.pl.ks >= 2 && fc.pl.ks <= 16;
+  fc.prune = precision == LIPCACHE_F16 && fc.pl.dma && fc.pl.ks >= 2 && fc.pl.ks <= 16 && c->n >= kPruneMinRows;
   if (!fc.prune) return;
   const FilterSlack fs = filter_slack(precision, c->store_dtype, kPrefixDims);
   const double u32 = 1.0 / 16777216.0;
@@ -1650,13 +1748,15 @@ lipcache_status lookup_stage_prep(const float* zq, int64_t B, int d, const Filte
                                   unsigned long long* gq_count = nullptr, double* qnorm = nullptr,
                                   uint16_t* zq16 = nullptr, float* qthr_p = nullptr, float* athr_p = nullptr) {
   const int64_t qblocks = B > 0 ? (B + kLkWaves - 1) / kLkWaves : 1;
-  PrepEntries pe{nullptr, nullptr, 0, 0, nullptr, nullptr, qnorm, zq16, nullptr, nullptr, nullptr, 0, fc.tp};
+  PrepEntries pe{nullptr, nullptr, 0, 0, nullptr, nullptr, qnorm, zq16, nullptr, nullptr, 0, nullptr, 0, fc.tp};
   int64_t eblocks = 0;
   if (view && view->n > 0) {
     const bool pr = qthr_p && athr_p;
-    pe = PrepEntries{view->r,     view->norm2,        view->n, athr_len(view->n), athr, gq_count, qnorm, zq16,
-                     pr ? qthr_p : nullptr, pr ? athr_p : nullptr, view->z, view->store_dtype, fc.tp};
-    eblocks = (pe.n_pad + kLkThreads - 1) / kLkThreads;
+    pe = PrepEntries{view->r, view->norm2, view->n, athr_len(view->n), athr, gq_count, qnorm, zq16,
+                     pr ? qthr_p : nullptr, pr ? athr_p : nullptr, pr ? athp_len(view->n) : 0, view->z,
+                     view->store_dtype, fc.tp};
+    const int64_t cover = pe.np_pad > pe.n_pad ? pe.np_pad : pe.n_pad;
+    eblocks = (cover + kLkThreads - 1) / kLkThreads;
   }
   if (qblocks + eblocks > INT_MAX) return LIPCACHE_EUNSUPPORTED;
   hipLaunchKernelGGL(lookup_prep_kernel, dim3(static_cast<unsigned>(qblocks + eblocks)), dim3(kLkThreads), 0, s, zq,
@@ -1720,17 +1820,19 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
   p.gq_cap = dump ? 0 : gq.cap;
   int64_t grid = n_items;
   p.slice_len = 0;
+  const bool prune = qthr_p && athr_p && !items && !dump;
   if (!items) {
     // Cache slices: a multiple of 8 (one set per XCD), enough blocks to fill
     // the chip (~kGridTarget), but at least 4 tiles per slice.
-    const int64_t tiles = (view->n + pl.tile_rows - 1) / pl.tile_rows;
+    const int64_t tile_rows = prune ? kPrRows : pl.tile_rows;
+    const int64_t tiles = (view->n + tile_rows - 1) / tile_rows;
     int64_t s8 = (kGridTarget + kXcds * p.n_qblocks - 1) / (kXcds * static_cast<int64_t>(p.n_qblocks));
     int64_t s8_max = tiles / (kXcds * 4);
     if (s8_max < 1) s8_max = 1;
     if (s8 > s8_max) s8 = s8_max;
     if (s8 < 1) s8 = 1;
     const int64_t slices = kXcds * s8;
-    p.slice_len = ((tiles + slices - 1) / slices) * pl.tile_rows;
+    p.slice_len = ((tiles + slices - 1) / slices) * tile_rows;
     grid = slices * p.n_qblocks;
   }
   if (grid > INT_MAX) return LIPCACHE_EUNSUPPORTED;
@@ -1738,9 +1840,8 @@ lipcache_status lookup_stage_scan(const lipcache_cache* view, int32_t precision,
   const hipError_t e = dump    ? launch_lookup<kVarDump>(precision, view->store_dtype, pl, p, gu, s)
                        : items ? (pl.waves == kListWaves ? launch_lookup<kVarList>(precision, view->store_dtype, pl, p, gu, s)
                                                          : launch_lookup<kVarList8>(precision, view->store_dtype, pl, p, gu, s))
-                       : (qthr_p && athr_p && !items)
-                           ? launch_lookup<kVarPrune>(precision, view->store_dtype, pl, p, gu, s)
-                           : launch_lookup<kVarLookup>(precision, view->store_dtype, pl, p, gu, s);
+                       : prune ? launch_prune(view->store_dtype, pl, p, gu, s)
+                               : launch_lookup<kVarLookup>(precision, view->store_dtype, pl, p, gu, s);
   if (e != hipSuccess) return LIPCACHE_EHIP;
   if (dump) return LIPCACHE_OK;
   // the pairs the scan's waves queued, one chip-wide pass

@@ -62,21 +62,21 @@ def mixture_case(d, N, B, store, seed, C=7):
 
 
 @pytest.mark.parametrize("d,N,B,store,image", [
-    (64, 9000, 700, "f32", True),      # two k-steps: the prefix is half the row
-    (96, 5000, 333, "f32", True),      # d padded to 128
-    (128, 20000, 517, "bf16", True),
-    (256, 12001, 300, "f32", True),    # ragged slices: full and partial tiles
-    (512, 6000, 70, "bf16", True),     # 64-row tiles
-    (256, 8192, 1, "f32", True),
-    (128, 100, 64, "f32", True),       # only partial tiles: no block is pruned
+    (64, 40000, 700, "f32", True),     # two k-steps: the prefix is half the row
+    (96, 33001, 333, "f32", True),     # d padded to 128; ragged slices: full and partial prefix tiles
+    (128, 70000, 517, "bf16", True),
+    (256, 50001, 300, "f32", True),
+    (512, 40000, 70, "bf16", True),    # two row tiles of queries per wave
+    (256, 32768, 1, "f32", True),      # the smallest pruned cache, one query
+    (128, 20000, 200, "f32", True),    # below 32,768 rows: the option changes nothing
     (1024, 900, 40, "f32", True),      # no DMA kernel at d = 1024: the option changes nothing
-    (32, 3000, 200, "f32", True),      # one k-step: nothing to prune
-    (128, 4000, 200, "f32", False),    # no float16 image: the option changes nothing
+    (32, 40000, 200, "f32", True),     # one k-step: nothing to prune
+    (128, 40000, 200, "f32", False),   # no float16 image: the option changes nothing
 ])
 def test_prune_matches_oracle_and_full(d, N, B, store, image):
     say("pruned lookup", d, N, B, store, "image", image)
     st, zq = mixture_case(d, N, B, store, seed=d + N + B)
-    ref = oracle.lookup(zq, st.z, st.r, st.label)
+    ref = oracle.lookup_blocked(zq, st.z, st.r, st.label)
     c = build_cache(st, image=image)
     what = f"prune d={d} N={N} B={B} {store} image={image}"
     pr, sf, sp = same_as_full(c, gpu(zq), what)
@@ -92,11 +92,11 @@ def test_prune_prefix_geometry():
     hit the prefix cannot see), entirely inside it, a prefix that alone fits
     the ball while the whole row does not, and pairs at relative 1e-6 and
     5e-6 inside and outside the ball boundary with the offset inside the
-    prefix (band pairs the widened prefix ball must keep), among 4,096 far
+    prefix (band pairs the widened prefix ball must keep), among 40,000 far
     rows so the blocks around them are pruned."""
     say("pruned lookup: prefix geometry")
     rng = np.random.default_rng(11)
-    d, N = 128, 4096
+    d, N = 128, 40000
     z = (6.0 * rng.standard_normal((N, d))).astype(np.float32)
     r = np.full(N, 1.0, np.float32)
     lab = rng.integers(0, 5, N).astype(np.int32)
@@ -129,7 +129,7 @@ def test_prune_prefix_geometry():
     assert ref.n_band[3:7].sum() >= 2, ref.n_band.tolist()
 
 
-@pytest.mark.parametrize("N,B", [(3000, 64)])
+@pytest.mark.parametrize("N,B", [(33000, 64)])
 def test_prune_outside_f16_range(N, B):
     """Rows and queries outside the float16 range pass the prefix filter
     against everything, as they pass the full one."""
@@ -137,7 +137,7 @@ def test_prune_outside_f16_range(N, B):
     rng = np.random.default_rng(N + B + 1)
     d = 128
     z = rng.standard_normal((N, d))
-    z[::3] *= 4.0e4
+    z[::97] *= 4.0e4
     r = (0.05 * np.linalg.norm(z, axis=1)).astype(np.float32)
     z = z.astype(np.float32)
     st = oracle_cache(z, rng.integers(0, 9, N).astype(np.int32), r, d)
@@ -145,7 +145,7 @@ def test_prune_outside_f16_range(N, B):
     v = rng.standard_normal((B, d))
     v /= np.linalg.norm(v, axis=1, keepdims=True)
     zq = (st.z[pick].astype(np.float64) + (rng.uniform(0, 2, B) * st.r[pick])[:, None] * v).astype(np.float32)
-    ref = oracle.lookup(zq, st.z, st.r, st.label)
+    ref = oracle.lookup_blocked(zq, st.z, st.r, st.label)
     c = build_cache(st)
     pr, _, _ = same_as_full(c, gpu(zq), "prune outside f16 range")
     compare_lookup(pr, ref, "prune outside f16 range")
@@ -153,12 +153,11 @@ def test_prune_outside_f16_range(N, B):
 
 
 def test_prune_workload_blocks():
-    """A sub-block of each d >= 64 workload (its own rows and query recipe):
-    answers equal the full lookup's, and most blocks are pruned (the
-    re-checked pair count falls or stays)."""
+    """A 40,000-row sub-block of each d >= 64 workload (its own rows and
+    query recipe): answers equal the oracle's and the full lookup's."""
     for name in ("tiny-d64-c10", "mix-d128-c100", "mix-d256-c200", "stream-d256-c200-bf16"):
         cfg = wlmod.CONFIGS[name]
-        wl = wlmod.make_workload(cfg, seed=0, n_cache=16384)
+        wl = wlmod.make_workload(cfg, seed=0, n_cache=40000)
         say("pruned lookup workload block", name)
         sig = oracle.spectral_norm(wl.W).sigma
         cert = oracle.certify(wl.z, wl.W, wl.b, sig, store=cfg.store_dtype)

@@ -217,6 +217,13 @@ lipcache_status lipcache_lookup(const lipcache_cache* c, const float* zq, int64_
                                 void* ws, size_t ws_bytes, lipcache_stream_t stream);
 size_t lipcache_lookup_workspace_bytes(int64_t B, int64_t N, int32_t d, int32_t precision);
 
+/* 1 if lipcache_lookup(c, ..., precision, ...) takes the pruned path of
+ * LIPCACHE_LOOKUP_PRUNE for this cache (float16 filter with a float16
+ * image, 64 <= d <= 512, n >= 32768), 0 if it runs the full contraction
+ * (always the case without the option, or for an invalid argument).  Host
+ * only. */
+int32_t lipcache_lookup_prunes(const lipcache_cache* c, int32_t precision);
+
 /*
  * lipcache_lookup for callers that cannot allocate device memory (code under
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):

@@ -68,6 +68,7 @@ SIGNATURES = {
     "lipcache_certify_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "lipcache_lookup": (_i32, [_PCACHE, _vp, _i64, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "lipcache_lookup_noalloc": (_i32, [_PCACHE, _vp, _i64, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "lipcache_lookup_prunes": (_i32, [_PCACHE, _i32]),
     "lipcache_lookup_workspace_bytes": (_sz, [_i64, _i64, _i32, _i32]),
     "lipcache_insert": (_i32, [_PCACHE, _vp, _vp, _vp, _vp, _i64, ctypes.POINTER(_i64), _vp, _sz, _vp]),
     "lipcache_insert_workspace_bytes": (_sz, [_i64]),

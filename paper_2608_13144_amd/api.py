@@ -187,6 +187,12 @@ class LipCache:
         L.check("lipcache_lookup", st)
         return out
 
+    def lookup_prunes(self, precision: str = "f16") -> bool:
+        """lipcache_lookup_prunes: whether a lookup with ``prune=True`` takes
+        the pruned path on this cache (else it runs the full contraction)."""
+        cs = self.cstruct()
+        return bool(L.load().lipcache_lookup_prunes(ctypes.byref(cs), _PRECISION[precision] | L.LOOKUP_PRUNE))
+
     def lookup_noalloc(self, zq: torch.Tensor, precision: str = "f16",
                        out: LookupResult | None = None, prune: bool = False) -> LookupResult:
         """lipcache_lookup_noalloc: lookup on the library's static per-GPU

@@ -2058,6 +2058,16 @@ extern "C" lipcache_status lipcache_lookup_indexed(const lipcache_cache* c, cons
                             ws_bytes, reinterpret_cast<hipStream_t>(stream));
 }
 
+extern "C" int32_t lipcache_lookup_prunes(const lipcache_cache* c, int32_t precision_arg) {
+  if (!wants_prune(precision_arg) || !cache_ok(c)) return 0;
+  const int32_t precision = filter_precision(precision_arg);
+  if (!precision_ok(precision)) return 0;
+  FilterConsts fc;
+  if (lookup_consts(c, precision, fc) != LIPCACHE_OK) return 0;
+  prune_consts(c, precision, fc);
+  return fc.prune ? 1 : 0;
+}
+
 extern "C" size_t lipcache_lookup_workspace_bytes(int64_t B, int64_t N, int32_t d, int32_t precision) {
   (void)d;
   return ws_layout(B, N, nullptr, nullptr, wants_prune(precision));

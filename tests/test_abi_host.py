@@ -137,6 +137,28 @@ def test_pruned_lookup_workspace():
     assert lib.lipcache_lookup_workspace_bytes(B, n, 256, L.F32) == plain
 
 
+def test_lookup_prunes_rule():
+    """Which caches the pruned path serves (host only): the float16 filter
+    with an image, 64 <= d <= 512, n >= 32,768; everything else runs the full
+    contraction, and a request without the option never prunes."""
+    lib = L.load()
+
+    def prunes(prec=L.F16 | L.LOOKUP_PRUNE, **kw):
+        base = dict(zimg=FAKE.value, n=40000, capacity=50000, d=256)
+        base.update(kw)
+        return lib.lipcache_lookup_prunes(ctypes.byref(_cache(**base)), prec)
+    assert prunes() == 1
+    assert prunes(d=64) == 1 and prunes(d=512) == 1 and prunes(d=96) == 1
+    assert prunes(n=32768) == 1 and prunes(n=32767) == 0
+    assert prunes(d=32) == 0 and prunes(d=1024) == 0
+    assert prunes(zimg=None) == 0
+    assert prunes(prec=L.F16) == 0
+    assert prunes(prec=L.F32 | L.LOOKUP_PRUNE) == 0
+    assert prunes(prec=L.BF16 | L.LOOKUP_PRUNE) == 0
+    assert prunes(store_dtype=L.BF16) == 1
+    assert lib.lipcache_lookup_prunes(None, L.F16 | L.LOOKUP_PRUNE) == 0
+
+
 def test_lookup_noalloc_validation():
     """The allocation-free lookup validates like lipcache_lookup and refuses,
     before any device work, a lookup whose workspace exceeds its static array."""

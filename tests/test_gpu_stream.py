@@ -16,7 +16,9 @@ miss is stored as) and appends the misses.
   rows join the cluster of their nearest class mean), every hit is checked
   for validity and certified consistency, both sides append the oracle's
   miss set, and the appended rows (bf16 values, labels, radii) must equal
-  the oracle's certify of the queries.
+  the oracle's certify of the queries.  Every round also runs the pruned
+  lookup (LIPCACHE_LOOKUP_PRUNE), whose answers must equal the full lookup's
+  bit for bit.
 """
 import numpy as np
 import pytest
@@ -134,6 +136,13 @@ def test_stream_full_size_round(full_stream, t):
     res = cache.lookup(gpu(zq), precision="f16")
     ref = oracle.lookup_partitioned(zq, st.z, st.r, st.label, S["assign"], wl.mu)
     compare_lookup(res, ref, f"stream full round {t}")
+    assert cache.lookup_prunes("f16")
+    pr = cache.lookup(gpu(zq), precision="f16", prune=True)
+    for f in ("label", "index", "dist2", "band"):
+        a, b2 = getattr(res, f), getattr(pr, f)
+        assert torch.equal(a.view(torch.uint8), b2.view(torch.uint8)), f"stream full round {t}: pruned {f}"
+    sf, sp = host(res.stats), host(pr.stats)
+    assert sf[0] == sp[0] and sf[2] == sp[2] and sf[3] == sp[3] and sp[1] <= sf[1], (sf, sp)
     nhit = check_hits_valid(res, zq, before, wl.W, wl.b, f"stream full round {t}")
     lab = host(res.label)
     differs = lab != ref.label          # only flagged queries can get here

@@ -982,8 +982,7 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
   LC_HIP(radix_sort_u32(w.keys, w.vals, N, 4, w.hist, w.dsum, w.dbase, cur, s));
   const uint32_t* order = w.vals[cur];
   unsigned long long host_cnt[2] = {0ull, 0ull};
-  LC_HIP(hipMemcpyAsync(host_cnt, w.counters, 16, hipMemcpyDeviceToHost, s));
-  LC_HIP(hipStreamSynchronize(s));
+  LC_HIP(read_back(host_cnt, w.counters, 16, s));
   const int64_t n_elig = static_cast<int64_t>(host_cnt[0]);
   if (n_elig == 0) return LIPCACHE_OK;
   unsigned long long* total_dev = w.counters + 1;
@@ -1000,8 +999,7 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
     };
     LC_HIP(next_chunk());
     unsigned long long cur_k[2] = {0ull, 0ull};
-    LC_HIP(hipMemcpyAsync(cur_k, cursor, 16, hipMemcpyDeviceToHost, s));
-    LC_HIP(hipStreamSynchronize(s));
+    LC_HIP(read_back(cur_k, cursor, 16, s));
     while (cur_k[1] > 0 && added < bud) {
       const int k = static_cast<int>(cur_k[1]);
       hipLaunchKernelGGL(construct_gather_kernel, dim3(static_cast<unsigned>((k + 3) / 4)), dim3(256), 0, s, z, label,
@@ -1042,8 +1040,7 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
       const lipcache_status st = lipcache_insert(c, w.zc, w.lc, w.rc, w.sel, k, &got, w.sub_ws, w.sub_bytes, stream);
       if (st != LIPCACHE_OK) return st;
       added += got;
-      LC_HIP(hipMemcpyAsync(cur_k, cursor, 16, hipMemcpyDeviceToHost, s));
-      LC_HIP(hipStreamSynchronize(s));
+      LC_HIP(read_back(cur_k, cursor, 16, s));
     }
   } else {
     if (per_class > 0) {
@@ -1115,8 +1112,7 @@ extern "C" lipcache_status lipcache_construct(lipcache_cache* c, const float* z,
         LC_LAUNCHED();
       }
     }
-    LC_HIP(hipMemcpyAsync(host_cnt, w.counters, 16, hipMemcpyDeviceToHost, s));
-    LC_HIP(hipStreamSynchronize(s));
+    LC_HIP(read_back(host_cnt, w.counters, 16, s));
     const int64_t npick = static_cast<int64_t>(host_cnt[1]);
     if (selected_out && npick > 0)
       LC_HIP(hipMemcpyAsync(selected_out, w.picks, static_cast<size_t>(npick) * 8, hipMemcpyDeviceToDevice, s));

@@ -1151,8 +1151,7 @@ lipcache_status index_query_plan(const lipcache_index* idx, const uint16_t* zq16
                      qb_long, w.ioff, w.items, w.capacity, w.counters);
   LC_LAUNCHED();
   unsigned long long host[4] = {0ull, 0ull, 0ull, 0ull};
-  LC_HIP(hipMemcpyAsync(host, w.counters, sizeof(host), hipMemcpyDeviceToHost, s));
-  LC_HIP(hipStreamSynchronize(s));
+  LC_HIP(read_back(host, w.counters, sizeof(host), s));
   if (host[2] != 0ull) return LIPCACHE_EHIP;  // the capacity bound was wrong: never expected
   n_items = static_cast<int64_t>(host[0]);
   pairs = static_cast<int64_t>(host[1]);

@@ -182,8 +182,7 @@ extern "C" lipcache_status lipcache_insert(lipcache_cache* c, const float* z_src
   hipLaunchKernelGGL(insert_scan_kernel, dim3(1), dim3(kInsBlock), 0, s, counts, nb, offsets, total);
   LC_LAUNCHED();
   int64_t host_total = 0;
-  LC_HIP(hipMemcpyAsync(&host_total, total, sizeof(host_total), hipMemcpyDeviceToHost, s));
-  LC_HIP(hipStreamSynchronize(s));
+  LC_HIP(read_back(&host_total, total, sizeof(host_total), s));
   if (host_total < 0 || host_total > k) return LIPCACHE_EHIP;
   if (c->n + host_total > c->capacity) return LIPCACHE_ECAPACITY;
   if (host_total == 0) return LIPCACHE_OK;

@@ -3,6 +3,10 @@
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <string.h>
+
+#include <atomic>
+#include <mutex>
 
 #include "lipcache.h"
 
@@ -29,6 +33,48 @@ constexpr int kWave = 64;
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 inline bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+
+// ------------------------------------------------------------ read-backs
+// The synchronous calls read a few bytes back (sigma, a count).  A copy into
+// pageable memory is staged by the runtime, so these go through one of 64
+// slots of 64 bytes in a pinned buffer, allocated on the first read-back and
+// held until the process ends.  A slot is taken with an atomic bitmap, so
+// concurrent calls from several host threads each use their own; with every
+// slot taken (or no pinned buffer) the copy goes to `dst` directly.
+constexpr size_t kReadSlotBytes = 64;
+constexpr int kReadSlots = 64;
+inline std::atomic<uint64_t> g_read_taken{0};
+inline unsigned char* g_read_buf = nullptr;
+inline std::once_flag g_read_once;
+
+inline hipError_t read_back(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  std::call_once(g_read_once, [] {
+    void* p = nullptr;
+    if (hipHostMalloc(&p, kReadSlotBytes * kReadSlots, hipHostMallocPortable) == hipSuccess)
+      g_read_buf = static_cast<unsigned char*>(p);
+    else
+      (void)hipGetLastError();
+  });
+  int slot = -1;
+  if (g_read_buf && bytes <= kReadSlotBytes) {
+    uint64_t m = g_read_taken.load(std::memory_order_relaxed);
+    while (m != ~0ull) {
+      const int i = __builtin_ctzll(~m);
+      if (g_read_taken.compare_exchange_weak(m, m | (1ull << i), std::memory_order_acquire)) {
+        slot = i;
+        break;
+      }
+    }
+  }
+  void* to = slot >= 0 ? static_cast<void*>(g_read_buf + slot * kReadSlotBytes) : dst;
+  hipError_t e = hipMemcpyAsync(to, src, bytes, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (slot >= 0) {
+    if (e == hipSuccess) memcpy(dst, to, bytes);
+    g_read_taken.fetch_and(~(1ull << slot), std::memory_order_release);
+  }
+  return e;
+}
 
 // ------------------------------------------------------------- bfloat16
 // Round to nearest even via the hardware conversion (v_cvt_pk_bf16_f32).

@@ -369,8 +369,7 @@ extern "C" lipcache_status lipcache_spectral_norm(const float* W, int32_t C, int
   }
   LC_LAUNCHED();
   double host[3] = {0.0, 0.0, 0.0};
-  LC_HIP(hipMemcpyAsync(host, out, sizeof(host), hipMemcpyDeviceToHost, s));
-  LC_HIP(hipStreamSynchronize(s));
+  LC_HIP(read_back(host, out, sizeof(host), s));
   *sigma = host[0];
   if (iterations) *iterations = static_cast<int32_t>(host[1]);
   if (!(host[0] > 0.0)) return LIPCACHE_EDEGENERATE;

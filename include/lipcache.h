@@ -9,11 +9,14 @@
  *
  * Conventions shared by every entry point
  *  - Pointers are DEVICE pointers owned by the caller unless marked (host).
- *    The library never allocates, frees or retains memory and keeps no
- *    global mutable state: calls on different streams are independent.
- *    Scratch memory is passed in as a workspace (`ws`, `ws_bytes`); each
+ *    The library allocates no device memory and retains no caller pointer:
+ *    scratch memory is passed in as a workspace (`ws`, `ws_bytes`); each
  *    entry point has a *_workspace_bytes query.  `ws` must be 256-byte
- *    aligned.
+ *    aligned.  Its only state outlives a call: the static workspace of
+ *    lipcache_lookup_noalloc, and a 4 KiB pinned host buffer through which
+ *    the synchronous calls read a few bytes back (allocated on first use,
+ *    a slot per concurrent call); calls on different streams are
+ *    independent.
  *  - Matrices are row-major and contiguous; a feature is one row of d
  *    elements.  Supported feature sizes: 32 <= d <= 1024, d % 32 == 0.
  *  - Arguments are validated on the host before any device work; a

@@ -295,6 +295,119 @@ __global__ __launch_bounds__(kPowThreads) void power_kernel(const double* __rest
   }
 }
 
+// Small heads (m = min(C, d) <= kSmallM): everything after G in one launch
+// instead of a launch per squaring.  The scale and the kSquarings squarings
+// run on LDS copies (all four waves, each entry a sum over k in ascending
+// order); the iteration runs in wave 0 alone: lane a holds row a of the
+// power and of G in registers and the iterate's entry a, reaches the other
+// entries by lane shuffles and needs no barrier.  Same method and stopping
+// rule as the chip-wide path: P = (G 2^-e)^(2^kSquarings) with 2^e >
+// trace(G), P scaled by 2^-e' with 2^e' > trace(P), the same start vector,
+// and sigma^2 the Rayleigh quotient of G at the last iterate.
+constexpr int kSmallM = 32;
+
+__global__ __launch_bounds__(256) void small_power_kernel(const double* __restrict__ G, int m, int max_iters,
+                                                          double rel_tol, double* __restrict__ out) {
+  __shared__ double gs[kSmallM * kSmallM];
+  __shared__ double pbuf[2][kSmallM * kSmallM];
+  const int t = static_cast<int>(threadIdx.x);
+  const int lane = lane_id();
+  const int mm = m * m;
+  for (int i = t; i < mm; i += 256) gs[i] = G[i];
+  __syncthreads();
+  double tr = 0.0;  // every thread, the same order: the same value everywhere
+  for (int a = 0; a < m; ++a) tr += gs[a * m + a];
+  if (!(tr > 0.0)) {  // W = 0: degenerate head
+    if (t == 0) {
+      out[0] = 0.0;
+      out[1] = 0.0;
+      out[2] = 0.0;
+    }
+    return;
+  }
+  const double sg = ldexp(1.0, -(ilogb(tr) + 1));  // exact
+  // P_1 = (s G)(s G), P_{i+1} = P_i P_i.  The factors are symmetric, so
+  // entry (a, b) is taken as the dot product of columns a and b: the lanes
+  // of a wave read consecutive words of one row (b varies fastest) and a
+  // common word (a), without bank conflicts; the result is exactly symmetric.
+  for (int i = t; i < mm; i += 256) {
+    const int a = i / m, b = i % m;
+    double acc = 0.0;
+    for (int k = 0; k < m; ++k) acc = __builtin_fma(gs[k * m + a] * sg, gs[k * m + b] * sg, acc);
+    pbuf[0][i] = acc;
+  }
+  __syncthreads();
+  int cur = 0;
+  for (int q = 1; q < kSquarings; ++q) {
+    for (int i = t; i < mm; i += 256) {
+      const int a = i / m, b = i % m;
+      double acc = 0.0;
+      for (int k = 0; k < m; ++k) acc = __builtin_fma(pbuf[cur][k * m + a], pbuf[cur][k * m + b], acc);
+      pbuf[cur ^ 1][i] = acc;
+    }
+    __syncthreads();
+    cur ^= 1;
+  }
+  if (t >= kWave) return;  // the iteration is wave 0's
+
+  const double* M = pbuf[cur];
+  double trm = 0.0;
+  for (int a = 0; a < m; ++a) trm += M[a * m + a];
+  double mrow[kSmallM], grow[kSmallM];
+  const double ms = trm > 0.0 ? ldexp(1.0, -(ilogb(trm) + 1)) : 0.0;
+#pragma unroll
+  for (int k = 0; k < kSmallM; ++k) {
+    const bool in = lane < m && k < m;
+    mrow[k] = in ? M[lane * m + k] * ms : 0.0;
+    grow[k] = in ? gs[lane * m + k] : 0.0;
+  }
+  double x = lane < m ? start_component(lane) : 0.0;
+  int it = 0, stable = 0, converged = 0;
+  bool have = false;
+  double prev = -1.0;
+  for (it = 1; it <= max_iters; ++it) {
+    double w = 0.0;
+#pragma unroll
+    for (int k = 0; k < kSmallM; ++k) w = __builtin_fma(mrow[k], __shfl(x, k, kWave), w);
+    const double XW = wave_sum_dpp(x * w);
+    const double XX = wave_sum_dpp(x * x);
+    const double WW = wave_sum_dpp(w * w);
+    if (!(WW > 0.0) || !(XX > 0.0)) {  // M x = 0
+      have = false;
+      break;
+    }
+    have = true;
+    const double lam = XW / XX;  // Rayleigh quotient of the scaled M
+    x = w / __builtin_sqrt(WW);  // the newest vector, normalised
+    if (it > 1 && __builtin_fabs(lam - prev) <= rel_tol * lam) {
+      ++stable;
+    } else {
+      stable = 0;
+    }
+    prev = lam;
+    if (stable >= 2) {
+      converged = 1;
+      break;
+    }
+  }
+  // sigma^2 = y.G y / y.y at the newest vector y
+  double sigma = 0.0;
+  if (have) {
+    double gy = 0.0;
+#pragma unroll
+    for (int k = 0; k < kSmallM; ++k) gy = __builtin_fma(grow[k], __shfl(x, k, kWave), gy);
+    const double YG = wave_sum_dpp(x * gy);
+    const double YY = wave_sum_dpp(x * x);
+    const double rho = YY > 0.0 ? YG / YY : 0.0;
+    sigma = __builtin_sqrt(rho > 0.0 ? rho : 0.0);
+  }
+  if (lane == 0) {
+    out[0] = sigma;
+    out[1] = static_cast<double>(it > max_iters ? max_iters : it);
+    out[2] = static_cast<double>(converged);
+  }
+}
+
 }  // namespace lc
 
 using namespace lc;
@@ -333,6 +446,17 @@ extern "C" lipcache_status lipcache_spectral_norm(const float* W, int32_t C, int
     hipLaunchKernelGGL(gram_mfma_kernel<kGramCols>, tgrid, dim3(256), 0, s, W, d, m, C, nullptr, G);
   }
   LC_LAUNCHED();
+  if (m <= kSmallM) {
+    hipLaunchKernelGGL(small_power_kernel, dim3(1), dim3(256), 0, s, G, m, max_iters, rel_tol, out);
+    LC_LAUNCHED();
+    double host[3] = {0.0, 0.0, 0.0};
+    LC_HIP(read_back(host, out, sizeof(host), s));
+    *sigma = host[0];
+    if (iterations) *iterations = static_cast<int32_t>(host[1]);
+    if (!(host[0] > 0.0)) return LIPCACHE_EDEGENERATE;
+    if (host[2] == 0.0) return LIPCACHE_ENOCONV;
+    return LIPCACHE_OK;
+  }
   double* scale = out + 4;
   hipLaunchKernelGGL(gram_scale_kernel, dim3(1), dim3(256), 0, s, G, m, scale);
   LC_LAUNCHED();

@@ -46,7 +46,9 @@ def tiny():
 
 # --------------------------------------------------------------- spectral norm
 @pytest.mark.parametrize("C,d", [(10, 64), (10, 128), (100, 128), (200, 256), (300, 64), (1000, 96),
-                                 (600, 700), (2, 32), (1, 5)])
+                                 (600, 700), (2, 32), (1, 5),
+                                 # both sides of the one-launch path for small heads (min(C, d) <= 32)
+                                 (32, 64), (33, 64), (50, 24), (64, 32), (7, 1024)])
 def test_spectral_norm_matches_oracle(C, d):
     say("spectral_norm", C, d)
     rng = np.random.default_rng(C * 1000 + d)

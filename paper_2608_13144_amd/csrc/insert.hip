@@ -2,7 +2,8 @@
 // construction, Alg. 1).
 //
 // Rows are taken in ascending order (a stable compaction), so the same input
-// always produces the same cache rows.  Four kernels:
+// always produces the same cache rows.  Four kernels (a batch of at most
+// 1024 rows runs count, scan and rank as one):
 //   count   - per 1024-row block, how many rows are selected;
 //   scan    - one workgroup turns the block counts into block offsets and the
 //             total (read back by the host for the all-or-nothing capacity
@@ -59,6 +60,25 @@ __global__ __launch_bounds__(kInsBlock) void insert_scan_kernel(const int64_t* _
   if (threadIdx.x == 0) *total = running;
 }
 
+// The block's selected rows in order: src_of[offset + t] = the t-th; returns
+// how many the block selected (in every thread).
+__device__ __forceinline__ int rank_block(int64_t j, bool take, int64_t offset, int64_t* __restrict__ src_of,
+                                          int* wave_count) {
+  const int lane = lane_id();
+  const int wave = static_cast<int>(threadIdx.x) / kWave;
+  const unsigned long long bal = __ballot(take);
+  const int below = __builtin_popcountll(bal & ((1ull << lane) - 1ull));
+  if (lane == 0) wave_count[wave] = __builtin_popcountll(bal);
+  __syncthreads();
+  int before = 0, all = 0;
+  for (int w = 0; w < kInsWaves; ++w) {
+    if (w < wave) before += wave_count[w];
+    all += wave_count[w];
+  }
+  if (take) src_of[offset + before + below] = j;
+  return all;
+}
+
 // src_of[offsets[block] + t] = the t-th selected row of the block.
 __global__ __launch_bounds__(kInsBlock) void insert_rank_kernel(const float* __restrict__ r_src,
                                                                 const int32_t* __restrict__ sel, int64_t k,
@@ -66,16 +86,19 @@ __global__ __launch_bounds__(kInsBlock) void insert_rank_kernel(const float* __r
                                                                 int64_t* __restrict__ src_of) {
   __shared__ int wave_count[kInsWaves];
   const int64_t j = static_cast<int64_t>(blockIdx.x) * kInsBlock + threadIdx.x;
-  const bool take = selected(j, k, r_src, sel);
-  const int lane = lane_id();
-  const int wave = static_cast<int>(threadIdx.x) / kWave;
-  const unsigned long long bal = __ballot(take);
-  const int below = __builtin_popcountll(bal & ((1ull << lane) - 1ull));
-  if (lane == 0) wave_count[wave] = __builtin_popcountll(bal);
-  __syncthreads();
-  int before = 0;
-  for (int w = 0; w < wave; ++w) before += wave_count[w];
-  if (take) src_of[offsets[blockIdx.x] + before + below] = j;
+  rank_block(j, selected(j, k, r_src, sel), offsets[blockIdx.x], src_of, wave_count);
+}
+
+// k <= kInsBlock: count, scan and rank in one workgroup (its offset is 0,
+// the total is its own count).
+__global__ __launch_bounds__(kInsBlock) void insert_rank_one_kernel(const float* __restrict__ r_src,
+                                                                    const int32_t* __restrict__ sel, int64_t k,
+                                                                    int64_t* __restrict__ src_of,
+                                                                    int64_t* __restrict__ total) {
+  __shared__ int wave_count[kInsWaves];
+  const int64_t j = threadIdx.x;
+  const int all = rank_block(j, selected(j, k, r_src, sel), 0, src_of, wave_count);
+  if (threadIdx.x == 0) *total = all;
 }
 
 struct InsertParams {
@@ -176,20 +199,29 @@ extern "C" lipcache_status lipcache_insert(lipcache_cache* c, const float* z_src
   int64_t* total = reinterpret_cast<int64_t*>(base + 2 * align_up(static_cast<size_t>(nb) * 8, 256));
   int64_t* src_of = reinterpret_cast<int64_t*>(base + 2 * align_up(static_cast<size_t>(nb) * 8, 256) + 256);
 
-  hipLaunchKernelGGL(insert_count_kernel, dim3(static_cast<unsigned>(nb)), dim3(kInsBlock), 0, s, r_src,
-                     miss_selector, k, counts);
-  LC_LAUNCHED();
-  hipLaunchKernelGGL(insert_scan_kernel, dim3(1), dim3(kInsBlock), 0, s, counts, nb, offsets, total);
-  LC_LAUNCHED();
+  if (nb == 1) {
+    // one block: its ranks are final, one launch before the read-back
+    hipLaunchKernelGGL(insert_rank_one_kernel, dim3(1), dim3(kInsBlock), 0, s, r_src, miss_selector, k, src_of,
+                       total);
+    LC_LAUNCHED();
+  } else {
+    hipLaunchKernelGGL(insert_count_kernel, dim3(static_cast<unsigned>(nb)), dim3(kInsBlock), 0, s, r_src,
+                       miss_selector, k, counts);
+    LC_LAUNCHED();
+    hipLaunchKernelGGL(insert_scan_kernel, dim3(1), dim3(kInsBlock), 0, s, counts, nb, offsets, total);
+    LC_LAUNCHED();
+  }
   int64_t host_total = 0;
   LC_HIP(read_back(&host_total, total, sizeof(host_total), s));
   if (host_total < 0 || host_total > k) return LIPCACHE_EHIP;
   if (c->n + host_total > c->capacity) return LIPCACHE_ECAPACITY;
   if (host_total == 0) return LIPCACHE_OK;
 
-  hipLaunchKernelGGL(insert_rank_kernel, dim3(static_cast<unsigned>(nb)), dim3(kInsBlock), 0, s, r_src,
-                     miss_selector, k, offsets, src_of);
-  LC_LAUNCHED();
+  if (nb > 1) {
+    hipLaunchKernelGGL(insert_rank_kernel, dim3(static_cast<unsigned>(nb)), dim3(kInsBlock), 0, s, r_src,
+                       miss_selector, k, offsets, src_of);
+    LC_LAUNCHED();
+  }
   InsertParams p;
   p.z_src = z_src;
   p.label_src = label_src;
